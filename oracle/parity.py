@@ -1,0 +1,134 @@
+"""GPU-versus-oracle acceptance check -- TEST INFRASTRUCTURE ONLY.
+
+Rules (paths first, then values):
+
+1. Paths.  For every (token, tree) the device path is walked level by level.
+   At the first level where its node differs from the oracle's, the oracle
+   must have flagged the parent visit as a near tie
+   (|logit| < tie_rel * ||x|| * ||W_in row||).  From there on the device path
+   is re-evaluated in fp64 along its own nodes, and every later step must
+   follow the sign of its fp64 logit (0 goes left) or be a near tie itself.
+   Any other difference fails.
+2. Counts.  ``n_near_tie`` = tokens with any flagged visit on the oracle
+   path; ``n_path_divergent`` = tokens whose device path differs anywhere.
+3. Values.  Per token, ||y_dev - y_ref||_2 / ||y_ref||_2 <= tol, with y_ref
+   evaluated in fp64 along the DEVICE path.
+
+Elementwise relative error is meaningless near zero, hence the normwise
+form; the largest elementwise error scaled by ||y_ref||_inf is reported too.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import DEFAULT_TIE_REL, eval_path
+
+
+def widen(a: np.ndarray) -> np.ndarray:
+    """float32 or bf16-bit-pattern (uint16) array -> float64, exactly."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def _row_norm(w: np.ndarray, t: int, n: int) -> float:
+    return float(np.linalg.norm(widen(w[t, n])))
+
+
+def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nodes_dev=None,
+          tol: float = 1e-5, act="gelu", tie_rel: float = DEFAULT_TIE_REL, rows=None,
+          base_dev=None) -> dict:
+    """Compare device results with the oracle.
+
+    ``rows``: optional token indices the oracle output covers (sampled check);
+    ``x`` and the device arrays are then indexed by it.  ``base_dev``: an
+    optional [B,H] term the device added to FFF(x) (residual or accumulate),
+    subtracted before comparing.
+    """
+    y_dev = widen(y_dev)
+    if base_dev is not None:
+        y_dev = y_dev - widen(base_dev)
+    if rows is not None:
+        rows = np.asarray(rows)
+        y_dev = y_dev[rows]
+        x_rows = np.asarray(x)[rows]
+        if nodes_dev is not None:
+            nodes_dev = np.asarray(nodes_dev)[rows]
+    else:
+        x_rows = np.asarray(x)
+    y_ref = oracle_out["y"].copy()
+    nodes_or = oracle_out["nodes"]
+    tie_or = oracle_out["near_tie"]
+    B = y_ref.shape[0]
+    report = {"tokens": int(B), "n_near_tie": int(tie_or.reshape(B, -1).any(axis=1).sum()),
+              "n_path_divergent": 0, "path_failures": [], "value_failures": []}
+
+    if nodes_dev is not None:
+        nodes_dev = np.asarray(nodes_dev).reshape(nodes_or.shape)
+        diverged = np.nonzero((nodes_dev != nodes_or).reshape(B, -1).any(axis=1))[0]
+        report["n_path_divergent"] = int(diverged.size)
+        for b in diverged:
+            xb = x_rows[b]
+            ok = True
+            for t in range(n_trees):
+                pd, po = nodes_dev[b, t], nodes_or[b, t]
+                if np.array_equal(pd, po):
+                    continue
+                first = int(np.nonzero(pd != po)[0][0])
+                if first == 0 or not tie_or[b, t, first - 1]:
+                    ok = False
+                    report["path_failures"].append((int(b), t, first, "diverged at a non-tie"))
+                    break
+            if not ok:
+                continue
+            try:
+                y_path, logits_path = eval_path(xb, w_in, w_out, depth, n_trees, nodes_dev[b], act)
+            except ValueError:
+                report["path_failures"].append((int(b), -1, -1, "illegal device path"))
+                continue
+            xnorm = float(np.linalg.norm(widen(xb)))
+            for t in range(n_trees):
+                pd = nodes_dev[b, t]
+                for level in range(depth):
+                    logit = logits_path[t, level]
+                    want = 2 * int(pd[level]) + 1 + (1 if logit > 0 else 0)
+                    if int(pd[level + 1]) != want:
+                        thresh = tie_rel * xnorm * _row_norm(w_in, t, int(pd[level]))
+                        if not abs(logit) < thresh:
+                            ok = False
+                            report["path_failures"].append((int(b), t, level, "wrong sign off-tie"))
+                            break
+                if not ok:
+                    break
+            if ok:
+                y_ref[b] = y_path
+
+    diff = np.linalg.norm(y_dev - y_ref, axis=1)
+    ref = np.linalg.norm(y_ref, axis=1)
+    err = diff / np.maximum(ref, 1e-30)
+    err[(ref == 0) & (diff == 0)] = 0.0
+    if nodes_dev is None:
+        # Without device paths a near-tie token may have branched the other way; skip those.
+        skip = tie_or.reshape(B, -1).any(axis=1)
+        err = np.where(skip, 0.0, err)
+        report["n_skipped_near_tie"] = int(skip.sum())
+    amax = np.max(np.abs(y_ref), axis=1)
+    elem = np.max(np.abs(y_dev - y_ref), axis=1) / np.maximum(amax, 1e-30)
+    report["max_normwise_err"] = float(err.max()) if B else 0.0
+    report["max_elem_err_over_inf"] = float(elem.max()) if B else 0.0
+    bad = np.nonzero(err > tol)[0]
+    report["value_failures"] = [(int(b), float(err[b])) for b in bad[:20]]
+    report["n_value_failures"] = int(bad.size)
+    report["ok"] = (not report["path_failures"]) and bad.size == 0
+    return report
+
+
+def assert_parity(*args, **kwargs) -> dict:
+    rep = check(*args, **kwargs)
+    if not rep["ok"]:
+        raise AssertionError(
+            f"parity failed: {len(rep['path_failures'])} path failures "
+            f"(first: {rep['path_failures'][:3]}), {rep['n_value_failures']} value failures "
+            f"(first: {rep['value_failures'][:3]}), max normwise err {rep['max_normwise_err']:.3e}")
+    return rep

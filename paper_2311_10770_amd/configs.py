@@ -1,0 +1,66 @@
+"""Named FFF workloads (shapes, dtypes and seeds), used by tests and the benchmark.
+
+Depth counts edges on a root-to-leaf path, so a tree of depth D has
+2**(D+1) - 1 nodes and a token visits D+1 of them (UltraFastBERT-KxD naming,
+Section 2.1 and Table 1 of the paper).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+from .synth import BF16, F32, n_nodes
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    seed: int
+    n_tokens: int
+    hidden: int
+    depth: int
+    n_trees: int
+    x_dtype: str
+    w_dtype: str
+    y_dtype: str
+    layers: int = 1
+    note: str = ""
+    sweep: tuple = field(default_factory=tuple)
+
+    @property
+    def nodes(self) -> int:
+        return n_nodes(self.depth)
+
+    def w_elem_bytes(self) -> int:
+        return 2 if self.w_dtype == BF16 else 4
+
+    def gathered_bytes_per_token(self) -> int:
+        """Weight bytes one token reads: one W_in row and one W_out row per visited node."""
+        return self.n_trees * (self.depth + 1) * 2 * self.hidden * self.w_elem_bytes()
+
+    def flops_per_token(self) -> int:
+        """Multiply-adds of the dot product and of the output accumulation, 2 flops each."""
+        return 4 * self.hidden * self.n_trees * (self.depth + 1)
+
+
+WORKLOADS = {
+    # One tree of depth 3 (15 nodes): the small case the oracle finishes instantly.
+    "d3_h768_b128_f32": Workload("d3_h768_b128_f32", 1, 128, 768, 3, 1, F32, F32, F32),
+    # UltraFastBERT-1x11 layer at the paper's speed-test batch: 128 sequences x 128 tokens.
+    "d11_h768_b16384_f32": Workload("d11_h768_b16384_f32", 2, 16384, 768, 11, 1, F32, F32, F32),
+    # Same tree in bf16, 65536 tokens: the headline throughput workload.
+    "d11_h768_b65536_bf16": Workload("d11_h768_b65536_bf16", 3, 65536, 768, 11, 1, BF16, BF16, BF16),
+    # Same, bf16 weights with fp32 activations in and out.
+    "d11_h768_b65536_w_bf16": Workload("d11_h768_b65536_w_bf16", 3, 65536, 768, 11, 1, F32, BF16, F32),
+    # UltraFastBERT-4x9: four trees of depth 9 (4 x 1023 nodes), outputs summed.
+    "4x9_h768_b16384_f32": Workload("4x9_h768_b16384_f32", 4, 16384, 768, 9, 4, F32, F32, F32),
+    # Four trees of depth 8 (4 x 511 nodes).
+    "4x8_h768_b16384_f32": Workload("4x8_h768_b16384_f32", 4, 16384, 768, 8, 4, F32, F32, F32),
+    # Twelve stacked 4x9 layers with a residual, x <- x + FFF(x).
+    "4x9_h768_b16384_f32_x12": Workload("4x9_h768_b16384_f32_x12", 4, 16384, 768, 9, 4, F32, F32, F32,
+                                        layers=12),
+    # LLM-width tree: depth 15 (65535 nodes) at hidden 4096, batch sweep.
+    "d15_h4096_bf16": Workload("d15_h4096_bf16", 5, 8192, 4096, 15, 1, BF16, BF16, BF16,
+                               sweep=(1, 64, 1024, 8192)),
+}
+
+HEADLINE = "d11_h768_b65536_bf16"
