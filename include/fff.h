@@ -1,0 +1,145 @@
+/*
+ * fff.h -- C ABI of libfff.so: fast-feedforward (FFF) inference on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operation is the FFF forward pass of "Exponentially Faster Language
+ * Modeling" (Belcak and Wattenhofer, 2023): conditional matrix multiplication
+ * (CMM, Algorithm 1) followed by the output accumulation, with the model
+ * changes of Section 2.1 (the same activation at every node, output weights
+ * on every node, no biases, leaf size 1, several trees summed).  For every
+ * token b and tree t, starting at the root n = 0, at each level l = 0..D:
+ *
+ *     logit  = <x[b,:], W_in[t,n,:]>
+ *     y[b,:] += act(logit) * W_out[t,n,:]
+ *     n      = 2n + 1 + (logit > 0)          (if l < D; a zero logit goes left)
+ *
+ * so each token visits D+1 of the N = 2^(D+1) - 1 nodes of each tree.
+ *
+ * Conventions shared by every entry point:
+ *   - depth D counts edges on a root-to-leaf path (UltraFastBERT-KxD naming,
+ *     Table 1): depth 11 is the 4095-node tree of UltraFastBERT-1x11.
+ *   - layouts (all row-major, contiguous, no strides):
+ *       x      [n_tokens, hidden]
+ *       y      [n_tokens, hidden]
+ *       W_in   [n_trees, N, hidden], node rows in heap order (children of n
+ *       W_out  [n_trees, N, hidden]  are 2n+1 and 2n+2); row n of tree t
+ *                                    starts at element (t*N + n)*hidden.
+ *   - every data pointer is a DEVICE pointer owned by the caller; the library
+ *     never frees or retains them.  Base pointers must be 16-byte aligned.
+ *   - arithmetic is fp32 (bf16 inputs are widened exactly); bf16 outputs are
+ *     rounded to nearest even.
+ *   - work is enqueued on hip_stream (NULL = the null stream) and the call
+ *     returns without waiting; device faults surface at the caller's next
+ *     synchronisation.
+ *   - every argument check runs before any HIP call; on a non-zero return no
+ *     device work has been enqueued, except FFF_ERR_HIP, which reports a
+ *     failed HIP call (see fff_last_hip_error).
+ *   - the library is reentrant; its only global state is a per-device
+ *     property cache and the thread-local last HIP error.
+ */
+#ifndef FFF_H_
+#define FFF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FFF_VERSION 100 /* major * 100 + minor */
+
+typedef enum {
+    FFF_OK = 0,
+    FFF_ERR_INVALID_ARG = -1, /* a null pointer, bad size, bad enum, misalignment or x/y overlap */
+    FFF_ERR_UNSUPPORTED = -2, /* valid request this build has no kernel for */
+    FFF_ERR_WORKSPACE = -3,   /* grouped mode without enough workspace */
+    FFF_ERR_HIP = -4          /* a HIP runtime call failed */
+} fff_status;
+
+typedef enum { FFF_F32 = 0, FFF_BF16 = 1 } fff_dtype;
+
+/* GELU in its exact form z*Phi(z) (the paper's activation, Section 2.1), its
+ * tanh approximation, or the identity (for exact integer tests). */
+typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2 } fff_act;
+
+/* DESCENT: one sub-wave per token walks the tree, the top levels served from
+ * LDS.  GROUPED: tokens are first bucketed by their node at a split level
+ * and each bucket's subtree is walked by workgroups on one XCD (needs a
+ * workspace).  GENERIC: any hidden size, one wave per token.  AUTO picks. */
+typedef enum {
+    FFF_MODE_AUTO = 0,
+    FFF_MODE_DESCENT = 1,
+    FFF_MODE_GROUPED = 2,
+    FFF_MODE_GENERIC = 3
+} fff_mode;
+
+/* What is written to y: FFF(x); y + FFF(x); or x + FFF(x) (the residual of a
+ * transformer block, needs x and y of the same hidden size). */
+typedef enum { FFF_OUT_STORE = 0, FFF_OUT_ACCUMULATE = 1, FFF_OUT_RESIDUAL = 2 } fff_out;
+
+/*
+ * fff_forward -- y = FFF(x) with the exact GELU, the paper's layer
+ * (Algorithm 1 with the Section 2.1 changes).
+ *
+ *   x, W_in, W_out, y : device pointers, layouts above; x and y must not overlap
+ *                       (W_in and W_out may alias).
+ *   depth             : 0..24.       n_trees : >= 1.
+ *   n_tokens          : >= 0 (0 is a no-op returning FFF_OK).
+ *   hidden            : >= 1.
+ *   x_dtype, w_dtype, y_dtype : FFF_F32 or FFF_BF16, independently.
+ *   hip_stream        : a hipStream_t, or NULL.
+ * Returns an fff_status.
+ */
+int fff_forward(const void* x, const void* W_in, const void* W_out, int32_t depth, int32_t n_trees,
+                void* y, int64_t n_tokens, int32_t hidden, int32_t x_dtype, int32_t w_dtype,
+                int32_t y_dtype, void* hip_stream);
+
+/* Full form.  Zero-initialise, then set the fields; a zeroed struct with the
+ * pointers and sizes filled in is the fff_forward call. */
+typedef struct {
+    const void* x;
+    const void* W_in;
+    const void* W_out;
+    void* y;
+    int64_t n_tokens;
+    int32_t hidden;
+    int32_t depth;
+    int32_t n_trees;
+    int32_t x_dtype, w_dtype, y_dtype; /* fff_dtype */
+    int32_t act;                       /* fff_act */
+    int32_t mode;                      /* fff_mode */
+    int32_t out_mode;                  /* fff_out */
+    int32_t lds_levels;   /* top tree levels cached in LDS (DESCENT); 0 = default choice,
+                             -1 = none, k > 0 = exactly k (FFF_ERR_UNSUPPORTED if too big) */
+    int32_t split_level;  /* GROUPED: level whose node buckets the tokens; 0 = default */
+    int32_t* nodes_out;   /* optional device [n_tokens, n_trees, depth+1]: node visited per level */
+    float* logits_out;    /* optional device [n_tokens, n_trees, depth+1]: fp32 logit per level */
+    void* workspace;      /* GROUPED: device scratch of fff_workspace_bytes() bytes, 256-aligned */
+    size_t workspace_bytes;
+    void* hip_stream;
+} fff_args;
+
+int fff_forward_ex(const fff_args* a);
+
+/* Device scratch bytes GROUPED mode needs for n_tokens tokens at the given
+ * split level (0 = the default for this depth).  Returns 0 if grouped mode
+ * does not apply to the shape. */
+size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,
+                           int32_t split_level);
+
+/* Short human-readable description of the kernel and launch fff_forward_ex
+ * would use for these arguments (after validation), written into buf
+ * (NUL-terminated, truncated to len).  Makes no HIP call other than the
+ * cached device-property query.  Returns an fff_status. */
+int fff_describe(const fff_args* a, char* buf, size_t len);
+
+const char* fff_status_str(int status);
+int fff_last_hip_error(void); /* raw hipError_t behind the calling thread's last FFF_ERR_HIP */
+int fff_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FFF_H_ */

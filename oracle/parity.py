@@ -11,17 +11,30 @@ Rules (paths first, then values):
    Any other difference fails.
 2. Counts.  ``n_near_tie`` = tokens with any flagged visit on the oracle
    path; ``n_path_divergent`` = tokens whose device path differs anywhere.
-3. Values.  Per token, ||y_dev - y_ref||_2 / ||y_ref||_2 <= tol, with y_ref
-   evaluated in fp64 along the DEVICE path.
+3. Values.  Per token, ||y_dev - y_ref||_2 <= tol * ||y_ref||_2 + allowance,
+   with y_ref evaluated in fp64 along the DEVICE path.  The allowance is the
+   first-order effect of rounding the fp32 logits:
+       allowance = sum over visits of |act'(l)| * gamma * ||x|| ||W_in[n]|| ||W_out[n]||
+   where gamma * ||x|| ||W_in[n]|| bounds the error of an fp32 dot product
+   (gamma = 64 unit roundoffs covers a per-lane chain plus a cross-lane tree
+   of up to 64 terms).  It matters only when y itself is tiny next to the
+   terms that feed it -- e.g. a single visited node with a strongly negative
+   logit, where GELU's relative slope (about |l|) amplifies the logit's
+   absolute rounding -- and tokens that need it are counted
+   (``n_conditioned``).
 
 Elementwise relative error is meaningless near zero, hence the normwise
 form; the largest elementwise error scaled by ||y_ref||_inf is reported too.
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 from . import DEFAULT_TIE_REL, eval_path
+
+DOT_GAMMA = 64 * 2.0 ** -24
 
 
 def widen(a: np.ndarray) -> np.ndarray:
@@ -36,9 +49,29 @@ def _row_norm(w: np.ndarray, t: int, n: int) -> float:
     return float(np.linalg.norm(widen(w[t, n])))
 
 
+def row_norms(w: np.ndarray, chunk: int = 4096) -> np.ndarray:
+    """||row||_2 of every [T, N, H] weight row, as float64 [T, N] (chunked to bound memory)."""
+    T, N, _ = w.shape
+    out = np.empty((T, N))
+    for t in range(T):
+        for n0 in range(0, N, chunk):
+            out[t, n0:n0 + chunk] = np.linalg.norm(widen(w[t, n0:n0 + chunk]), axis=1)
+    return out
+
+
+def act_slope(logits: np.ndarray, act) -> np.ndarray:
+    """|d act / d l| at the given logits (GELU: Phi(l) + l*phi(l); identity: 1)."""
+    if act in ("identity", 2):
+        return np.ones_like(logits)
+    erf = np.vectorize(math.erf, otypes=[float])
+    phi_cdf = 0.5 * (1.0 + erf(logits / math.sqrt(2.0)))
+    pdf = np.exp(-0.5 * logits * logits) / math.sqrt(2.0 * math.pi)
+    return np.abs(phi_cdf + logits * pdf)
+
+
 def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nodes_dev=None,
           tol: float = 1e-5, act="gelu", tie_rel: float = DEFAULT_TIE_REL, rows=None,
-          base_dev=None) -> dict:
+          base_dev=None, dot_gamma: float = DOT_GAMMA) -> dict:
     """Compare device results with the oracle.
 
     ``rows``: optional token indices the oracle output covers (sampled check);
@@ -58,6 +91,8 @@ def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nod
     else:
         x_rows = np.asarray(x)
     y_ref = oracle_out["y"].copy()
+    nodes_ref = oracle_out["nodes"].copy()
+    logits_ref = oracle_out["logits"].copy()
     nodes_or = oracle_out["nodes"]
     tie_or = oracle_out["near_tie"]
     B = y_ref.shape[0]
@@ -103,11 +138,23 @@ def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nod
                     break
             if ok:
                 y_ref[b] = y_path
+                nodes_ref[b] = nodes_dev[b]
+                logits_ref[b] = logits_path
 
     diff = np.linalg.norm(y_dev - y_ref, axis=1)
     ref = np.linalg.norm(y_ref, axis=1)
     err = diff / np.maximum(ref, 1e-30)
     err[(ref == 0) & (diff == 0)] = 0.0
+    # first-order allowance for fp32 logit rounding (see module docstring)
+    nin, nout = row_norms(w_in), row_norms(w_out)
+    tidx = np.arange(n_trees)[None, :, None]
+    xnorm = np.linalg.norm(widen(x_rows), axis=1)
+    terms = act_slope(logits_ref, act) * nin[tidx, nodes_ref] * nout[tidx, nodes_ref]
+    allowance = dot_gamma * xnorm * terms.reshape(B, -1).sum(axis=1)
+    conditioned = (err > tol) & (diff <= tol * ref + allowance)
+    report["n_conditioned"] = int(conditioned.sum())
+    report["max_normwise_err_raw"] = float(err.max()) if B else 0.0
+    err = np.where(conditioned, 0.0, err)
     if nodes_dev is None:
         # Without device paths a near-tie token may have branched the other way; skip those.
         skip = tie_or.reshape(B, -1).any(axis=1)

@@ -1,1 +1,10 @@
-"""MI355X-native fast-feedforward (FFF) inference: conditional matrix multiplication on gfx950."""
+"""MI355X-native fast-feedforward (FFF) inference: conditional matrix multiplication on gfx950.
+
+The compute lives in ``libfff.so`` (HIP kernels behind the C ABI of
+``include/fff.h``); this package is its ctypes binding plus the seeded
+synthetic-input generators and the named workloads.
+"""
+from .fff import (  # noqa: F401
+    FffArgs, FffError, describe, forward, forward_plain, from_numpy, load_library, make_args, status_str,
+    to_numpy, version, workspace_bytes,
+)

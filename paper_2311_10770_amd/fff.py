@@ -1,0 +1,214 @@
+"""ctypes binding of libfff.so (include/fff.h).
+
+Argument marshalling only: tensors become device pointers, enums become
+ints, and every step of the FFF forward runs in the library's HIP kernels.
+The library must be built (``python -m paper_2311_10770_amd.build``); there
+is no fallback path, and a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from ctypes import c_char_p, c_int, c_int32, c_int64, c_size_t, c_void_p
+from pathlib import Path
+
+import torch
+
+LIB_PATH = Path(__file__).resolve().with_name("libfff.so")
+
+FFF_OK, FFF_ERR_INVALID_ARG, FFF_ERR_UNSUPPORTED, FFF_ERR_WORKSPACE, FFF_ERR_HIP = 0, -1, -2, -3, -4
+FFF_F32, FFF_BF16 = 0, 1
+ACTS = {"gelu": 0, "gelu_erf": 0, "gelu_tanh": 1, "identity": 2}
+MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3}
+OUTS = {"store": 0, "accumulate": 1, "residual": 2}
+_TORCH_DT = {torch.float32: FFF_F32, torch.bfloat16: FFF_BF16}
+
+
+class FffArgs(ctypes.Structure):
+    """Mirror of ``fff_args`` in include/fff.h."""
+
+    _fields_ = [
+        ("x", c_void_p), ("W_in", c_void_p), ("W_out", c_void_p), ("y", c_void_p),
+        ("n_tokens", c_int64), ("hidden", c_int32), ("depth", c_int32), ("n_trees", c_int32),
+        ("x_dtype", c_int32), ("w_dtype", c_int32), ("y_dtype", c_int32),
+        ("act", c_int32), ("mode", c_int32), ("out_mode", c_int32),
+        ("lds_levels", c_int32), ("split_level", c_int32),
+        ("nodes_out", c_void_p), ("logits_out", c_void_p),
+        ("workspace", c_void_p), ("workspace_bytes", c_size_t),
+        ("hip_stream", c_void_p),
+    ]
+
+
+class FffError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+_lib = None
+
+EXPORTS = ("fff_forward", "fff_forward_ex", "fff_workspace_bytes", "fff_describe", "fff_status_str",
+           "fff_last_hip_error", "fff_version")
+
+
+def load_library(path: Path | str | None = None):
+    """Load libfff.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    p = Path(path) if path else LIB_PATH
+    if not p.exists():
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2311_10770_amd.build`")
+    lib = ctypes.CDLL(str(p))
+    lib.fff_forward.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_int64, c_int32,
+                                c_int32, c_int32, c_int32, c_void_p]
+    lib.fff_forward.restype = c_int
+    lib.fff_forward_ex.argtypes = [ctypes.POINTER(FffArgs)]
+    lib.fff_forward_ex.restype = c_int
+    lib.fff_workspace_bytes.argtypes = [c_int64, c_int32, c_int32, c_int32, c_int32]
+    lib.fff_workspace_bytes.restype = c_size_t
+    lib.fff_describe.argtypes = [ctypes.POINTER(FffArgs), c_char_p, c_size_t]
+    lib.fff_describe.restype = c_int
+    lib.fff_status_str.argtypes = [c_int]
+    lib.fff_status_str.restype = c_char_p
+    lib.fff_last_hip_error.argtypes = []
+    lib.fff_last_hip_error.restype = c_int
+    lib.fff_version.argtypes = []
+    lib.fff_version.restype = c_int
+    _lib = lib
+    return lib
+
+
+def status_str(rc: int) -> str:
+    return load_library().fff_status_str(rc).decode()
+
+
+def _check(rc: int):
+    if rc != FFF_OK:
+        lib = load_library()
+        msg = status_str(rc)
+        if rc == FFF_ERR_HIP:
+            msg += f" (hipError {lib.fff_last_hip_error()})"
+        raise FffError(rc, msg)
+
+
+def _dt(t: torch.Tensor, what: str) -> int:
+    try:
+        return _TORCH_DT[t.dtype]
+    except KeyError:
+        raise ValueError(f"{what} must be float32 or bfloat16, got {t.dtype}") from None
+
+
+def _dev_tensor(t, what, device):
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what} must be a torch.Tensor")
+    if t.device != device:
+        raise ValueError(f"{what} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t
+
+
+def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out="store", lds_levels=0,
+              split_level=0, nodes_out=None, logits_out=None, workspace=None, stream=None) -> FffArgs:
+    """Validate tensor-level properties and fill an ``fff_args``."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x must be a 2-D tensor [n_tokens, hidden]")
+    device = x.device
+    if device.type != "cuda":
+        raise ValueError("x must be a GPU tensor")
+    for t, what in ((w_in, "W_in"), (w_out, "W_out"), (y, "y")):
+        _dev_tensor(t, what, device)
+    _dev_tensor(x, "x", device)
+    B, H = x.shape
+    N = (1 << (depth + 1)) - 1
+    if tuple(w_in.shape) != (n_trees, N, H) or tuple(w_out.shape) != (n_trees, N, H):
+        raise ValueError(f"W_in/W_out must be [{n_trees}, {N}, {H}], got {tuple(w_in.shape)}, {tuple(w_out.shape)}")
+    if w_in.dtype != w_out.dtype:
+        raise ValueError("W_in and W_out must share a dtype")
+    if tuple(y.shape) != (B, H):
+        raise ValueError(f"y must be [{B}, {H}], got {tuple(y.shape)}")
+    for t, what in ((nodes_out, "nodes_out"), (logits_out, "logits_out")):
+        if t is not None:
+            _dev_tensor(t, what, device)
+            if t.numel() != B * n_trees * (depth + 1):
+                raise ValueError(f"{what} must hold n_tokens*n_trees*(depth+1) elements")
+    if nodes_out is not None and nodes_out.dtype != torch.int32:
+        raise ValueError("nodes_out must be int32")
+    if logits_out is not None and logits_out.dtype != torch.float32:
+        raise ValueError("logits_out must be float32")
+    a = FffArgs()
+    a.x, a.W_in, a.W_out, a.y = x.data_ptr(), w_in.data_ptr(), w_out.data_ptr(), y.data_ptr()
+    a.n_tokens, a.hidden, a.depth, a.n_trees = B, H, depth, n_trees
+    a.x_dtype, a.w_dtype, a.y_dtype = _dt(x, "x"), _dt(w_in, "W_in"), _dt(y, "y")
+    a.act = ACTS[act] if isinstance(act, str) else int(act)
+    a.mode = MODES[mode] if isinstance(mode, str) else int(mode)
+    a.out_mode = OUTS[out] if isinstance(out, str) else int(out)
+    a.lds_levels, a.split_level = int(lds_levels), int(split_level)
+    a.nodes_out = nodes_out.data_ptr() if nodes_out is not None else None
+    a.logits_out = logits_out.data_ptr() if logits_out is not None else None
+    if workspace is not None:
+        _dev_tensor(workspace, "workspace", device)
+        a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    a.hip_stream = s.cuda_stream
+    return a
+
+
+def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=None, **kw):
+    """FFF forward through ``fff_forward_ex``; returns y (allocated if not given)."""
+    if y is None:
+        y = torch.empty(x.shape, dtype=y_dtype or x.dtype, device=x.device)
+    a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
+    lib = load_library()
+    with torch.cuda.device(x.device):
+        _check(lib.fff_forward_ex(ctypes.byref(a)))
+    return y
+
+
+def forward_plain(x, w_in, w_out, depth: int, n_trees: int, y, stream=None):
+    """The six-argument call ``fff_forward(x, W_in, W_out, depth, n_trees, y, ...)`` (exact GELU, store)."""
+    a = make_args(x, w_in, w_out, depth, n_trees, y, stream=stream)
+    lib = load_library()
+    with torch.cuda.device(x.device):
+        _check(lib.fff_forward(a.x, a.W_in, a.W_out, depth, n_trees, a.y, a.n_tokens, a.hidden, a.x_dtype,
+                               a.w_dtype, a.y_dtype, a.hip_stream))
+    return y
+
+
+def describe(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, **kw) -> str:
+    """The kernel and launch shape ``forward`` would use."""
+    if y is None:
+        y = torch.empty(x.shape, dtype=kw.pop("y_dtype", None) or x.dtype, device=x.device)
+    kw.pop("y_dtype", None)
+    a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
+    buf = ctypes.create_string_buffer(512)
+    with torch.cuda.device(x.device):
+        _check(load_library().fff_describe(ctypes.byref(a), buf, len(buf)))
+    return buf.value.decode()
+
+
+def workspace_bytes(n_tokens: int, depth: int, n_trees: int, hidden: int, split_level: int = 0) -> int:
+    return int(load_library().fff_workspace_bytes(n_tokens, depth, n_trees, hidden, split_level))
+
+
+def version() -> int:
+    return int(load_library().fff_version())
+
+
+def from_numpy(a, device) -> torch.Tensor:
+    """numpy float32 / int32 array, or uint16 bf16 bit patterns, -> tensor on ``device``."""
+    import numpy as np
+
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def to_numpy(t: torch.Tensor):
+    """Tensor -> numpy; bfloat16 comes back as uint16 bit patterns."""
+    import numpy as np
+
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()

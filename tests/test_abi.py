@@ -1,0 +1,115 @@
+"""The C ABI without a GPU: exports, struct layout, and argument validation.
+
+Every call here fails validation (or is a zero-token no-op), which the ABI
+promises happens before any HIP call, so nothing touches a device.
+"""
+import ctypes
+import re
+import subprocess
+
+import pytest
+
+from paper_2311_10770_amd import build as native_build
+from paper_2311_10770_amd import fff as binding
+from tests.conftest import ROOT
+
+HEADER = ROOT / "include" / "fff.h"
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", HEADER.read_text(), flags=re.S)
+    return sorted(set(re.findall(r"\b(fff_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not binding.LIB_PATH.exists():
+        native_build.build_lib("libfff.so")
+    return binding.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", str(binding.LIB_PATH)], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    assert set(names) <= exported
+    assert not {e for e in exported if not e.startswith("fff_") and not e.startswith("_init")
+                and not e.startswith("_fini")}, "only the fff_ ABI is exported"
+
+
+def test_struct_layout_matches_c(tmp_path):
+    fields = [f[0] for f in binding.FffArgs._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "fff.h"\nint main(void){\n'
+                   + 'printf("%zu\\n", sizeof(fff_args));\n'
+                   + "".join(f'printf("%zu\\n", offsetof(fff_args, {f}));\n' for f in fields) + "return 0;}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", str(ROOT / "include"), str(src), "-o", str(exe)], check=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(binding.FffArgs)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(binding.FffArgs, f).offset == off, f
+
+
+def test_version_and_status_strings(lib):
+    assert lib.fff_version() == 100
+    for rc in (0, -1, -2, -3, -4):
+        assert lib.fff_status_str(rc).decode().startswith("FFF_")
+    assert lib.fff_status_str(7) == b"unknown fff status"
+    assert lib.fff_last_hip_error() == 0
+
+
+P = 0x100000  # an aligned fake device address; validation never dereferences it
+
+
+def good_args(**over):
+    a = binding.FffArgs()
+    a.x, a.W_in, a.W_out, a.y = P, P * 16, P * 16, P * 64
+    a.n_tokens, a.hidden, a.depth, a.n_trees = 4, 64, 3, 1
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("over", [
+    dict(n_tokens=-1), dict(hidden=0), dict(depth=-1), dict(depth=25), dict(n_trees=0),
+    dict(x_dtype=2), dict(w_dtype=-1), dict(y_dtype=5), dict(act=3), dict(mode=9), dict(out_mode=3),
+    dict(lds_levels=-2), dict(split_level=4), dict(split_level=-1),
+    dict(x=None), dict(W_in=None), dict(W_out=None), dict(y=None),
+    dict(x=P + 4), dict(y=P * 64 + 8), dict(W_in=P * 16 + 2),
+    dict(y=P + 64),                           # overlaps x
+    dict(nodes_out=P * 64 + 16),              # overlaps y
+    dict(nodes_out=P * 256, logits_out=P * 256 + 16),
+    dict(n_tokens=1 << 62),                   # size overflow
+])
+def test_invalid_arguments_rejected_before_hip(lib, over):
+    a = good_args(**over)
+    assert lib.fff_forward_ex(ctypes.byref(a)) == binding.FFF_ERR_INVALID_ARG
+    buf = ctypes.create_string_buffer(64)
+    assert lib.fff_describe(ctypes.byref(a), buf, len(buf)) == binding.FFF_ERR_INVALID_ARG
+    assert lib.fff_last_hip_error() == 0
+
+
+def test_null_args_and_zero_tokens(lib):
+    assert lib.fff_forward_ex(None) == binding.FFF_ERR_INVALID_ARG
+    a = binding.FffArgs()
+    a.n_tokens, a.hidden, a.depth, a.n_trees = 0, 768, 11, 1
+    assert lib.fff_forward_ex(ctypes.byref(a)) == binding.FFF_OK  # no pointers needed, nothing enqueued
+    assert lib.fff_forward(None, None, None, 11, 1, None, 0, 768, 0, 0, 0, None) == binding.FFF_OK
+    assert lib.fff_forward(None, None, None, 11, 1, None, 5, 768, 0, 0, 0, None) == binding.FFF_ERR_INVALID_ARG
+
+
+def test_workspace_bytes_rejects_bad_shapes(lib):
+    assert lib.fff_workspace_bytes(-1, 11, 1, 768, 0) == 0
+    assert lib.fff_workspace_bytes(100, 25, 1, 768, 0) == 0
+    assert lib.fff_workspace_bytes(100, 11, 0, 768, 0) == 0
+    assert lib.fff_workspace_bytes(100, 11, 1, 768, 12) == 0
+
+
+def test_build_flags_disable_packed_fp32():
+    flags = " ".join(native_build.COMMON)
+    assert "-packed-fp32-ops" in flags and "--offload-arch=gfx950" in flags

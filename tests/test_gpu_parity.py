@@ -1,0 +1,205 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Paths must match the oracle node for node except after a flagged near tie;
+outputs must meet the per-token normwise bar (1e-5 for fp32 outputs, 2e-2
+for bf16 outputs), evaluated along the device's own path.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import parity
+from paper_2311_10770_amd import synth
+from paper_2311_10770_amd.configs import WORKLOADS
+from tests.gpu_util import DEV, TORCH_DT, check_layer, layer, run_fff, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+# ------------------------------------------------------------ named workloads
+
+
+@pytest.mark.parametrize("name", ["d3_h768_b128_f32", "d11_h768_b16384_f32", "d11_h768_b65536_bf16",
+                                  "d11_h768_b65536_w_bf16", "4x9_h768_b16384_f32", "4x8_h768_b16384_f32"])
+def test_workload_full_size(fff_lib, name):
+    w = WORKLOADS[name]
+    L = synth.make_layer(w.seed, w.n_tokens, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    check_layer(fff_lib, name, L, w.depth, w.n_trees, w.y_dtype)
+
+
+def test_llm_width_tree_batch_sweep(fff_lib):
+    """Depth 15 (65535 nodes) at hidden 4096, bf16; smaller batches are prefixes of the largest draw."""
+    w = WORKLOADS["d15_h4096_bf16"]
+    L = synth.make_layer(w.seed, max(w.sweep), w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    for B in w.sweep:
+        Lb = dict(L, x=L["x"][:B])
+        check_layer(fff_lib, f"d15_h4096 B={B}", Lb, w.depth, w.n_trees, w.y_dtype)
+
+
+def test_stacked_layers_teacher_forced(fff_lib):
+    """Twelve 4x9 layers with x <- x + FFF(x); each layer is checked on the device's own input."""
+    w = WORKLOADS["4x9_h768_b16384_f32_x12"]
+    B = 4096
+    x = synth.make_x(w.seed, B, w.hidden, "f32")
+    for layer_idx in range(w.layers):
+        wi, wo = synth.make_weights(w.seed, w.hidden, w.depth, w.n_trees, "f32", layer=layer_idx + 1)
+        L = {"x": x, "w_in": wi, "w_out": wo}
+        got = run_fff(fff_lib, L, w.depth, w.n_trees, "f32", out="residual")
+        ref = oracle.forward(x, wi, wo, w.depth, w.n_trees)
+        parity.assert_parity(x, wi, wo, w.depth, w.n_trees, ref, got["y"], got["nodes"], tol=1e-5, base_dev=x)
+        x = got["y"].astype(np.float32)
+
+
+# ------------------------------------------------------ shapes, dtypes, edges
+
+DTYPE_COMBOS = [("f32", "f32", "f32"), ("bf16", "bf16", "bf16"), ("f32", "bf16", "f32"), ("bf16", "bf16", "f32"),
+                ("bf16", "f32", "f32"), ("f32", "f32", "bf16"), ("f32", "bf16", "bf16"), ("bf16", "f32", "bf16")]
+
+
+@pytest.mark.parametrize("xd,wd,yd", DTYPE_COMBOS)
+@pytest.mark.parametrize("H", [768, 1024, 4096])
+def test_dtype_combinations_fast_widths(fff_lib, xd, wd, yd, H):
+    depth = 6 if H == 4096 else 8
+    L = layer(20 + H, 777, H, depth, 1, xd, wd)
+    check_layer(fff_lib, f"{xd}/{wd}/{yd} H={H}", L, depth, 1, yd)
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 63, 64, 65, 255, 257, 1000, 4097])
+def test_ragged_token_counts(fff_lib, B):
+    L = layer(30, B, 768, 11, 1, "bf16", "bf16")
+    check_layer(fff_lib, f"ragged B={B}", L, 11, 1, "bf16")
+
+
+@pytest.mark.parametrize("H", [1, 2, 8, 63, 100, 767, 769, 1536, 2048])
+@pytest.mark.parametrize("wd", ["f32", "bf16"])
+def test_generic_hidden_sizes(fff_lib, H, wd):
+    L = layer(40 + H, 200, H, 5, 2, wd, wd)
+    check_layer(fff_lib, f"generic H={H} w={wd}", L, 5, 2, "f32")
+
+
+@pytest.mark.parametrize("depth,trees", [(0, 1), (0, 64), (1, 3), (11, 4), (14, 1), (2, 300)])
+def test_depth_and_tree_edges(fff_lib, depth, trees):
+    L = layer(50 + depth, 300, 768, depth, trees, "f32", "f32")
+    check_layer(fff_lib, f"depth={depth} trees={trees}", L, depth, trees, "f32")
+
+
+@pytest.mark.parametrize("mode", ["descent", "generic"])
+def test_modes_agree(fff_lib, mode):
+    L = layer(60, 3000, 768, 11, 2, "f32", "bf16")
+    check_layer(fff_lib, f"mode={mode}", L, 11, 2, "f32", mode=mode)
+
+
+@pytest.mark.parametrize("lds_levels", [-1, 1, 3, 5])
+def test_lds_levels_do_not_change_bits(fff_lib, lds_levels):
+    L = layer(70, 2000, 768, 11, 1, "bf16", "bf16")
+    base = run_fff(fff_lib, L, 11, 1, "f32", lds_levels=-1)
+    got = run_fff(fff_lib, L, 11, 1, "f32", lds_levels=lds_levels)
+    assert np.array_equal(base["y"], got["y"]) and np.array_equal(base["nodes"], got["nodes"])
+
+
+def test_activation_variants(fff_lib):
+    L = layer(80, 500, 768, 9, 1, "f32", "f32")
+    check_layer(fff_lib, "gelu_tanh", L, 9, 1, "f32", act="gelu_tanh")
+    check_layer(fff_lib, "identity", L, 9, 1, "f32", act="identity")
+
+
+@pytest.mark.parametrize("H,mode", [(768, "descent"), (40, "generic")])
+def test_small_integers_identity_bit_exact_with_ties(fff_lib, H, mode):
+    """Identity activation on small integers: every value is an exact integer, so the device
+    must match the oracle bit for bit, including logits of exactly zero (they go left)."""
+    D, T, B = 6, 2, 300
+    L = synth.small_int_layer(9, B, H, D, T)
+    for b in range(0, B, 5):  # exact zero at the root of tree 0
+        w0 = L["w_in"][0, 0]
+        i, j = np.nonzero(w0)[0][:2]
+        L["x"][b] = 0
+        L["x"][b, i], L["x"][b, j] = w0[j], -w0[i]
+    got = run_fff(fff_lib, L, D, T, "f32", act="identity", mode=mode)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], D, T, act="identity")
+    assert np.array_equal(got["nodes"], ref["nodes"])
+    assert np.array_equal(got["y"].astype(np.float64), ref["y"])
+    assert np.all(got["nodes"][::5, 0, 1] == 1)
+
+
+def test_out_modes(fff_lib):
+    L = layer(90, 1500, 768, 10, 1, "f32", "f32")
+    y0 = synth.make_x(91, 1500, 768, "f32")
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 10, 1)
+    acc = run_fff(fff_lib, L, 10, 1, "f32", y_init=y0, out="accumulate")
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 10, 1, ref, acc["y"], acc["nodes"], tol=1e-5, base_dev=y0)
+    res = run_fff(fff_lib, L, 10, 1, "f32", out="residual")
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 10, 1, ref, res["y"], res["nodes"], tol=1e-5,
+                         base_dev=L["x"])
+
+
+def test_plain_six_argument_entry_point(fff_lib):
+    L = layer(100, 999, 768, 11, 1, "bf16", "bf16")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    y = torch.empty((999, 768), dtype=torch.bfloat16, device=DEV)
+    fff_lib.forward_plain(x, wi, wo, 11, 1, y)
+    torch.cuda.synchronize()
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 11, 1)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 11, 1, ref, fff_lib.to_numpy(y), None, tol=2e-2)
+
+
+# ------------------------------------------------- determinism, streams, guards
+
+
+def test_deterministic(fff_lib):
+    L = layer(110, 20000, 768, 11, 1, "bf16", "bf16")
+    a = run_fff(fff_lib, L, 11, 1, "bf16")
+    b = run_fff(fff_lib, L, 11, 1, "bf16")
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
+
+
+def test_non_default_stream(fff_lib):
+    L = layer(120, 4000, 768, 11, 1, "f32", "f32")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    s = torch.cuda.Stream(device=DEV)
+    y = torch.empty((4000, 768), dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        fff_lib.forward(x, wi, wo, 11, 1, y)
+    s.synchronize()
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 11, 1)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 11, 1, ref, y.cpu().numpy(), None, tol=1e-5)
+
+
+@pytest.mark.parametrize("yd,mode", [("bf16", "descent"), ("f32", "descent"), ("f32", "generic")])
+def test_guard_bands_untouched(fff_lib, yd, mode):
+    B, H, D = 517, 768, 11
+    L = layer(130, B, H, D, 1, "bf16", "bf16")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    pad = 4096
+    buf = torch.full((B * H + 2 * pad,), 12345.0, dtype=TORCH_DT[yd], device=DEV)
+    y = buf[pad:pad + B * H].view(B, H)
+    nbuf = torch.full((B * (D + 1) + 2 * pad,), -99, dtype=torch.int32, device=DEV)
+    nodes = nbuf[pad:pad + B * (D + 1)]
+    fff_lib.forward(x, wi, wo, D, 1, y, nodes_out=nodes, mode=mode)
+    torch.cuda.synchronize()
+    assert torch.all(buf[:pad] == 12345.0) and torch.all(buf[-pad:] == 12345.0)
+    assert torch.all(nbuf[:pad] == -99) and torch.all(nbuf[-pad:] == -99)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], D, 1)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], D, 1, ref, fff_lib.to_numpy(y), nodes.view(B, 1, D + 1)
+                         .cpu().numpy(), tol=tol_for("bf16", yd))
+
+
+def test_describe_names_the_kernel(fff_lib):
+    L = layer(140, 64, 768, 11, 1, "bf16", "bf16")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    d = fff_lib.describe(x, wi, wo, 11, 1)
+    assert d.startswith("descent<") and "lds_levels=" in d
+    d = fff_lib.describe(x, wi, wo, 11, 1, mode="generic")
+    assert d.startswith("generic")
+
+
+def test_errors_surface_as_exceptions(fff_lib):
+    L = layer(150, 16, 768, 3, 1, "f32", "f32")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x, wi, wo, 3, 1, lds_levels=9)  # more levels than the tree has
+    with pytest.raises(ValueError):
+        fff_lib.forward(x, wi[:, :7], wo, 3, 1)
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x, wi, wo, 3, 1, y=x)  # x and y overlap
