@@ -12,7 +12,8 @@ throughput it reports:
   visited node) over the kernel's mean launch time, against the 8 TB/s HBM
   peak, plus measured HBM traffic when a counter summary is supplied;
 * dense: a dense 768 -> 3072 -> 768 GELU feedforward on the same tokens
-  (bf16 GEMMs through torch, i.e. hipBLASLt), and the speedup over it;
+  (bf16 hipBLASLt GEMMs with the GELU fused into the first GEMM's epilogue,
+  fastest heuristic candidate), and the speedup over it;
 * cpu_baseline: the fp64 CPU oracle on the host cores over a bounded sample.
 """
 from __future__ import annotations
@@ -50,6 +51,8 @@ def parse():
     ap.add_argument("--traffic", default=None,
                     help="JSON with measured HBM bytes per launch of the FFF kernel (from rocprofv3 counters)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled parity check after timing")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="also launch a plain copy of this many MiB 5 times (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -113,6 +116,16 @@ def main():
     def step():
         fff.forward(x, wi, wo, w.depth, w.n_trees, y, **kw)
 
+    if args.copy_calib_mb:
+        from paper_2311_10770_amd import benchlib
+
+        src = torch.empty(args.copy_calib_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            benchlib.copy(src, dst)
+        torch.cuda.synchronize()
+        del src, dst
+
     t = time_launches(step, args.steps, args.warmup, stream)
     ms = t["region_ms"] / args.steps
     tokens_per_s = B / (ms / 1e3)
@@ -134,9 +147,18 @@ def main():
         "kernel_us": {"mean": t["mean_ms"] * 1e3, "min": t["min_ms"] * 1e3, "std": t["std_ms"] * 1e3},
     }
 
+    # Measured HBM bytes per launch from a committed counter summary, valid only while the
+    # kernel sources are the ones the counters were taken on.
+    from paper_2311_10770_amd.rocprof_summary import kernel_source_hash
+
     traffic = None
-    if args.traffic and Path(args.traffic).exists():
-        traffic = json.loads(Path(args.traffic).read_text()).get("hbm_bytes_per_launch")
+    tpath = Path(args.traffic) if args.traffic else ROOT / "profiles" / f"traffic_{w.name}_{args.mode}.json"
+    if tpath.exists():
+        summ = json.loads(tpath.read_text())
+        if summ.get("kernel_source_hash") == kernel_source_hash():
+            traffic = summ.get("hbm_bytes_per_launch")
+        else:
+            log(f"{tpath.name} was taken on other kernel sources: traffic unreported")
     out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                        "basis": f"gathered weight bytes per launch = {w.gathered_bytes_per_token()} B/token x {B} "
@@ -145,20 +167,34 @@ def main():
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
     if not args.no_dense:
+        from paper_2311_10770_amd import benchlib
+
         H, F = w.hidden, 3072 if w.hidden == 768 else 4 * w.hidden
         g = torch.Generator(device="cpu").manual_seed(1234)
         w1 = (torch.randn(F, H, generator=g) / H ** 0.5).to(dev, torch.bfloat16)
         w2 = (torch.randn(H, F, generator=g) / F ** 0.5).to(dev, torch.bfloat16)
         xb = x if x.dtype == torch.bfloat16 else x.to(torch.bfloat16)
+        dense = benchlib.DenseFF(xb, w1, w2)
+        nd = max(20, args.steps // 2)
+        td = time_launches(dense, nd, 10, stream)
+        dense_ms = td["region_ms"] / nd
+        # sanity: the fused-epilogue GEMMs compute the dense layer (tanh- vs erf-GELU differ slightly)
+        ref = torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb[:1024].float(),
+                                         w1.float())), w2.float())
+        rel = float((dense.y[:1024].float() - ref).norm() / ref.norm())
 
-        def dense():
+        def dense_unfused():
             torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
 
-        td = time_launches(dense, max(20, args.steps // 2), 10, stream)
-        dense_ms = td["region_ms"] / max(20, args.steps // 2)
-        out["dense"] = {"what": f"dense FF {H}->{F}->{H}, GELU, bf16 GEMMs via torch (hipBLASLt), same tokens",
-                        "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms}
-        log(f"dense: {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x")
+        tu = time_launches(dense_unfused, nd, 5, stream)
+        unfused_ms = tu["region_ms"] / nd
+        out["dense"] = {"what": f"dense FF {H}->{F}->{H} on the same tokens, bf16: {dense.info}",
+                        "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
+                        "rel_err_vs_fp32_torch": rel,
+                        "torch_unfused_ms": unfused_ms, "speedup_fff_over_torch_unfused": unfused_ms / ms}
+        dense.close()
+        log(f"dense (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x "
+            f"(rel err {rel:.1e}); torch unfused {unfused_ms * 1e3:.1f} us")
 
     if not args.no_check:
         import oracle

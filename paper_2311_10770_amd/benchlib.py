@@ -1,0 +1,70 @@
+"""ctypes binding of libfffbench.so: the hipBLASLt dense feedforward comparator
+and the copy kernel used to calibrate HBM counters.  Benchmark-only."""
+from __future__ import annotations
+
+import ctypes
+from ctypes import c_char_p, c_int, c_int32, c_int64, c_void_p
+from pathlib import Path
+
+import torch
+
+LIB_PATH = Path(__file__).resolve().with_name("libfffbench.so")
+_lib = None
+
+
+def load():
+    global _lib
+    if _lib is None:
+        if not LIB_PATH.exists():
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2311_10770_amd.build`")
+        lib = ctypes.CDLL(str(LIB_PATH))
+        lib.fffb_dense_ff_create.argtypes = [c_int64, c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                             c_void_p, c_void_p]
+        lib.fffb_dense_ff_create.restype = c_void_p
+        lib.fffb_dense_ff_info.argtypes = [c_void_p]
+        lib.fffb_dense_ff_info.restype = c_char_p
+        lib.fffb_dense_ff_run.argtypes = [c_void_p] * 6 + [c_void_p]
+        lib.fffb_dense_ff_run.restype = c_int
+        lib.fffb_dense_ff_destroy.argtypes = [c_void_p]
+        lib.fffb_dense_ff_destroy.restype = None
+        lib.fffb_copy.argtypes = [c_void_p, c_void_p, c_int64, c_void_p]
+        lib.fffb_copy.restype = c_int
+        _lib = lib
+    return _lib
+
+
+class DenseFF:
+    """y = GELU(x W1^T) W2^T in bf16 on hipBLASLt, GELU fused in the first GEMM's epilogue."""
+
+    def __init__(self, x: torch.Tensor, w1: torch.Tensor, w2: torch.Tensor, stream=None):
+        lib = load()
+        self.x, self.w1, self.w2 = x, w1, w2
+        B, H = x.shape
+        F = w1.shape[0]
+        self.h = torch.empty((B, F), dtype=torch.bfloat16, device=x.device)
+        self.y = torch.empty((B, H), dtype=torch.bfloat16, device=x.device)
+        self.stream = (stream or torch.cuda.current_stream(x.device)).cuda_stream
+        self.handle = lib.fffb_dense_ff_create(B, H, F, x.data_ptr(), w1.data_ptr(), w2.data_ptr(),
+                                               self.h.data_ptr(), self.y.data_ptr(), self.stream)
+        if not self.handle:
+            raise RuntimeError("hipBLASLt dense FF setup failed")
+        self.info = lib.fffb_dense_ff_info(self.handle).decode()
+
+    def __call__(self):
+        rc = load().fffb_dense_ff_run(self.handle, self.x.data_ptr(), self.w1.data_ptr(), self.w2.data_ptr(),
+                                      self.h.data_ptr(), self.y.data_ptr(), self.stream)
+        if rc != 0:
+            raise RuntimeError(f"hipBLASLt matmul failed ({rc})")
+        return self.y
+
+    def close(self):
+        if self.handle:
+            load().fffb_dense_ff_destroy(self.handle)
+            self.handle = None
+
+
+def copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
+    s = (stream or torch.cuda.current_stream(src.device)).cuda_stream
+    rc = load().fffb_copy(src.data_ptr(), dst.data_ptr(), src.numel() * src.element_size(), s)
+    if rc != 0:
+        raise RuntimeError(f"fffb_copy failed ({rc})")

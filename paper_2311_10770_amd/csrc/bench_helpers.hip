@@ -1,0 +1,175 @@
+// bench_helpers.hip -- benchmark-only helpers (libfffbench.so), not part of
+// the FFF library:
+//   * a dense feedforward y = GELU(x W1^T) W2^T on hipBLASLt (bf16 in/out,
+//     fp32 accumulate, MFMA), GELU fused into the first GEMM's epilogue, the
+//     fastest of the heuristic's candidate algorithms picked by timing --
+//     the dense layer the FFF is compared against;
+//   * a plain vectorised copy kernel whose HBM counter readings calibrate the
+//     traffic measured for the FFF kernels.
+#include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#define FFFB_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+struct Gemm {
+    hipblasLtMatmulDesc_t desc = nullptr;
+    hipblasLtMatrixLayout_t a = nullptr, b = nullptr, d = nullptr;
+    hipblasLtMatmulAlgo_t algo{};
+    bool have_algo = false;
+};
+
+struct DenseFF {
+    hipblasLtHandle_t lt = nullptr;
+    Gemm g1, g2;
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    int64_t tokens = 0;
+    int hidden = 0, width = 0;
+    char info[256] = {0};
+};
+
+constexpr size_t kWorkspace = 64u << 20;
+
+bool lt_ok(hipblasStatus_t s) { return s == HIPBLAS_STATUS_SUCCESS; }
+
+// Column-major view of row-major tensors: D[m x n] = op(A) * B with
+// A stored as a row-major [m, k] matrix (transposed col-major k x m).
+bool make_gemm(DenseFF* ff, Gemm* g, uint64_t m, uint64_t n, uint64_t k, bool gelu) {
+    if (!lt_ok(hipblasLtMatmulDescCreate(&g->desc, HIPBLAS_COMPUTE_32F, HIP_R_32F))) return false;
+    hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
+    hipblasLtMatmulDescSetAttribute(g->desc, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof ta);
+    hipblasLtMatmulDescSetAttribute(g->desc, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof tb);
+    if (gelu) {
+        hipblasLtEpilogue_t ep = HIPBLASLT_EPILOGUE_GELU;
+        if (!lt_ok(hipblasLtMatmulDescSetAttribute(g->desc, HIPBLASLT_MATMUL_DESC_EPILOGUE, &ep, sizeof ep)))
+            return false;
+    }
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->a, HIP_R_16BF, k, m, k))) return false;
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->b, HIP_R_16BF, k, n, k))) return false;
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->d, HIP_R_16BF, m, n, m))) return false;
+    (void)ff;
+    return true;
+}
+
+hipblasStatus_t run_gemm(DenseFF* ff, Gemm* g, const void* A, const void* B, void* D, hipStream_t s,
+                         const hipblasLtMatmulAlgo_t* algo) {
+    const float alpha = 1.0f, beta = 0.0f;
+    return hipblasLtMatmul(ff->lt, g->desc, &alpha, A, g->a, B, g->b, &beta, D, g->d, D, g->d, algo, ff->ws,
+                           ff->ws_bytes, s);
+}
+
+// Time every heuristic candidate on the real buffers and keep the fastest.
+bool tune(DenseFF* ff, Gemm* g, const void* A, const void* B, void* D, hipStream_t s, float* best_ms) {
+    hipblasLtMatmulPreference_t pref;
+    if (!lt_ok(hipblasLtMatmulPreferenceCreate(&pref))) return false;
+    uint64_t ws = ff->ws_bytes;
+    hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &ws, sizeof ws);
+    hipblasLtMatmulHeuristicResult_t res[16];
+    int n = 0;
+    hipblasStatus_t st = hipblasLtMatmulAlgoGetHeuristic(ff->lt, g->desc, g->a, g->b, g->d, g->d, pref, 16, res, &n);
+    hipblasLtMatmulPreferenceDestroy(pref);
+    if (!lt_ok(st) || n < 1) return false;
+    hipEvent_t e0, e1;
+    hipEventCreate(&e0);
+    hipEventCreate(&e1);
+    float best = 1e30f;
+    for (int i = 0; i < n; ++i) {
+        if (res[i].state != HIPBLAS_STATUS_SUCCESS || res[i].workspaceSize > ff->ws_bytes) continue;
+        if (!lt_ok(run_gemm(ff, g, A, B, D, s, &res[i].algo))) continue;
+        hipEventRecord(e0, s);
+        for (int r = 0; r < 10; ++r) run_gemm(ff, g, A, B, D, s, &res[i].algo);
+        hipEventRecord(e1, s);
+        hipEventSynchronize(e1);
+        float ms = 0.f;
+        hipEventElapsedTime(&ms, e0, e1);
+        if (ms < best) {
+            best = ms;
+            g->algo = res[i].algo;
+            g->have_algo = true;
+        }
+    }
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+    *best_ms = best / 10.0f;
+    return g->have_algo;
+}
+
+__global__ void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n) {
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        dst[i] = src[i];
+}
+
+}  // namespace
+
+FFFB_EXPORT void fffb_dense_ff_destroy(void* handle) {
+    DenseFF* ff = static_cast<DenseFF*>(handle);
+    if (!ff) return;
+    for (Gemm* g : {&ff->g1, &ff->g2}) {
+        if (g->a) hipblasLtMatrixLayoutDestroy(g->a);
+        if (g->b) hipblasLtMatrixLayoutDestroy(g->b);
+        if (g->d) hipblasLtMatrixLayoutDestroy(g->d);
+        if (g->desc) hipblasLtMatmulDescDestroy(g->desc);
+    }
+    if (ff->ws) hipFree(ff->ws);
+    if (ff->lt) hipblasLtDestroy(ff->lt);
+    delete ff;
+}
+
+// Create a tuned dense FF for [tokens, hidden] -> [tokens, width] -> [tokens, hidden], bf16.
+// Buffers are used for tuning only (contents are overwritten).  Returns NULL on failure.
+FFFB_EXPORT void* fffb_dense_ff_create(int64_t tokens, int32_t hidden, int32_t width, const void* x, const void* w1,
+                                       const void* w2, void* h, void* y, void* stream) {
+    DenseFF* ff = new DenseFF();
+    ff->tokens = tokens;
+    ff->hidden = hidden;
+    ff->width = width;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    bool ok = lt_ok(hipblasLtCreate(&ff->lt)) && hipMalloc(&ff->ws, kWorkspace) == hipSuccess;
+    ff->ws_bytes = ok ? kWorkspace : 0;
+    ok = ok && make_gemm(ff, &ff->g1, width, tokens, hidden, true) && make_gemm(ff, &ff->g2, hidden, tokens, width, false);
+    float t1 = 0, t2 = 0;
+    ok = ok && tune(ff, &ff->g1, w1, x, h, s, &t1) && tune(ff, &ff->g2, w2, h, y, s, &t2);
+    if (!ok) {
+        std::fprintf(stderr, "fffb_dense_ff_create: hipBLASLt setup failed\n");
+        fffb_dense_ff_destroy(ff);
+        return nullptr;
+    }
+    std::snprintf(ff->info, sizeof ff->info, "hipBLASLt bf16, GELU epilogue; tuned gemm1 %.1f us, gemm2 %.1f us",
+                  t1 * 1e3f, t2 * 1e3f);
+    return ff;
+}
+
+FFFB_EXPORT const char* fffb_dense_ff_info(void* handle) {
+    return handle ? static_cast<DenseFF*>(handle)->info : "";
+}
+
+// h = GELU(x W1^T); y = h W2^T.  Returns 0 or the failing hipblasStatus_t.
+FFFB_EXPORT int fffb_dense_ff_run(void* handle, const void* x, const void* w1, const void* w2, void* h, void* y,
+                                  void* stream) {
+    DenseFF* ff = static_cast<DenseFF*>(handle);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipblasStatus_t st = run_gemm(ff, &ff->g1, w1, x, h, s, &ff->g1.algo);
+    if (!lt_ok(st)) return int(st);
+    st = run_gemm(ff, &ff->g2, w2, h, y, s, &ff->g2.algo);
+    return lt_ok(st) ? 0 : int(st);
+}
+
+// dst = src, bytes a multiple of 16, both 16-byte aligned.
+FFFB_EXPORT int fffb_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+    if ((bytes & 15) || (reinterpret_cast<uintptr_t>(src) & 15) || (reinterpret_cast<uintptr_t>(dst) & 15)) return -1;
+    const int64_t n = bytes / 16;
+    if (n == 0) return 0;
+    const int block = 256;
+    const int64_t grid = std::min<int64_t>((n + block - 1) / block, 256 * 16);
+    hipLaunchKernelGGL(copy_kernel, dim3(unsigned(grid)), dim3(block), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const uint4*>(src), reinterpret_cast<uint4*>(dst), n);
+    return hipGetLastError() == hipSuccess ? 0 : -2;
+}

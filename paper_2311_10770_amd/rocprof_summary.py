@@ -1,0 +1,90 @@
+"""Summarise rocprofv3 CSV output for one kernel: mean duration from a
+kernel-trace stats file, and HBM bytes per dispatch from FETCH_SIZE /
+WRITE_SIZE counter runs, scaled by what the same counters read for the
+plain copy kernel of known size launched beside it (bench.py --copy-calib-mb).
+
+    python -m paper_2311_10770_amd.rocprof_summary --kernel descent_kernel \\
+        --stats DIR/kernel_stats.csv --fetch DIR_F/counter_collection.csv \\
+        --write DIR_W/counter_collection.csv --copy-mb 512 --out summary.json
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+from pathlib import Path
+
+PKG = Path(__file__).resolve().parent
+COPY_KERNEL = "copy_kernel"
+
+
+def kernel_source_hash() -> str:
+    """Hash of the kernel sources: counter figures are void once these change."""
+    h = hashlib.sha256()
+    for name in ("fff_kernels.hip", "fff_device.hpp"):
+        p = PKG / "csrc" / name
+        if p.exists():
+            h.update(p.read_bytes())
+    return h.hexdigest()[:16]
+
+
+def read_stats(path: Path, kernel: str) -> dict:
+    rows = list(csv.DictReader(open(path)))
+    for r in rows:
+        if kernel in r["Name"]:
+            return {"name": r["Name"], "calls": int(r["Calls"]), "mean_us": float(r["AverageNs"]) / 1e3,
+                    "min_us": float(r["MinNs"]) / 1e3, "max_us": float(r["MaxNs"]) / 1e3}
+    raise KeyError(f"{kernel} not in {path}")
+
+
+def read_counter(path: Path, counter: str, kernel: str) -> list:
+    vals = []
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] == counter and kernel in r["Kernel_Name"]:
+            vals.append(float(r["Counter_Value"]))
+    if not vals:
+        raise KeyError(f"no {counter} rows for {kernel} in {path}")
+    return vals
+
+
+def summarise(kernel: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int) -> dict:
+    out = {"kernel": kernel, "kernel_source_hash": kernel_source_hash()}
+    if stats:
+        out["duration"] = read_stats(stats, kernel)
+    copy_bytes = copy_mb * (1 << 20)
+    total = 0.0
+    for what, path in (("FETCH_SIZE", fetch), ("WRITE_SIZE", write)):
+        if not path:
+            continue
+        k = read_counter(path, what, kernel)
+        c = read_counter(path, what, COPY_KERNEL)
+        k_kib, c_kib = sum(k) / len(k), sum(c) / len(c)
+        scale = copy_bytes / (c_kib * 1024.0)  # true bytes per counted byte, from the copy
+        out[what] = {"kernel_kib_per_dispatch": k_kib, "copy_kib_per_dispatch": c_kib,
+                     "copy_true_bytes": copy_bytes, "scale": scale, "bytes_per_dispatch": k_kib * 1024.0 * scale,
+                     "dispatches": len(k)}
+        total += k_kib * 1024.0 * scale
+    if fetch and write:
+        out["hbm_bytes_per_launch"] = total
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--kernel", required=True)
+    ap.add_argument("--stats", type=Path)
+    ap.add_argument("--fetch", type=Path)
+    ap.add_argument("--write", type=Path)
+    ap.add_argument("--copy-mb", type=int, default=512)
+    ap.add_argument("--out", type=Path)
+    a = ap.parse_args()
+    s = summarise(a.kernel, a.stats, a.fetch, a.write, a.copy_mb)
+    text = json.dumps(s, indent=1)
+    if a.out:
+        a.out.write_text(text + "\n")
+    print(text)
+
+
+if __name__ == "__main__":
+    main()
