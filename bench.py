@@ -159,10 +159,12 @@ def main():
             traffic = summ.get("hbm_bytes_per_launch")
         else:
             log(f"{tpath.name} was taken on other kernel sources: traffic unreported")
+    kernels = "walk_kernel + emit_kernel" if plan.startswith("grouped") else plan.split("<")[0] + "_kernel"
     out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                       "basis": f"gathered weight bytes per launch = {w.gathered_bytes_per_token()} B/token x {B} "
-                                f"tokens, over the mean launch time; served by LDS/L2/MALL, not all from HBM"}
+                       "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
+                       "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x {B} "
+                                f"tokens, over the mean time of one forward call ({kernels}, HIP events on the "
+                                f"launch stream); served by LDS/L2/MALL, not all from HBM"}
     flops = w.flops_per_token() * B
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 

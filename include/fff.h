@@ -63,10 +63,16 @@ typedef enum { FFF_F32 = 0, FFF_BF16 = 1 } fff_dtype;
  * tanh approximation, or the identity (for exact integer tests). */
 typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2 } fff_act;
 
-/* DESCENT: one sub-wave per token walks the tree, the top levels served from
- * LDS.  GROUPED: tokens are first bucketed by their node at a split level
- * and each bucket's subtree is walked by workgroups on one XCD (needs a
- * workspace).  GENERIC: any hidden size, one wave per token.  AUTO picks. */
+/* DESCENT: one kernel; a 16/32/64-lane group per token walks each tree and
+ * accumulates the output, the top levels served from LDS.
+ * GROUPED: two kernels; the walk (the CMM proper) stores every token's leaf
+ * and activations in the workspace, then the output rows are accumulated with
+ * tokens grouped by their tree-0 node at a split level, each group's subtree
+ * handled by the workgroups of one XCD so that its rows stay in that XCD's L2.
+ * GENERIC: any hidden size, one wave per token.
+ * AUTO: GROUPED for single-tree layers with hidden <= 1024 when a large enough
+ * workspace is passed, else DESCENT when a kernel is compiled for the hidden
+ * size and types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,
     FFF_MODE_DESCENT = 1,
@@ -112,19 +118,23 @@ typedef struct {
     int32_t out_mode;                  /* fff_out */
     int32_t lds_levels;   /* top tree levels cached in LDS (DESCENT); 0 = default choice,
                              -1 = none, k > 0 = exactly k (FFF_ERR_UNSUPPORTED if too big) */
-    int32_t split_level;  /* GROUPED: level whose node buckets the tokens; 0 = default */
+    int32_t split_level;  /* GROUPED: group tokens by their tree-0 node at this level (3..depth);
+                             0 = default (min(depth, 5) for one tree, else none);
+                             -1 = keep token order */
     int32_t* nodes_out;   /* optional device [n_tokens, n_trees, depth+1]: node visited per level */
     float* logits_out;    /* optional device [n_tokens, n_trees, depth+1]: fp32 logit per level */
-    void* workspace;      /* GROUPED: device scratch of fff_workspace_bytes() bytes, 256-aligned */
+    void* workspace;      /* GROUPED: device scratch of at least fff_workspace_bytes() bytes,
+                             256-byte aligned, disjoint from every other buffer; its contents
+                             are overwritten (FFF_ERR_WORKSPACE if missing or too small) */
     size_t workspace_bytes;
     void* hip_stream;
 } fff_args;
 
 int fff_forward_ex(const fff_args* a);
 
-/* Device scratch bytes GROUPED mode needs for n_tokens tokens at the given
- * split level (0 = the default for this depth).  Returns 0 if grouped mode
- * does not apply to the shape. */
+/* Device scratch bytes GROUPED mode needs for n_tokens tokens: one fp32
+ * activation per visited node and one int32 leaf per (token, tree).  The
+ * split level (-1..depth) does not change it.  Returns 0 for invalid shapes. */
 size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,
                            int32_t split_level);
 

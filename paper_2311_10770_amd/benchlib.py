@@ -29,6 +29,10 @@ def load():
         lib.fffb_dense_ff_destroy.restype = None
         lib.fffb_copy.argtypes = [c_void_p, c_void_p, c_int64, c_void_p]
         lib.fffb_copy.restype = c_int
+        lib.fffb_mb_read.argtypes = [c_void_p, c_int64, c_int64, c_void_p, c_int, c_void_p]
+        lib.fffb_mb_read.restype = c_int
+        lib.fffb_mb_gather.argtypes = [c_void_p, c_int64, c_int, c_int, c_int, c_int, c_void_p, c_void_p]
+        lib.fffb_mb_gather.restype = c_int
         _lib = lib
     return _lib
 

@@ -107,7 +107,69 @@ __global__ void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ d
         dst[i] = src[i];
 }
 
+// Microbenchmarks of the memory hierarchy (the rooflines the FFF kernels run against).
+// mb_read: every thread streams 16-byte vectors from a footprint of (mask + 1)
+// vectors, `total` vectors in all (wrapping), so the footprint decides whether
+// L2, MALL or HBM serves them.
+__global__ void mb_read_kernel(const uint4* __restrict__ buf, int64_t mask, int64_t total, uint32_t* out) {
+    uint32_t acc = 0;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x) {
+        const uint4 v = buf[i & mask];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u) out[0] = acc;  // keeps the loads alive; practically never stores
+}
+
+// mb_gather: groups of 16 lanes gather whole rows (`row_vecs` 16-byte vectors)
+// from a table of `rows` rows; `steps` rows per group.  dependent = 0: row ids
+// come from a hash (independent loads); dependent = 1: each row id is derived
+// from the previous row's data, a serial chain like a tree walk.
+__global__ void mb_gather_kernel(const uint4* __restrict__ table, int64_t rows, int row_vecs, int steps, int dependent,
+                                 uint32_t* out) {
+    const int lane = threadIdx.x & 15;
+    const int64_t group = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 4;
+    uint32_t h = uint32_t(group) * 2654435761u + 12345u;
+    uint32_t acc = 0;
+    for (int s = 0; s < steps; ++s) {
+        const uint32_t key = dependent ? (h ^ acc) : h;
+        const int64_t row = int64_t((key * 2246822519u) >> 7) % rows;
+        const uint4* r = table + row * row_vecs;
+        uint32_t part = 0;
+        for (int c = lane; c < row_vecs; c += 16) {
+            const uint4 v = r[c];
+            part ^= v.x ^ v.y ^ v.z ^ v.w;
+        }
+        // fold the group's lanes so every lane sees the same value (a stand-in for the dot product reduction)
+        part ^= __shfl_xor(part, 8, 16);
+        part ^= __shfl_xor(part, 4, 16);
+        part ^= __shfl_xor(part, 2, 16);
+        part ^= __shfl_xor(part, 1, 16);
+        acc += part & 1u;
+        h = h * 1664525u + 1013904223u;
+    }
+    if (acc == 0x7fffffffu) out[0] = acc;
+}
+
 }  // namespace
+
+FFFB_EXPORT int fffb_mb_read(const void* buf, int64_t footprint_bytes, int64_t total_bytes, void* out, int grid,
+                             void* stream) {
+    const int64_t nvec = footprint_bytes / 16;
+    if (nvec < 1 || (nvec & (nvec - 1)) || total_bytes < 16 || grid < 1) return -1;
+    hipLaunchKernelGGL(mb_read_kernel, dim3(grid), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const uint4*>(buf), nvec - 1, total_bytes / 16, reinterpret_cast<uint32_t*>(out));
+    return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+FFFB_EXPORT int fffb_mb_gather(const void* table, int64_t rows, int row_bytes, int groups, int steps, int dependent,
+                               void* out, void* stream) {
+    if (rows < 1 || row_bytes < 16 || (row_bytes & 15) || groups < 16 || (groups % 16) || steps < 1) return -1;
+    const int threads = groups * 16;
+    hipLaunchKernelGGL(mb_gather_kernel, dim3(threads / 256), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const uint4*>(table), rows, row_bytes / 16, steps, dependent,
+                       reinterpret_cast<uint32_t*>(out));
+    return hipGetLastError() == hipSuccess ? 0 : -2;
+}
 
 FFFB_EXPORT void fffb_dense_ff_destroy(void* handle) {
     DenseFF* ff = static_cast<DenseFF*>(handle);

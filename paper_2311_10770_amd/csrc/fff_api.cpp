@@ -86,7 +86,7 @@ int validate(const fff_args* a, fff::Params* p) {
     if (a->mode < FFF_MODE_AUTO || a->mode > FFF_MODE_GENERIC) return FFF_ERR_INVALID_ARG;
     if (a->out_mode < FFF_OUT_STORE || a->out_mode > FFF_OUT_RESIDUAL) return FFF_ERR_INVALID_ARG;
     if (a->lds_levels < -1 || a->lds_levels > kMaxDepth + 1) return FFF_ERR_INVALID_ARG;
-    if (a->split_level < 0 || a->split_level > a->depth) return FFF_ERR_INVALID_ARG;
+    if (a->split_level < -1 || a->split_level > a->depth) return FFF_ERR_INVALID_ARG;
 
     const int64_t sx = a->x_dtype == FFF_BF16 ? 2 : 4;
     const int64_t sw = a->w_dtype == FFF_BF16 ? 2 : 4;
@@ -121,7 +121,6 @@ int validate(const fff_args* a, fff::Params* p) {
     p->y = a->y;
     p->nodes_out = a->nodes_out;
     p->logits_out = a->logits_out;
-    p->perm = nullptr;
     p->n_tokens = a->n_tokens;
     p->n_nodes = nodes;
     p->hidden = a->hidden;
@@ -136,13 +135,38 @@ int validate(const fff_args* a, fff::Params* p) {
     return FFF_OK;
 }
 
+// Workspace checks for a grouped plan: present, big enough, 256-byte aligned,
+// and disjoint from every tensor the kernels read or write.
+int check_workspace(const fff_args* a) {
+    const size_t need = fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
+    if (!a->workspace || a->workspace_bytes < need || (reinterpret_cast<uintptr_t>(a->workspace) & 255u))
+        return FFF_ERR_WORKSPACE;
+    const int64_t wsb = int64_t(need);
+    const int64_t act = a->n_tokens * a->hidden;
+    const int64_t rec = a->n_tokens * a->n_trees * (a->depth + 1) * 4;
+    const int64_t wbytes = ((int64_t(1) << (a->depth + 1)) - 1) * a->n_trees * a->hidden * (a->w_dtype ? 2 : 4);
+    if (overlap(a->workspace, wsb, a->x, act * (a->x_dtype ? 2 : 4)) ||
+        overlap(a->workspace, wsb, a->y, act * (a->y_dtype ? 2 : 4)) ||
+        overlap(a->workspace, wsb, a->W_in, wbytes) || overlap(a->workspace, wsb, a->W_out, wbytes) ||
+        (a->nodes_out && overlap(a->workspace, wsb, a->nodes_out, rec)) ||
+        (a->logits_out && overlap(a->workspace, wsb, a->logits_out, rec)))
+        return FFF_ERR_INVALID_ARG;
+    return FFF_OK;
+}
+
 int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
     int rc = validate(a, p);
     if (rc != FFF_OK) return rc;
     fff::DeviceInfo dev;
     rc = current_device_info(&dev);
     if (rc != FFF_OK) return rc;
-    return fff::plan_forward(*p, a->mode, a->lds_levels, a->split_level, dev, plan);
+    const size_t need = fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
+    const bool have_ws = a->workspace && a->workspace_bytes >= need &&
+                         (reinterpret_cast<uintptr_t>(a->workspace) & 255u) == 0;
+    rc = fff::plan_forward(*p, a->mode, a->lds_levels, a->split_level, have_ws, dev, plan);
+    if (rc != FFF_OK) return rc;
+    if (plan->kind == fff::KIND_GROUPED && a->n_tokens > 0) return check_workspace(a);
+    return FFF_OK;
 }
 
 }  // namespace
@@ -185,7 +209,7 @@ FFF_EXPORT int fff_forward(const void* x, const void* W_in, const void* W_out, i
 
 FFF_EXPORT size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,
                                       int32_t split_level) {
-    if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1 || hidden < 1 || split_level < 0 ||
+    if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1 || hidden < 1 || split_level < -1 ||
         split_level > depth)
         return 0;
     return fff::grouped_workspace_bytes(n_tokens, depth, n_trees, split_level);
@@ -197,9 +221,15 @@ FFF_EXPORT int fff_describe(const fff_args* a, char* buf, size_t len) {
     const int rc = plan_for(a, &p, &plan);
     if (rc != FFF_OK) return rc;
     if (buf && len) {
-        std::snprintf(buf, len, "%s grid=%d block=%d lanes_per_token=%d lds_levels=%d lds_bytes=%zu split_level=%d",
-                      plan.name, plan.grid, plan.block, plan.lanes, plan.lds_levels, plan.lds_bytes,
-                      plan.split_level);
+        static const char* kinds[] = {"none", "descent", "generic", "grouped"};
+        int n = std::snprintf(buf, len, "%s<%s> lanes_per_token=%d lds_levels=%d", kinds[plan.kind], plan.name,
+                              plan.lanes, plan.lds_levels);
+        if (plan.kind == fff::KIND_GROUPED && n > 0 && size_t(n) < len)
+            n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d", plan.emit_lds_levels,
+                               plan.split_level);
+        for (int i = 0; i < plan.n_launch && n > 0 && size_t(n) < len; ++i)
+            n += std::snprintf(buf + n, len - n, " | launch%d grid=%d block=%d lds_bytes=%zu", i,
+                               plan.launch[i].grid, plan.launch[i].block, plan.launch[i].lds_bytes);
     }
     return FFF_OK;
 }

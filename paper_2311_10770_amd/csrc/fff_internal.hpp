@@ -18,7 +18,6 @@ struct Params {
     void* y;
     int32_t* nodes_out;   // optional [B, T, D+1]
     float* logits_out;    // optional [B, T, D+1]
-    const int32_t* perm;  // optional token order (grouped mode); nullptr = identity
     int64_t n_tokens;
     int64_t n_nodes;      // per tree: 2^(D+1) - 1
     int32_t hidden;
@@ -27,8 +26,14 @@ struct Params {
     int32_t x_bf16, w_bf16, y_bf16;
     int32_t act;
     int32_t out_mode;
-    int32_t lds_levels;   // levels staged in LDS (descent kernel)
+    int32_t lds_levels;   // levels staged in LDS
+    // grouped mode: views into the caller's workspace
+    float* ws_act;        // [B, T, D+1] activation of every visited node
+    int32_t* ws_leaf;     // [B, T] leaf reached in each tree
+    int32_t split_level;  // group tokens by their tree-0 node at this level; 0 = keep token order
 };
+
+constexpr int XCDS = 8;  // MI355X: 8 XCDs, workgroups dealt to them round-robin
 
 struct DeviceInfo {
     int device = -1;
@@ -39,27 +44,37 @@ struct DeviceInfo {
 
 enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3 };
 
+struct Launch {
+    const void* kernel = nullptr;  // __global__ function handle
+    int grid = 0;                  // blocks
+    int block = 0;                 // threads per block
+    size_t lds_bytes = 0;          // dynamic LDS per block
+};
+
 struct Plan {
     int kind = KIND_NONE;
-    const void* kernel = nullptr;  // __global__ function handle
+    Launch launch[3];              // descent/generic: [0]; grouped: walk, scatter (optional), emit
+    int n_launch = 0;
     int lanes = 0;                 // lanes per token
-    int block = 0;                 // threads per block
-    int grid = 0;                  // blocks
-    int lds_levels = 0;
-    size_t lds_bytes = 0;          // dynamic LDS per block
+    int lds_levels = 0;            // descent, generic, grouped walk
+    int emit_lds_levels = 0;       // grouped emit
     int split_level = 0;           // grouped mode
     const char* name = "";
 };
 
 // Fills *plan for a validated request; returns an fff_status value.
-int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, const DeviceInfo& dev,
-                 Plan* plan);
+// have_workspace: the caller passed a workspace big enough for grouped mode
+// (AUTO only picks grouped mode then).
+int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, bool have_workspace,
+                 const DeviceInfo& dev, Plan* plan);
 
 // Enqueues the planned work on stream; returns the first failing HIP error.
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
 
-// Grouped mode scratch size (0 = not applicable).
+// Grouped mode scratch size for a resolved split level (0 = no bucketing).
 size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t split_level);
+// Split level used when the caller asks for the default (0 in fff_args).
+int default_split_level(int32_t depth, int32_t n_trees);
 
 }  // namespace fff

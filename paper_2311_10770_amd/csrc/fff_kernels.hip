@@ -1,18 +1,28 @@
-// fff_kernels.hip -- gfx950 kernels for FFF inference (conditional matrix
-// multiplication, Algorithm 1 of the paper, with the Section 2.1 model:
-// activation and output row at every visited node, trees summed).
+// fff_kernels.hip -- gfx950 kernels for FFF inference: conditional matrix
+// multiplication (Algorithm 1 of the paper) followed by the output
+// accumulation, with the Section 2.1 model (activation and output row at every
+// visited node, no biases, trees summed).
 //
-// descent_kernel: a group of LANES lanes (16, 32 or 64) owns one token.  The
-//   token's x slice and its fp32 output accumulators stay in registers for the
-//   whole walk; each level gathers one W_in row and one W_out row (16-byte
-//   vector loads, LANES*16 contiguous bytes per instruction), reduces the dot
-//   product across the group with DPP / permlane swaps, and picks the child.
-//   The top lds_levels levels of every tree are staged once per workgroup into
-//   LDS (the paper's advice to preload the weights of the sub-trees a token
-//   will need, Section 3.2).  Grid-stride over token groups.
-// generic_kernel: any hidden size; one wave per token; logits first, with the
-//   visited (node, activation) pairs kept in LDS, then the output rows summed
-//   one 64-element column block at a time.
+// Every kernel gives one token to a group of LANES lanes (16, 32 or 64) that
+// keeps the token's x slice in registers; per level it gathers whole weight
+// rows with 16-byte loads, reduces the dot product across the group with DPP
+// row rotations and permlane swaps, and branches on the sign.  Per tree the
+// work runs in three phases (fff_common.hpp): walk (W_in only, level logits
+// parked one per lane), one activation evaluation for all levels, then the
+// W_out rows of the now-known path accumulated into fp32 registers.
+//
+// DESCENT (descent_kernel): all three phases in one kernel; the top tree
+//   levels of W_in and W_out are staged once per workgroup into LDS (the
+//   paper's advice to preload the weights of the sub-trees a token needs,
+//   Section 3.2).
+// GROUPED (walk_kernel + emit_kernel): the walk -- the CMM of Algorithm 1 --
+//   writes each token's leaf and activations to the workspace; the emit
+//   kernel then accumulates the output rows.  With a split level k, tokens are
+//   grouped by their tree-0 node at level k and every subtree is emitted by
+//   workgroups of one XCD (blockIdx % 8), so the subtree's W_out rows stay in
+//   that XCD's L2 instead of being fetched by all eight.
+// GENERIC (generic_kernel): any hidden size, one wave per token.
+#include "fff_common.hpp"
 #include "fff_device.hpp"
 #include "fff_internal.hpp"
 
@@ -25,194 +35,45 @@
 
 namespace fff {
 
-enum { OUT_STORE = 0, OUT_ACCUMULATE = 1, OUT_RESIDUAL = 2 };
 enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3 };
 // status values mirrored from fff.h
 enum { ST_OK = 0, ST_INVALID = -1, ST_UNSUPPORTED = -2, ST_WORKSPACE = -3 };
 
-// ----------------------------------------------------------------------------
-// descent kernel
-// ----------------------------------------------------------------------------
+// Copy rows [0, Nk) of every tree's matrix into LDS, [T][Nk][stride] vectors,
+// at vector offset `off` within each stride (W_in and W_out interleave in the
+// descent kernel: stride 2*ROWV, offsets 0 and ROWV).
+template <int ROWV, int BLOCK>
+__device__ __forceinline__ void stage_rows(uint4* lds, const void* w, int T, int64_t N, int Nk, int stride,
+                                           int off) {
+    const uint4* src = reinterpret_cast<const uint4*>(w);
+    const int64_t total = int64_t(T) * Nk * ROWV;
+    for (int64_t i = threadIdx.x; i < total; i += BLOCK) {
+        const int64_t v = i % ROWV;
+        const int64_t tn = i / ROWV;
+        const int64_t t = tn / Nk, node = tn % Nk;
+        lds[tn * stride + off + v] = src[(t * N + node) * ROWV + v];
+    }
+}
 
-template <int LANES, int NV, bool XBF, bool WBF>
-struct Shape {
-    static constexpr int EV = WBF ? 8 : 4;  // W elements per 16-byte vector
-    static constexpr int E = NV * EV;       // elements a lane owns
-    static constexpr int H = LANES * E;     // hidden size
-    static constexpr int TPW = 64 / LANES;  // tokens per wave
-    static constexpr int ROWV = LANES * NV; // 16-byte vectors per W row
-};
-
-// Lane sl of a group owns, for c = 0..NV-1, the EV consecutive elements
-// starting at element (c*LANES + sl)*EV: every load instruction covers one
-// contiguous LANES*16-byte span of the row.
-template <int LANES, int NV, bool XBF, bool WBF>
-struct XRegs;
-
-template <int LANES, int NV>
-struct XRegs<LANES, NV, true, true> {  // bf16 x with bf16 W: keep packed pairs for dot2
-    uint4 v[NV];
-    __device__ void load(const void* x, int64_t tok, int sl) {
-        const uint4* row = reinterpret_cast<const uint4*>(x) + tok * (LANES * NV);
+// Per-visit records (optional outputs): node and logit of every level.
+template <int LANES>
+__device__ __forceinline__ void write_records(const Params& p, const LevelRegs<LANES>& lv, uint32_t leaf1,
+                                              int64_t tok, int t, int sl) {
+    const int D = p.depth;
 #pragma unroll
-        for (int c = 0; c < NV; ++c) v[c] = row[c * LANES + sl];
-    }
-    __device__ float dot(const uint4* w) const {
-        float s = 0.0f;
-#pragma unroll
-        for (int c = 0; c < NV; ++c) {
-            s = dot2_bf16(v[c].x, w[c].x, s);
-            s = dot2_bf16(v[c].y, w[c].y, s);
-            s = dot2_bf16(v[c].z, w[c].z, s);
-            s = dot2_bf16(v[c].w, w[c].w, s);
-        }
-        return s;
-    }
-    __device__ float elem(int c, int e) const {
-        const uint32_t u = word(v[c], e >> 1);
-        return (e & 1) ? bf16_hi(u) : bf16_lo(u);
-    }
-};
-
-template <int LANES, int NV>
-struct XRegs<LANES, NV, false, true> {  // fp32 x with bf16 W
-    float f[NV * 8];
-    __device__ void load(const void* x, int64_t tok, int sl) {
-        const float4* row = reinterpret_cast<const float4*>(x) + tok * (LANES * NV * 2);
-#pragma unroll
-        for (int c = 0; c < NV; ++c) {
-            const float4 a = row[(c * LANES + sl) * 2], b = row[(c * LANES + sl) * 2 + 1];
-            f[c * 8 + 0] = a.x; f[c * 8 + 1] = a.y; f[c * 8 + 2] = a.z; f[c * 8 + 3] = a.w;
-            f[c * 8 + 4] = b.x; f[c * 8 + 5] = b.y; f[c * 8 + 6] = b.z; f[c * 8 + 7] = b.w;
-        }
-    }
-    __device__ float dot(const uint4* w) const {
-        float s = 0.0f;
-#pragma unroll
-        for (int c = 0; c < NV; ++c)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t u = word(w[c], j);
-                s = __builtin_fmaf(f[c * 8 + 2 * j], bf16_lo(u), s);
-                s = __builtin_fmaf(f[c * 8 + 2 * j + 1], bf16_hi(u), s);
-            }
-        return s;
-    }
-    __device__ float elem(int c, int e) const { return f[c * 8 + e]; }
-};
-
-template <int LANES, int NV, bool XBF>
-struct XRegsF32W {  // fp32 W: x held as fp32 (bf16 x widened once)
-    float f[NV * 4];
-    __device__ void load(const void* x, int64_t tok, int sl) {
-        if constexpr (XBF) {
-            const uint2* row = reinterpret_cast<const uint2*>(x) + tok * (LANES * NV);
-#pragma unroll
-            for (int c = 0; c < NV; ++c) {
-                const uint2 a = row[c * LANES + sl];
-                f[c * 4 + 0] = bf16_lo(a.x); f[c * 4 + 1] = bf16_hi(a.x);
-                f[c * 4 + 2] = bf16_lo(a.y); f[c * 4 + 3] = bf16_hi(a.y);
-            }
-        } else {
-            const float4* row = reinterpret_cast<const float4*>(x) + tok * (LANES * NV);
-#pragma unroll
-            for (int c = 0; c < NV; ++c) {
-                const float4 a = row[c * LANES + sl];
-                f[c * 4 + 0] = a.x; f[c * 4 + 1] = a.y; f[c * 4 + 2] = a.z; f[c * 4 + 3] = a.w;
-            }
-        }
-    }
-    __device__ float dot(const uint4* w) const {
-        float s = 0.0f;
-#pragma unroll
-        for (int c = 0; c < NV; ++c)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) s = __builtin_fmaf(f[c * 4 + j], __uint_as_float(word(w[c], j)), s);
-        return s;
-    }
-    __device__ float elem(int c, int e) const { return f[c * 4 + e]; }
-};
-template <int LANES, int NV>
-struct XRegs<LANES, NV, false, false> : XRegsF32W<LANES, NV, false> {};
-template <int LANES, int NV>
-struct XRegs<LANES, NV, true, false> : XRegsF32W<LANES, NV, true> {};
-
-template <int NV, bool WBF>
-__device__ __forceinline__ void axpy(float* acc, float a, const uint4* w) {
-#pragma unroll
-    for (int c = 0; c < NV; ++c) {
-        if constexpr (WBF) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t u = word(w[c], j);
-                acc[c * 8 + 2 * j] = __builtin_fmaf(a, bf16_lo(u), acc[c * 8 + 2 * j]);
-                acc[c * 8 + 2 * j + 1] = __builtin_fmaf(a, bf16_hi(u), acc[c * 8 + 2 * j + 1]);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[c * 4 + j] = __builtin_fmaf(a, __uint_as_float(word(w[c], j)), acc[c * 4 + j]);
+    for (int r = 0; r < LevelRegs<LANES>::NR; ++r) {
+        const int l = r * LANES + sl;
+        if (l <= D) {
+            const int64_t rec = (tok * p.n_trees + t) * (D + 1) + l;
+            if (p.nodes_out) p.nodes_out[rec] = int32_t((leaf1 >> (D - l)) - 1);
+            if (p.logits_out) p.logits_out[rec] = lv.v[r];
         }
     }
 }
 
-// Final combine and store of one token's output slice.
-template <int LANES, int NV, bool XBF, bool WBF>
-__device__ __forceinline__ void store_output(const Params& p, const XRegs<LANES, NV, XBF, WBF>& xr, float* acc,
-                                             int64_t tok, int sl) {
-    using S = Shape<LANES, NV, XBF, WBF>;
-    constexpr int EV = S::EV;
-    if (p.out_mode == OUT_RESIDUAL) {
-#pragma unroll
-        for (int c = 0; c < NV; ++c)
-#pragma unroll
-            for (int e = 0; e < EV; ++e) acc[c * EV + e] += xr.elem(c, e);
-    }
-    if (p.y_bf16) {
-        uint16_t* yrow = reinterpret_cast<uint16_t*>(p.y) + tok * S::H;
-#pragma unroll
-        for (int c = 0; c < NV; ++c) {
-            uint16_t* dst = yrow + (c * LANES + sl) * EV;
-            if constexpr (EV == 8) {
-                uint4* d = reinterpret_cast<uint4*>(dst);
-                if (p.out_mode == OUT_ACCUMULATE) {
-                    const uint4 o = *d;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const uint32_t u = word(o, j);
-                        acc[c * 8 + 2 * j] += bf16_lo(u);
-                        acc[c * 8 + 2 * j + 1] += bf16_hi(u);
-                    }
-                }
-                *d = make_uint4(pack_bf16x2(acc[c * 8 + 0], acc[c * 8 + 1]), pack_bf16x2(acc[c * 8 + 2], acc[c * 8 + 3]),
-                                pack_bf16x2(acc[c * 8 + 4], acc[c * 8 + 5]), pack_bf16x2(acc[c * 8 + 6], acc[c * 8 + 7]));
-            } else {
-                uint2* d = reinterpret_cast<uint2*>(dst);
-                if (p.out_mode == OUT_ACCUMULATE) {
-                    const uint2 o = *d;
-                    acc[c * 4 + 0] += bf16_lo(o.x); acc[c * 4 + 1] += bf16_hi(o.x);
-                    acc[c * 4 + 2] += bf16_lo(o.y); acc[c * 4 + 3] += bf16_hi(o.y);
-                }
-                *d = make_uint2(pack_bf16x2(acc[c * 4 + 0], acc[c * 4 + 1]), pack_bf16x2(acc[c * 4 + 2], acc[c * 4 + 3]));
-            }
-        }
-    } else {
-        float* yrow = reinterpret_cast<float*>(p.y) + tok * S::H;
-#pragma unroll
-        for (int c = 0; c < NV; ++c) {
-            float4* d = reinterpret_cast<float4*>(yrow + (c * LANES + sl) * EV);
-#pragma unroll
-            for (int q = 0; q < EV / 4; ++q) {
-                float4 v = make_float4(acc[c * EV + 4 * q], acc[c * EV + 4 * q + 1], acc[c * EV + 4 * q + 2],
-                                       acc[c * EV + 4 * q + 3]);
-                if (p.out_mode == OUT_ACCUMULATE) {
-                    const float4 o = d[q];
-                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-                }
-                d[q] = v;
-            }
-        }
-    }
-}
+// ----------------------------------------------------------------------------
+// DESCENT: one fused kernel
+// ----------------------------------------------------------------------------
 
 template <int LANES, int NV, bool XBF, bool WBF, int BLOCK>
 __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
@@ -220,76 +81,185 @@ __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
     constexpr int WAVES = BLOCK / 64;
     extern __shared__ uint4 lds_rows[];  // [T][Nk][2][ROWV]: W_in row then W_out row
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
     const int sl = lane % LANES;
     const int sub = lane / LANES;
-    const int T = p.n_trees;
-    const int D = p.depth;
-    const int K = p.lds_levels;
+    const int T = p.n_trees, D = p.depth, K = p.lds_levels;
     const int64_t N = p.n_nodes;
-    const int64_t Nk = (int64_t(1) << K) - 1;
-
+    const int Nk = (1 << K) - 1;
     if (K > 0) {
-        const int64_t total = int64_t(T) * Nk * 2 * S::ROWV;
-        const uint4* win = reinterpret_cast<const uint4*>(p.w_in);
-        const uint4* wout = reinterpret_cast<const uint4*>(p.w_out);
-        for (int64_t i = tid; i < total; i += BLOCK) {
-            const int64_t v = i % S::ROWV;
-            const int64_t r = i / S::ROWV;  // (t*Nk + node)*2 + mat
-            const int64_t tn = r >> 1;
-            const int64_t t = tn / Nk, node = tn % Nk;
-            const uint4* src = (r & 1) ? wout : win;
-            lds_rows[i] = src[(t * N + node) * S::ROWV + v];
-        }
+        stage_rows<S::ROWV, BLOCK>(lds_rows, p.w_in, T, N, Nk, 2 * S::ROWV, 0);
+        stage_rows<S::ROWV, BLOCK>(lds_rows, p.w_out, T, N, Nk, 2 * S::ROWV, S::ROWV);
         __syncthreads();
     }
-
-    const uint4* win = reinterpret_cast<const uint4*>(p.w_in);
-    const uint4* wout = reinterpret_cast<const uint4*>(p.w_out);
+    const int KD = K < D + 1 ? K : D + 1;
     const int64_t n_groups = (p.n_tokens + S::TPW - 1) / S::TPW;
     for (int64_t g = int64_t(blockIdx.x) * WAVES + wave; g < n_groups; g += int64_t(gridDim.x) * WAVES) {
         const int64_t slot_raw = g * S::TPW + sub;
         const bool valid = slot_raw < p.n_tokens;
-        const int64_t slot = valid ? slot_raw : p.n_tokens - 1;  // idle groups redo the last token, store nothing
-        const int64_t tok = p.perm ? int64_t(p.perm[slot]) : slot;
-
+        const int64_t tok = valid ? slot_raw : p.n_tokens - 1;  // idle groups redo the last token, store nothing
         XRegs<LANES, NV, XBF, WBF> xr;
         xr.load(p.x, tok, sl);
         float acc[S::E];
 #pragma unroll
         for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
-
         for (int t = 0; t < T; ++t) {
-            int64_t n = 0;
-            for (int l = 0; l <= D; ++l) {
-                uint4 wi[NV], wo[NV];
-                if (l < K) {
-                    const uint4* rows = lds_rows + ((int64_t(t) * Nk + n) * 2) * S::ROWV;
+            const uint4* win = reinterpret_cast<const uint4*>(p.w_in) + int64_t(t) * N * S::ROWV + sl;
+            const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + int64_t(t) * N * S::ROWV + sl;
+            const uint4* lrows = lds_rows + int64_t(t) * Nk * 2 * S::ROWV + sl;
+            LevelRegs<LANES> lv;
+            const uint32_t leaf1 = walk_tree<LANES, NV, XBF, WBF>(xr, lrows, 2 * S::ROWV, win, KD, D, sl, lv);
+            LevelRegs<LANES> av;
 #pragma unroll
-                    for (int c = 0; c < NV; ++c) wi[c] = rows[c * LANES + sl];
-#pragma unroll
-                    for (int c = 0; c < NV; ++c) wo[c] = rows[S::ROWV + c * LANES + sl];
-                } else {
-                    const int64_t base = (int64_t(t) * N + n) * S::ROWV + sl;
-#pragma unroll
-                    for (int c = 0; c < NV; ++c) wi[c] = win[base + c * LANES];
-#pragma unroll
-                    for (int c = 0; c < NV; ++c) wo[c] = wout[base + c * LANES];
-                }
-                const float logit = group_sum<LANES>(xr.dot(wi));
-                const float a = activation(logit, p.act);
-                if (sl == 0 && valid) {
-                    const int64_t rec = (tok * T + t) * (D + 1) + l;
-                    if (p.nodes_out) p.nodes_out[rec] = int32_t(n);
-                    if (p.logits_out) p.logits_out[rec] = logit;
-                }
-                axpy<NV, WBF>(acc, a, wo);
-                n = 2 * n + 1 + (logit > 0.0f ? 1 : 0);
-            }
+            for (int r = 0; r < LevelRegs<LANES>::NR; ++r) av.v[r] = activation(lv.v[r], p.act);
+            if ((p.nodes_out || p.logits_out) && valid) write_records<LANES>(p, lv, leaf1, tok, t, sl);
+            const uint4* lout = lrows + S::ROWV;
+            emit_levels<LANES, NV, WBF>(
+                acc, KD, D, [&](int l) { return lout + int64_t((leaf1 >> (D - l)) - 1) * 2 * S::ROWV; },
+                [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                [&](int l) { return av.get(l, lane); });
         }
         if (valid) store_output<LANES, NV, XBF, WBF>(p, xr, acc, tok, sl);
+    }
+}
+
+// ----------------------------------------------------------------------------
+// GROUPED: walk kernel (CMM) then emit kernel
+// ----------------------------------------------------------------------------
+
+template <int LANES, int NV, bool XBF, bool WBF, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
+    using S = Shape<LANES, NV, XBF, WBF>;
+    constexpr int WAVES = BLOCK / 64;
+    extern __shared__ uint4 lds_in[];  // [T][Nk][ROWV] W_in rows of the top levels
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int sl = lane % LANES;
+    const int sub = lane / LANES;
+    const int T = p.n_trees, D = p.depth, K = p.lds_levels;
+    const int64_t N = p.n_nodes;
+    const int Nk = (1 << K) - 1;
+    if (K > 0) {
+        stage_rows<S::ROWV, BLOCK>(lds_in, p.w_in, T, N, Nk, S::ROWV, 0);
+        __syncthreads();
+    }
+    const int KD = K < D + 1 ? K : D + 1;
+    const int64_t n_groups = (p.n_tokens + S::TPW - 1) / S::TPW;
+    for (int64_t g = int64_t(blockIdx.x) * WAVES + wave; g < n_groups; g += int64_t(gridDim.x) * WAVES) {
+        const int64_t slot_raw = g * S::TPW + sub;
+        const bool valid = slot_raw < p.n_tokens;
+        const int64_t tok = valid ? slot_raw : p.n_tokens - 1;
+        XRegs<LANES, NV, XBF, WBF> xr;
+        xr.load(p.x, tok, sl);
+        for (int t = 0; t < T; ++t) {
+            const uint4* win = reinterpret_cast<const uint4*>(p.w_in) + int64_t(t) * N * S::ROWV + sl;
+            const uint4* lrows = lds_in + int64_t(t) * Nk * S::ROWV + sl;
+            LevelRegs<LANES> lv;
+            const uint32_t leaf1 = walk_tree<LANES, NV, XBF, WBF>(xr, lrows, S::ROWV, win, KD, D, sl, lv);
+            if (valid) {
+                const int64_t rec0 = (tok * T + t) * (D + 1);
+#pragma unroll
+                for (int r = 0; r < LevelRegs<LANES>::NR; ++r) {
+                    const int l = r * LANES + sl;
+                    if (l <= D) p.ws_act[rec0 + l] = activation(lv.v[r], p.act);
+                }
+                if (sl == 0) p.ws_leaf[tok * T + t] = int32_t(leaf1 - 1);
+                if (p.nodes_out || p.logits_out) write_records<LANES>(p, lv, leaf1, tok, t, sl);
+            }
+        }
+    }
+}
+
+constexpr int EMIT_SCAN_PER_THREAD = 4;
+
+// Subtree of a token at the split level k (tree 0), and the XCD that owns it.
+__device__ __forceinline__ int owner_xcd(const Params& p, int64_t tok) {
+    const int k = p.split_level, D = p.depth;
+    const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * p.n_trees]) + 1;
+    const uint32_t bucket = (leaf1 >> (D - k)) - (1u << k);  // node at level k minus the level's first node
+    return int(bucket % XCDS);
+}
+
+template <int LANES, int NV, bool XBF, bool WBF, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
+    using S = Shape<LANES, NV, XBF, WBF>;
+    constexpr int WAVES = BLOCK / 64;
+    constexpr int SCAN = BLOCK * EMIT_SCAN_PER_THREAD;
+    extern __shared__ uint4 lds_out[];  // [T][Nk][ROWV] W_out rows of the top levels
+    __shared__ int32_t queue[SCAN];
+    __shared__ int32_t queue_len;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int sl = lane % LANES;
+    const int sub = lane / LANES;
+    const int T = p.n_trees, D = p.depth, K = p.lds_levels;
+    const int64_t N = p.n_nodes;
+    const int Nk = (1 << K) - 1;
+    if (K > 0) stage_rows<S::ROWV, BLOCK>(lds_out, p.w_out, T, N, Nk, S::ROWV, 0);
+    const int KD = K < D + 1 ? K : D + 1;
+
+    // Token range of this workgroup.  Grouped by subtree: the workgroups of XCD
+    // x (blockIdx % 8 == x) split the whole batch between them and each keeps
+    // only the tokens whose subtree x owns.
+    const bool affine = p.split_level > 0;
+    const int xcd = affine ? int(blockIdx.x % XCDS) : 0;
+    const int64_t nloc = affine ? gridDim.x / XCDS : gridDim.x;
+    const int64_t local = affine ? blockIdx.x / XCDS : blockIdx.x;
+    const int64_t chunk = (p.n_tokens + nloc - 1) / nloc;
+    const int64_t b0 = local * chunk;
+    const int64_t b1 = b0 + chunk < p.n_tokens ? b0 + chunk : p.n_tokens;
+
+    for (int64_t base = b0; base < b1; base += SCAN) {
+        int count;
+        if (affine) {
+            if (tid == 0) queue_len = 0;
+            __syncthreads();  // also orders the LDS staging before first use
+#pragma unroll
+            for (int i = 0; i < EMIT_SCAN_PER_THREAD; ++i) {
+                const int64_t b = base + int64_t(i) * BLOCK + tid;
+                const bool take = b < b1 && owner_xcd(p, b) == xcd;
+                const uint64_t mask = __ballot(take);
+                const int before = __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0));
+                int wbase = 0;
+                if (lane == 0 && mask) wbase = atomicAdd(&queue_len, __popcll(mask));
+                wbase = __builtin_amdgcn_readfirstlane(wbase);
+                if (take) queue[wbase + before] = int32_t(b);
+            }
+            __syncthreads();
+            count = queue_len;
+        } else {
+            if (base == b0) __syncthreads();  // LDS staging
+            count = int(b1 - base < SCAN ? b1 - base : SCAN);
+        }
+        const int groups = (count + S::TPW - 1) / S::TPW;
+        for (int g = wave; g < groups; g += WAVES) {
+            const int idx_raw = g * S::TPW + sub;
+            const bool valid = idx_raw < count;
+            const int idx = valid ? idx_raw : count - 1;
+            const int64_t tok = affine ? int64_t(queue[idx]) : base + idx;
+            float acc[S::E];
+#pragma unroll
+            for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
+            for (int t = 0; t < T; ++t) {
+                const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * T + t]) + 1;
+                const float* arec = p.ws_act + (tok * T + t) * (D + 1);  // one address per group
+                const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + int64_t(t) * N * S::ROWV + sl;
+                const uint4* lrows = lds_out + int64_t(t) * Nk * S::ROWV + sl;
+                emit_levels<LANES, NV, WBF>(
+                    acc, KD, D, [&](int l) { return lrows + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                    [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                    [&](int l) { return arec[l]; });
+            }
+            XRegs<LANES, NV, XBF, WBF> xr;
+            if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
+            if (valid) store_output<LANES, NV, XBF, WBF>(p, xr, acc, tok, sl);
+        }
+        if (affine) __syncthreads();  // the queue is refilled next round
     }
 }
 
@@ -318,7 +288,7 @@ __global__ __launch_bounds__(GENERIC_BLOCK) void generic_kernel(Params p) {
     float* s_act = reinterpret_cast<float*>(s_node + P);
 
     for (int64_t slot = int64_t(blockIdx.x) * WAVES + wave; slot < p.n_tokens; slot += int64_t(gridDim.x) * WAVES) {
-        const int64_t tok = p.perm ? int64_t(p.perm[slot]) : slot;
+        const int64_t tok = slot;
         const int64_t xoff = tok * H;
         for (int t = 0; t < T; ++t) {
             int64_t n = 0;
@@ -372,40 +342,46 @@ __global__ __launch_bounds__(GENERIC_BLOCK) void generic_kernel(Params p) {
 // planning
 // ----------------------------------------------------------------------------
 
-constexpr int DESCENT_BLOCK = 256;
-constexpr size_t DEFAULT_LDS_BUDGET = 32 * 1024;  // per 256-thread block: keeps 4-5 blocks per CU
+constexpr int BLOCK = 256;
+constexpr size_t DESCENT_LDS_BUDGET = 32 * 1024;  // per 256-thread block: keeps 4-5 blocks per CU
+constexpr size_t WALK_LDS_BUDGET = 24 * 1024;     // the walk kernel runs at 6-8 waves per SIMD
+constexpr size_t EMIT_LDS_BUDGET = 32 * 1024;
 constexpr int GENERIC_MAX_PAIRS = 2048;
 
-struct DescentVariant {
+struct Variant {
     int hidden;
     bool xbf, wbf;
     int lanes;
-    const void* kernel;
+    const void* descent;
+    const void* walk;
+    const void* emit;
     const char* name;
 };
 
-#define FFF_DESCENT(H, XB, WB, L, NV)                                                                  \
-    DescentVariant {                                                                                   \
-        H, XB, WB, L, reinterpret_cast<const void*>(&descent_kernel<L, NV, XB, WB, DESCENT_BLOCK>),    \
-            "descent<lanes=" #L ",nv=" #NV ",x=" #XB ",w=" #WB ">"                                     \
+#define FFF_VARIANT(H, XB, WB, L, NV)                                                        \
+    Variant {                                                                                \
+        H, XB, WB, L, reinterpret_cast<const void*>(&descent_kernel<L, NV, XB, WB, BLOCK>),  \
+            reinterpret_cast<const void*>(&walk_kernel<L, NV, XB, WB, BLOCK>),               \
+            reinterpret_cast<const void*>(&emit_kernel<L, NV, XB, WB, BLOCK>),               \
+            "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                             \
     }
 
-static const DescentVariant kDescent[] = {
+static const Variant kVariants[] = {
     // H = 768 (BERT-base width)
-    FFF_DESCENT(768, true, true, 16, 6),
-    FFF_DESCENT(768, false, true, 16, 6),
-    FFF_DESCENT(768, false, false, 32, 6),
-    FFF_DESCENT(768, true, false, 32, 6),
+    FFF_VARIANT(768, true, true, 16, 6),
+    FFF_VARIANT(768, false, true, 16, 6),
+    FFF_VARIANT(768, false, false, 32, 6),
+    FFF_VARIANT(768, true, false, 32, 6),
     // H = 1024
-    FFF_DESCENT(1024, true, true, 16, 8),
-    FFF_DESCENT(1024, false, true, 16, 8),
-    FFF_DESCENT(1024, false, false, 32, 8),
-    FFF_DESCENT(1024, true, false, 32, 8),
+    FFF_VARIANT(1024, true, true, 16, 8),
+    FFF_VARIANT(1024, false, true, 16, 8),
+    FFF_VARIANT(1024, false, false, 32, 8),
+    FFF_VARIANT(1024, true, false, 32, 8),
     // H = 4096 (LLM width)
-    FFF_DESCENT(4096, true, true, 64, 8),
-    FFF_DESCENT(4096, false, true, 64, 8),
-    FFF_DESCENT(4096, false, false, 64, 16),
-    FFF_DESCENT(4096, true, false, 64, 16),
+    FFF_VARIANT(4096, true, true, 64, 8),
+    FFF_VARIANT(4096, false, true, 64, 8),
+    FFF_VARIANT(4096, false, false, 64, 16),
+    FFF_VARIANT(4096, true, false, 64, 16),
 };
 
 static const void* generic_kernel_for(bool xbf, bool wbf) {
@@ -432,76 +408,139 @@ static int blocks_per_cu(int device, const void* kernel, int block, size_t lds) 
     return n;
 }
 
-static size_t descent_lds_bytes(const Params& p, int levels) {
+static size_t rows_lds_bytes(const Params& p, int levels, int matrices) {
     if (levels <= 0) return 0;
     const size_t row_bytes = size_t(p.hidden) * (p.w_bf16 ? 2 : 4);
-    return size_t(p.n_trees) * ((size_t(1) << levels) - 1) * 2 * row_bytes;
+    return size_t(p.n_trees) * ((size_t(1) << levels) - 1) * matrices * row_bytes;
 }
 
-int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, const DeviceInfo& dev,
-                 Plan* plan) {
-    (void)split_level_req;
+// Levels to stage: the caller's explicit k (checked), none (-1), or the most that fit the budget.
+static int pick_levels(const Params& p, int req, int matrices, size_t budget, size_t limit, bool* ok) {
+    *ok = true;
+    if (req < 0) return 0;
+    if (req > 0) {
+        if (req > p.depth + 1 || rows_lds_bytes(p, req, matrices) > limit) *ok = false;
+        return req;
+    }
+    int k = 0;
+    while (k < p.depth + 1 && k < 20 && rows_lds_bytes(p, k + 1, matrices) <= budget) ++k;
+    return k;
+}
+
+static int resident_grid(const DeviceInfo& dev, const void* kernel, size_t lds, int64_t want) {
+    const int64_t resident = int64_t(dev.cu_count) * blocks_per_cu(dev.device, kernel, BLOCK, lds);
+    return int(std::max<int64_t>(1, std::min(want, resident)));
+}
+
+int default_split_level(int32_t depth, int32_t n_trees) {
+    // Tokens are grouped by tree 0 only; with several trees the other trees' rows are not
+    // XCD-local and the grouping costs more than it saves (measured), so keep token order.
+    return depth >= 3 && n_trees == 1 ? std::min(depth, 5) : 0;
+}
+
+static size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t /*split_level*/) {
+    const size_t recs = size_t(n_tokens) * size_t(n_trees);
+    return align256(recs * size_t(depth + 1) * sizeof(float)) + align256(recs * sizeof(int32_t));
+}
+
+int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, bool have_workspace,
+                 const DeviceInfo& dev, Plan* plan) {
     *plan = Plan{};
-    const DescentVariant* dv = nullptr;
-    for (const auto& v : kDescent)
-        if (v.hidden == p.hidden && v.xbf == bool(p.x_bf16) && v.wbf == bool(p.w_bf16)) dv = &v;
+    const Variant* v = nullptr;
+    for (const auto& c : kVariants)
+        if (c.hidden == p.hidden && c.xbf == bool(p.x_bf16) && c.wbf == bool(p.w_bf16)) v = &c;
+    if ((mode == MODE_DESCENT || mode == MODE_GROUPED) && !v) return ST_UNSUPPORTED;
+    if (mode == MODE_AUTO) {
+        // Measured on MI355X: the two-kernel grouped path wins for single trees with 16/32-lane
+        // tokens (hidden <= 1024); the fused kernel wins for multi-tree layers and 64-lane tokens.
+        if (!v) mode = MODE_GENERIC;
+        else if (have_workspace && p.n_trees == 1 && v->lanes < 64 && p.depth >= 3) mode = MODE_GROUPED;
+        else mode = MODE_DESCENT;
+    }
 
-    if (mode == MODE_GROUPED) return ST_UNSUPPORTED;
-    if (mode == MODE_DESCENT && !dv) return ST_UNSUPPORTED;
-
-    if (dv && mode != MODE_GENERIC) {
-        int levels;
-        if (lds_levels_req < 0) {
-            levels = 0;
-        } else if (lds_levels_req > 0) {
-            levels = lds_levels_req;
-            if (levels > p.depth + 1 || descent_lds_bytes(p, levels) > dev.lds_per_block) return ST_UNSUPPORTED;
-        } else {
-            levels = 0;
-            while (levels < p.depth + 1 && levels < 20 && descent_lds_bytes(p, levels + 1) <= DEFAULT_LDS_BUDGET)
-                ++levels;
-        }
+    if (mode == MODE_DESCENT) {
+        bool ok;
+        const int k = pick_levels(p, lds_levels_req, 2, DESCENT_LDS_BUDGET, dev.lds_per_block, &ok);
+        if (!ok) return ST_UNSUPPORTED;
         plan->kind = KIND_DESCENT;
-        plan->kernel = dv->kernel;
-        plan->lanes = dv->lanes;
-        plan->block = DESCENT_BLOCK;
-        plan->lds_levels = levels;
-        plan->lds_bytes = descent_lds_bytes(p, levels);
-        plan->name = dv->name;
-        const int tpw = 64 / dv->lanes;
-        const int64_t groups = (p.n_tokens + tpw - 1) / tpw;
-        const int64_t want = (groups + DESCENT_BLOCK / 64 - 1) / (DESCENT_BLOCK / 64);
-        const int64_t resident =
-            int64_t(dev.cu_count) * blocks_per_cu(dev.device, dv->kernel, DESCENT_BLOCK, plan->lds_bytes);
-        plan->grid = int(std::max<int64_t>(1, std::min(want, resident)));
+        plan->lanes = v->lanes;
+        plan->lds_levels = k;
+        plan->name = v->name;
+        Launch& L = plan->launch[plan->n_launch++];
+        L.kernel = v->descent;
+        L.block = BLOCK;
+        L.lds_bytes = rows_lds_bytes(p, k, 2);
+        const int64_t groups = (p.n_tokens + 64 / v->lanes - 1) / (64 / v->lanes);
+        L.grid = resident_grid(dev, L.kernel, L.lds_bytes, (groups + BLOCK / 64 - 1) / (BLOCK / 64));
+        return ST_OK;
+    }
+
+    if (mode == MODE_GROUPED) {
+        int split = split_level_req == 0 ? default_split_level(p.depth, p.n_trees) : split_level_req;
+        if (split < 0) split = 0;
+        if (split != 0 && (split < 3 || split > p.depth)) return ST_UNSUPPORTED;  // at least one subtree per XCD
+        bool ok_w, ok_e;
+        const int kw = pick_levels(p, lds_levels_req, 1, WALK_LDS_BUDGET, dev.lds_per_block, &ok_w);
+        const int ke = pick_levels(p, lds_levels_req, 1, EMIT_LDS_BUDGET, dev.lds_per_block, &ok_e);
+        if (!ok_w || !ok_e) return ST_UNSUPPORTED;
+        plan->kind = KIND_GROUPED;
+        plan->lanes = v->lanes;
+        plan->lds_levels = kw;
+        plan->split_level = split;
+        plan->name = v->name;
+        const int64_t groups = (p.n_tokens + 64 / v->lanes - 1) / (64 / v->lanes);
+        const int64_t want = (groups + BLOCK / 64 - 1) / (BLOCK / 64);
+        Launch& W = plan->launch[plan->n_launch++];
+        W.kernel = v->walk;
+        W.block = BLOCK;
+        W.lds_bytes = rows_lds_bytes(p, kw, 1);
+        W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want);
+        Launch& E = plan->launch[plan->n_launch++];
+        E.kernel = v->emit;
+        E.block = BLOCK;
+        E.lds_bytes = rows_lds_bytes(p, ke, 1);
+        int eg = resident_grid(dev, E.kernel, E.lds_bytes, want);
+        if (split) eg = std::max(XCDS, eg / XCDS * XCDS);  // every XCD gets the same number of workgroups
+        E.grid = eg;
+        plan->emit_lds_levels = ke;
         return ST_OK;
     }
 
     const int pairs = p.n_trees * (p.depth + 1);
     if (pairs > GENERIC_MAX_PAIRS) return ST_UNSUPPORTED;
     plan->kind = KIND_GENERIC;
-    plan->kernel = generic_kernel_for(p.x_bf16, p.w_bf16);
     plan->lanes = 64;
-    plan->block = GENERIC_BLOCK;
-    plan->lds_bytes = size_t(GENERIC_BLOCK / 64) * 2 * size_t(pairs) * 4;
-    plan->name = "generic<wave per token>";
-    const int64_t want = (p.n_tokens + GENERIC_BLOCK / 64 - 1) / (GENERIC_BLOCK / 64);
-    const int64_t resident =
-        int64_t(dev.cu_count) * blocks_per_cu(dev.device, plan->kernel, GENERIC_BLOCK, plan->lds_bytes);
-    plan->grid = int(std::max<int64_t>(1, std::min(want, resident)));
+    plan->name = "wave per token";
+    Launch& L = plan->launch[plan->n_launch++];
+    L.kernel = generic_kernel_for(p.x_bf16, p.w_bf16);
+    L.block = GENERIC_BLOCK;
+    L.lds_bytes = size_t(GENERIC_BLOCK / 64) * 2 * size_t(pairs) * 4;
+    L.grid = resident_grid(dev, L.kernel, L.lds_bytes, (p.n_tokens + GENERIC_BLOCK / 64 - 1) / (GENERIC_BLOCK / 64));
     return ST_OK;
 }
 
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream) {
-    (void)workspace;
-    (void)workspace_bytes;
     Params q = p;
     q.lds_levels = plan.lds_levels;
-    void* args[] = {&q};
-    return hipLaunchKernel(plan.kernel, dim3(plan.grid), dim3(plan.block), args, plan.lds_bytes, stream);
+    if (plan.kind == KIND_GROUPED) {
+        const size_t recs = size_t(p.n_tokens) * size_t(p.n_trees);
+        char* ws = static_cast<char*>(workspace);
+        q.ws_act = reinterpret_cast<float*>(ws);
+        q.ws_leaf = reinterpret_cast<int32_t*>(ws + align256(recs * size_t(p.depth + 1) * sizeof(float)));
+        q.split_level = plan.split_level;
+        (void)workspace_bytes;
+    }
+    for (int i = 0; i < plan.n_launch; ++i) {
+        const Launch& L = plan.launch[i];
+        if (plan.kind == KIND_GROUPED && i == 1) q.lds_levels = plan.emit_lds_levels;
+        void* args[] = {&q};
+        const hipError_t e = hipLaunchKernel(L.kernel, dim3(L.grid), dim3(L.block), args, L.lds_bytes, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
-
-size_t grouped_workspace_bytes(int64_t, int32_t, int32_t, int32_t) { return 0; }
 
 }  // namespace fff

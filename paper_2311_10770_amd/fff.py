@@ -154,10 +154,30 @@ def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out
     return a
 
 
+_WORKSPACES: dict = {}
+
+
+def workspace_for(n_tokens: int, depth: int, n_trees: int, hidden: int, device) -> torch.Tensor:
+    """A cached device workspace large enough for grouped mode (reused across calls on one device;
+    calls that overlap on different streams must pass their own)."""
+    need = workspace_bytes(n_tokens, depth, n_trees, hidden, 0)
+    dev = torch.device(device)
+    ws = _WORKSPACES.get(dev)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        _WORKSPACES[dev] = ws
+    return ws
+
+
 def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=None, **kw):
-    """FFF forward through ``fff_forward_ex``; returns y (allocated if not given)."""
+    """FFF forward through ``fff_forward_ex``; returns y (allocated if not given).
+
+    In auto and grouped mode a cached per-device workspace is passed unless ``workspace`` is
+    given (calls that may overlap on different streams must pass their own)."""
     if y is None:
         y = torch.empty(x.shape, dtype=y_dtype or x.dtype, device=x.device)
+    if kw.get("mode", "auto") in ("grouped", "auto", 0, 2) and kw.get("workspace") is None:
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     lib = load_library()
     with torch.cuda.device(x.device):
@@ -180,6 +200,8 @@ def describe(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, **kw) -> str:
     if y is None:
         y = torch.empty(x.shape, dtype=kw.pop("y_dtype", None) or x.dtype, device=x.device)
     kw.pop("y_dtype", None)
+    if kw.get("mode", "auto") in ("grouped", "auto", 0, 2) and kw.get("workspace") is None:
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     buf = ctypes.create_string_buffer(512)
     with torch.cuda.device(x.device):

@@ -1,9 +1,11 @@
-"""Summarise rocprofv3 CSV output for one kernel: mean duration from a
-kernel-trace stats file, and HBM bytes per dispatch from FETCH_SIZE /
-WRITE_SIZE counter runs, scaled by what the same counters read for the
-plain copy kernel of known size launched beside it (bench.py --copy-calib-mb).
+"""Summarise rocprofv3 CSV output for the kernels of one FFF step: mean
+duration from a kernel-trace stats file, and HBM bytes per dispatch from
+FETCH_SIZE / WRITE_SIZE counter runs, scaled by what the same counters read
+for the plain copy kernel of known size launched beside it (bench.py
+--copy-calib-mb).  ``--kernel`` takes comma-separated name fragments; a step
+launches each named kernel once, so per-step figures are their sums.
 
-    python -m paper_2311_10770_amd.rocprof_summary --kernel descent_kernel \\
+    python -m paper_2311_10770_amd.rocprof_summary --kernel walk_kernel,emit_kernel \\
         --stats DIR/kernel_stats.csv --fetch DIR_F/counter_collection.csv \\
         --write DIR_W/counter_collection.csv --copy-mb 512 --out summary.json
 """
@@ -48,23 +50,29 @@ def read_counter(path: Path, counter: str, kernel: str) -> list:
     return vals
 
 
-def summarise(kernel: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int) -> dict:
-    out = {"kernel": kernel, "kernel_source_hash": kernel_source_hash()}
+def summarise(kernels: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int) -> dict:
+    names = [k for k in kernels.split(",") if k]
+    out = {"kernels": names, "kernel_source_hash": kernel_source_hash()}
     if stats:
-        out["duration"] = read_stats(stats, kernel)
+        durs = [read_stats(stats, k) for k in names]
+        out["duration"] = {"per_kernel": durs, "step_mean_us": sum(d["mean_us"] for d in durs)}
     copy_bytes = copy_mb * (1 << 20)
     total = 0.0
     for what, path in (("FETCH_SIZE", fetch), ("WRITE_SIZE", write)):
         if not path:
             continue
-        k = read_counter(path, what, kernel)
         c = read_counter(path, what, COPY_KERNEL)
-        k_kib, c_kib = sum(k) / len(k), sum(c) / len(c)
+        c_kib = sum(c) / len(c)
         scale = copy_bytes / (c_kib * 1024.0)  # true bytes per counted byte, from the copy
-        out[what] = {"kernel_kib_per_dispatch": k_kib, "copy_kib_per_dispatch": c_kib,
-                     "copy_true_bytes": copy_bytes, "scale": scale, "bytes_per_dispatch": k_kib * 1024.0 * scale,
-                     "dispatches": len(k)}
-        total += k_kib * 1024.0 * scale
+        per = {}
+        for k in names:
+            v = read_counter(path, what, k)
+            per[k] = {"kib_per_dispatch": sum(v) / len(v), "dispatches": len(v),
+                      "bytes_per_dispatch": sum(v) / len(v) * 1024.0 * scale}
+        step = sum(d["bytes_per_dispatch"] for d in per.values())
+        out[what] = {"copy_kib_per_dispatch": c_kib, "copy_true_bytes": copy_bytes, "scale": scale,
+                     "per_kernel": per, "bytes_per_step": step}
+        total += step
     if fetch and write:
         out["hbm_bytes_per_launch"] = total
     return out

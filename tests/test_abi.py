@@ -78,7 +78,7 @@ def good_args(**over):
 @pytest.mark.parametrize("over", [
     dict(n_tokens=-1), dict(hidden=0), dict(depth=-1), dict(depth=25), dict(n_trees=0),
     dict(x_dtype=2), dict(w_dtype=-1), dict(y_dtype=5), dict(act=3), dict(mode=9), dict(out_mode=3),
-    dict(lds_levels=-2), dict(split_level=4), dict(split_level=-1),
+    dict(lds_levels=-2), dict(split_level=4), dict(split_level=-2),
     dict(x=None), dict(W_in=None), dict(W_out=None), dict(y=None),
     dict(x=P + 4), dict(y=P * 64 + 8), dict(W_in=P * 16 + 2),
     dict(y=P + 64),                           # overlaps x

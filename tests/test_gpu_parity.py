@@ -84,10 +84,74 @@ def test_depth_and_tree_edges(fff_lib, depth, trees):
     check_layer(fff_lib, f"depth={depth} trees={trees}", L, depth, trees, "f32")
 
 
-@pytest.mark.parametrize("mode", ["descent", "generic"])
+@pytest.mark.parametrize("mode", ["descent", "generic", "grouped"])
 def test_modes_agree(fff_lib, mode):
     L = layer(60, 3000, 768, 11, 2, "f32", "bf16")
     check_layer(fff_lib, f"mode={mode}", L, 11, 2, "f32", mode=mode)
+
+
+# --------------------------------------------------------------- grouped mode
+
+
+@pytest.mark.parametrize("name", ["d11_h768_b65536_bf16", "d11_h768_b16384_f32", "4x9_h768_b16384_f32"])
+def test_grouped_full_size(fff_lib, name):
+    w = WORKLOADS[name]
+    L = synth.make_layer(w.seed, w.n_tokens, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    check_layer(fff_lib, f"grouped {name}", L, w.depth, w.n_trees, w.y_dtype, mode="grouped")
+
+
+@pytest.mark.parametrize("split", [-1, 0, 3, 4, 6, 11])
+@pytest.mark.parametrize("B", [1, 7, 1000, 5003])
+def test_grouped_split_levels_and_ragged(fff_lib, split, B):
+    L = layer(160 + B, B, 768, 11, 1, "bf16", "bf16")
+    check_layer(fff_lib, f"grouped split={split} B={B}", L, 11, 1, "bf16", mode="grouped", split_level=split)
+
+
+@pytest.mark.parametrize("xd,wd,yd", DTYPE_COMBOS)
+@pytest.mark.parametrize("H", [768, 4096])
+def test_grouped_dtype_combinations(fff_lib, xd, wd, yd, H):
+    depth = 6 if H == 4096 else 9
+    L = layer(170 + H, 900, H, depth, 2, xd, wd)
+    check_layer(fff_lib, f"grouped {xd}/{wd}/{yd} H={H}", L, depth, 2, yd, mode="grouped")
+
+
+def test_grouped_matches_descent_bitwise(fff_lib):
+    """Same per-token arithmetic in the same order: the two modes agree bit for bit."""
+    L = layer(180, 20000, 768, 11, 1, "bf16", "bf16")
+    a = run_fff(fff_lib, L, 11, 1, "bf16", mode="descent")
+    b = run_fff(fff_lib, L, 11, 1, "bf16", mode="grouped")
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
+    assert np.array_equal(a["logits"], b["logits"])
+
+
+def test_grouped_out_modes_and_skewed_routing(fff_lib):
+    B = 6000
+    x = synth.make_clustered_x(190, B, 768, "f32")
+    wi, wo = synth.make_weights(190, 768, 11, 1, "f32")
+    L = {"x": x, "w_in": wi, "w_out": wo}
+    ref = oracle.forward(x, wi, wo, 11, 1)
+    res = run_fff(fff_lib, L, 11, 1, "f32", mode="grouped", out="residual")
+    parity.assert_parity(x, wi, wo, 11, 1, ref, res["y"], res["nodes"], tol=1e-5, base_dev=x)
+    y0 = synth.make_x(191, B, 768, "f32")
+    acc = run_fff(fff_lib, L, 11, 1, "f32", y_init=y0, mode="grouped", out="accumulate")
+    parity.assert_parity(x, wi, wo, 11, 1, ref, acc["y"], acc["nodes"], tol=1e-5, base_dev=y0)
+
+
+def test_grouped_workspace_errors(fff_lib):
+    L = layer(200, 512, 768, 11, 1, "bf16", "bf16")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    need = fff_lib.workspace_bytes(512, 11, 1, 768)
+    assert need >= 512 * 12 * 4 + 512 * 4
+    small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
+    with pytest.raises(fff_lib.FffError) as e:
+        fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", workspace=small)
+    assert e.value.status == fff_lib.fff.FFF_ERR_WORKSPACE
+    big = torch.empty(need + 4096, dtype=torch.uint8, device=DEV)
+    with pytest.raises(fff_lib.FffError) as e:
+        fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", workspace=big[16:])  # misaligned
+    assert e.value.status == fff_lib.fff.FFF_ERR_WORKSPACE
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", split_level=2)  # fewer subtrees than XCDs
 
 
 @pytest.mark.parametrize("lds_levels", [-1, 1, 3, 5])
@@ -188,10 +252,16 @@ def test_guard_bands_untouched(fff_lib, yd, mode):
 def test_describe_names_the_kernel(fff_lib):
     L = layer(140, 64, 768, 11, 1, "bf16", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
-    d = fff_lib.describe(x, wi, wo, 11, 1)
+    d = fff_lib.describe(x, wi, wo, 11, 1)  # auto with the binding's workspace: grouped for one tree
+    assert d.startswith("grouped<"), d
+    d = fff_lib.describe(x, wi, wo, 11, 1, mode="descent")
     assert d.startswith("descent<") and "lds_levels=" in d
+    wi4 = fff_lib.from_numpy(np.concatenate([L["w_in"]] * 4), DEV)
+    assert fff_lib.describe(x, wi4, wi4, 11, 4).startswith("descent<")  # several trees: fused kernel
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="generic")
     assert d.startswith("generic")
+    d = fff_lib.describe(x, wi, wo, 11, 1, mode="grouped")
+    assert d.startswith("grouped<") and "split_level=5" in d and "launch1" in d
 
 
 def test_errors_surface_as_exceptions(fff_lib):
