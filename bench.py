@@ -14,7 +14,8 @@ throughput it reports:
 * dense: a dense 768 -> 3072 -> 768 GELU feedforward on the same tokens
   (bf16 hipBLASLt GEMMs with the GELU fused into the first GEMM's epilogue,
   fastest heuristic candidate), and the speedup over it;
-* cpu_baseline: the fp64 CPU oracle on the host cores over a bounded sample.
+* cpu_baseline: the fp64 CPU oracle on the host cores over a bounded sample,
+  whose outputs are also compared with the device's for the same tokens.
 """
 from __future__ import annotations
 
@@ -50,33 +51,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall budget of the oracle timing")
     ap.add_argument("--traffic", default=None,
                     help="JSON with measured HBM bytes per launch of the FFF kernel (from rocprofv3 counters)")
-    ap.add_argument("--no-check", action="store_true", help="skip the sampled parity check after timing")
+    ap.add_argument("--no-check", action="store_true",
+                    help="skip comparing the device output with the oracle on the CPU leg's sample")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also launch a plain copy of this many MiB 5 times (HBM counter calibration)")
     return ap.parse_args()
-
-
-def time_launches(fn, steps: int, warmup: int, stream):
-    """Mean per-launch time from per-launch event pairs, and the whole timed region."""
-    import torch
-
-    for _ in range(warmup):
-        fn()
-    torch.cuda.synchronize()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    t0 = time.perf_counter()
-    for i in range(steps):
-        starts[i].record(stream)
-        fn()
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    region_ms = starts[0].elapsed_time(ends[-1])
-    return {"mean_ms": sum(per) / steps, "min_ms": min(per), "max_ms": max(per),
-            "std_ms": (sum((p - sum(per) / steps) ** 2 for p in per) / steps) ** 0.5,
-            "region_ms": region_ms, "wall_s": wall}
 
 
 def main():
@@ -91,7 +70,7 @@ def main():
     import torch
 
     import paper_2311_10770_amd as fff
-    from paper_2311_10770_amd import synth
+    from paper_2311_10770_amd import benchlib, synth
     from paper_2311_10770_amd.configs import HEADLINE, WORKLOADS
 
     w = WORKLOADS[args.workload or HEADLINE]
@@ -117,8 +96,6 @@ def main():
         fff.forward(x, wi, wo, w.depth, w.n_trees, y, **kw)
 
     if args.copy_calib_mb:
-        from paper_2311_10770_amd import benchlib
-
         src = torch.empty(args.copy_calib_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
         for _ in range(5):
@@ -126,7 +103,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    t = time_launches(step, args.steps, args.warmup, stream)
+    t = benchlib.time_launches(step, args.steps, args.warmup, stream)
     ms = t["region_ms"] / args.steps
     tokens_per_s = B / (ms / 1e3)
     gathered = w.gathered_bytes_per_token() * B
@@ -169,8 +146,6 @@ def main():
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
     if not args.no_dense:
-        from paper_2311_10770_amd import benchlib
-
         H, F = w.hidden, 3072 if w.hidden == 768 else 4 * w.hidden
         g = torch.Generator(device="cpu").manual_seed(1234)
         w1 = (torch.randn(F, H, generator=g) / H ** 0.5).to(dev, torch.bfloat16)
@@ -178,7 +153,7 @@ def main():
         xb = x if x.dtype == torch.bfloat16 else x.to(torch.bfloat16)
         dense = benchlib.DenseFF(xb, w1, w2)
         nd = max(20, args.steps // 2)
-        td = time_launches(dense, nd, 10, stream)
+        td = benchlib.time_launches(dense, nd, 10, stream)
         dense_ms = td["region_ms"] / nd
         # sanity: the fused-epilogue GEMMs compute the dense layer (tanh- vs erf-GELU differ slightly)
         ref = torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb[:1024].float(),
@@ -188,7 +163,7 @@ def main():
         def dense_unfused():
             torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
 
-        tu = time_launches(dense_unfused, nd, 5, stream)
+        tu = benchlib.time_launches(dense_unfused, nd, 5, stream)
         unfused_ms = tu["region_ms"] / nd
         out["dense"] = {"what": f"dense FF {H}->{F}->{H} on the same tokens, bf16: {dense.info}",
                         "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
@@ -198,28 +173,15 @@ def main():
         log(f"dense (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x "
             f"(rel err {rel:.1e}); torch unfused {unfused_ms * 1e3:.1f} us")
 
-    if not args.no_check:
+    if not args.no_cpu_baseline:
+        # The CPU leg: the fp64 oracle timed on the host cores over the first n tokens.  Its
+        # outputs for those tokens are also compared with the device's (after the timed region).
         import oracle
         from oracle import parity
 
-        rows = np.random.default_rng(0).choice(B, size=min(B, 2048), replace=False)
-        nodes = torch.empty((B, w.n_trees, w.depth + 1), dtype=torch.int32, device=dev)
-        fff.forward(x, wi, wo, w.depth, w.n_trees, y, nodes_out=nodes, **kw)
-        torch.cuda.synchronize()
-        ref = oracle.forward(L["x"][rows], L["w_in"], L["w_out"], w.depth, w.n_trees)
-        rep = parity.check(L["x"], L["w_in"], L["w_out"], w.depth, w.n_trees, ref, fff.to_numpy(y),
-                           nodes.cpu().numpy(), tol=2e-2 if w.y_dtype == "bf16" else 1e-5, rows=rows)
-        out["parity_sample"] = {"tokens": int(rows.size), "ok": rep["ok"],
-                                "max_normwise_err": rep["max_normwise_err"],
-                                "n_near_tie": rep["n_near_tie"], "n_path_divergent": rep["n_path_divergent"]}
-        log("parity sample:", out["parity_sample"])
-
-    if not args.no_cpu_baseline:
-        import oracle
-
         threads = oracle.default_threads()
         n = min(B, 4096)
-        oracle.forward(L["x"][:n], L["w_in"], L["w_out"], w.depth, w.n_trees, records=False, threads=threads)
+        ref = oracle.forward(L["x"][:n], L["w_in"], L["w_out"], w.depth, w.n_trees, threads=threads)
         done, t0 = 0, time.perf_counter()
         while True:
             oracle.forward(L["x"][:n], L["w_in"], L["w_out"], w.depth, w.n_trees, records=False, threads=threads)
@@ -231,6 +193,18 @@ def main():
                                "sample": f"first {n} tokens of the same batch, repeated {done // n}x over "
                                          f"{el:.1f}s wall, fp64 C oracle on {threads} host threads"}
         log(f"cpu oracle: {done / el:.0f} tok/s on {threads} threads")
+        if not args.no_check:
+            nodes = torch.empty((B, w.n_trees, w.depth + 1), dtype=torch.int32, device=dev)
+            fff.forward(x, wi, wo, w.depth, w.n_trees, y, nodes_out=nodes, **kw)
+            torch.cuda.synchronize()
+            rows = np.arange(n)
+            rep = parity.check(L["x"], L["w_in"], L["w_out"], w.depth, w.n_trees, ref, fff.to_numpy(y),
+                               nodes.cpu().numpy(), tol=2e-2 if w.y_dtype == "bf16" else 1e-5, rows=rows)
+            out["cpu_baseline"]["check"] = {"tokens": n, "ok": rep["ok"],
+                                            "max_normwise_err": rep["max_normwise_err"],
+                                            "n_near_tie": rep["n_near_tie"],
+                                            "n_path_divergent": rep["n_path_divergent"]}
+            log("device vs oracle on the sample:", out["cpu_baseline"]["check"])
 
     print(json.dumps(out), flush=True)
 

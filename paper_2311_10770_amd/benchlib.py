@@ -3,6 +3,7 @@ and the copy kernel used to calibrate HBM counters.  Benchmark-only."""
 from __future__ import annotations
 
 import ctypes
+import time
 from ctypes import c_char_p, c_int, c_int32, c_int64, c_void_p
 from pathlib import Path
 
@@ -72,3 +73,24 @@ def copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
     rc = load().fffb_copy(src.data_ptr(), dst.data_ptr(), src.numel() * src.element_size(), s)
     if rc != 0:
         raise RuntimeError(f"fffb_copy failed ({rc})")
+
+
+def time_launches(fn, steps: int, warmup: int, stream):
+    """Mean per-launch time from per-launch event pairs on `stream`, and the whole timed region."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record(stream)
+        fn()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    region_ms = starts[0].elapsed_time(ends[-1])
+    return {"mean_ms": sum(per) / steps, "min_ms": min(per), "max_ms": max(per),
+            "std_ms": (sum((p - sum(per) / steps) ** 2 for p in per) / steps) ** 0.5,
+            "region_ms": region_ms, "wall_s": wall}

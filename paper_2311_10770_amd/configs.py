@@ -64,3 +64,16 @@ WORKLOADS = {
 }
 
 HEADLINE = "d11_h768_b65536_bf16"
+
+
+# The UltraFastBERT-KxD family of Table 1: K trees of depth D, all with about
+# 4095 trainable neurons per layer (N_T = K * (2**(D+1) - 1)); a token uses
+# N_I = K * (D+1) of them.  K = 3072, D = 0 is the dense feedforward layer of
+# BERT-base.  Timed with the same kernels at the paper's speed-test batch.
+KXD_FAMILY = ((3072, 0), (1536, 1), (512, 2), (256, 3), (128, 4), (64, 5), (32, 6), (16, 7), (8, 8), (4, 9),
+              (2, 10), (1, 11))
+
+
+def kxd_workload(k: int, d: int, dtype: str = BF16, n_tokens: int = 16384, hidden: int = 768) -> Workload:
+    return Workload(f"{k}x{d}_h{hidden}_b{n_tokens}_{dtype}", 6, n_tokens, hidden, d, k, dtype, dtype, dtype,
+                    note="UltraFastBERT-KxD family (Table 1)")

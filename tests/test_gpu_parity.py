@@ -51,6 +51,19 @@ def test_stacked_layers_teacher_forced(fff_lib):
         x = got["y"].astype(np.float32)
 
 
+# ------------------------------------------------ the KxD family of Table 1
+
+from paper_2311_10770_amd.configs import KXD_FAMILY  # noqa: E402
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k,d", KXD_FAMILY)
+def test_kxd_family(fff_lib, k, d, dtype):
+    """Every UltraFastBERT-KxD shape through the default plan, 131 tokens (ragged)."""
+    L = layer(6, 131, 768, d, k, dtype, dtype)
+    check_layer(fff_lib, f"{k}x{d} {dtype}", L, d, k, dtype)
+
+
 # ------------------------------------------------------ shapes, dtypes, edges
 
 DTYPE_COMBOS = [("f32", "f32", "f32"), ("bf16", "bf16", "bf16"), ("f32", "bf16", "f32"), ("bf16", "bf16", "f32"),

@@ -53,3 +53,17 @@ def test_workload_table():
     assert w.nodes == 4095
     assert w.gathered_bytes_per_token() == 12 * 2 * 768 * 2
     assert WORKLOADS["d15_h4096_bf16"].nodes == 65535
+
+
+def test_kxd_family_is_table1():
+    """The swept shapes are exactly Table 1's UltraFastBERT-KxD models, with its N_T."""
+    from paper_2311_10770_amd.configs import KXD_FAMILY, kxd_workload
+    from tests.conftest import read_table
+
+    table = {(int(r[1]), int(r[2])): int(r[3]) for r in read_table("table1_neuron_counts.txt")}
+    assert set(KXD_FAMILY) == set(table)
+    for k, d in KXD_FAMILY:
+        w = kxd_workload(k, d)
+        assert w.n_trees * w.nodes == table[(k, d)]
+        assert w.n_trees == k and w.depth == d and w.n_tokens == 16384 and w.hidden == 768
+        assert w.gathered_bytes_per_token() == k * (d + 1) * 2 * 768 * 2
