@@ -6,7 +6,8 @@ path (``paper_2311_10770_amd``) and neither imports the other.
 
 The arithmetic lives in ``fff_oracle.c`` (plain C, fp64, built with gcc into
 ``liboracle.so``); this module only marshals numpy arrays.  Inputs are numpy
-arrays: float32, or uint16 holding bf16 bit patterns.
+arrays: float32, or uint16 holding bf16 bit patterns (the FFF input may also
+be float64, e.g. the output of ``layer_norm``).
 """
 from __future__ import annotations
 
@@ -56,6 +57,10 @@ def _load():
     lib.oracle_eval_path.argtypes = [vp, ctypes.c_int, vp, vp, ctypes.c_int, i32, i32, i32,
                                      ctypes.c_int, vp, vp, vp]
     lib.oracle_eval_path.restype = ctypes.c_int
+    lib.oracle_layer_norm.argtypes = [vp, ctypes.c_int, i64, i32, vp, vp, dbl, vp]
+    lib.oracle_layer_norm.restype = ctypes.c_int
+    lib.oracle_round_bf16.argtypes = [vp, i64, vp]
+    lib.oracle_round_bf16.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -65,7 +70,9 @@ def _dtype_code(a: np.ndarray) -> int:
         return 0
     if a.dtype == np.uint16:
         return 1
-    raise TypeError(f"oracle inputs must be float32 or uint16 (bf16 bits), got {a.dtype}")
+    if a.dtype == np.float64:
+        return 2
+    raise TypeError(f"oracle inputs must be float32, float64 or uint16 (bf16 bits), got {a.dtype}")
 
 
 def _ptr(a):
@@ -139,3 +146,75 @@ def eval_path(x_row: np.ndarray, w_in: np.ndarray, w_out: np.ndarray, depth: int
     if rc != 0:
         raise RuntimeError(f"oracle_eval_path failed with {rc}")
     return y, logits
+
+
+def _widen(a: np.ndarray) -> np.ndarray:
+    """Exact float64 value of a float32 / float64 / bf16-bits array."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def layer_norm(x: np.ndarray, gamma=None, beta=None, eps: float = 1e-12) -> np.ndarray:
+    """Row-wise LayerNorm of x [B,H] in fp64 (biased variance, eps inside the root)."""
+    x = np.ascontiguousarray(x)
+    B, H = x.shape
+    g = None if gamma is None else np.ascontiguousarray(_widen(gamma).reshape(H))
+    b = None if beta is None else np.ascontiguousarray(_widen(beta).reshape(H))
+    out = np.empty((B, H), dtype=np.float64)
+    rc = _load().oracle_layer_norm(_ptr(x), _dtype_code(x), B, H, _ptr(g), _ptr(b), float(eps), _ptr(out))
+    if rc != 0:
+        raise RuntimeError(f"oracle_layer_norm failed with {rc}")
+    return out
+
+
+def round_bf16(v: np.ndarray) -> np.ndarray:
+    """Nearest bf16 (ties to even) of float64 values, as uint16 bit patterns."""
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = np.empty(v.shape, dtype=np.uint16)
+    rc = _load().oracle_round_bf16(_ptr(v), v.size, _ptr(out))
+    if rc != 0:
+        raise RuntimeError(f"oracle_round_bf16 failed with {rc}")
+    return out
+
+
+def store_as(v: np.ndarray, dtype: str) -> np.ndarray:
+    """A float64 result stored in a device dtype: float32 (nearest) or bf16 bits (nearest even)."""
+    return round_bf16(v) if dtype == "bf16" else v.astype(np.float32)
+
+
+def block(x: np.ndarray, w_in: np.ndarray, w_out: np.ndarray, depth: int, n_trees: int, norm=None,
+          act="gelu", tie_rel: float = DEFAULT_TIE_REL, threads: int | None = None) -> dict:
+    """The intermediate layer of a pre-norm block, x + FFF(norm(x)), in fp64.
+
+    ``norm``: None (FFF of x itself) or a dict with ``gamma``, ``beta`` (arrays or
+    None) and ``eps``: LayerNorm first.  Returns ``forward``'s dict for the FFF
+    input ``u`` (also returned), with ``y`` replaced by x + FFF(u) and the bare
+    FFF output kept as ``fff``.
+    """
+    u = x if norm is None else layer_norm(x, norm.get("gamma"), norm.get("beta"), norm["eps"])
+    out = forward(u, w_in, w_out, depth, n_trees, act=act, tie_rel=tie_rel, threads=threads)
+    out["fff"] = out["y"]
+    out["y"] = _widen(x) + out["fff"]
+    out["u"] = _widen(u)
+    return out
+
+
+def stack(x: np.ndarray, layers, depth: int, n_trees: int, store_dtype: str, norm_eps=None, act="gelu",
+          threads: int | None = None) -> list:
+    """Layers x_{i+1} = store(x_i + FFF_i(norm_i(x_i))), each result stored in ``store_dtype``.
+
+    ``layers``: a list of dicts with ``w_in``, ``w_out`` and, when ``norm_eps`` is
+    not None, optional ``gamma`` / ``beta``.  Returns the per-layer ``block``
+    dicts, each with ``x_in`` (the stored input) and ``x_out`` (the stored output).
+    """
+    outs = []
+    for lay in layers:
+        norm = None if norm_eps is None else {"gamma": lay.get("gamma"), "beta": lay.get("beta"), "eps": norm_eps}
+        r = block(x, lay["w_in"], lay["w_out"], depth, n_trees, norm=norm, act=act, threads=threads)
+        r["x_in"] = x
+        x = store_as(r["y"], store_dtype)
+        r["x_out"] = x
+        outs.append(r)
+    return outs

@@ -34,6 +34,11 @@
  *
  * Near-tie flag: |logit| < tie_rel * ||x_b||_2 * ||W_in[t,n]||_2.  A GPU path
  * may legitimately branch differently only at such a node.
+ *
+ * Around the layer (the intermediate layer of a pre-norm crammedBERT block,
+ * Section 2.1): oracle_layer_norm gives the LayerNorm that feeds the FFF,
+ * and oracle_round_bf16 the round-to-nearest-even storage of a result in
+ * bf16; the residual sum itself is one addition, done by the caller.
  */
 #include <math.h>
 #include <pthread.h>
@@ -41,12 +46,13 @@
 #include <stdlib.h>
 #include <string.h>
 
-enum { OR_F32 = 0, OR_BF16 = 1 };
+enum { OR_F32 = 0, OR_BF16 = 1, OR_F64 = 2 };
 enum { OR_ACT_GELU_ERF = 0, OR_ACT_GELU_TANH = 1, OR_ACT_IDENTITY = 2 };
 
 /* Exact widening of one stored element to double. */
 static double widen_one(const void* base, int dtype, int64_t i) {
     if (dtype == OR_F32) return (double)((const float*)base)[i];
+    if (dtype == OR_F64) return ((const double*)base)[i];
     uint32_t bits = (uint32_t)((const uint16_t*)base)[i] << 16;
     float f;
     memcpy(&f, &bits, sizeof f);
@@ -135,7 +141,8 @@ static void* run_tokens(void* arg) {
 static int check_common(const void* w_in, const void* w_out, int x_dtype, int w_dtype,
                         int32_t hidden, int32_t depth, int32_t n_trees, int act) {
     if (!w_in || !w_out) return -1;
-    if ((x_dtype != OR_F32 && x_dtype != OR_BF16) || (w_dtype != OR_F32 && w_dtype != OR_BF16))
+    if ((x_dtype != OR_F32 && x_dtype != OR_BF16 && x_dtype != OR_F64) ||
+        (w_dtype != OR_F32 && w_dtype != OR_BF16))
         return -1;
     if (hidden < 1 || depth < 0 || depth > 30 || n_trees < 1) return -1;
     if (act < OR_ACT_GELU_ERF || act > OR_ACT_IDENTITY) return -1;
@@ -228,5 +235,62 @@ int oracle_eval_path(const void* x_row, int x_dtype, const void* w_in, const voi
         }
     }
     free(xr); free(wr);
+    return 0;
+}
+
+/* LayerNorm of every row of x[B,H] (Ba, Kiros and Hinton): with the row mean
+ * mu = sum_i x_i / H and the biased variance var = sum_i (x_i - mu)^2 / H,
+ * out_i = (x_i - mu) / sqrt(var + eps) * gamma_i + beta_i.  gamma and beta
+ * may be NULL (ones and zeros).  Two passes over each row, in fp64.  Returns
+ * 0, or -1 on bad arguments. */
+int oracle_layer_norm(const void* x, int x_dtype, int64_t n_tokens, int32_t hidden, const double* gamma,
+                      const double* beta, double eps, double* out) {
+    if (!x || !out || n_tokens < 0 || hidden < 1 || !(eps >= 0.0)) return -1;
+    if (x_dtype != OR_F32 && x_dtype != OR_BF16 && x_dtype != OR_F64) return -1;
+    const int32_t H = hidden;
+    for (int64_t b = 0; b < n_tokens; ++b) {
+        double* o = out + b * H;
+        widen_row(x, x_dtype, b * H, H, o);
+        double mu = 0.0;
+        for (int32_t i = 0; i < H; ++i) mu += o[i];
+        mu /= H;
+        double var = 0.0;
+        for (int32_t i = 0; i < H; ++i) var += (o[i] - mu) * (o[i] - mu);
+        var /= H;
+        const double inv = 1.0 / sqrt(var + eps);
+        for (int32_t i = 0; i < H; ++i) {
+            double v = (o[i] - mu) * inv;
+            if (gamma) v *= gamma[i];
+            if (beta) v += beta[i];
+            o[i] = v;
+        }
+    }
+    return 0;
+}
+
+/* bf16 storage of doubles: the bf16 value nearest to v (ties to the even
+ * significand), returned as its 16-bit pattern.  bf16 has fp32's exponent
+ * range and 8 significant bits, so for |v| = m * 2^e with m in [0.5, 1) the
+ * spacing is 2^(e-8), or 2^-133 below the normal range.  Values past the
+ * largest finite bf16 by half a spacing or more become infinities. */
+int oracle_round_bf16(const double* in, int64_t n, uint16_t* out) {
+    if ((!in || !out) && n > 0) return -1;
+    for (int64_t k = 0; k < n; ++k) {
+        const double v = in[k];
+        double r = v;
+        if (v != 0.0 && isfinite(v)) {
+            int e;
+            frexp(v, &e);
+            int q = e - 8;
+            if (q < -133) q = -133;
+            r = ldexp(nearbyint(ldexp(v, -q)), q);  /* default rounding mode: ties to even */
+            if (fabs(r) > 3.3895313892515355e38) r = v > 0 ? INFINITY : -INFINITY;
+        }
+        const float f = (float)r;  /* exact: r has at most 8 significant bits */
+        uint32_t bits;
+        memcpy(&bits, &f, sizeof bits);
+        if (isnan(v)) bits = 0x7FC00000u;
+        out[k] = (uint16_t)(bits >> 16);
+    }
     return 0;
 }

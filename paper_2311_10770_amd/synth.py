@@ -9,10 +9,13 @@ benchmark is shape-only: 128 sequences of 128 tokens, hidden width 768,
 Section 3.3):
 
 * every tensor comes from ``numpy.random.default_rng([seed, layer, tensor])``
-  with tensor 0 = x, 1 = W_in, 2 = W_out;
+  with tensor 0 = x, 1 = W_in, 2 = W_out, 3 = LayerNorm gain, 4 = LayerNorm
+  shift;
 * x ~ N(0, 1), drawn as float32;
 * W_in, W_out ~ N(0, 1/H) (variance 1/H, so logits are roughly N(0, 1)),
   drawn as float32 and multiplied by float32(1/sqrt(H));
+* LayerNorm gain 1 + 0.1 N(0, 1) and shift 0.1 N(0, 1), float32 (trained
+  values are not available; these keep the normalised input near unit scale);
 * bf16 tensors are the round-to-nearest-even bf16 of those float32 draws,
   stored as their uint16 bit patterns.
 
@@ -27,7 +30,7 @@ F32 = "f32"
 BF16 = "bf16"
 DTYPES = (F32, BF16)
 
-TENSOR_X, TENSOR_W_IN, TENSOR_W_OUT = 0, 1, 2
+TENSOR_X, TENSOR_W_IN, TENSOR_W_OUT, TENSOR_GAMMA, TENSOR_BETA = 0, 1, 2, 3, 4
 
 
 def n_nodes(depth: int) -> int:
@@ -84,6 +87,13 @@ def make_weights(seed: int, hidden: int, depth: int, n_trees: int, w_dtype: str,
     w_in = gaussian_f32((seed, layer, TENSOR_W_IN), shape, scale)
     w_out = gaussian_f32((seed, layer, TENSOR_W_OUT), shape, scale)
     return as_dtype(w_in, w_dtype), as_dtype(w_out, w_dtype)
+
+
+def make_norm(seed: int, hidden: int, layer: int = 0) -> tuple[np.ndarray, np.ndarray]:
+    """float32 LayerNorm gain and shift of one layer."""
+    gamma = np.float32(1.0) + gaussian_f32((seed, layer, TENSOR_GAMMA), (hidden,), 0.1)
+    beta = gaussian_f32((seed, layer, TENSOR_BETA), (hidden,), 0.1)
+    return gamma.astype(np.float32), beta
 
 
 def make_layer(seed: int, n_tokens: int, hidden: int, depth: int, n_trees: int,
