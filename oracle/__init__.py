@@ -107,6 +107,8 @@ def forward(x: np.ndarray, w_in: np.ndarray, w_out: np.ndarray, depth: int, n_tr
     w_out = np.ascontiguousarray(w_out)
     if w_in.dtype != w_out.dtype:
         raise TypeError("W_in and W_out must share a dtype")
+    if w_in.dtype == np.float64:
+        raise TypeError("weights are float32 or bf16 bits")
     B, H = x.shape
     N = (1 << (depth + 1)) - 1
     if w_in.shape != (n_trees, N, H) or w_out.shape != (n_trees, N, H):
