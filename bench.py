@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--tokens", type=int, default=None, help="override the workload's token count")
     ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "generic"])
     ap.add_argument("--lds-levels", type=int, default=0)
+    ap.add_argument("--norm", action="store_true", help="LayerNorm before every layer (gain/shift drawn per layer)")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall budget of the oracle timing")
@@ -80,20 +81,47 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
 
-    log(f"workload {w.name}: B={B} H={w.hidden} depth={w.depth} trees={w.n_trees} "
-        f"x/W/y={w.x_dtype}/{w.w_dtype}/{w.y_dtype}")
-    L = synth.make_layer(w.seed, B, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    NL = w.layers
+    log(f"workload {w.name}: B={B} H={w.hidden} depth={w.depth} trees={w.n_trees} layers={NL} "
+        f"x/W/y={w.x_dtype}/{w.w_dtype}/{w.y_dtype} norm={args.norm}")
+    kw = dict(mode=args.mode, lds_levels=args.lds_levels)
+    if NL == 1:
+        L = synth.make_layer(w.seed, B, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+        layers_np = [{"w_in": L["w_in"], "w_out": L["w_out"]}]
+    else:
+        # a stack: layer i's weights (and LayerNorm parameters) are drawn with layer index i + 1
+        L = {"x": synth.make_x(w.seed, B, w.hidden, w.x_dtype)}
+        layers_np = []
+        for i in range(NL):
+            wi_np, wo_np = synth.make_weights(w.seed, w.hidden, w.depth, w.n_trees, w.w_dtype, layer=i + 1)
+            layers_np.append({"w_in": wi_np, "w_out": wo_np})
+    if args.norm:
+        for i, lay in enumerate(layers_np):
+            lay["gamma"], lay["beta"] = synth.make_norm(w.seed, w.hidden, layer=i + 1 if NL > 1 else 0)
+        kw.update(norm="layernorm", norm_eps=1e-12)
     x = fff.from_numpy(L["x"], dev)
-    wi = fff.from_numpy(L["w_in"], dev)
-    wo = fff.from_numpy(L["w_out"], dev)
+    dlayers = [tuple(fff.from_numpy(lay[k], dev) for k in ("w_in", "w_out", "gamma", "beta") if k in lay)
+               for lay in layers_np]
+    wi, wo = dlayers[0][0], dlayers[0][1]
     ydt = torch.bfloat16 if w.y_dtype == "bf16" else torch.float32
     y = torch.empty((B, w.hidden), dtype=ydt, device=dev)
-    kw = dict(mode=args.mode, lds_levels=args.lds_levels)
-    plan = fff.describe(x, wi, wo, w.depth, w.n_trees, y, **kw)
-    log("plan:", plan)
 
-    def step():
-        fff.forward(x, wi, wo, w.depth, w.n_trees, y, **kw)
+    def layer_kw(i):
+        if not args.norm:
+            return {}
+        return dict(norm_gamma=dlayers[i][2], norm_beta=dlayers[i][3])
+
+    if NL == 1:
+        plan = fff.describe(x, wi, wo, w.depth, w.n_trees, y, **kw, **layer_kw(0))
+
+        def step():
+            fff.forward(x, wi, wo, w.depth, w.n_trees, y, **kw, **layer_kw(0))
+    else:
+        plan = fff.describe_stack(x, dlayers, w.depth, w.n_trees, y, **kw)
+
+        def step():
+            fff.forward_stack(x, dlayers, w.depth, w.n_trees, y, **kw)
+    log("plan:", plan)
 
     if args.copy_calib_mb:
         src = torch.empty(args.copy_calib_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
@@ -106,7 +134,7 @@ def main():
     t = benchlib.time_launches(step, args.steps, args.warmup, stream)
     ms = t["region_ms"] / args.steps
     tokens_per_s = B / (ms / 1e3)
-    gathered = w.gathered_bytes_per_token() * B
+    gathered = w.gathered_bytes_per_token() * B * NL
     achieved = gathered / (t["mean_ms"] / 1e3) / 1e9
     log(f"fff: {ms * 1e3:.1f} us/step (launch mean {t['mean_ms'] * 1e3:.1f} us, std {t['std_ms'] * 1e3:.1f}), "
         f"{tokens_per_s / 1e6:.1f} M tok/s, gathered {achieved:.0f} GB/s")
@@ -117,10 +145,12 @@ def main():
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.w_dtype == "bf16" else "f32",
         "data": "synthetic (seeded Gaussian x ~ N(0,1), W ~ N(0,1/H); no trained weights)",
-        "config": {"workload": f"FFF layer, {w.n_trees} tree(s) of depth {w.depth} "
+        "config": {"workload": (f"{NL} stacked " if NL > 1 else "") +
+                               f"FFF layer{'s' if NL > 1 else ''}{' with LayerNorm' if args.norm else ''}, "
+                               f"{w.n_trees} tree(s) of depth {w.depth} "
                                f"({w.nodes} nodes), d={w.hidden}, {B} tokens, x/W/y {w.x_dtype}/{w.w_dtype}/{w.y_dtype}",
                    "name": w.name, "n_tokens": B, "hidden": w.hidden, "depth": w.depth, "n_trees": w.n_trees,
-                   "mode": args.mode, "plan": plan},
+                   "layers": NL, "norm": bool(args.norm), "mode": args.mode, "plan": plan},
         "kernel_us": {"mean": t["mean_ms"] * 1e3, "min": t["min_ms"] * 1e3, "std": t["std_ms"] * 1e3},
     }
 
@@ -136,14 +166,25 @@ def main():
             traffic = summ.get("hbm_bytes_per_launch")
         else:
             log(f"{tpath.name} was taken on other kernel sources: traffic unreported")
-    kernels = "walk_kernel + emit_kernel" if plan.startswith("grouped") else plan.split("<")[0] + "_kernel"
+    kernels = "walk_kernel + emit_kernel" if "grouped<" in plan else plan.split("<")[0].split()[-1] + "_kernel"
+    if plan.startswith("per-layer"):
+        kernels = f"{NL} launches of {kernels}"
     out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
                        "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x {B} "
-                                f"tokens, over the mean time of one forward call ({kernels}, HIP events on the "
-                                f"launch stream); served by LDS/L2/MALL, not all from HBM"}
-    flops = w.flops_per_token() * B
+                                f"tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, HIP "
+                                f"events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
+    flops = w.flops_per_token() * B * NL
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
+
+    if NL > 1:
+        # the persistent stack kernel (mode descent) beside the planned step
+        kd = dict(kw, mode="descent")
+        tk = benchlib.time_launches(lambda: fff.forward_stack(x, dlayers, w.depth, w.n_trees, y, **kd),
+                                    max(10, args.steps // 4), 3, stream)
+        out["stack"] = {"persistent_kernel_ms": tk["mean_ms"], "step_ms": t["mean_ms"],
+                        "persistent_plan": fff.describe_stack(x, dlayers, w.depth, w.n_trees, y, **kd)}
+        log(f"persistent stack kernel: {tk['mean_ms'] * 1e3:.1f} us vs the planned step {t['mean_ms'] * 1e3:.1f} us")
 
     if not args.no_dense:
         H, F = w.hidden, 3072 if w.hidden == 768 else 4 * w.hidden
@@ -152,8 +193,13 @@ def main():
         w2 = (torch.randn(H, F, generator=g) / F ** 0.5).to(dev, torch.bfloat16)
         xb = x if x.dtype == torch.bfloat16 else x.to(torch.bfloat16)
         dense = benchlib.DenseFF(xb, w1, w2)
+
+        def dense_step():  # one dense layer per FFF layer of the workload
+            for _ in range(NL):
+                dense()
+
         nd = max(20, args.steps // 2)
-        td = benchlib.time_launches(dense, nd, 10, stream)
+        td = benchlib.time_launches(dense_step, nd, 10, stream)
         dense_ms = td["region_ms"] / nd
         # sanity: the fused-epilogue GEMMs compute the dense layer (tanh- vs erf-GELU differ slightly)
         ref = torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb[:1024].float(),
@@ -161,11 +207,12 @@ def main():
         rel = float((dense.y[:1024].float() - ref).norm() / ref.norm())
 
         def dense_unfused():
-            torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
+            for _ in range(NL):
+                torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
 
         tu = benchlib.time_launches(dense_unfused, nd, 5, stream)
         unfused_ms = tu["region_ms"] / nd
-        out["dense"] = {"what": f"dense FF {H}->{F}->{H} on the same tokens, bf16: {dense.info}",
+        out["dense"] = {"what": f"{NL} x " * (NL > 1) + f"dense FF {H}->{F}->{H} on the same tokens, bf16: {dense.info}",
                         "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
                         "rel_err_vs_fp32_torch": rel,
                         "torch_unfused_ms": unfused_ms, "speedup_fff_over_torch_unfused": unfused_ms / ms}
@@ -180,11 +227,19 @@ def main():
         from oracle import parity
 
         threads = oracle.default_threads()
-        n = min(B, 4096)
-        ref = oracle.forward(L["x"][:n], L["w_in"], L["w_out"], w.depth, w.n_trees, threads=threads)
+        n = min(B, 4096 if NL == 1 else 1024)
+        eps = kw.get("norm_eps")
+
+        def cpu_pass(records):
+            if NL == 1 and not args.norm:
+                return oracle.forward(L["x"][:n], layers_np[0]["w_in"], layers_np[0]["w_out"], w.depth, w.n_trees,
+                                      records=records, threads=threads)
+            return oracle.stack(L["x"][:n], layers_np, w.depth, w.n_trees, w.y_dtype, norm_eps=eps, threads=threads)
+
+        ref = cpu_pass(True)
         done, t0 = 0, time.perf_counter()
         while True:
-            oracle.forward(L["x"][:n], L["w_in"], L["w_out"], w.depth, w.n_trees, records=False, threads=threads)
+            cpu_pass(False)
             done += n
             if time.perf_counter() - t0 >= args.cpu_seconds:
                 break
@@ -194,13 +249,33 @@ def main():
                                          f"{el:.1f}s wall, fp64 C oracle on {threads} host threads"}
         log(f"cpu oracle: {done / el:.0f} tok/s on {threads} threads")
         if not args.no_check:
-            nodes = torch.empty((B, w.n_trees, w.depth + 1), dtype=torch.int32, device=dev)
-            fff.forward(x, wi, wo, w.depth, w.n_trees, y, nodes_out=nodes, **kw)
+            # the last layer, on the device's own input to it, against the oracle's block
+            nodes = torch.empty((NL, B, w.n_trees, w.depth + 1), dtype=torch.int32, device=dev)
+            x_last = x
+            if NL > 1:
+                prev = torch.empty_like(y)
+                fff.forward_stack(x, dlayers[:-1], w.depth, w.n_trees, prev, mode=args.mode,
+                                  lds_levels=args.lds_levels, **({} if not args.norm else
+                                                                 dict(norm="layernorm", norm_eps=eps)))
+                x_last = prev
+            step()
+            fff.forward(x_last, dlayers[-1][0], dlayers[-1][1], w.depth, w.n_trees, torch.empty_like(y),
+                        nodes_out=nodes[-1], out="residual" if NL > 1 else "store", **kw, **layer_kw(NL - 1))
             torch.cuda.synchronize()
-            rows = np.arange(n)
-            rep = parity.check(L["x"], L["w_in"], L["w_out"], w.depth, w.n_trees, ref, fff.to_numpy(y),
-                               nodes.cpu().numpy(), tol=2e-2 if w.y_dtype == "bf16" else 1e-5, rows=rows)
-            out["cpu_baseline"]["check"] = {"tokens": n, "ok": rep["ok"],
+            xl = fff.to_numpy(x_last)[:n]
+            lay = layers_np[-1]
+            if NL == 1 and not args.norm:
+                r = ref
+                u, base = L["x"][:n], None
+            else:
+                r = oracle.block(xl, lay["w_in"], lay["w_out"], w.depth, w.n_trees,
+                                 norm={"gamma": lay.get("gamma"), "beta": lay.get("beta"), "eps": eps}
+                                 if args.norm else None, threads=threads)
+                u, base = r["u"], (xl if NL > 1 else None)
+                r = dict(r, y=r["fff"])
+            rep = parity.check(u, lay["w_in"], lay["w_out"], w.depth, w.n_trees, r, fff.to_numpy(y)[:n],
+                               nodes[-1].cpu().numpy()[:n], tol=2e-2 if w.y_dtype == "bf16" else 1e-5, base_dev=base)
+            out["cpu_baseline"]["check"] = {"tokens": n, "layer_checked": NL - 1, "ok": rep["ok"],
                                             "max_normwise_err": rep["max_normwise_err"],
                                             "n_near_tie": rep["n_near_tie"],
                                             "n_path_divergent": rep["n_path_divergent"]}

@@ -26,6 +26,8 @@
  *                                    starts at element (t*N + n)*hidden.
  *   - every data pointer is a DEVICE pointer owned by the caller; the library
  *     never frees or retains them.  Base pointers must be 16-byte aligned.
+ *   - y may be the very buffer x (in place) when x_dtype == y_dtype; any other
+ *     overlap of an output with an input is rejected.
  *   - arithmetic is fp32 (bf16 inputs are widened exactly); bf16 outputs are
  *     rounded to nearest even.
  *   - work is enqueued on hip_stream (NULL = the null stream) and the call
@@ -47,7 +49,7 @@
 extern "C" {
 #endif
 
-#define FFF_VERSION 100 /* major * 100 + minor */
+#define FFF_VERSION 101 /* major * 100 + minor */
 
 typedef enum {
     FFF_OK = 0,
@@ -80,16 +82,24 @@ typedef enum {
     FFF_MODE_GENERIC = 3
 } fff_mode;
 
-/* What is written to y: FFF(x); y + FFF(x); or x + FFF(x) (the residual of a
- * transformer block, needs x and y of the same hidden size). */
+/* What is written to y: FFF(u); y + FFF(u); or x + FFF(u) (the residual of a
+ * transformer block), where u is x or its LayerNorm (fff_norm). */
 typedef enum { FFF_OUT_STORE = 0, FFF_OUT_ACCUMULATE = 1, FFF_OUT_RESIDUAL = 2 } fff_out;
+
+/* Normalisation applied to x before the tree walk.  The paper's layer replaces
+ * the feedforward network inside crammedBERT's pre-norm intermediate layers
+ * (Section 2.1), whose input is the LayerNorm of the residual stream:
+ *   u_i = (x_i - mean(x)) / sqrt(var(x) + eps) * gamma_i + beta_i,
+ * mean and biased variance over the hidden dimension, computed in fp32 per
+ * token inside the kernels; the residual (FFF_OUT_RESIDUAL) adds the raw x. */
+typedef enum { FFF_NORM_NONE = 0, FFF_NORM_LAYERNORM = 1 } fff_norm;
 
 /*
  * fff_forward -- y = FFF(x) with the exact GELU, the paper's layer
  * (Algorithm 1 with the Section 2.1 changes).
  *
- *   x, W_in, W_out, y : device pointers, layouts above; x and y must not overlap
- *                       (W_in and W_out may alias).
+ *   x, W_in, W_out, y : device pointers, layouts above; y is x itself (same dtype)
+ *                       or disjoint from it (W_in and W_out may alias).
  *   depth             : 0..24.       n_trees : >= 1.
  *   n_tokens          : >= 0 (0 is a no-op returning FFF_OK).
  *   hidden            : >= 1.
@@ -128,6 +138,10 @@ typedef struct {
                              are overwritten (FFF_ERR_WORKSPACE if missing or too small) */
     size_t workspace_bytes;
     void* hip_stream;
+    int32_t norm;              /* fff_norm */
+    float norm_eps;            /* LayerNorm: >= 0 and finite (BERT uses 1e-12) */
+    const float* norm_gamma;   /* LayerNorm: device fp32 [hidden] gain, or NULL for ones */
+    const float* norm_beta;    /* LayerNorm: device fp32 [hidden] shift, or NULL for zeros */
 } fff_args;
 
 int fff_forward_ex(const fff_args* a);
@@ -143,6 +157,43 @@ size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int
  * (NUL-terminated, truncated to len).  Makes no HIP call other than the
  * cached device-property query.  Returns an fff_status. */
 int fff_describe(const fff_args* a, char* buf, size_t len);
+
+/* One layer of a stack: device pointers to its weights ([n_trees, N, hidden]
+ * each, the same layout as fff_args) and, with FFF_NORM_LAYERNORM, its
+ * LayerNorm gain and shift (fp32 [hidden], NULL for ones / zeros). */
+typedef struct {
+    const void* W_in;
+    const void* W_out;
+    const float* norm_gamma;
+    const float* norm_beta;
+} fff_layer;
+
+/*
+ * fff_forward_stack -- n_layers intermediate layers applied in sequence:
+ *     x_0 = x,   x_{i+1} = x_i + FFF_i(norm_i(x_i)),   y = x_{n_layers},
+ * each x_{i+1} rounded to the storage type (y_dtype) exactly as n_layers
+ * chained fff_forward_ex calls with FFF_OUT_RESIDUAL would store it (a
+ * stack of the Section 2.1 layers; tokens are independent, so the whole stack
+ * can run per token).  With mode DESCENT one persistent kernel keeps each
+ * token's x_i in registers through all layers (x read once, y written once;
+ * the result equals the chained calls bit for bit); AUTO, GROUPED and GENERIC
+ * run the layers as separate launches of that mode's single-layer plan, in
+ * place on y (AUTO: measured faster for most stacks on MI355X).
+ *
+ *   a        : shapes, dtypes, act, mode, norm, norm_eps, records, workspace
+ *              and stream as for fff_forward_ex, with these rules:
+ *              out_mode must be FFF_OUT_RESIDUAL; x_dtype == y_dtype; x and y
+ *              are the same buffer or disjoint; W_in, W_out, norm_gamma and
+ *              norm_beta must be NULL (they come from layers[]); nodes_out and
+ *              logits_out, when set, are [n_layers, n_tokens, n_trees, depth+1].
+ *   layers   : HOST array of n_layers descriptors (read during the call only).
+ *   n_layers : >= 1.
+ * Returns an fff_status.  On FFF_ERR_HIP some layers may have been enqueued.
+ */
+int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers);
+
+/* fff_describe for a stack. */
+int fff_describe_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers, char* buf, size_t len);
 
 const char* fff_status_str(int status);
 int fff_last_hip_error(void); /* raw hipError_t behind the calling thread's last FFF_ERR_HIP */

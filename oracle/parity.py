@@ -179,3 +179,24 @@ def assert_parity(*args, **kwargs) -> dict:
             f"(first: {rep['path_failures'][:3]}), {rep['n_value_failures']} value failures "
             f"(first: {rep['value_failures'][:3]}), max normwise err {rep['max_normwise_err']:.3e}")
     return rep
+
+
+def bf16_total_excess(y_dev_bits: np.ndarray, total_ref: np.ndarray, fff_ref: np.ndarray, tol: float) -> float:
+    """Check of a bf16 output that stores a residual sum x + FFF(u), per element.
+
+    The device stores the rounding of x + f_dev with f_dev within the FFF bar
+    of the exact f (||f_dev - f|| <= tol ||f||, per token), so every element
+    lies within one bf16 spacing of the fp64 total r = x + f plus tol ||f||:
+    the rounding moves it by at most half a spacing at the fp32 sum, and the
+    FFF error by at most its norm.  Spacing at r: 2^(e-8) for |r| in
+    [2^(e-1), 2^e), floored at the subnormal step 2^-133.  Returns the worst
+    ratio of the error to that bound (must be <= 1).
+    """
+    d = widen(y_dev_bits)
+    r = np.asarray(total_ref, dtype=np.float64)
+    if r.size == 0:
+        return 0.0
+    _, e = np.frexp(r)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    bound = spacing + tol * np.linalg.norm(np.asarray(fff_ref, dtype=np.float64), axis=1, keepdims=True)
+    return float(np.max(np.abs(d - r) / bound))

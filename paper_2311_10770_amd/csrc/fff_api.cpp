@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -71,12 +72,44 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 bool overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+    if (!a || !b) return false;
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
     return a0 < b0 + uintptr_t(bbytes) && b0 < a0 + uintptr_t(abytes);
 }
 
-// Full validation; fills the kernel parameter block.  No HIP calls.
-int validate(const fff_args* a, fff::Params* p) {
+struct Span {
+    const void* ptr;
+    int64_t bytes;
+};
+
+// Everything a call reads and writes, for the overlap rules.
+struct Buffers {
+    Span x, y, nodes, logits;
+    Span weights[2 * fff::STACK_MAX_LAYERS * 4];  // W_in, W_out, gamma, beta of every layer (read only)
+    int n_weights = 0;
+};
+
+// Outputs must not overlap each other nor any input, except that y may be x
+// itself (in place, same dtype).
+bool overlaps_ok(const Buffers& b, bool same_dtype) {
+    const Span outs[] = {b.y, b.nodes, b.logits};
+    for (int i = 0; i < 3; ++i) {
+        const Span& o = outs[i];
+        if (!o.ptr) continue;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(o.ptr, o.bytes, outs[j].ptr, outs[j].bytes)) return false;
+        const bool in_place = i == 0 && o.ptr == b.x.ptr && same_dtype;
+        if (!in_place && overlap(o.ptr, o.bytes, b.x.ptr, b.x.bytes)) return false;
+        for (int k = 0; k < b.n_weights; ++k)
+            if (overlap(o.ptr, o.bytes, b.weights[k].ptr, b.weights[k].bytes)) return false;
+    }
+    return true;
+}
+
+// Checks shared by the single-layer and stack entry points: sizes, enums and
+// the norm fields.  Fills the kernel parameter block (without weights).  No
+// HIP calls.
+int validate_shapes(const fff_args* a, int64_t rec_layers, fff::Params* p, int64_t* rec_bytes) {
     if (!a) return FFF_ERR_INVALID_ARG;
     if (a->n_tokens < 0 || a->hidden < 1 || a->depth < 0 || a->depth > kMaxDepth || a->n_trees < 1)
         return FFF_ERR_INVALID_ARG;
@@ -87,37 +120,21 @@ int validate(const fff_args* a, fff::Params* p) {
     if (a->out_mode < FFF_OUT_STORE || a->out_mode > FFF_OUT_RESIDUAL) return FFF_ERR_INVALID_ARG;
     if (a->lds_levels < -1 || a->lds_levels > kMaxDepth + 1) return FFF_ERR_INVALID_ARG;
     if (a->split_level < -1 || a->split_level > a->depth) return FFF_ERR_INVALID_ARG;
+    if (a->norm != FFF_NORM_NONE && a->norm != FFF_NORM_LAYERNORM) return FFF_ERR_INVALID_ARG;
+    if (a->norm == FFF_NORM_LAYERNORM && !(a->norm_eps >= 0.0f && a->norm_eps <= 3.0e38f)) return FFF_ERR_INVALID_ARG;
 
-    const int64_t sx = a->x_dtype == FFF_BF16 ? 2 : 4;
-    const int64_t sw = a->w_dtype == FFF_BF16 ? 2 : 4;
-    const int64_t sy = a->y_dtype == FFF_BF16 ? 2 : 4;
     const int64_t nodes = (int64_t(1) << (a->depth + 1)) - 1;
     int64_t act_elems = 0, w_rows = 0, w_elems = 0, rec = 0, tmp = 0;
     if (!mul_ok(a->n_tokens, a->hidden, &act_elems) || !mul_ok(act_elems, 4, &tmp)) return FFF_ERR_INVALID_ARG;
     if (!mul_ok(nodes, a->n_trees, &w_rows) || !mul_ok(w_rows, a->hidden, &w_elems) || !mul_ok(w_elems, 4, &tmp))
         return FFF_ERR_INVALID_ARG;
-    if (!mul_ok(a->n_tokens, int64_t(a->n_trees) * (a->depth + 1), &rec) || !mul_ok(rec, 4, &tmp))
+    if (!mul_ok(a->n_tokens, int64_t(a->n_trees) * (a->depth + 1), &rec) || !mul_ok(rec, 4 * rec_layers, &tmp))
         return FFF_ERR_INVALID_ARG;
     if (w_rows > INT32_MAX) return FFF_ERR_INVALID_ARG;
-
-    if (a->n_tokens > 0) {
-        if (!a->x || !a->W_in || !a->W_out || !a->y) return FFF_ERR_INVALID_ARG;
-        if (!aligned16(a->x) || !aligned16(a->W_in) || !aligned16(a->W_out) || !aligned16(a->y))
-            return FFF_ERR_INVALID_ARG;
-        if (a->nodes_out && !aligned16(a->nodes_out)) return FFF_ERR_INVALID_ARG;
-        if (a->logits_out && !aligned16(a->logits_out)) return FFF_ERR_INVALID_ARG;
-        if (overlap(a->x, act_elems * sx, a->y, act_elems * sy)) return FFF_ERR_INVALID_ARG;
-        if (a->nodes_out && overlap(a->nodes_out, rec * 4, a->y, act_elems * sy)) return FFF_ERR_INVALID_ARG;
-        if (a->logits_out && overlap(a->logits_out, rec * 4, a->y, act_elems * sy)) return FFF_ERR_INVALID_ARG;
-        if (a->nodes_out && a->logits_out && overlap(a->nodes_out, rec * 4, a->logits_out, rec * 4))
-            return FFF_ERR_INVALID_ARG;
-    }
-    (void)sw;
+    *rec_bytes = tmp;
 
     *p = fff::Params{};
     p->x = a->x;
-    p->w_in = a->W_in;
-    p->w_out = a->W_out;
     p->y = a->y;
     p->nodes_out = a->nodes_out;
     p->logits_out = a->logits_out;
@@ -132,6 +149,59 @@ int validate(const fff_args* a, fff::Params* p) {
     p->act = a->act;
     p->out_mode = a->out_mode;
     p->lds_levels = 0;
+    p->norm = a->norm;
+    p->norm_eps = a->norm_eps;
+    return FFF_OK;
+}
+
+// Pointer rules for one call: present, aligned, and the overlap rules over the
+// given layers' weights.  Only when n_tokens > 0.
+int validate_pointers(const fff_args* a, const fff_layer* layers, int n_layers, int64_t rec_bytes) {
+    if (a->n_tokens == 0) return FFF_OK;
+    const int64_t act = a->n_tokens * a->hidden;
+    const int64_t wbytes =
+        ((int64_t(1) << (a->depth + 1)) - 1) * a->n_trees * a->hidden * (a->w_dtype == FFF_BF16 ? 2 : 4);
+    const int64_t nbytes = int64_t(a->hidden) * 4;
+    if (!a->x || !a->y || !aligned16(a->x) || !aligned16(a->y)) return FFF_ERR_INVALID_ARG;
+    if (a->nodes_out && !aligned16(a->nodes_out)) return FFF_ERR_INVALID_ARG;
+    if (a->logits_out && !aligned16(a->logits_out)) return FFF_ERR_INVALID_ARG;
+    Buffers b;
+    b.x = {a->x, act * (a->x_dtype == FFF_BF16 ? 2 : 4)};
+    b.y = {a->y, act * (a->y_dtype == FFF_BF16 ? 2 : 4)};
+    b.nodes = {a->nodes_out, rec_bytes};
+    b.logits = {a->logits_out, rec_bytes};
+    for (int i = 0; i < n_layers; ++i) {
+        const fff_layer& L = layers[i];
+        if (!L.W_in || !L.W_out || !aligned16(L.W_in) || !aligned16(L.W_out)) return FFF_ERR_INVALID_ARG;
+        const bool norm = a->norm == FFF_NORM_LAYERNORM;
+        if (norm && ((L.norm_gamma && !aligned16(L.norm_gamma)) || (L.norm_beta && !aligned16(L.norm_beta))))
+            return FFF_ERR_INVALID_ARG;
+        if (b.n_weights + 4 > int(sizeof b.weights / sizeof b.weights[0])) return FFF_ERR_INVALID_ARG;
+        b.weights[b.n_weights++] = {L.W_in, wbytes};
+        b.weights[b.n_weights++] = {L.W_out, wbytes};
+        if (norm) {
+            b.weights[b.n_weights++] = {L.norm_gamma, nbytes};
+            b.weights[b.n_weights++] = {L.norm_beta, nbytes};
+        }
+    }
+    if (!overlaps_ok(b, a->x_dtype == a->y_dtype)) return FFF_ERR_INVALID_ARG;
+    return FFF_OK;
+}
+
+// Full validation of a single-layer call; fills the kernel parameter block.
+int validate(const fff_args* a, fff::Params* p) {
+    int64_t rec_bytes = 0;
+    int rc = validate_shapes(a, 1, p, &rec_bytes);
+    if (rc != FFF_OK) return rc;
+    const fff_layer L = {a->W_in, a->W_out, a->norm_gamma, a->norm_beta};
+    rc = validate_pointers(a, &L, 1, rec_bytes);
+    if (rc != FFF_OK) return rc;
+    p->w_in = a->W_in;
+    p->w_out = a->W_out;
+    if (a->norm == FFF_NORM_LAYERNORM) {
+        p->gamma = a->norm_gamma;
+        p->beta = a->norm_beta;
+    }
     return FFF_OK;
 }
 
@@ -145,11 +215,13 @@ int check_workspace(const fff_args* a) {
     const int64_t act = a->n_tokens * a->hidden;
     const int64_t rec = a->n_tokens * a->n_trees * (a->depth + 1) * 4;
     const int64_t wbytes = ((int64_t(1) << (a->depth + 1)) - 1) * a->n_trees * a->hidden * (a->w_dtype ? 2 : 4);
+    const int64_t nbytes = int64_t(a->hidden) * 4;
     if (overlap(a->workspace, wsb, a->x, act * (a->x_dtype ? 2 : 4)) ||
         overlap(a->workspace, wsb, a->y, act * (a->y_dtype ? 2 : 4)) ||
         overlap(a->workspace, wsb, a->W_in, wbytes) || overlap(a->workspace, wsb, a->W_out, wbytes) ||
-        (a->nodes_out && overlap(a->workspace, wsb, a->nodes_out, rec)) ||
-        (a->logits_out && overlap(a->workspace, wsb, a->logits_out, rec)))
+        overlap(a->workspace, wsb, a->nodes_out, rec) || overlap(a->workspace, wsb, a->logits_out, rec) ||
+        (a->norm && (overlap(a->workspace, wsb, a->norm_gamma, nbytes) ||
+                     overlap(a->workspace, wsb, a->norm_beta, nbytes))))
         return FFF_ERR_INVALID_ARG;
     return FFF_OK;
 }
@@ -169,9 +241,7 @@ int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
     return FFF_OK;
 }
 
-}  // namespace
-
-FFF_EXPORT int fff_forward_ex(const fff_args* a) {
+int forward_one(const fff_args* a) {
     fff::Params p;
     {
         const int rc = validate(a, &p);
@@ -184,6 +254,99 @@ FFF_EXPORT int fff_forward_ex(const fff_args* a) {
     const hipError_t e =
         fff::run_forward(p, plan, a->workspace, a->workspace_bytes, reinterpret_cast<hipStream_t>(a->hip_stream));
     if (e != hipSuccess) return hip_fail(e);
+    return FFF_OK;
+}
+
+// ------------------------------------------------------------------ stacks
+
+constexpr int kMaxStackLayers = 4096;
+
+int validate_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers, fff::Params* p) {
+    if (!a || n_layers < 1 || n_layers > kMaxStackLayers || !layers) return FFF_ERR_INVALID_ARG;
+    if (a->W_in || a->W_out || a->norm_gamma || a->norm_beta) return FFF_ERR_INVALID_ARG;
+    if (a->out_mode != FFF_OUT_RESIDUAL || a->x_dtype != a->y_dtype) return FFF_ERR_INVALID_ARG;
+    int64_t rec_bytes = 0;
+    int rc = validate_shapes(a, n_layers, p, &rec_bytes);
+    if (rc != FFF_OK) return rc;
+    // overlap rules in windows of layers (the buffer table is bounded); every
+    // window is checked against x, y and the records
+    constexpr int kWindow = fff::STACK_MAX_LAYERS;
+    for (int i0 = 0; i0 < n_layers; i0 += kWindow) {
+        rc = validate_pointers(a, layers + i0, std::min(kWindow, n_layers - i0), rec_bytes);
+        if (rc != FFF_OK) return rc;
+    }
+    return FFF_OK;
+}
+
+// DESCENT runs the stack in the persistent stack kernel; the other modes run
+// one launch per layer.  AUTO takes the per-layer launches: measured on
+// MI355X, the persistent kernel saves the re-reads of x but loses L2
+// locality (its workgroups drift apart across layers, so several layers'
+// rows compete for each XCD's L2), and it was slower for most stacks.
+int plan_stack_for(const fff_args* a, const fff::Params& p, fff::Plan* plan, bool* use_kernel) {
+    *use_kernel = false;
+    if (a->mode != FFF_MODE_DESCENT) return FFF_OK;
+    fff::DeviceInfo dev;
+    int rc = current_device_info(&dev);
+    if (rc != FFF_OK) return rc;
+    rc = fff::plan_stack(p, a->lds_levels, dev, plan);
+    if (rc == FFF_OK) *use_kernel = true;
+    return rc;
+}
+
+// Single-layer arguments for layer i of a stack run as separate launches.
+fff_args layer_args(const fff_args* a, const fff_layer* layers, int i) {
+    fff_args b = *a;
+    const int64_t rec = a->n_tokens * a->n_trees * (a->depth + 1);
+    b.x = i == 0 ? a->x : a->y;
+    b.W_in = layers[i].W_in;
+    b.W_out = layers[i].W_out;
+    b.norm_gamma = layers[i].norm_gamma;
+    b.norm_beta = layers[i].norm_beta;
+    b.nodes_out = a->nodes_out ? a->nodes_out + i * rec : nullptr;
+    b.logits_out = a->logits_out ? a->logits_out + i * rec : nullptr;
+    return b;
+}
+
+}  // namespace
+
+FFF_EXPORT int fff_forward_ex(const fff_args* a) { return forward_one(a); }
+
+FFF_EXPORT int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers) {
+    fff::Params p;
+    int rc = validate_stack(a, layers, n_layers, &p);
+    if (rc != FFF_OK) return rc;
+    if (a->n_tokens == 0) return FFF_OK;
+    fff::Plan plan;
+    bool use_kernel = false;
+    rc = plan_stack_for(a, p, &plan, &use_kernel);
+    if (rc != FFF_OK) return rc;
+    if (!use_kernel) {
+        for (int i = 0; i < n_layers; ++i) {
+            const fff_args b = layer_args(a, layers, i);
+            rc = forward_one(&b);
+            if (rc != FFF_OK) return rc;
+        }
+        return FFF_OK;
+    }
+    const int64_t rec = a->n_tokens * a->n_trees * (a->depth + 1);
+    fff::StackParams sp;
+    std::memset(&sp, 0, sizeof sp);
+    sp.rec_stride = rec;
+    for (int i0 = 0; i0 < n_layers; i0 += fff::STACK_MAX_LAYERS) {
+        sp.p = p;
+        sp.p.x = i0 == 0 ? a->x : a->y;
+        sp.p.nodes_out = a->nodes_out ? a->nodes_out + i0 * rec : nullptr;
+        sp.p.logits_out = a->logits_out ? a->logits_out + i0 * rec : nullptr;
+        sp.n_layers = std::min(fff::STACK_MAX_LAYERS, n_layers - i0);
+        for (int j = 0; j < sp.n_layers; ++j) {
+            const fff_layer& L = layers[i0 + j];
+            const bool norm = a->norm == FFF_NORM_LAYERNORM;
+            sp.layer[j] = {L.W_in, L.W_out, norm ? L.norm_gamma : nullptr, norm ? L.norm_beta : nullptr};
+        }
+        const hipError_t e = fff::run_stack(sp, plan, reinterpret_cast<hipStream_t>(a->hip_stream));
+        if (e != hipSuccess) return hip_fail(e);
+    }
     return FFF_OK;
 }
 
@@ -215,22 +378,48 @@ FFF_EXPORT size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n
     return fff::grouped_workspace_bytes(n_tokens, depth, n_trees, split_level);
 }
 
+namespace {
+void format_plan(const fff::Plan& plan, const char* prefix, char* buf, size_t len) {
+    if (!buf || !len) return;
+    static const char* kinds[] = {"none", "descent", "generic", "grouped", "stack"};
+    int n = std::snprintf(buf, len, "%s%s<%s> lanes_per_token=%d lds_levels=%d", prefix, kinds[plan.kind],
+                          plan.name, plan.lanes, plan.lds_levels);
+    if (plan.kind == fff::KIND_GROUPED && n > 0 && size_t(n) < len)
+        n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d", plan.emit_lds_levels,
+                           plan.split_level);
+    for (int i = 0; i < plan.n_launch && n > 0 && size_t(n) < len; ++i)
+        n += std::snprintf(buf + n, len - n, " | launch%d grid=%d block=%d lds_bytes=%zu", i, plan.launch[i].grid,
+                           plan.launch[i].block, plan.launch[i].lds_bytes);
+}
+}  // namespace
+
 FFF_EXPORT int fff_describe(const fff_args* a, char* buf, size_t len) {
     fff::Params p;
     fff::Plan plan;
     const int rc = plan_for(a, &p, &plan);
     if (rc != FFF_OK) return rc;
-    if (buf && len) {
-        static const char* kinds[] = {"none", "descent", "generic", "grouped"};
-        int n = std::snprintf(buf, len, "%s<%s> lanes_per_token=%d lds_levels=%d", kinds[plan.kind], plan.name,
-                              plan.lanes, plan.lds_levels);
-        if (plan.kind == fff::KIND_GROUPED && n > 0 && size_t(n) < len)
-            n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d", plan.emit_lds_levels,
-                               plan.split_level);
-        for (int i = 0; i < plan.n_launch && n > 0 && size_t(n) < len; ++i)
-            n += std::snprintf(buf + n, len - n, " | launch%d grid=%d block=%d lds_bytes=%zu", i,
-                               plan.launch[i].grid, plan.launch[i].block, plan.launch[i].lds_bytes);
+    format_plan(plan, "", buf, len);
+    return FFF_OK;
+}
+
+FFF_EXPORT int fff_describe_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers, char* buf,
+                                  size_t len) {
+    fff::Params p;
+    int rc = validate_stack(a, layers, n_layers, &p);
+    if (rc != FFF_OK) return rc;
+    fff::Plan plan;
+    bool use_kernel = false;
+    rc = plan_stack_for(a, p, &plan, &use_kernel);
+    if (rc != FFF_OK) return rc;
+    if (use_kernel) {
+        format_plan(plan, "", buf, len);
+        return FFF_OK;
     }
+    const fff_args b = layer_args(a, layers, 0);
+    fff::Params pb;
+    rc = plan_for(&b, &pb, &plan);
+    if (rc != FFF_OK) return rc;
+    format_plan(plan, "per-layer ", buf, len);
     return FFF_OK;
 }
 

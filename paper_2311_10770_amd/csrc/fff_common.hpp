@@ -48,6 +48,13 @@ struct XRegs<LANES, NV, true, true> {  // bf16 x with bf16 W: keep packed pairs 
         const uint32_t u = word(v[c], e >> 1);
         return (e & 1) ? bf16_hi(u) : bf16_lo(u);
     }
+    // Replace x by the bf16 rounding of vals (laid out like an output slice).
+    __device__ void set_from(const float* vals, bool /*to_bf16: always*/) {
+#pragma unroll
+        for (int c = 0; c < NV; ++c)
+            v[c] = make_uint4(pack_bf16x2(vals[c * 8 + 0], vals[c * 8 + 1]), pack_bf16x2(vals[c * 8 + 2], vals[c * 8 + 3]),
+                              pack_bf16x2(vals[c * 8 + 4], vals[c * 8 + 5]), pack_bf16x2(vals[c * 8 + 6], vals[c * 8 + 7]));
+    }
 };
 
 template <int LANES, int NV>
@@ -75,6 +82,27 @@ struct XRegs<LANES, NV, false, true> {  // fp32 x with bf16 W
         return s;
     }
     __device__ float elem(int c, int e) const { return f[c * 8 + e]; }
+    // x stored as bf16 (xbf) or fp32, widened into this fp32 layout.
+    __device__ void load_widen(const void* x, bool xbf, int64_t tok, int sl) {
+        if (!xbf) {
+            load(x, tok, sl);
+            return;
+        }
+        const uint4* row = reinterpret_cast<const uint4*>(x) + tok * (LANES * NV);
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+            const uint4 a = row[c * LANES + sl];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f[c * 8 + 2 * j] = bf16_lo(word(a, j));
+                f[c * 8 + 2 * j + 1] = bf16_hi(word(a, j));
+            }
+        }
+    }
+    __device__ void set_from(const float* vals, bool to_bf16) {
+#pragma unroll
+        for (int i = 0; i < NV * 8; ++i) f[i] = to_bf16 ? bf16_to_f32(f32_to_bf16(vals[i])) : vals[i];
+    }
 };
 
 template <int LANES, int NV, bool XBF>
@@ -107,11 +135,81 @@ struct XRegsF32W {  // fp32 W: x held as fp32 (bf16 x widened once)
         return s;
     }
     __device__ float elem(int c, int e) const { return f[c * 4 + e]; }
+    __device__ void load_widen(const void* x, bool xbf, int64_t tok, int sl) {
+        if (xbf) {
+            XRegsF32W<LANES, NV, true> t;
+            t.load(x, tok, sl);
+#pragma unroll
+            for (int i = 0; i < NV * 4; ++i) f[i] = t.f[i];
+        } else {
+            XRegsF32W<LANES, NV, false> t;
+            t.load(x, tok, sl);
+#pragma unroll
+            for (int i = 0; i < NV * 4; ++i) f[i] = t.f[i];
+        }
+    }
+    __device__ void set_from(const float* vals, bool to_bf16) {
+#pragma unroll
+        for (int i = 0; i < NV * 4; ++i) f[i] = to_bf16 ? bf16_to_f32(f32_to_bf16(vals[i])) : vals[i];
+    }
 };
 template <int LANES, int NV>
 struct XRegs<LANES, NV, false, false> : XRegsF32W<LANES, NV, false> {};
 template <int LANES, int NV>
 struct XRegs<LANES, NV, true, false> : XRegsF32W<LANES, NV, true> {};
+
+// Zeros standing in for an absent LayerNorm gain or shift in the register
+// kernels (hidden <= 4096), so that those loads need no branch.
+constexpr int NORM_TABLE = 4096;
+static __device__ float g_norm_zeros[NORM_TABLE];
+
+// LayerNorm of one token held in fp32 registers (f in the layout above, EV
+// elements per vector): mean and biased variance over all H elements, summed
+// per lane then across the group (every lane gets the same bits), then
+// f = (f - mean) / sqrt(var + eps) * gamma + beta.  gamma / beta may be null.
+template <int LANES, int NV, bool WBF>
+__device__ __forceinline__ void layer_norm_regs(float* f, const float* gamma, const float* beta, float eps,
+                                                int sl) {
+    constexpr int EV = WBF ? 8 : 4;
+    constexpr int E = NV * EV;
+    constexpr float H = float(LANES * E);
+    static_assert(LANES * E <= NORM_TABLE, "zero table too short");
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) s += f[i];
+    const float mean = group_sum<LANES>(s) / H;
+    float q = 0.0f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        f[i] -= mean;  // centred in place: x and x - mean are never both live
+        q = __builtin_fmaf(f[i], f[i], q);
+    }
+    const float var = group_sum<LANES>(q) / H;
+    const float rstd = 1.0f / sqrtf(var + eps);
+    const bool has_gamma = gamma != nullptr;
+    const float* gp = has_gamma ? gamma : g_norm_zeros;
+    const float* bp = beta ? beta : g_norm_zeros;
+    // One vector of gain and shift at a time: hoisting all of them above the
+    // statistics would hold 2*E extra registers at the kernel's peak.  The
+    // empty asm statements pin the order (loads of chunk c, then its FMAs, then
+    // chunk c+1); they emit no instructions.
+#pragma unroll
+    for (int c = 0; c < NV; ++c) {
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int q4 = 0; q4 < EV / 4; ++q4) {
+            const int col = (c * LANES + sl) * EV + 4 * q4;
+            const float4 g = *reinterpret_cast<const float4*>(gp + col);
+            const float4 b = *reinterpret_cast<const float4*>(bp + col);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float& v = f[c * EV + 4 * q4 + j];
+                v = __builtin_fmaf(v * rstd, has_gamma ? fword(g, j) : 1.0f, fword(b, j));
+                asm volatile("" : "+v"(v));
+            }
+        }
+    }
+}
 
 template <int NV, bool WBF>
 __device__ __forceinline__ void axpy(float* acc, float a, const uint4* w) {
@@ -131,11 +229,11 @@ __device__ __forceinline__ void axpy(float* acc, float a, const uint4* w) {
     }
 }
 
-// Final combine and store of one token's output slice.
-template <int LANES, int NV, bool XBF, bool WBF>
-__device__ __forceinline__ void store_output(const Params& p, const XRegs<LANES, NV, XBF, WBF>& xr, float* acc,
-                                             int64_t tok, int sl) {
-    using S = Shape<LANES, NV, XBF, WBF>;
+// Final combine and store of one token's output slice; xr (anything with
+// elem(c, e) in the lane layout) supplies x for the residual.
+template <int LANES, int NV, bool WBF, class XR>
+__device__ __forceinline__ void store_output(const Params& p, const XR& xr, float* acc, int64_t tok, int sl) {
+    using S = Shape<LANES, NV, false, WBF>;
     constexpr int EV = S::EV;
     if (p.out_mode == OUT_RESIDUAL) {
 #pragma unroll

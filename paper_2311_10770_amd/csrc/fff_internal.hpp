@@ -31,6 +31,30 @@ struct Params {
     float* ws_act;        // [B, T, D+1] activation of every visited node
     int32_t* ws_leaf;     // [B, T] leaf reached in each tree
     int32_t split_level;  // group tokens by their tree-0 node at this level; 0 = keep token order
+    // LayerNorm prologue (norm = 1): u = (x - mean) / sqrt(var + eps) * gamma + beta
+    int32_t norm;
+    float norm_eps;
+    const float* gamma;   // [H] or null (ones)
+    const float* beta;    // [H] or null (zeros)
+};
+
+// One layer of a stack: its weights and LayerNorm parameters.
+struct LayerPtrs {
+    const void* w_in;
+    const void* w_out;
+    const float* gamma;
+    const float* beta;
+};
+
+// Layers handled by one launch of the stack kernel (the table travels in the
+// kernel arguments); longer stacks take several launches, in place on y.
+constexpr int STACK_MAX_LAYERS = 32;
+
+struct StackParams {
+    Params p;             // x, y, shapes, dtypes, norm, records base; w_in/w_out unused
+    int32_t n_layers;
+    int64_t rec_stride;   // elements between consecutive layers' records
+    LayerPtrs layer[STACK_MAX_LAYERS];
 };
 
 constexpr int XCDS = 8;  // MI355X: 8 XCDs, workgroups dealt to them round-robin
@@ -42,7 +66,7 @@ struct DeviceInfo {
     size_t lds_per_cu = 0;     // bytes
 };
 
-enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3 };
+enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4 };
 
 struct Launch {
     const void* kernel = nullptr;  // __global__ function handle
@@ -71,6 +95,13 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
 // Enqueues the planned work on stream; returns the first failing HIP error.
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
+
+// Stack of layers in one persistent kernel: fills *plan (KIND_STACK) when a
+// kernel is instantiated for the shape and types, else returns ST_UNSUPPORTED.
+int plan_stack(const Params& p, int lds_levels_req, const DeviceInfo& dev, Plan* plan);
+
+// Enqueues the stack kernel for layers [0, n) of sp (n <= STACK_MAX_LAYERS).
+hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream);
 
 // Grouped mode scratch size for a resolved split level (0 = no bucketing).
 size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t split_level);

@@ -57,17 +57,46 @@ __device__ __forceinline__ void stage_rows(uint4* lds, const void* w, int T, int
 
 // Per-visit records (optional outputs): node and logit of every level.
 template <int LANES>
-__device__ __forceinline__ void write_records(const Params& p, const LevelRegs<LANES>& lv, uint32_t leaf1,
-                                              int64_t tok, int t, int sl) {
+__device__ __forceinline__ void write_records(int32_t* nodes, float* logits, const Params& p,
+                                              const LevelRegs<LANES>& lv, uint32_t leaf1, int64_t tok, int t, int sl) {
     const int D = p.depth;
 #pragma unroll
     for (int r = 0; r < LevelRegs<LANES>::NR; ++r) {
         const int l = r * LANES + sl;
         if (l <= D) {
             const int64_t rec = (tok * p.n_trees + t) * (D + 1) + l;
-            if (p.nodes_out) p.nodes_out[rec] = int32_t((leaf1 >> (D - l)) - 1);
-            if (p.logits_out) p.logits_out[rec] = lv.v[r];
+            if (nodes) nodes[rec] = int32_t((leaf1 >> (D - l)) - 1);
+            if (logits) logits[rec] = lv.v[r];
         }
+    }
+}
+
+// The FFF input of one token in registers: x itself in its stored layout, or
+// (NORM) x widened to fp32 and layer-normalised.
+template <int LANES, int NV, bool XBF, bool WBF, bool NORM>
+using XIn = XRegs<LANES, NV, NORM ? false : XBF, WBF>;
+
+template <int LANES, int NV, bool XBF, bool WBF, bool NORM>
+__device__ __forceinline__ void load_input(XIn<LANES, NV, XBF, WBF, NORM>& xr, const Params& p, int64_t tok,
+                                           int sl) {
+    if constexpr (NORM) {
+        xr.load_widen(p.x, p.x_bf16, tok, sl);
+        layer_norm_regs<LANES, NV, WBF>(xr.f, p.gamma, p.beta, p.norm_eps, sl);
+    } else {
+        xr.load(p.x, tok, sl);
+    }
+}
+
+// Combine and store; with NORM the residual adds the raw x, reloaded.
+template <int LANES, int NV, bool XBF, bool WBF, bool NORM>
+__device__ __forceinline__ void finish_token(const Params& p, const XIn<LANES, NV, XBF, WBF, NORM>& xr, float* acc,
+                                             int64_t tok, int sl) {
+    if (NORM && p.out_mode == OUT_RESIDUAL) {
+        XRegs<LANES, NV, false, WBF> raw;
+        raw.load_widen(p.x, p.x_bf16, tok, sl);
+        store_output<LANES, NV, WBF>(p, raw, acc, tok, sl);
+    } else {
+        store_output<LANES, NV, WBF>(p, xr, acc, tok, sl);
     }
 }
 
@@ -75,9 +104,11 @@ __device__ __forceinline__ void write_records(const Params& p, const LevelRegs<L
 // DESCENT: one fused kernel
 // ----------------------------------------------------------------------------
 
-template <int LANES, int NV, bool XBF, bool WBF, int BLOCK>
+template <int LANES, int NV, bool XBF, bool WBF, int BLOCK, bool NORM>
 __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
+    static_assert(!(NORM && XBF), "normalised inputs are held in fp32");
     using S = Shape<LANES, NV, XBF, WBF>;
+    constexpr bool XR_BF = NORM ? false : XBF;
     constexpr int WAVES = BLOCK / 64;
     extern __shared__ uint4 lds_rows[];  // [T][Nk][2][ROWV]: W_in row then W_out row
 
@@ -99,8 +130,8 @@ __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
         const int64_t slot_raw = g * S::TPW + sub;
         const bool valid = slot_raw < p.n_tokens;
         const int64_t tok = valid ? slot_raw : p.n_tokens - 1;  // idle groups redo the last token, store nothing
-        XRegs<LANES, NV, XBF, WBF> xr;
-        xr.load(p.x, tok, sl);
+        XIn<LANES, NV, XBF, WBF, NORM> xr;
+        load_input<LANES, NV, XBF, WBF, NORM>(xr, p, tok, sl);
         float acc[S::E];
 #pragma unroll
         for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
@@ -109,18 +140,19 @@ __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
             const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + int64_t(t) * N * S::ROWV + sl;
             const uint4* lrows = lds_rows + int64_t(t) * Nk * 2 * S::ROWV + sl;
             LevelRegs<LANES> lv;
-            const uint32_t leaf1 = walk_tree<LANES, NV, XBF, WBF>(xr, lrows, 2 * S::ROWV, win, KD, D, sl, lv);
+            const uint32_t leaf1 = walk_tree<LANES, NV, XR_BF, WBF>(xr, lrows, 2 * S::ROWV, win, KD, D, sl, lv);
             LevelRegs<LANES> av;
 #pragma unroll
             for (int r = 0; r < LevelRegs<LANES>::NR; ++r) av.v[r] = activation(lv.v[r], p.act);
-            if ((p.nodes_out || p.logits_out) && valid) write_records<LANES>(p, lv, leaf1, tok, t, sl);
+            if ((p.nodes_out || p.logits_out) && valid)
+                write_records<LANES>(p.nodes_out, p.logits_out, p, lv, leaf1, tok, t, sl);
             const uint4* lout = lrows + S::ROWV;
             emit_levels<LANES, NV, WBF>(
                 acc, KD, D, [&](int l) { return lout + int64_t((leaf1 >> (D - l)) - 1) * 2 * S::ROWV; },
                 [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
                 [&](int l) { return av.get(l, lane); });
         }
-        if (valid) store_output<LANES, NV, XBF, WBF>(p, xr, acc, tok, sl);
+        if (valid) finish_token<LANES, NV, XBF, WBF, NORM>(p, xr, acc, tok, sl);
     }
 }
 
@@ -128,9 +160,11 @@ __global__ __launch_bounds__(BLOCK) void descent_kernel(Params p) {
 // GROUPED: walk kernel (CMM) then emit kernel
 // ----------------------------------------------------------------------------
 
-template <int LANES, int NV, bool XBF, bool WBF, int BLOCK>
+template <int LANES, int NV, bool XBF, bool WBF, int BLOCK, bool NORM>
 __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
+    static_assert(!(NORM && XBF), "normalised inputs are held in fp32");
     using S = Shape<LANES, NV, XBF, WBF>;
+    constexpr bool XR_BF = NORM ? false : XBF;
     constexpr int WAVES = BLOCK / 64;
     extern __shared__ uint4 lds_in[];  // [T][Nk][ROWV] W_in rows of the top levels
 
@@ -151,13 +185,13 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
         const int64_t slot_raw = g * S::TPW + sub;
         const bool valid = slot_raw < p.n_tokens;
         const int64_t tok = valid ? slot_raw : p.n_tokens - 1;
-        XRegs<LANES, NV, XBF, WBF> xr;
-        xr.load(p.x, tok, sl);
+        XIn<LANES, NV, XBF, WBF, NORM> xr;
+        load_input<LANES, NV, XBF, WBF, NORM>(xr, p, tok, sl);
         for (int t = 0; t < T; ++t) {
             const uint4* win = reinterpret_cast<const uint4*>(p.w_in) + int64_t(t) * N * S::ROWV + sl;
             const uint4* lrows = lds_in + int64_t(t) * Nk * S::ROWV + sl;
             LevelRegs<LANES> lv;
-            const uint32_t leaf1 = walk_tree<LANES, NV, XBF, WBF>(xr, lrows, S::ROWV, win, KD, D, sl, lv);
+            const uint32_t leaf1 = walk_tree<LANES, NV, XR_BF, WBF>(xr, lrows, S::ROWV, win, KD, D, sl, lv);
             if (valid) {
                 const int64_t rec0 = (tok * T + t) * (D + 1);
 #pragma unroll
@@ -166,7 +200,8 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
                     if (l <= D) p.ws_act[rec0 + l] = activation(lv.v[r], p.act);
                 }
                 if (sl == 0) p.ws_leaf[tok * T + t] = int32_t(leaf1 - 1);
-                if (p.nodes_out || p.logits_out) write_records<LANES>(p, lv, leaf1, tok, t, sl);
+                if (p.nodes_out || p.logits_out)
+                    write_records<LANES>(p.nodes_out, p.logits_out, p, lv, leaf1, tok, t, sl);
             }
         }
     }
@@ -257,9 +292,102 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
             }
             XRegs<LANES, NV, XBF, WBF> xr;
             if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
-            if (valid) store_output<LANES, NV, XBF, WBF>(p, xr, acc, tok, sl);
+            if (valid) store_output<LANES, NV, WBF>(p, xr, acc, tok, sl);
         }
         if (affine) __syncthreads();  // the queue is refilled next round
+    }
+}
+
+// ----------------------------------------------------------------------------
+// STACK: several layers x <- x + FFF_i(norm_i(x)) in one persistent kernel
+// ----------------------------------------------------------------------------
+//
+// Tokens are independent through the whole stack, so a group keeps its token's
+// x in registers from the first layer to the last: x is read once and y
+// written once.  Each workgroup takes chunks of WAVES token groups and runs
+// every layer on the chunk; the top levels of the current layer are staged
+// into LDS between two barriers, so all waves of a block move through the
+// layers together.  Per layer the arithmetic is exactly the descent kernel's
+// (same loads, same reduction and accumulation order, the residual sum rounded
+// to the storage type), so the stack equals chained single-layer calls bit for
+// bit.  NORM: x is held as fp32 values of the storage type (p.x_bf16 says
+// which) and each layer normalises a copy.
+template <int LANES, int NV, bool XBF, bool WBF, int BLOCK, bool NORM>
+__global__ __launch_bounds__(BLOCK) void stack_kernel(StackParams sp) {
+    static_assert(!(NORM && XBF), "normalised inputs are held in fp32");
+    using S = Shape<LANES, NV, XBF, WBF>;
+    using XS = XRegs<LANES, NV, XBF, WBF>;
+    constexpr int WAVES = BLOCK / 64;
+    extern __shared__ uint4 lds_rows[];  // [T][Nk][2][ROWV] of the current layer
+
+    const Params& p = sp.p;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int sl = lane % LANES;
+    const int sub = lane / LANES;
+    const int T = p.n_trees, D = p.depth, K = p.lds_levels;
+    const int64_t N = p.n_nodes;
+    const int Nk = (1 << K) - 1;
+    const int KD = K < D + 1 ? K : D + 1;
+    const bool to_bf16 = p.y_bf16;
+    const int64_t n_groups = (p.n_tokens + S::TPW - 1) / S::TPW;
+    const int64_t n_chunks = (n_groups + WAVES - 1) / WAVES;
+    // The chunk loop and the layer loop have the same trip counts in every wave
+    // of the block, so every wave reaches every barrier.
+    for (int64_t ch = blockIdx.x; ch < n_chunks; ch += gridDim.x) {
+        const int64_t g = ch * WAVES + wave;
+        const bool active = g < n_groups;  // wave-uniform
+        const int64_t slot_raw = g * S::TPW + sub;
+        const bool valid = slot_raw < p.n_tokens;
+        const int64_t tok = valid ? slot_raw : p.n_tokens - 1;
+        XS xs;
+        if (active) {
+            if constexpr (NORM) xs.load_widen(p.x, p.x_bf16, tok, sl);
+            else xs.load(p.x, tok, sl);
+        }
+        for (int li = 0; li < sp.n_layers; ++li) {
+            const LayerPtrs L = sp.layer[li];
+            if (K > 0) {
+                __syncthreads();  // the previous layer's rows are no longer read
+                stage_rows<S::ROWV, BLOCK>(lds_rows, L.w_in, T, N, Nk, 2 * S::ROWV, 0);
+                stage_rows<S::ROWV, BLOCK>(lds_rows, L.w_out, T, N, Nk, 2 * S::ROWV, S::ROWV);
+                __syncthreads();
+            }
+            if (!active) continue;
+            float acc[S::E];
+#pragma unroll
+            for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
+            XS u = xs;
+            if constexpr (NORM) layer_norm_regs<LANES, NV, WBF>(u.f, L.gamma, L.beta, p.norm_eps, sl);
+            int32_t* nodes = p.nodes_out ? p.nodes_out + li * sp.rec_stride : nullptr;
+            float* logits = p.logits_out ? p.logits_out + li * sp.rec_stride : nullptr;
+            for (int t = 0; t < T; ++t) {
+                const uint4* win = reinterpret_cast<const uint4*>(L.w_in) + int64_t(t) * N * S::ROWV + sl;
+                const uint4* wout = reinterpret_cast<const uint4*>(L.w_out) + int64_t(t) * N * S::ROWV + sl;
+                const uint4* lrows = lds_rows + int64_t(t) * Nk * 2 * S::ROWV + sl;
+                LevelRegs<LANES> lv;
+                const uint32_t leaf1 = walk_tree<LANES, NV, XBF, WBF>(u, lrows, 2 * S::ROWV, win, KD, D, sl, lv);
+                LevelRegs<LANES> av;
+#pragma unroll
+                for (int r = 0; r < LevelRegs<LANES>::NR; ++r) av.v[r] = activation(lv.v[r], p.act);
+                if ((nodes || logits) && valid) write_records<LANES>(nodes, logits, p, lv, leaf1, tok, t, sl);
+                const uint4* lout = lrows + S::ROWV;
+                emit_levels<LANES, NV, WBF>(
+                    acc, KD, D, [&](int l) { return lout + int64_t((leaf1 >> (D - l)) - 1) * 2 * S::ROWV; },
+                    [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                    [&](int l) { return av.get(l, lane); });
+            }
+            if (li + 1 < sp.n_layers) {
+                // x_{i+1} = storage rounding of x_i + FFF_i, as a stored-and-reloaded residual would be
+#pragma unroll
+                for (int c = 0; c < NV; ++c)
+#pragma unroll
+                    for (int e = 0; e < S::EV; ++e) acc[c * S::EV + e] += xs.elem(c, e);
+                xs.set_from(acc, to_bf16);
+            } else if (valid) {
+                store_output<LANES, NV, WBF>(p, xs, acc, tok, sl);  // out_mode is RESIDUAL
+            }
+        }
     }
 }
 
@@ -290,13 +418,31 @@ __global__ __launch_bounds__(GENERIC_BLOCK) void generic_kernel(Params p) {
     for (int64_t slot = int64_t(blockIdx.x) * WAVES + wave; slot < p.n_tokens; slot += int64_t(gridDim.x) * WAVES) {
         const int64_t tok = slot;
         const int64_t xoff = tok * H;
+        // LayerNorm statistics of the token (norm = 1); u_h is formed on the fly below
+        float mean = 0.0f, rstd = 1.0f;
+        if (p.norm) {
+            float s = 0.0f;
+            for (int h = lane; h < H; h += 64) s += load_elem<XBF>(p.x, xoff + h);
+            mean = group_sum<64>(s) / float(H);
+            float q = 0.0f;
+            for (int h = lane; h < H; h += 64) {
+                const float d = load_elem<XBF>(p.x, xoff + h) - mean;
+                q = __builtin_fmaf(d, d, q);
+            }
+            rstd = 1.0f / sqrtf(group_sum<64>(q) / float(H) + p.norm_eps);
+        }
+        auto input = [&](int h) {
+            const float v = load_elem<XBF>(p.x, xoff + h);
+            if (!p.norm) return v;
+            return __builtin_fmaf((v - mean) * rstd, p.gamma ? p.gamma[h] : 1.0f, p.beta ? p.beta[h] : 0.0f);
+        };
         for (int t = 0; t < T; ++t) {
             int64_t n = 0;
             for (int l = 0; l <= D; ++l) {
                 const int64_t woff = (int64_t(t) * N + n) * H;
                 float part = 0.0f;
                 for (int h = lane; h < H; h += 64)
-                    part = __builtin_fmaf(load_elem<XBF>(p.x, xoff + h), load_elem<WBF>(p.w_in, woff + h), part);
+                    part = __builtin_fmaf(input(h), load_elem<WBF>(p.w_in, woff + h), part);
                 const float logit = group_sum<64>(part);
                 const float a = activation(logit, p.act);
                 const int idx = t * (D + 1) + l;
@@ -355,15 +501,22 @@ struct Variant {
     const void* descent;
     const void* walk;
     const void* emit;
+    const void* stack;
+    // LayerNorm prologue: x widened to fp32 whatever its storage type
+    const void* descent_norm;
+    const void* walk_norm;
+    const void* stack_norm;
     const char* name;
 };
 
-#define FFF_VARIANT(H, XB, WB, L, NV)                                                        \
-    Variant {                                                                                \
-        H, XB, WB, L, reinterpret_cast<const void*>(&descent_kernel<L, NV, XB, WB, BLOCK>),  \
-            reinterpret_cast<const void*>(&walk_kernel<L, NV, XB, WB, BLOCK>),               \
-            reinterpret_cast<const void*>(&emit_kernel<L, NV, XB, WB, BLOCK>),               \
-            "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                             \
+#define FFF_K(...) reinterpret_cast<const void*>(&__VA_ARGS__)
+#define FFF_VARIANT(H, XB, WB, L, NV)                                                                         \
+    Variant {                                                                                                 \
+        H, XB, WB, L, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                     \
+            FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<L, NV, XB, WB, BLOCK>),        \
+            FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
+            FFF_K(walk_kernel<L, NV, false, WB, BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
+            "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
     }
 
 static const Variant kVariants[] = {
@@ -445,12 +598,18 @@ size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees,
     return align256(recs * size_t(depth + 1) * sizeof(float)) + align256(recs * sizeof(int32_t));
 }
 
+static const Variant* find_variant(const Params& p) {
+    for (const auto& c : kVariants)
+        if (c.hidden == p.hidden && c.xbf == bool(p.x_bf16) && c.wbf == bool(p.w_bf16)) return &c;
+    return nullptr;
+}
+
+static int64_t token_groups(const Params& p, int lanes) { return (p.n_tokens + 64 / lanes - 1) / (64 / lanes); }
+
 int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, bool have_workspace,
                  const DeviceInfo& dev, Plan* plan) {
     *plan = Plan{};
-    const Variant* v = nullptr;
-    for (const auto& c : kVariants)
-        if (c.hidden == p.hidden && c.xbf == bool(p.x_bf16) && c.wbf == bool(p.w_bf16)) v = &c;
+    const Variant* v = find_variant(p);
     if ((mode == MODE_DESCENT || mode == MODE_GROUPED) && !v) return ST_UNSUPPORTED;
     if (mode == MODE_AUTO) {
         // Measured on MI355X: the two-kernel grouped path wins for single trees with 16/32-lane
@@ -469,10 +628,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         plan->lds_levels = k;
         plan->name = v->name;
         Launch& L = plan->launch[plan->n_launch++];
-        L.kernel = v->descent;
+        L.kernel = p.norm ? v->descent_norm : v->descent;
         L.block = BLOCK;
         L.lds_bytes = rows_lds_bytes(p, k, 2);
-        const int64_t groups = (p.n_tokens + 64 / v->lanes - 1) / (64 / v->lanes);
+        const int64_t groups = token_groups(p, v->lanes);
         L.grid = resident_grid(dev, L.kernel, L.lds_bytes, (groups + BLOCK / 64 - 1) / (BLOCK / 64));
         return ST_OK;
     }
@@ -490,10 +649,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         plan->lds_levels = kw;
         plan->split_level = split;
         plan->name = v->name;
-        const int64_t groups = (p.n_tokens + 64 / v->lanes - 1) / (64 / v->lanes);
+        const int64_t groups = token_groups(p, v->lanes);
         const int64_t want = (groups + BLOCK / 64 - 1) / (BLOCK / 64);
         Launch& W = plan->launch[plan->n_launch++];
-        W.kernel = v->walk;
+        W.kernel = p.norm ? v->walk_norm : v->walk;
         W.block = BLOCK;
         W.lds_bytes = rows_lds_bytes(p, kw, 1);
         W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want);
@@ -519,6 +678,33 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     L.lds_bytes = size_t(GENERIC_BLOCK / 64) * 2 * size_t(pairs) * 4;
     L.grid = resident_grid(dev, L.kernel, L.lds_bytes, (p.n_tokens + GENERIC_BLOCK / 64 - 1) / (GENERIC_BLOCK / 64));
     return ST_OK;
+}
+
+int plan_stack(const Params& p, int lds_levels_req, const DeviceInfo& dev, Plan* plan) {
+    *plan = Plan{};
+    const Variant* v = find_variant(p);
+    if (!v) return ST_UNSUPPORTED;
+    bool ok;
+    const int k = pick_levels(p, lds_levels_req, 2, DESCENT_LDS_BUDGET, dev.lds_per_block, &ok);
+    if (!ok) return ST_UNSUPPORTED;
+    plan->kind = KIND_STACK;
+    plan->lanes = v->lanes;
+    plan->lds_levels = k;
+    plan->name = v->name;
+    Launch& L = plan->launch[plan->n_launch++];
+    L.kernel = p.norm ? v->stack_norm : v->stack;
+    L.block = BLOCK;
+    L.lds_bytes = rows_lds_bytes(p, k, 2);
+    L.grid = resident_grid(dev, L.kernel, L.lds_bytes, (token_groups(p, v->lanes) + BLOCK / 64 - 1) / (BLOCK / 64));
+    return ST_OK;
+}
+
+hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream) {
+    StackParams q = sp;
+    q.p.lds_levels = plan.lds_levels;
+    const Launch& L = plan.launch[0];
+    void* args[] = {&q};
+    return hipLaunchKernel(L.kernel, dim3(L.grid), dim3(L.block), args, L.lds_bytes, stream);
 }
 
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,

@@ -20,6 +20,7 @@ FFF_F32, FFF_BF16 = 0, 1
 ACTS = {"gelu": 0, "gelu_erf": 0, "gelu_tanh": 1, "identity": 2}
 MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3}
 OUTS = {"store": 0, "accumulate": 1, "residual": 2}
+NORMS = {None: 0, "none": 0, "layernorm": 1}
 _TORCH_DT = {torch.float32: FFF_F32, torch.bfloat16: FFF_BF16}
 
 
@@ -35,7 +36,14 @@ class FffArgs(ctypes.Structure):
         ("nodes_out", c_void_p), ("logits_out", c_void_p),
         ("workspace", c_void_p), ("workspace_bytes", c_size_t),
         ("hip_stream", c_void_p),
+        ("norm", c_int32), ("norm_eps", ctypes.c_float), ("norm_gamma", c_void_p), ("norm_beta", c_void_p),
     ]
+
+
+class FffLayer(ctypes.Structure):
+    """Mirror of ``fff_layer`` in include/fff.h."""
+
+    _fields_ = [("W_in", c_void_p), ("W_out", c_void_p), ("norm_gamma", c_void_p), ("norm_beta", c_void_p)]
 
 
 class FffError(RuntimeError):
@@ -46,8 +54,8 @@ class FffError(RuntimeError):
 
 _lib = None
 
-EXPORTS = ("fff_forward", "fff_forward_ex", "fff_workspace_bytes", "fff_describe", "fff_status_str",
-           "fff_last_hip_error", "fff_version")
+EXPORTS = ("fff_forward", "fff_forward_ex", "fff_workspace_bytes", "fff_describe", "fff_forward_stack",
+           "fff_describe_stack", "fff_status_str", "fff_last_hip_error", "fff_version")
 
 
 def load_library(path: Path | str | None = None):
@@ -68,6 +76,11 @@ def load_library(path: Path | str | None = None):
     lib.fff_workspace_bytes.restype = c_size_t
     lib.fff_describe.argtypes = [ctypes.POINTER(FffArgs), c_char_p, c_size_t]
     lib.fff_describe.restype = c_int
+    lib.fff_forward_stack.argtypes = [ctypes.POINTER(FffArgs), ctypes.POINTER(FffLayer), c_int32]
+    lib.fff_forward_stack.restype = c_int
+    lib.fff_describe_stack.argtypes = [ctypes.POINTER(FffArgs), ctypes.POINTER(FffLayer), c_int32, c_char_p,
+                                       c_size_t]
+    lib.fff_describe_stack.restype = c_int
     lib.fff_status_str.argtypes = [c_int]
     lib.fff_status_str.restype = c_char_p
     lib.fff_last_hip_error.argtypes = []
@@ -108,38 +121,62 @@ def _dev_tensor(t, what, device):
     return t
 
 
-def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out="store", lds_levels=0,
-              split_level=0, nodes_out=None, logits_out=None, workspace=None, stream=None) -> FffArgs:
-    """Validate tensor-level properties and fill an ``fff_args``."""
-    if not isinstance(x, torch.Tensor) or x.dim() != 2:
-        raise ValueError("x must be a 2-D tensor [n_tokens, hidden]")
-    device = x.device
-    if device.type != "cuda":
-        raise ValueError("x must be a GPU tensor")
-    for t, what in ((w_in, "W_in"), (w_out, "W_out"), (y, "y")):
+def _check_weights(w_in, w_out, depth, n_trees, H, device):
+    for t, what in ((w_in, "W_in"), (w_out, "W_out")):
         _dev_tensor(t, what, device)
-    _dev_tensor(x, "x", device)
-    B, H = x.shape
     N = (1 << (depth + 1)) - 1
     if tuple(w_in.shape) != (n_trees, N, H) or tuple(w_out.shape) != (n_trees, N, H):
         raise ValueError(f"W_in/W_out must be [{n_trees}, {N}, {H}], got {tuple(w_in.shape)}, {tuple(w_out.shape)}")
     if w_in.dtype != w_out.dtype:
         raise ValueError("W_in and W_out must share a dtype")
+
+
+def _check_norm_param(t, what, H, device):
+    if t is None:
+        return None
+    _dev_tensor(t, what, device)
+    if t.dtype != torch.float32 or t.numel() != H:
+        raise ValueError(f"{what} must be a float32 tensor of {H} elements")
+    return t.data_ptr()
+
+
+def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out="store", lds_levels=0,
+              split_level=0, nodes_out=None, logits_out=None, workspace=None, stream=None, norm=None,
+              norm_eps=1e-12, norm_gamma=None, norm_beta=None, n_layers=1) -> FffArgs:
+    """Validate tensor-level properties and fill an ``fff_args``.  ``w_in`` / ``w_out`` may be None
+    (stacks pass their weights per layer); records then hold ``n_layers`` layers."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x must be a 2-D tensor [n_tokens, hidden]")
+    device = x.device
+    if device.type != "cuda":
+        raise ValueError("x must be a GPU tensor")
+    _dev_tensor(y, "y", device)
+    _dev_tensor(x, "x", device)
+    B, H = x.shape
+    if w_in is not None or w_out is not None:
+        _check_weights(w_in, w_out, depth, n_trees, H, device)
     if tuple(y.shape) != (B, H):
         raise ValueError(f"y must be [{B}, {H}], got {tuple(y.shape)}")
     for t, what in ((nodes_out, "nodes_out"), (logits_out, "logits_out")):
         if t is not None:
             _dev_tensor(t, what, device)
-            if t.numel() != B * n_trees * (depth + 1):
-                raise ValueError(f"{what} must hold n_tokens*n_trees*(depth+1) elements")
+            if t.numel() != n_layers * B * n_trees * (depth + 1):
+                raise ValueError(f"{what} must hold n_layers*n_tokens*n_trees*(depth+1) elements")
     if nodes_out is not None and nodes_out.dtype != torch.int32:
         raise ValueError("nodes_out must be int32")
     if logits_out is not None and logits_out.dtype != torch.float32:
         raise ValueError("logits_out must be float32")
     a = FffArgs()
-    a.x, a.W_in, a.W_out, a.y = x.data_ptr(), w_in.data_ptr(), w_out.data_ptr(), y.data_ptr()
+    a.x, a.y = x.data_ptr(), y.data_ptr()
+    if w_in is not None:
+        a.W_in, a.W_out = w_in.data_ptr(), w_out.data_ptr()
+        a.w_dtype = _dt(w_in, "W_in")
     a.n_tokens, a.hidden, a.depth, a.n_trees = B, H, depth, n_trees
-    a.x_dtype, a.w_dtype, a.y_dtype = _dt(x, "x"), _dt(w_in, "W_in"), _dt(y, "y")
+    a.x_dtype, a.y_dtype = _dt(x, "x"), _dt(y, "y")
+    a.norm = NORMS[norm] if norm is None or isinstance(norm, str) else int(norm)
+    a.norm_eps = float(norm_eps)
+    a.norm_gamma = _check_norm_param(norm_gamma, "norm_gamma", H, device)
+    a.norm_beta = _check_norm_param(norm_beta, "norm_beta", H, device)
     a.act = ACTS[act] if isinstance(act, str) else int(act)
     a.mode = MODES[mode] if isinstance(mode, str) else int(mode)
     a.out_mode = OUTS[out] if isinstance(out, str) else int(out)
@@ -183,6 +220,56 @@ def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=Non
     with torch.cuda.device(x.device):
         _check(lib.fff_forward_ex(ctypes.byref(a)))
     return y
+
+
+def _stack_args(x, layers, depth, n_trees, y, kw):
+    """fff_args and the fff_layer array of a stack; ``layers`` holds (W_in, W_out[, gamma[, beta]])."""
+    if not layers:
+        raise ValueError("a stack needs at least one layer")
+    H = x.shape[1]
+    arr = (FffLayer * len(layers))()
+    w_dt = None
+    for i, lay in enumerate(layers):
+        w_in, w_out = lay[0], lay[1]
+        gamma = lay[2] if len(lay) > 2 else None
+        beta = lay[3] if len(lay) > 3 else None
+        _check_weights(w_in, w_out, depth, n_trees, H, x.device)
+        if w_dt is None:
+            w_dt = w_in.dtype
+        elif w_in.dtype != w_dt:
+            raise ValueError("every layer's weights must share a dtype")
+        arr[i].W_in, arr[i].W_out = w_in.data_ptr(), w_out.data_ptr()
+        arr[i].norm_gamma = _check_norm_param(gamma, f"layer {i} gamma", H, x.device)
+        arr[i].norm_beta = _check_norm_param(beta, f"layer {i} beta", H, x.device)
+    kw.setdefault("out", "residual")
+    a = make_args(x, None, None, depth, n_trees, y, n_layers=len(layers), **kw)
+    a.w_dtype = _TORCH_DT[w_dt]
+    return a, arr
+
+
+def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
+    """Layers x <- x + FFF_i(norm_i(x)) through ``fff_forward_stack``; returns y (allocated if not given,
+    of x's dtype; y may be x itself).  ``layers``: sequence of (W_in, W_out[, gamma[, beta]])."""
+    if y is None:
+        y = torch.empty_like(x)
+    if kw.get("mode", "auto") in ("grouped", 2) and kw.get("workspace") is None:
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+    a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
+    with torch.cuda.device(x.device):
+        _check(load_library().fff_forward_stack(ctypes.byref(a), arr, len(layers)))
+    return y
+
+
+def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str:
+    if y is None:
+        y = torch.empty_like(x)
+    if kw.get("mode", "auto") in ("grouped", 2) and kw.get("workspace") is None:
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+    a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
+    buf = ctypes.create_string_buffer(512)
+    with torch.cuda.device(x.device):
+        _check(load_library().fff_describe_stack(ctypes.byref(a), arr, len(layers), buf, len(buf)))
+    return buf.value.decode()
 
 
 def forward_plain(x, w_in, w_out, depth: int, n_trees: int, y, stream=None):

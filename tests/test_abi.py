@@ -56,7 +56,7 @@ def test_struct_layout_matches_c(tmp_path):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fff_version() == 100
+    assert lib.fff_version() == 101
     for rc in (0, -1, -2, -3, -4):
         assert lib.fff_status_str(rc).decode().startswith("FFF_")
     assert lib.fff_status_str(7) == b"unknown fff status"
@@ -85,6 +85,13 @@ def good_args(**over):
     dict(nodes_out=P * 64 + 16),              # overlaps y
     dict(nodes_out=P * 256, logits_out=P * 256 + 16),
     dict(n_tokens=1 << 62),                   # size overflow
+    dict(y=P * 16 + 64),                      # output overlaps the weights
+    dict(nodes_out=P + 32),                   # records overlap x
+    dict(y=P, y_dtype=1),                     # in place needs one dtype
+    dict(norm=2), dict(norm=1, norm_eps=-1.0), dict(norm=1, norm_eps=float("nan")),
+    dict(norm=1, norm_eps=float("inf")),
+    dict(norm=1, norm_gamma=P * 128 + 4),     # misaligned gain
+    dict(norm=1, norm_beta=P * 64 + 256),     # shift overlaps y
 ])
 def test_invalid_arguments_rejected_before_hip(lib, over):
     a = good_args(**over)
@@ -113,3 +120,49 @@ def test_workspace_bytes_rejects_bad_shapes(lib):
 def test_build_flags_disable_packed_fp32():
     flags = " ".join(native_build.COMMON)
     assert "-packed-fp32-ops" in flags and "--offload-arch=gfx950" in flags
+
+
+def stack_args(**over):
+    a = good_args(out_mode=binding.OUTS["residual"])
+    a.W_in = a.W_out = None
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+def layers(n, **over):
+    arr = (binding.FffLayer * max(n, 1))()
+    for i in range(n):
+        arr[i].W_in, arr[i].W_out = P * (16 + 8 * i), P * (20 + 8 * i)
+        for k, v in over.items():
+            setattr(arr[i], k, v)
+    return arr
+
+
+@pytest.mark.parametrize("over,lover,n", [
+    ({}, {}, 0),                                            # no layers
+    (dict(W_in=P * 16), {}, 2),                             # weights come from the layer table
+    (dict(norm_gamma=P * 128), {}, 2),
+    (dict(out_mode=0), {}, 2),                              # a stack is residual
+    (dict(y_dtype=1), {}, 2),                               # one residual-stream dtype
+    ({}, dict(W_out=None), 2),
+    ({}, dict(W_in=P * 16 + 8), 2),
+    (dict(norm=1), dict(norm_gamma=P * 128 + 4), 2),
+    ({}, dict(W_in=P * 64), 2),                             # weights overlap y
+    (dict(nodes_out=P * 256, logits_out=P * 256 + 4 * 4 * 4 * 2), {}, 3),  # records of 3 layers overlap
+])
+def test_stack_invalid_arguments(lib, over, lover, n):
+    a = stack_args(**over)
+    arr = layers(n, **lover)
+    assert lib.fff_forward_stack(ctypes.byref(a), arr, n) == binding.FFF_ERR_INVALID_ARG
+    buf = ctypes.create_string_buffer(64)
+    assert lib.fff_describe_stack(ctypes.byref(a), arr, n, buf, len(buf)) == binding.FFF_ERR_INVALID_ARG
+    assert lib.fff_last_hip_error() == 0
+
+
+def test_stack_null_table_and_zero_tokens(lib):
+    a = stack_args()
+    assert lib.fff_forward_stack(ctypes.byref(a), None, 2) == binding.FFF_ERR_INVALID_ARG
+    assert lib.fff_forward_stack(None, layers(1), 1) == binding.FFF_ERR_INVALID_ARG
+    a.n_tokens = 0
+    assert lib.fff_forward_stack(ctypes.byref(a), layers(3), 3) == binding.FFF_OK

@@ -284,5 +284,10 @@ def test_errors_surface_as_exceptions(fff_lib):
         fff_lib.forward(x, wi, wo, 3, 1, lds_levels=9)  # more levels than the tree has
     with pytest.raises(ValueError):
         fff_lib.forward(x, wi[:, :7], wo, 3, 1)
+    buf = torch.zeros(17 * 768, device=DEV)
+    xb = buf[:16 * 768].view(16, 768)
+    xb.copy_(x)
     with pytest.raises(fff_lib.FffError):
-        fff_lib.forward(x, wi, wo, 3, 1, y=x)  # x and y overlap
+        fff_lib.forward(xb, wi, wo, 3, 1, y=buf[768:].view(16, 768))  # y overlaps x without being x
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x[:8], wi, wo, 3, 1, y=wi.view(-1)[:8 * 768].view(8, 768))  # y overlaps W_in

@@ -94,3 +94,25 @@ def test_conditioning_allowance_only_covers_logit_rounding():
     # 1000 units is not rounding
     y_bad = ref["y"] + slope * 250 * dl * w_out[0, 0]
     assert not parity.check(x, w_in, w_out, 0, 1, ref, y_bad, ref["nodes"])["ok"]
+
+
+def test_bf16_total_excess_accepts_rounding_and_rejects_a_spacing_error():
+    """The residual-output bound: rounding of x + f passes; an error of two spacings fails; tiny totals
+    are judged against the FFF bar, not their own spacing."""
+    from paper_2311_10770_amd import synth
+
+    rng = np.random.default_rng(7)
+    x = synth.as_dtype(rng.standard_normal((50, 64)).astype(np.float32), "bf16")
+    f = rng.standard_normal((50, 64)) * 0.1
+    total = parity.widen(x) + f
+    stored = oracle.round_bf16(total)
+    assert parity.bf16_total_excess(stored, total, f, 1e-5) <= 0.5 + 1e-9
+    bad = stored.copy()
+    bad[3, 5] = np.uint16(int(bad[3, 5]) + 2)  # two spacings off (same binade)
+    assert parity.bf16_total_excess(bad, total, f, 1e-5) > 1.0
+    # a total that cancels to ~1e-9: one bf16 spacing there is tiny, the FFF bar (1e-5 ||f||) is not
+    t2 = total.copy()
+    t2[0, 0] = 1e-9
+    s2 = oracle.round_bf16(t2)
+    s2[0, 0] = oracle.round_bf16(np.array([1e-9 + 1e-6]))[0]
+    assert parity.bf16_total_excess(s2, t2, f, 1e-5) <= 1.0
