@@ -7,7 +7,8 @@ path (``paper_2311_10770_amd``) and neither imports the other.
 The arithmetic lives in ``fff_oracle.c`` (plain C, fp64, built with gcc into
 ``liboracle.so``); this module only marshals numpy arrays.  Inputs are numpy
 arrays: float32, or uint16 holding bf16 bit patterns (the FFF input may also
-be float64, e.g. the output of ``layer_norm``).
+be float64, e.g. the output of ``layer_norm``, and so may the weights of
+the finite-difference pins).
 """
 from __future__ import annotations
 
@@ -61,6 +62,11 @@ def _load():
     lib.oracle_layer_norm.restype = ctypes.c_int
     lib.oracle_round_bf16.argtypes = [vp, i64, vp]
     lib.oracle_round_bf16.restype = ctypes.c_int
+    lib.oracle_activation_grad.argtypes = [dbl, ctypes.c_int]
+    lib.oracle_activation_grad.restype = dbl
+    lib.oracle_backward.argtypes = [vp, ctypes.c_int, vp, vp, ctypes.c_int, vp, vp, i64, i32, i32, i32,
+                                    ctypes.c_int, vp, vp, vp]
+    lib.oracle_backward.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -87,6 +93,10 @@ def activation(z: float, act="gelu") -> float:
     return _load().oracle_activation(float(z), _act(act))
 
 
+def activation_grad(z: float, act="gelu") -> float:
+    return _load().oracle_activation_grad(float(z), _act(act))
+
+
 def default_threads() -> int:
     try:
         return max(1, len(os.sched_getaffinity(0)))
@@ -107,8 +117,6 @@ def forward(x: np.ndarray, w_in: np.ndarray, w_out: np.ndarray, depth: int, n_tr
     w_out = np.ascontiguousarray(w_out)
     if w_in.dtype != w_out.dtype:
         raise TypeError("W_in and W_out must share a dtype")
-    if w_in.dtype == np.float64:
-        raise TypeError("weights are float32 or bf16 bits")
     B, H = x.shape
     N = (1 << (depth + 1)) - 1
     if w_in.shape != (n_trees, N, H) or w_out.shape != (n_trees, N, H):
@@ -220,3 +228,30 @@ def stack(x: np.ndarray, layers, depth: int, n_trees: int, store_dtype: str, nor
         r["x_out"] = x
         outs.append(r)
     return outs
+
+
+def backward(x: np.ndarray, w_in: np.ndarray, w_out: np.ndarray, depth: int, n_trees: int, dy: np.ndarray,
+             path: np.ndarray, act="gelu") -> dict:
+    """Hard-routed backward in fp64 along the given paths [B, T, D+1].
+
+    Returns ``dx`` [B,H], ``dw_in`` and ``dw_out`` [T,N,H] (float64; rows off
+    every path are zero)."""
+    x = np.ascontiguousarray(x)
+    w_in = np.ascontiguousarray(w_in)
+    w_out = np.ascontiguousarray(w_out)
+    B, H = x.shape
+    N = (1 << (depth + 1)) - 1
+    if w_in.shape != (n_trees, N, H) or w_out.shape != (n_trees, N, H) or w_in.dtype != w_out.dtype:
+        raise ValueError("weights must be [T, N, H] of one dtype")
+    dy = np.ascontiguousarray(_widen(dy).reshape(B, H))
+    path = np.ascontiguousarray(path, dtype=np.int32).reshape(B, n_trees, depth + 1)
+    dx = np.empty((B, H))
+    dwi = np.empty((n_trees, N, H))
+    dwo = np.empty((n_trees, N, H))
+    rc = _load().oracle_backward(_ptr(x), _dtype_code(x), _ptr(w_in), _ptr(w_out), _dtype_code(w_in), _ptr(dy),
+                                 _ptr(path), B, H, depth, n_trees, _act(act), _ptr(dx), _ptr(dwi), _ptr(dwo))
+    if rc == -3:
+        raise ValueError("a path is not a root-to-leaf walk")
+    if rc != 0:
+        raise RuntimeError(f"oracle_backward failed with {rc}")
+    return {"dx": dx, "dw_in": dwi, "dw_out": dwo}

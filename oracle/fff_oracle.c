@@ -142,7 +142,7 @@ static int check_common(const void* w_in, const void* w_out, int x_dtype, int w_
                         int32_t hidden, int32_t depth, int32_t n_trees, int act) {
     if (!w_in || !w_out) return -1;
     if ((x_dtype != OR_F32 && x_dtype != OR_BF16 && x_dtype != OR_F64) ||
-        (w_dtype != OR_F32 && w_dtype != OR_BF16))
+        (w_dtype != OR_F32 && w_dtype != OR_BF16 && w_dtype != OR_F64))
         return -1;
     if (hidden < 1 || depth < 0 || depth > 30 || n_trees < 1) return -1;
     if (act < OR_ACT_GELU_ERF || act > OR_ACT_IDENTITY) return -1;
@@ -292,5 +292,85 @@ int oracle_round_bf16(const double* in, int64_t n, uint16_t* out) {
         if (isnan(v)) bits = 0x7FC00000u;
         out[k] = (uint16_t)(bits >> 16);
     }
+    return 0;
+}
+
+/* d act / dz: GELU'(z) = Phi(z) + z phi(z) with phi the standard normal
+ * density; the tanh form's derivative follows from d tanh(u) = 1 - tanh(u)^2;
+ * identity: 1. */
+double oracle_activation_grad(double z, int act) {
+    if (act == OR_ACT_GELU_ERF)
+        return 0.5 * (1.0 + erf(z / sqrt(2.0))) + z * exp(-0.5 * z * z) / sqrt(2.0 * 3.14159265358979323846);
+    if (act == OR_ACT_GELU_TANH) {
+        const double c = sqrt(2.0 / 3.14159265358979323846);
+        const double u = c * (z + 0.044715 * z * z * z);
+        const double t = tanh(u);
+        return 0.5 * (1.0 + t) + 0.5 * z * (1.0 - t * t) * c * (1.0 + 3.0 * 0.044715 * z * z);
+    }
+    return 1.0;
+}
+
+/* Backward of the layer with the routing held fixed (hard routing): the tree
+ * walk's branch decisions are not differentiable, so gradients flow only
+ * through the D+1 visited nodes of every (token, tree).  With the given path
+ * n_l, logits l_l = <x_b, W_in[t,n_l]> and a_l = act(l_l), y_b = sum a_l
+ * W_out[t,n_l], and the upstream gradient dy_b:
+ *   dW_out[t,n_l] += a_l dy_b
+ *   da_l           = <dy_b, W_out[t,n_l]>
+ *   dl_l           = da_l act'(l_l)
+ *   dW_in[t,n_l]  += dl_l x_b
+ *   dx_b          += dl_l W_in[t,n_l]
+ * path is [B, T, D+1] and must be root-to-leaf walks; dy, dx are [B,H] and
+ * dw_in, dw_out [T,N,H], all double, overwritten (rows off every path are
+ * zero); dx, dw_in or dw_out may be NULL.  The logits are recomputed here
+ * from x and W_in.  Single-threaded.  Returns 0, -1 on bad arguments, -2 on
+ * allocation failure, -3 if a path is not a root-to-leaf walk. */
+int oracle_backward(const void* x, int x_dtype, const void* w_in, const void* w_out, int w_dtype,
+                    const double* dy, const int32_t* path, int64_t n_tokens, int32_t hidden, int32_t depth,
+                    int32_t n_trees, int act, double* dx, double* dw_in, double* dw_out) {
+    if (check_common(w_in, w_out, x_dtype, w_dtype, hidden, depth, n_trees, act)) return -1;
+    if (n_tokens < 0 || ((!x || !dy || !path) && n_tokens > 0)) return -1;
+    const int32_t H = hidden, D = depth, T = n_trees;
+    const int64_t N = ((int64_t)1 << (D + 1)) - 1;
+    for (int64_t b = 0; b < n_tokens; ++b)
+        for (int32_t t = 0; t < T; ++t) {
+            const int32_t* p = path + (b * T + t) * (D + 1);
+            if (p[0] != 0) return -3;
+            for (int32_t l = 1; l <= D; ++l)
+                if (p[l] != 2 * p[l - 1] + 1 && p[l] != 2 * p[l - 1] + 2) return -3;
+        }
+    if (dw_in) memset(dw_in, 0, sizeof(double) * (size_t)(T * N * H));
+    if (dw_out) memset(dw_out, 0, sizeof(double) * (size_t)(T * N * H));
+    double* xr = (double*)malloc(sizeof(double) * (size_t)H);
+    double* wi = (double*)malloc(sizeof(double) * (size_t)H);
+    double* wo = (double*)malloc(sizeof(double) * (size_t)H);
+    if (!xr || !wi || !wo) {
+        free(xr); free(wi); free(wo);
+        return -2;
+    }
+    for (int64_t b = 0; b < n_tokens; ++b) {
+        widen_row(x, x_dtype, b * H, H, xr);
+        const double* g = dy + b * H;
+        double* dxr = dx ? dx + b * H : NULL;
+        if (dxr)
+            for (int32_t i = 0; i < H; ++i) dxr[i] = 0.0;
+        for (int32_t t = 0; t < T; ++t) {
+            const int32_t* p = path + (b * T + t) * (D + 1);
+            for (int32_t l = 0; l <= D; ++l) {
+                const int64_t row = ((int64_t)t * N + p[l]) * H;
+                widen_row(w_in, w_dtype, row, H, wi);
+                widen_row(w_out, w_dtype, row, H, wo);
+                const double logit = dot(xr, wi, H);
+                const double a = oracle_activation(logit, act);
+                const double dl = dot(g, wo, H) * oracle_activation_grad(logit, act);
+                for (int32_t i = 0; i < H; ++i) {
+                    if (dw_out) dw_out[row + i] += a * g[i];
+                    if (dw_in) dw_in[row + i] += dl * xr[i];
+                    if (dxr) dxr[i] += dl * wi[i];
+                }
+            }
+        }
+    }
+    free(xr); free(wi); free(wo);
     return 0;
 }

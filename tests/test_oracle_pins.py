@@ -342,8 +342,8 @@ def test_rejects_bad_arguments():
         oracle.forward(x, w, w, 1, 1)  # wrong node count for depth 1
     with pytest.raises(TypeError):
         oracle.forward(x.astype(np.float16), w, w, 2, 1)
-    with pytest.raises(TypeError):  # fp64 is accepted for the input only (a LayerNorm output)
-        oracle.forward(x, w.astype(np.float64), w.astype(np.float64), 2, 1)
+    with pytest.raises(TypeError):
+        oracle.forward(x, w.astype(np.int32), w.astype(np.int32), 2, 1)
     assert oracle.forward(np.zeros((0, 4), np.float32), w, w, 2, 1)["y"].shape == (0, 4)
 
 
