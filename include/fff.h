@@ -192,6 +192,63 @@ typedef struct {
  */
 int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers);
 
+/*
+ * fff_backward -- gradients of one layer with the routing held fixed (hard
+ * routing: the branch decisions are not differentiable, so gradients flow
+ * through the D+1 visited nodes of every (token, tree) only; the training
+ * method that learns the routing is the original FFF paper's, cited in
+ * Section 2).  With the forward's leaves (path) and logits l, a = act(l),
+ * and dy = dLoss/dFFF(x):
+ *     dW_out[t,n] += a  * dy_b          for every visited node n
+ *     dl           = <dy_b, W_out[t,n]> * act'(l)
+ *     dW_in[t,n]  += dl * x_b
+ *     dx_b        += dl * W_in[t,n]
+ * (x is the FFF input; a residual or a LayerNorm around the layer is the
+ * caller's to differentiate).
+ *
+ * Work: a token kernel (dx and the per-visit pairs (a, dl)), a counting sort
+ * of the tokens by leaf (so that every node's tokens form one run at every
+ * level), and a weight kernel that sums each run in registers and adds it to
+ * dW with one fp32 atomic per element and run.  dx is deterministic; dW sums
+ * in an order that can vary from call to call (atomics), within fp32
+ * rounding.
+ */
+typedef struct {
+    const void* x;          /* [n_tokens, hidden] the layer's FFF input (x_dtype) */
+    const void* W_in;       /* [n_trees, N, hidden] (w_dtype) */
+    const void* W_out;
+    const void* dy;         /* [n_tokens, hidden] upstream gradient (dy_dtype) */
+    const int32_t* leaves;  /* [n_tokens, n_trees] leaf node reached: the forward's nodes_out[..., depth] */
+    const float* logits;    /* [n_tokens, n_trees, depth+1] the forward's logits_out */
+    void* dx;               /* [n_tokens, hidden] (dx_dtype), or NULL to skip */
+    float* dW_in;           /* [n_trees, N, hidden] fp32, or NULL to skip */
+    float* dW_out;          /* [n_trees, N, hidden] fp32, or NULL to skip */
+    int64_t n_tokens;
+    int32_t hidden;         /* a multiple of 4 */
+    int32_t depth;
+    int32_t n_trees;
+    int32_t x_dtype, w_dtype, dy_dtype, dx_dtype; /* fff_dtype */
+    int32_t act;            /* fff_act of the forward */
+    int32_t accumulate;     /* 0: dx, dW_in, dW_out overwritten (untouched dW rows become 0); 1: added to */
+    int32_t* bad_leaves;    /* optional device int32: incremented once per (token, tree) whose leaf is
+                               outside [2^depth - 1, 2^(depth+1) - 2]; such pairs contribute nothing */
+    void* workspace;        /* device scratch of fff_backward_workspace_bytes(), 256-byte aligned,
+                               disjoint from every other buffer */
+    size_t workspace_bytes;
+    void* hip_stream;
+} fff_backward_args;
+
+/* Every pointer is a caller-owned device pointer, 16-byte aligned (leaves,
+ * logits and bad_leaves 4-byte aligned); outputs overlap no input and no other
+ * output.  Validation runs before any HIP call; FFF_ERR_WORKSPACE when the
+ * workspace is missing or small.  Returns an fff_status. */
+int fff_backward(const fff_backward_args* a);
+
+/* Workspace fff_backward needs: per-visit pairs (8 bytes each), two int32
+ * arrays of 2^depth leaf bins per tree, one int32 token index per (token,
+ * tree), and per-tree totals.  0 for invalid shapes. */
+size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees);
+
 /* fff_describe for a stack. */
 int fff_describe_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers, char* buf, size_t len);
 

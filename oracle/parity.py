@@ -200,3 +200,120 @@ def bf16_total_excess(y_dev_bits: np.ndarray, total_ref: np.ndarray, fff_ref: np
     spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
     bound = spacing + tol * np.linalg.norm(np.asarray(fff_ref, dtype=np.float64), axis=1, keepdims=True)
     return float(np.max(np.abs(d - r) / bound))
+
+
+U32 = 2.0 ** -24  # fp32 unit roundoff
+
+
+def _act_grad_np(z, act):
+    from . import activation_grad
+    return np.vectorize(lambda v: activation_grad(float(v), act), otypes=[float])(z)
+
+
+def _act_np(z, act):
+    from . import activation
+    return np.vectorize(lambda v: activation(float(v), act), otypes=[float])(z)
+
+
+def backward_check(x, w_in, w_out, depth: int, n_trees: int, dy, path, logits_given, dev: dict, ref: dict,
+                   act="gelu", chunk: int = 2048) -> dict:
+    """Compare a device backward with the oracle's (both along ``path`` [B,T,D+1]).
+
+    Bounds are first order in the fp32 unit roundoff u and hold for ANY
+    summation order (atomics included): a sum of n terms computed in fp32 is
+    within (n-1) u sum|terms| of the exact one, and each term carries the error
+    of its coefficient:
+      a  = act(l):  |a_dev - a| <= |act'(l)| |l_given - l| + (8 + l^2) u |a|
+      dl = da act'(l), da = <dy, W_out[n]> (an fp32 dot):
+            |dl_dev - dl| <= |act'(l)| 64u ||dy|| ||W_out[n]|| + |da| e_g,
+            e_g = 0.8 |l_given - l| + (16 + l^2) u (Phi(l) + |l| phi(l))
+      The l^2 terms are erfc's condition number at -l/sqrt2 (about l^2 for
+      large |l|) applied to the rounding of its argument; e_g is absolute
+      because act' crosses zero; 0.8 bounds |act''| for GELU (the identity
+      has act'' = 0 and exact coefficients).
+    Per dW row: ||err|| <= sum_b [(n_row + 1) u |c_b| + e_b] ||v_b||  (v = dy or x);
+    per dx row: ||err|| <= sum_visits [(T(D+1) + 1) u |dl| + e_dl] ||W_in[n]||.
+    Also reports the largest error relative to sum_b |c_b| ||v_b|| (the scale
+    of the terms) and to the bound.
+    """
+    B, H = np.asarray(dy).shape
+    T, D = n_trees, depth
+    N = (1 << (D + 1)) - 1
+    xw = widen(x)
+    gw = widen(dy)
+    wi = w_in
+    wo = w_out
+    path = np.asarray(path).reshape(B, T, D + 1)
+    lg = np.asarray(logits_given, dtype=np.float64).reshape(B, T, D + 1)
+    s_out = np.zeros((T, N))
+    s_in = np.zeros((T, N))
+    b_out = np.zeros((T, N))
+    b_in = np.zeros((T, N))
+    cnt = np.zeros((T, N))
+    b_dx = np.zeros(B)
+    xn = np.linalg.norm(xw, axis=1)
+    gn = np.linalg.norm(gw, axis=1)
+    nwi, nwo = row_norms(wi), row_norms(wo)
+    for t in range(T):
+        np.add.at(cnt[t], path[:, t, :].reshape(-1), 1.0)
+    for b0 in range(0, B, chunk):
+        b1 = min(B, b0 + chunk)
+        for t in range(T):
+            nd = path[b0:b1, t, :]                            # [b, D+1]
+            rows_i = widen(wi[t][nd])                         # [b, D+1, H]
+            rows_o = widen(wo[t][nd])
+            l64 = np.einsum("bh,blh->bl", xw[b0:b1], rows_i)
+            da = np.einsum("bh,blh->bl", gw[b0:b1], rows_o)
+            g = _act_grad_np(l64, act)
+            a = _act_np(l64, act)
+            dl = da * g
+            dlg = np.abs(lg[b0:b1, t] - l64)
+            if act in ("identity", 2):
+                e_a = np.abs(g) * dlg
+                e_g = np.zeros_like(l64)
+            else:
+                pdf = np.exp(-0.5 * l64 * l64) / math.sqrt(2.0 * math.pi)
+                cdf = 0.5 * (1.0 + np.vectorize(math.erf, otypes=[float])(l64 / math.sqrt(2.0)))
+                e_a = np.abs(g) * dlg + (8 + l64 * l64) * U32 * np.abs(a)
+                e_g = 0.8 * dlg + (16 + l64 * l64) * U32 * (cdf + np.abs(l64) * pdf)
+            e_dl = np.abs(g) * 64 * U32 * gn[b0:b1, None] * nwo[t][nd] + np.abs(da) * e_g
+            n_row = cnt[t][nd]
+            co = ((n_row + 1) * U32 * np.abs(a) + e_a) * gn[b0:b1, None]
+            ci = ((n_row + 1) * U32 * np.abs(dl) + e_dl) * xn[b0:b1, None]
+            np.add.at(b_out[t], nd.reshape(-1), co.reshape(-1))
+            np.add.at(b_in[t], nd.reshape(-1), ci.reshape(-1))
+            np.add.at(s_out[t], nd.reshape(-1), (np.abs(a) * gn[b0:b1, None]).reshape(-1))
+            np.add.at(s_in[t], nd.reshape(-1), (np.abs(dl) * xn[b0:b1, None]).reshape(-1))
+            b_dx[b0:b1] += (((T * (D + 1) + 1) * U32 * np.abs(dl) + e_dl) * nwi[t][nd]).sum(axis=1)
+    rep = {"ok": True, "fail": []}
+    for name, bound, scale in (("dw_out", b_out, s_out), ("dw_in", b_in, s_in)):
+        if dev.get(name) is None:
+            continue
+        err = np.linalg.norm(widen(dev[name]) - ref[name], axis=2)
+        visited = cnt > 0
+        if np.any(widen(dev[name])[~visited] != 0):
+            rep["ok"] = False
+            rep["fail"].append(f"{name}: non-zero rows off every path")
+        bad = visited & (err > bound * 1.0000001)
+        if bad.any():
+            rep["ok"] = False
+            tt, nn = np.argwhere(bad)[0]
+            rep["fail"].append(f"{name}: {int(bad.sum())} rows past the bound, e.g. ({tt},{nn}) "
+                               f"err {err[tt, nn]:.3e} bound {bound[tt, nn]:.3e}")
+        rel = err[visited] / np.maximum(scale[visited], 1e-300)
+        rep[name + "_max_err_over_scale"] = float(rel.max()) if rel.size else 0.0
+        frac = err[visited] / np.maximum(bound[visited], 1e-300)
+        rep[name + "_max_err_over_bound"] = float(frac.max()) if frac.size else 0.0
+    if dev.get("dx") is not None:
+        err = np.linalg.norm(widen(dev["dx"]) - ref["dx"], axis=1)
+        bound = b_dx.copy()
+        if np.asarray(dev["dx"]).dtype == np.uint16:  # stored in bf16: half a spacing per element on top
+            bound += 2.0 ** -9 * np.linalg.norm(ref["dx"], axis=1) * 1.01
+        bad = err > bound * 1.0000001
+        if bad.any():
+            rep["ok"] = False
+            b = int(np.nonzero(bad)[0][0])
+            rep["fail"].append(f"dx: {int(bad.sum())} tokens past the bound, e.g. {b} err {err[b]:.3e} "
+                               f"bound {bound[b]:.3e}")
+        rep["dx_max_err_over_norm"] = float((err / np.maximum(np.linalg.norm(ref["dx"], axis=1), 1e-300)).max())
+    return rep

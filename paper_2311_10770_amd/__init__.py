@@ -5,6 +5,7 @@ The compute lives in ``libfff.so`` (HIP kernels behind the C ABI of
 synthetic-input generators and the named workloads.
 """
 from .fff import (  # noqa: F401
-    FffArgs, FffError, FffLayer, describe, describe_stack, forward, forward_plain, forward_stack, from_numpy,
-    load_library, make_args, status_str, to_numpy, version, workspace_bytes,
+    FffArgs, FffBackwardArgs, FffError, FffLayer, backward, backward_workspace_bytes, describe, describe_stack,
+    forward, forward_plain, forward_stack, from_numpy, load_library, make_args, status_str, to_numpy, version,
+    workspace_bytes,
 )

@@ -308,9 +308,116 @@ fff_args layer_args(const fff_args* a, const fff_layer* layers, int i) {
     return b;
 }
 
+// ---------------------------------------------------------------- backward
+
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+int validate_backward(const fff_backward_args* a, fff::BwdParams* p) {
+    if (!a) return FFF_ERR_INVALID_ARG;
+    if (a->n_tokens < 0 || a->hidden < 1 || a->hidden % 4 || a->depth < 0 || a->depth > kMaxDepth ||
+        a->n_trees < 1)
+        return FFF_ERR_INVALID_ARG;
+    for (int dt : {a->x_dtype, a->w_dtype, a->dy_dtype, a->dx_dtype})
+        if (dt != FFF_F32 && dt != FFF_BF16) return FFF_ERR_INVALID_ARG;
+    if (a->act < FFF_ACT_GELU_ERF || a->act > FFF_ACT_IDENTITY) return FFF_ERR_INVALID_ARG;
+    if (a->accumulate != 0 && a->accumulate != 1) return FFF_ERR_INVALID_ARG;
+    const int64_t nodes = (int64_t(1) << (a->depth + 1)) - 1;
+    int64_t act_elems = 0, w_rows = 0, w_elems = 0, pairs = 0, rec = 0, tmp = 0;
+    if (!mul_ok(a->n_tokens, a->hidden, &act_elems) || !mul_ok(act_elems, 4, &tmp)) return FFF_ERR_INVALID_ARG;
+    if (!mul_ok(nodes, a->n_trees, &w_rows) || !mul_ok(w_rows, a->hidden, &w_elems) || !mul_ok(w_elems, 4, &tmp))
+        return FFF_ERR_INVALID_ARG;
+    if (!mul_ok(a->n_tokens, a->n_trees, &pairs) || pairs > INT32_MAX) return FFF_ERR_INVALID_ARG;
+    if (!mul_ok(pairs, a->depth + 1, &rec) || !mul_ok(rec, 8, &tmp)) return FFF_ERR_INVALID_ARG;
+    if (w_rows > INT32_MAX) return FFF_ERR_INVALID_ARG;
+
+    *p = fff::BwdParams{};
+    if (a->n_tokens > 0) {
+        const bool need_x = a->dW_in != nullptr;
+        if (!a->W_in || !a->W_out || !a->dy || !a->leaves || !a->logits || (need_x && !a->x))
+            return FFF_ERR_INVALID_ARG;
+        for (const void* q : {a->x, a->W_in, a->W_out, a->dy, static_cast<const void*>(a->dx),
+                              static_cast<const void*>(a->dW_in), static_cast<const void*>(a->dW_out)})
+            if (q && !aligned16(q)) return FFF_ERR_INVALID_ARG;
+        for (const void* q : {static_cast<const void*>(a->leaves), static_cast<const void*>(a->logits),
+                              static_cast<const void*>(a->bad_leaves)})
+            if (q && !aligned4(q)) return FFF_ERR_INVALID_ARG;
+        const int64_t wbytes = w_elems * (a->w_dtype == FFF_BF16 ? 2 : 4);
+        const Span ins[] = {{a->x, act_elems * (a->x_dtype == FFF_BF16 ? 2 : 4)},
+                            {a->W_in, wbytes},
+                            {a->W_out, wbytes},
+                            {a->dy, act_elems * (a->dy_dtype == FFF_BF16 ? 2 : 4)},
+                            {a->leaves, pairs * 4},
+                            {a->logits, rec * 4}};
+        const Span outs[] = {{a->dx, act_elems * (a->dx_dtype == FFF_BF16 ? 2 : 4)},
+                             {a->dW_in, w_elems * 4},
+                             {a->dW_out, w_elems * 4},
+                             {a->bad_leaves, 4}};
+        for (int i = 0; i < 4; ++i) {
+            if (!outs[i].ptr) continue;
+            for (const Span& in : ins)
+                if (overlap(outs[i].ptr, outs[i].bytes, in.ptr, in.bytes)) return FFF_ERR_INVALID_ARG;
+            for (int j = i + 1; j < 4; ++j)
+                if (overlap(outs[i].ptr, outs[i].bytes, outs[j].ptr, outs[j].bytes)) return FFF_ERR_INVALID_ARG;
+        }
+        if (a->dW_in || a->dW_out) {
+            const size_t need = fff::bwd_workspace_bytes(a->n_tokens, a->depth, a->n_trees);
+            if (!a->workspace || a->workspace_bytes < need || (reinterpret_cast<uintptr_t>(a->workspace) & 255u))
+                return FFF_ERR_WORKSPACE;
+            for (const Span& q : ins)
+                if (overlap(a->workspace, int64_t(need), q.ptr, q.bytes)) return FFF_ERR_INVALID_ARG;
+            for (const Span& q : outs)
+                if (overlap(a->workspace, int64_t(need), q.ptr, q.bytes)) return FFF_ERR_INVALID_ARG;
+        }
+    }
+    p->x = a->x;
+    p->w_in = a->W_in;
+    p->w_out = a->W_out;
+    p->dy = a->dy;
+    p->leaves = a->leaves;
+    p->logits = a->logits;
+    p->dx = a->dx;
+    p->dw_in = a->dW_in;
+    p->dw_out = a->dW_out;
+    p->bad = a->bad_leaves;
+    p->n_tokens = a->n_tokens;
+    p->n_nodes = nodes;
+    p->hidden = a->hidden;
+    p->depth = a->depth;
+    p->n_trees = a->n_trees;
+    p->x_bf16 = a->x_dtype == FFF_BF16;
+    p->w_bf16 = a->w_dtype == FFF_BF16;
+    p->dy_bf16 = a->dy_dtype == FFF_BF16;
+    p->dx_bf16 = a->dx_dtype == FFF_BF16;
+    p->act = a->act;
+    p->accumulate = a->accumulate;
+    p->need_dw = (a->dW_in || a->dW_out) ? 1 : 0;
+    return FFF_OK;
+}
+
 }  // namespace
 
 FFF_EXPORT int fff_forward_ex(const fff_args* a) { return forward_one(a); }
+
+FFF_EXPORT int fff_backward(const fff_backward_args* a) {
+    fff::BwdParams p;
+    int rc = validate_backward(a, &p);
+    if (rc != FFF_OK) return rc;
+    if (a->n_tokens == 0 || (!a->dx && !a->dW_in && !a->dW_out)) return FFF_OK;
+    fff::DeviceInfo dev;
+    rc = current_device_info(&dev);
+    if (rc != FFF_OK) return rc;
+    if (p.need_dw) fff::bwd_workspace_views(p, a->workspace);
+    int status = FFF_OK;
+    const hipError_t e = fff::run_backward(p, dev, reinterpret_cast<hipStream_t>(a->hip_stream), &status);
+    if (status != FFF_OK) return status;
+    if (e != hipSuccess) return hip_fail(e);
+    return FFF_OK;
+}
+
+FFF_EXPORT size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees) {
+    if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1) return 0;
+    return fff::bwd_workspace_bytes(n_tokens, depth, n_trees);
+}
 
 FFF_EXPORT int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers) {
     fff::Params p;

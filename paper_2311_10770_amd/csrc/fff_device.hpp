@@ -63,14 +63,31 @@ __device__ __forceinline__ float group_sum(float v) {
 enum { ACT_GELU_ERF = 0, ACT_GELU_TANH = 1, ACT_IDENTITY = 2 };
 
 // GELU(z) = z * Phi(z) = z/2 * erfc(-z/sqrt 2); erfc keeps full relative
-// accuracy for negative z, where 1 + erf(z/sqrt 2) would cancel.
+// accuracy for negative z, where 1 + erf(z/sqrt 2) would cancel.  The tanh
+// approximation z/2 (1 + tanh u), u = sqrt(2/pi)(z + 0.044715 z^3), is
+// evaluated as z / (1 + exp(-2u)) (the same function, since
+// (1 + tanh u)/2 = 1/(1 + exp(-2u))), which does not cancel for negative z.
+__device__ __forceinline__ float gelu_tanh_u(float z) { return 0.79788456080286535588f * (z + 0.044715f * z * z * z); }
+
 __device__ __forceinline__ float activation(float z, int act) {
     if (act == ACT_GELU_ERF) return 0.5f * z * erfcf(-0.70710678118654752440f * z);
-    if (act == ACT_GELU_TANH) {
-        const float u = 0.79788456080286535588f * (z + 0.044715f * z * z * z);
-        return 0.5f * z * (1.0f + tanhf(u));
-    }
+    if (act == ACT_GELU_TANH) return z / (1.0f + expf(-2.0f * gelu_tanh_u(z)));
     return z;
+}
+
+// d act / dz.  GELU: Phi(z) + z phi(z) with phi the standard normal density.
+// Tanh form: with s = 1/(1 + exp(-2u)) and 1 - s = 1/(1 + exp(2u)),
+// d/dz [z s] = s + 2 z s (1 - s) du/dz.  Identity: 1.
+__device__ __forceinline__ float activation_grad(float z, int act) {
+    if (act == ACT_GELU_ERF)
+        return 0.5f * erfcf(-0.70710678118654752440f * z) + z * 0.39894228040143267794f * expf(-0.5f * z * z);
+    if (act == ACT_GELU_TANH) {
+        const float u = gelu_tanh_u(z);
+        const float s = 1.0f / (1.0f + expf(-2.0f * u));
+        const float sm = 1.0f / (1.0f + expf(2.0f * u));
+        return s + 2.0f * z * s * sm * 0.79788456080286535588f * (1.0f + 0.134145f * z * z);
+    }
+    return 1.0f;
 }
 
 }  // namespace fff

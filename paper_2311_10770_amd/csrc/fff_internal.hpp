@@ -57,6 +57,37 @@ struct StackParams {
     LayerPtrs layer[STACK_MAX_LAYERS];
 };
 
+// Backward (hard routing) argument block, passed by value.
+struct BwdParams {
+    const void* x;
+    const void* w_in;
+    const void* w_out;
+    const void* dy;
+    const int32_t* leaves;   // [B, T]
+    const float* logits;     // [B, T, D+1]
+    void* dx;                // [B, H] or null
+    float* dw_in;            // [T, N, H] or null
+    float* dw_out;           // [T, N, H] or null
+    int32_t* bad;            // optional counter of skipped (token, tree) pairs
+    int64_t n_tokens;
+    int64_t n_nodes;
+    int32_t hidden, depth, n_trees;
+    int32_t x_bf16, w_bf16, dy_bf16, dx_bf16;
+    int32_t act, accumulate;
+    // workspace views
+    float2* coef;            // [B, T, D+1]: (act(l), dLoss/dl) of every visit
+    int32_t* counts;         // [T, 2^D] tokens per leaf
+    int32_t* offs;           // [T, 2^D] first sorted position of each leaf, then the scatter cursor
+    int32_t* perm;           // [T, B] token indices sorted by leaf
+    int32_t* total;          // [T] valid (token, tree) pairs per tree
+    int32_t chunk;           // sorted tokens per wave in the weight kernel
+    int32_t need_dw;         // dW_in or dW_out requested
+};
+
+// Workspace of the backward; the views are carved by bwd_workspace_views.
+size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees);
+void bwd_workspace_views(BwdParams& p, void* workspace);
+
 constexpr int XCDS = 8;  // MI355X: 8 XCDs, workgroups dealt to them round-robin
 
 struct DeviceInfo {
@@ -95,6 +126,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
 // Enqueues the planned work on stream; returns the first failing HIP error.
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
+
+// Enqueues the backward on stream.  *status is ST_OK, or FFF_ERR_UNSUPPORTED's
+// value when no kernel fits (nothing enqueued); returns the first HIP error.
+hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, int* status);
 
 // Stack of layers in one persistent kernel: fills *plan (KIND_STACK) when a
 // kernel is instantiated for the shape and types, else returns ST_UNSUPPORTED.

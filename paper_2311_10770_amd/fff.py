@@ -46,6 +46,20 @@ class FffLayer(ctypes.Structure):
     _fields_ = [("W_in", c_void_p), ("W_out", c_void_p), ("norm_gamma", c_void_p), ("norm_beta", c_void_p)]
 
 
+class FffBackwardArgs(ctypes.Structure):
+    """Mirror of ``fff_backward_args`` in include/fff.h."""
+
+    _fields_ = [
+        ("x", c_void_p), ("W_in", c_void_p), ("W_out", c_void_p), ("dy", c_void_p),
+        ("leaves", c_void_p), ("logits", c_void_p),
+        ("dx", c_void_p), ("dW_in", c_void_p), ("dW_out", c_void_p),
+        ("n_tokens", c_int64), ("hidden", c_int32), ("depth", c_int32), ("n_trees", c_int32),
+        ("x_dtype", c_int32), ("w_dtype", c_int32), ("dy_dtype", c_int32), ("dx_dtype", c_int32),
+        ("act", c_int32), ("accumulate", c_int32), ("bad_leaves", c_void_p),
+        ("workspace", c_void_p), ("workspace_bytes", c_size_t), ("hip_stream", c_void_p),
+    ]
+
+
 class FffError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(msg)
@@ -55,7 +69,8 @@ class FffError(RuntimeError):
 _lib = None
 
 EXPORTS = ("fff_forward", "fff_forward_ex", "fff_workspace_bytes", "fff_describe", "fff_forward_stack",
-           "fff_describe_stack", "fff_status_str", "fff_last_hip_error", "fff_version")
+           "fff_describe_stack", "fff_backward", "fff_backward_workspace_bytes", "fff_status_str",
+           "fff_last_hip_error", "fff_version")
 
 
 def load_library(path: Path | str | None = None):
@@ -81,6 +96,10 @@ def load_library(path: Path | str | None = None):
     lib.fff_describe_stack.argtypes = [ctypes.POINTER(FffArgs), ctypes.POINTER(FffLayer), c_int32, c_char_p,
                                        c_size_t]
     lib.fff_describe_stack.restype = c_int
+    lib.fff_backward.argtypes = [ctypes.POINTER(FffBackwardArgs)]
+    lib.fff_backward.restype = c_int
+    lib.fff_backward_workspace_bytes.argtypes = [c_int64, c_int32, c_int32]
+    lib.fff_backward_workspace_bytes.restype = c_size_t
     lib.fff_status_str.argtypes = [c_int]
     lib.fff_status_str.restype = c_char_p
     lib.fff_last_hip_error.argtypes = []
@@ -270,6 +289,79 @@ def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str
     with torch.cuda.device(x.device):
         _check(load_library().fff_describe_stack(ctypes.byref(a), arr, len(layers), buf, len(buf)))
     return buf.value.decode()
+
+
+_BWD_WORKSPACES: dict = {}
+
+
+def backward_workspace_bytes(n_tokens: int, depth: int, n_trees: int) -> int:
+    return int(load_library().fff_backward_workspace_bytes(n_tokens, depth, n_trees))
+
+
+def backward(x, w_in, w_out, depth: int, n_trees: int, dy, leaves, logits, *, dx=None, dw_in=None, dw_out=None,
+             act="gelu", accumulate=False, bad_leaves=None, workspace=None, stream=None, want=("dx", "dw_in", "dw_out"),
+             dx_dtype=None):
+    """Hard-routed backward through ``fff_backward``.
+
+    ``leaves`` int32 [B, T] and ``logits`` float32 [B, T, D+1] come from the forward's records
+    (``nodes_out[..., depth]`` and ``logits_out``).  Outputs named in ``want`` are allocated
+    when not given (dx of ``dx_dtype`` or dy's dtype; dW in float32).  Returns (dx, dw_in, dw_out)."""
+    device = dy.device
+    B, H = dy.shape
+    N = (1 << (depth + 1)) - 1
+    _check_weights(w_in, w_out, depth, n_trees, H, device)
+    _dev_tensor(dy, "dy", device)
+    if x is not None:
+        _dev_tensor(x, "x", device)
+        if tuple(x.shape) != (B, H):
+            raise ValueError("x and dy must have the same shape")
+    for t, what, dt, n in ((leaves, "leaves", torch.int32, B * n_trees),
+                           (logits, "logits", torch.float32, B * n_trees * (depth + 1))):
+        _dev_tensor(t, what, device)
+        if t.dtype != dt or t.numel() != n:
+            raise ValueError(f"{what} must be {dt} with {n} elements")
+    if dx is None and "dx" in want:
+        dx = torch.empty((B, H), dtype=dx_dtype or dy.dtype, device=device)
+    if dw_in is None and "dw_in" in want:
+        dw_in = torch.empty((n_trees, N, H), dtype=torch.float32, device=device)
+    if dw_out is None and "dw_out" in want:
+        dw_out = torch.empty((n_trees, N, H), dtype=torch.float32, device=device)
+    for t, what in ((dw_in, "dw_in"), (dw_out, "dw_out")):
+        if t is not None:
+            _dev_tensor(t, what, device)
+            if t.dtype != torch.float32 or tuple(t.shape) != (n_trees, N, H):
+                raise ValueError(f"{what} must be float32 [{n_trees}, {N}, {H}]")
+    if dx is not None:
+        _dev_tensor(dx, "dx", device)
+    if (dw_in is not None or dw_out is not None) and workspace is None:
+        need = backward_workspace_bytes(B, depth, n_trees)
+        ws = _BWD_WORKSPACES.get(device)
+        if ws is None or ws.numel() < need:
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+            _BWD_WORKSPACES[device] = ws
+        workspace = ws
+    a = FffBackwardArgs()
+    a.x = x.data_ptr() if x is not None else None
+    a.W_in, a.W_out, a.dy = w_in.data_ptr(), w_out.data_ptr(), dy.data_ptr()
+    a.leaves, a.logits = leaves.data_ptr(), logits.data_ptr()
+    a.dx = dx.data_ptr() if dx is not None else None
+    a.dW_in = dw_in.data_ptr() if dw_in is not None else None
+    a.dW_out = dw_out.data_ptr() if dw_out is not None else None
+    a.n_tokens, a.hidden, a.depth, a.n_trees = B, H, depth, n_trees
+    a.x_dtype = _dt(x, "x") if x is not None else FFF_F32
+    a.w_dtype, a.dy_dtype = _dt(w_in, "W_in"), _dt(dy, "dy")
+    a.dx_dtype = _dt(dx, "dx") if dx is not None else FFF_F32
+    a.act = ACTS[act] if isinstance(act, str) else int(act)
+    a.accumulate = int(bool(accumulate))
+    if bad_leaves is not None:
+        _dev_tensor(bad_leaves, "bad_leaves", device)
+        a.bad_leaves = bad_leaves.data_ptr()
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    a.hip_stream = (stream if stream is not None else torch.cuda.current_stream(device)).cuda_stream
+    with torch.cuda.device(device):
+        _check(load_library().fff_backward(ctypes.byref(a)))
+    return dx, dw_in, dw_out
 
 
 def forward_plain(x, w_in, w_out, depth: int, n_trees: int, y, stream=None):

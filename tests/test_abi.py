@@ -41,18 +41,21 @@ def test_exports_every_declared_symbol(lib):
                 and not e.startswith("_fini")}, "only the fff_ ABI is exported"
 
 
-def test_struct_layout_matches_c(tmp_path):
-    fields = [f[0] for f in binding.FffArgs._fields_]
+@pytest.mark.parametrize("cls,cname", [(binding.FffArgs, "fff_args"), (binding.FffLayer, "fff_layer"),
+                                       (binding.FffBackwardArgs, "fff_backward_args")])
+def test_struct_layout_matches_c(tmp_path, cls, cname):
+    fields = [f[0] for f in cls._fields_]
     src = tmp_path / "layout.c"
     src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "fff.h"\nint main(void){\n'
-                   + 'printf("%zu\\n", sizeof(fff_args));\n'
-                   + "".join(f'printf("%zu\\n", offsetof(fff_args, {f}));\n' for f in fields) + "return 0;}\n")
+                   + f'printf("%zu\\n", sizeof({cname}));\n'
+                   + "".join(f'printf("%zu\\n", offsetof({cname}, {f}));\n' for f in fields) + "return 0;}\n")
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-std=c99", "-I", str(ROOT / "include"), str(src), "-o", str(exe)], check=True)
     vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()]
-    assert vals[0] == ctypes.sizeof(binding.FffArgs)
+    assert vals[0] == ctypes.sizeof(cls)
+    assert len(vals) - 1 == len(fields)
     for f, off in zip(fields, vals[1:]):
-        assert getattr(binding.FffArgs, f).offset == off, f
+        assert getattr(cls, f).offset == off, f
 
 
 def test_version_and_status_strings(lib):
@@ -166,3 +169,46 @@ def test_stack_null_table_and_zero_tokens(lib):
     assert lib.fff_forward_stack(None, layers(1), 1) == binding.FFF_ERR_INVALID_ARG
     a.n_tokens = 0
     assert lib.fff_forward_stack(ctypes.byref(a), layers(3), 3) == binding.FFF_OK
+
+
+def bwd_args(**over):
+    a = binding.FffBackwardArgs()
+    a.x, a.W_in, a.W_out, a.dy = P, P * 16, P * 24, P * 32
+    a.leaves, a.logits = P * 40, P * 48
+    a.dx, a.dW_in, a.dW_out = P * 64, P * 80, P * 96
+    a.n_tokens, a.hidden, a.depth, a.n_trees = 4, 64, 3, 1
+    a.workspace, a.workspace_bytes = P * 256, 1 << 20
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("over", [
+    dict(hidden=66), dict(hidden=0), dict(depth=25), dict(n_trees=0), dict(n_tokens=-1), dict(dy_dtype=2),
+    dict(dx_dtype=-1), dict(act=5), dict(accumulate=2),
+    dict(W_out=None), dict(dy=None), dict(leaves=None), dict(logits=None), dict(x=None),  # x needed for dW_in
+    dict(dx=P * 64 + 8), dict(leaves=P * 40 + 2),
+    dict(dx=P * 32 + 64),                      # dx overlaps dy
+    dict(dW_in=P * 96),                        # dW_in is dW_out
+    dict(dW_out=P * 16),                       # dW_out overwrites W_in
+    dict(workspace=P * 64),                    # workspace overlaps dx
+    dict(n_tokens=1 << 40),                    # tokens x trees past int32
+])
+def test_backward_invalid_arguments(lib, over):
+    a = bwd_args(**over)
+    assert lib.fff_backward(ctypes.byref(a)) == binding.FFF_ERR_INVALID_ARG
+    assert lib.fff_last_hip_error() == 0
+
+
+def test_backward_workspace_rules(lib):
+    need = lib.fff_backward_workspace_bytes(4, 3, 1)
+    assert need > 0 and lib.fff_backward_workspace_bytes(-1, 3, 1) == 0
+    assert lib.fff_backward_workspace_bytes(4, 25, 1) == 0
+    for over in (dict(workspace=None), dict(workspace_bytes=need - 1), dict(workspace=P * 256 + 16)):
+        assert lib.fff_backward(ctypes.byref(bwd_args(**over))) == binding.FFF_ERR_WORKSPACE
+    # dx only needs no workspace, and nothing requested or no tokens is a no-op
+    a = bwd_args(dW_in=None, dW_out=None, workspace=None, workspace_bytes=0, n_tokens=0)
+    assert lib.fff_backward(ctypes.byref(a)) == binding.FFF_OK
+    a = bwd_args(dx=None, dW_in=None, dW_out=None)
+    assert lib.fff_backward(ctypes.byref(a)) == binding.FFF_OK
+    assert lib.fff_backward(None) == binding.FFF_ERR_INVALID_ARG
