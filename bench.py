@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "generic"])
     ap.add_argument("--lds-levels", type=int, default=0)
     ap.add_argument("--norm", action="store_true", help="LayerNorm before every layer (gain/shift drawn per layer)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the hard-routed backward (dx, dW_in, dW_out from the forward's records) instead")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall budget of the oracle timing")
@@ -111,7 +113,25 @@ def main():
             return {}
         return dict(norm_gamma=dlayers[i][2], norm_beta=dlayers[i][3])
 
-    if NL == 1:
+    if args.backward:
+        if NL != 1 or args.norm:
+            sys.exit("--backward times one layer without LayerNorm")
+        rec = (B, w.n_trees, w.depth + 1)
+        nodes_rec = torch.empty(rec, dtype=torch.int32, device=dev)
+        logits_rec = torch.empty(rec, dtype=torch.float32, device=dev)
+        fff.forward(x, wi, wo, w.depth, w.n_trees, y, nodes_out=nodes_rec, logits_out=logits_rec, **kw)
+        leaves = nodes_rec[:, :, w.depth].contiguous()
+        dy = fff.from_numpy(synth.make_x(w.seed + 100, B, w.hidden, w.y_dtype), dev)
+        dx = torch.empty_like(x)
+        nn_ = (1 << (w.depth + 1)) - 1
+        dwi = torch.empty((w.n_trees, nn_, w.hidden), dtype=torch.float32, device=dev)
+        dwo = torch.empty_like(dwi)
+        plan = "backward: token kernel + counting sort by leaf + weight kernel"
+
+        def step():
+            fff.backward(x, wi, wo, w.depth, w.n_trees, dy, leaves, logits_rec, dx=dx, dw_in=dwi, dw_out=dwo,
+                         act="gelu")
+    elif NL == 1:
         plan = fff.describe(x, wi, wo, w.depth, w.n_trees, y, **kw, **layer_kw(0))
 
         def step():
@@ -140,7 +160,8 @@ def main():
         f"{tokens_per_s / 1e6:.1f} M tok/s, gathered {achieved:.0f} GB/s")
 
     out = {
-        "metric": "FFF tokens/s at d=768 depth 11; speedup vs dense 3072-FF; HBM GB/s",
+        "metric": ("FFF hard-routed backward tokens/s (dx, dW_in, dW_out)" if args.backward else
+                   "FFF tokens/s at d=768 depth 11; speedup vs dense 3072-FF; HBM GB/s"),
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.w_dtype == "bf16" else "f32",
@@ -167,6 +188,8 @@ def main():
         else:
             log(f"{tpath.name} was taken on other kernel sources: traffic unreported")
     kernels = "walk_kernel + emit_kernel" if "grouped<" in plan else plan.split("<")[0].split()[-1] + "_kernel"
+    if args.backward:
+        kernels = "bwd_token_kernel + bwd_scan/scatter + bwd_weight_kernel"
     if plan.startswith("per-layer"):
         kernels = f"{NL} launches of {kernels}"
     out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -174,7 +197,7 @@ def main():
                        "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x {B} "
                                 f"tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, HIP "
                                 f"events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
-    flops = w.flops_per_token() * B * NL
+    flops = w.flops_per_token() * B * NL * (2 if args.backward else 1)  # backward: dot + axpy + two row updates
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
     if NL > 1:
@@ -186,7 +209,7 @@ def main():
                         "persistent_plan": fff.describe_stack(x, dlayers, w.depth, w.n_trees, y, **kd)}
         log(f"persistent stack kernel: {tk['mean_ms'] * 1e3:.1f} us vs the planned step {t['mean_ms'] * 1e3:.1f} us")
 
-    if not args.no_dense:
+    if not args.no_dense and not args.backward:
         H, F = w.hidden, 3072 if w.hidden == 768 else 4 * w.hidden
         g = torch.Generator(device="cpu").manual_seed(1234)
         w1 = (torch.randn(F, H, generator=g) / H ** 0.5).to(dev, torch.bfloat16)
@@ -219,6 +242,9 @@ def main():
         dense.close()
         log(f"dense (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x "
             f"(rel err {rel:.1e}); torch unfused {unfused_ms * 1e3:.1f} us")
+
+    if args.backward:
+        args.no_cpu_baseline = True  # the backward's CPU leg and check live in the tests
 
     if not args.no_cpu_baseline:
         # The CPU leg: the fp64 oracle timed on the host cores over the first n tokens.  Its

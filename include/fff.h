@@ -208,10 +208,10 @@ int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_laye
  *
  * Work: a token kernel (dx and the per-visit pairs (a, dl)), a counting sort
  * of the tokens by leaf (so that every node's tokens form one run at every
- * level), and a weight kernel that sums each run in registers and adds it to
- * dW with one fp32 atomic per element and run.  dx is deterministic; dW sums
- * in an order that can vary from call to call (atomics), within fp32
- * rounding.
+ * level), a weight kernel that sums the runs of fixed pieces of the sorted
+ * order in registers (a run inside one piece is stored directly), and a
+ * fix-up kernel that adds the piece sums of runs crossing pieces in piece
+ * order.  No atomics on dx or dW: results are deterministic.
  */
 typedef struct {
     const void* x;          /* [n_tokens, hidden] the layer's FFF input (x_dtype) */
@@ -246,8 +246,9 @@ int fff_backward(const fff_backward_args* a);
 
 /* Workspace fff_backward needs: per-visit pairs (8 bytes each), two int32
  * arrays of 2^depth leaf bins per tree, one int32 token index per (token,
- * tree), and per-tree totals.  0 for invalid shapes. */
-size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees);
+ * tree), per-tree totals, and fp32 run sums (two slots of both matrices'
+ * rows per level and piece).  0 for invalid shapes. */
+size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
 
 /* fff_describe for a stack. */
 int fff_describe_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers, char* buf, size_t len);

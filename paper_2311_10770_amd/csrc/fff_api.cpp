@@ -360,7 +360,7 @@ int validate_backward(const fff_backward_args* a, fff::BwdParams* p) {
                 if (overlap(outs[i].ptr, outs[i].bytes, outs[j].ptr, outs[j].bytes)) return FFF_ERR_INVALID_ARG;
         }
         if (a->dW_in || a->dW_out) {
-            const size_t need = fff::bwd_workspace_bytes(a->n_tokens, a->depth, a->n_trees);
+            const size_t need = fff::bwd_workspace_bytes(a->n_tokens, a->depth, a->n_trees, a->hidden);
             if (!a->workspace || a->workspace_bytes < need || (reinterpret_cast<uintptr_t>(a->workspace) & 255u))
                 return FFF_ERR_WORKSPACE;
             for (const Span& q : ins)
@@ -414,9 +414,9 @@ FFF_EXPORT int fff_backward(const fff_backward_args* a) {
     return FFF_OK;
 }
 
-FFF_EXPORT size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees) {
-    if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1) return 0;
-    return fff::bwd_workspace_bytes(n_tokens, depth, n_trees);
+FFF_EXPORT size_t fff_backward_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
+    if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1 || hidden < 1) return 0;
+    return fff::bwd_workspace_bytes(n_tokens, depth, n_trees, hidden);
 }
 
 FFF_EXPORT int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_layers) {

@@ -15,11 +15,19 @@
 // 2. bwd_scan_kernel + bwd_scatter_kernel: counting sort of the tokens by
 //    leaf.  Sorted by leaf, the tokens through any node form one contiguous
 //    run at every level (a node's leaves are a contiguous range).
-// 3. bwd_weight_kernel: each wave walks a stretch of sorted tokens for one
-//    256-column slice, sums a*dy and dl*x per level in registers while the
-//    node stays the same, and adds each finished run to dW with one fp32
-//    atomic per element -- a handful of atomics per row and stretch instead
-//    of one per token.
+// 3. bwd_piece_kernel: the sorted order is cut into pieces of P positions;
+//    a wave walks one piece for one 256-column slice and sums a*dy and dl*x
+//    per level in registers while the node stays the same.  A run that starts
+//    and ends inside the piece has no other contributor: its dW row is stored
+//    directly.  A run that crosses a piece boundary leaves its piece sum in
+//    the workspace (slot 0: the run began before the piece; slot 1: it began
+//    in the piece and goes on).
+// 4. bwd_fixup_kernel: one task per node adds the piece sums of a crossing
+//    run in piece order and stores the row, and stores zero rows for nodes no
+//    token visits.  No atomics: every dW element has exactly one writer, and
+//    the results do not depend on scheduling.  (Device-scope fp32 atomics
+//    were measured at about 26 G/s on MI355X, where the L2 is per XCD; the
+//    root rows alone took over a thousand of them per element.)
 #include "fff_common.hpp"
 #include "fff_device.hpp"
 #include "fff_internal.hpp"
@@ -37,7 +45,7 @@ enum { ST_OK_ = 0, ST_UNSUPPORTED_ = -2 };
 constexpr int BWD_BLOCK = 256;
 constexpr int SCAN_BLOCK = 1024;
 constexpr int SLICE = 256;       // columns per wave in the weight kernel (64 lanes x 4)
-constexpr int LV = 12;           // levels handled per pass of the weight kernel
+constexpr int LV = 6;            // levels handled per pass of the piece kernel
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
@@ -280,85 +288,278 @@ __device__ __forceinline__ float4 load4(const void* base, bool bf, int64_t i) {
     return *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + i);
 }
 
-__device__ __forceinline__ void flush_row(float* dw, int64_t row, int col, bool active, const float* v) {
+// dW row slice: stored, or added to (accumulate); one writer per element.
+__device__ __forceinline__ void put_row(float* dw, int64_t at, bool active, bool accumulate, const float* v) {
     if (!dw || !active) return;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) unsafeAtomicAdd(dw + row + col + k, v[k]);
+    float4* d = reinterpret_cast<float4*>(dw + at);
+    float4 o = make_float4(v[0], v[1], v[2], v[3]);
+    if (accumulate) {
+        const float4 q = *d;
+        o.x += q.x; o.y += q.y; o.z += q.z; o.w += q.w;
+    }
+    *d = o;
 }
 
-__global__ __launch_bounds__(BWD_BLOCK) void bwd_weight_kernel(BwdParams p) {
+// Piece sum slot of (tree t, piece k, level l, slot, matrix m): H floats.
+__device__ __forceinline__ int64_t part_at(const BwdParams& p, int t, int64_t k, int l, int slot, int m) {
+    return ((((int64_t(t) * p.pieces + k) * (p.depth + 1) + l) * 2 + slot) * 2 + m) * p.hidden;
+}
+
+// Piece sums of both matrices into the workspace (a matrix not requested is skipped).
+__device__ __forceinline__ void put_part(const BwdParams& p, int t, int64_t k, int l, int slot, int col, bool active,
+                                         const float* o, const float* in) {
+    if (p.dw_out) put_row(p.part, part_at(p, t, k, l, slot, 0) + col, active, false, o);
+    if (p.dw_in) put_row(p.part, part_at(p, t, k, l, slot, 1) + col, active, false, in);
+}
+
+// One sorted token's inputs for the piece kernel.
+struct WTok {
+    uint32_t leaf1;
+    float4 gy, xv;
+    const float2* cf;
+};
+
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_piece_kernel(BwdParams p) {
     const int lane = threadIdx.x & 63;
     const int64_t wid = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
     const int T = p.n_trees, D = p.depth, H = p.hidden;
     const int64_t N = p.n_nodes;
     const int slices = (H + SLICE - 1) / SLICE;
-    const int64_t chunks = (p.n_tokens + p.chunk - 1) / p.chunk;
-    const int64_t per_tree = chunks * slices;
+    const int64_t per_tree = int64_t(p.pieces) * slices;
     if (wid >= per_tree * T) return;  // whole wave
     const int t = int(wid / per_tree);
     const int64_t r = wid % per_tree;
     const int s = int(r % slices);
-    const int64_t c = r / slices;
+    const int64_t k = r / slices;
     const int64_t total = p.total[t];
-    const int64_t p0 = c * p.chunk;
-    const int64_t p1 = std::min<int64_t>(p0 + p.chunk, total);
+    const int64_t p0 = k * p.piece;
+    const int64_t p1 = std::min<int64_t>(p0 + p.piece, total);
     if (p0 >= p1) return;
     const int col = s * SLICE + lane * 4;
     const bool active = col < H;  // H is a multiple of 4
     const int32_t* perm = p.perm + int64_t(t) * p.n_tokens;
+    // the tokens just before and just after the piece decide which runs cross its ends
+    const uint32_t prev1 = p0 > 0 ? uint32_t(p.leaves[int64_t(perm[p0 - 1]) * T + t]) + 1 : 0u;
+    const uint32_t next1 = p1 < total ? uint32_t(p.leaves[int64_t(perm[p1]) * T + t]) + 1 : 0u;
+
+    auto fetch = [&](int32_t b) {
+        WTok w;
+        w.leaf1 = uint32_t(p.leaves[int64_t(b) * T + t]) + 1;
+        w.gy = make_float4(0.f, 0.f, 0.f, 0.f);
+        w.xv = w.gy;
+        if (active) {
+            w.gy = load4(p.dy, p.dy_bf16, int64_t(b) * H + col);
+            w.xv = load4(p.x, p.x_bf16, int64_t(b) * H + col);
+        }
+        w.cf = p.coef + (int64_t(b) * T + t) * (D + 1);
+        return w;
+    };
+
     for (int l0 = 0; l0 <= D; l0 += LV) {
-        int64_t cur[LV];
+        int32_t cur[LV];    // node of the current run per level (wave-uniform)
+        uint32_t head = 0;  // bit j: the current run of level l0+j began before this piece
         float ao[LV][4], ai[LV][4];
 #pragma unroll
         for (int j = 0; j < LV; ++j) {
             cur[j] = -1;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) ao[j][k] = ai[j][k] = 0.0f;
+            for (int q = 0; q < 4; ++q) ao[j][q] = ai[j][q] = 0.0f;
         }
-        for (int64_t q = p0; q < p1; ++q) {
-            const int64_t b = perm[q];
-            const uint32_t leaf1 = uint32_t(p.leaves[b * T + t]) + 1;
-            float4 gy = make_float4(0.f, 0.f, 0.f, 0.f), xv = gy;
-            if (active) {
-                gy = load4(p.dy, p.dy_bf16, b * H + col);
-                xv = load4(p.x, p.x_bf16, b * H + col);
+        // a run ends inside the piece: complete (store) or the tail of a crossing run (slot 0)
+        auto end_run = [&](int j, int l) {
+            if (head & (1u << j)) {
+                put_part(p, t, k, l, 0, col, active, ao[j], ai[j]);
+            } else {
+                const int64_t row = (int64_t(t) * N + cur[j]) * H + col;
+                put_row(p.dw_out, row, active, p.accumulate, ao[j]);
+                put_row(p.dw_in, row, active, p.accumulate, ai[j]);
             }
-            const float2* cf = p.coef + (b * T + t) * (D + 1);
+        };
+        auto consume = [&](const WTok& w) {
 #pragma unroll
             for (int j = 0; j < LV; ++j) {
                 const int l = l0 + j;
                 if (l > D) break;
-                const int64_t node = int64_t(leaf1 >> (D - l)) - 1;
-                if (node != cur[j]) {  // a run ends (wave-uniform)
+                const int32_t node = int32_t(w.leaf1 >> (D - l)) - 1;
+                if (node != cur[j]) {  // a run starts (wave-uniform)
                     if (cur[j] >= 0) {
-                        const int64_t row = (int64_t(t) * N + cur[j]) * H;
-                        flush_row(p.dw_out, row, col, active, ao[j]);
-                        flush_row(p.dw_in, row, col, active, ai[j]);
+                        end_run(j, l);
+                        head &= ~(1u << j);
+                    } else if (prev1 != 0 && int32_t(prev1 >> (D - l)) - 1 == node) {
+                        head |= 1u << j;
                     }
                     cur[j] = node;
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) ao[j][k] = ai[j][k] = 0.0f;
+                    for (int q = 0; q < 4; ++q) ao[j][q] = ai[j][q] = 0.0f;
                 }
-                const float2 cc = cf[l];
-                ao[j][0] = __builtin_fmaf(cc.x, gy.x, ao[j][0]);
-                ao[j][1] = __builtin_fmaf(cc.x, gy.y, ao[j][1]);
-                ao[j][2] = __builtin_fmaf(cc.x, gy.z, ao[j][2]);
-                ao[j][3] = __builtin_fmaf(cc.x, gy.w, ao[j][3]);
-                ai[j][0] = __builtin_fmaf(cc.y, xv.x, ai[j][0]);
-                ai[j][1] = __builtin_fmaf(cc.y, xv.y, ai[j][1]);
-                ai[j][2] = __builtin_fmaf(cc.y, xv.z, ai[j][2]);
-                ai[j][3] = __builtin_fmaf(cc.y, xv.w, ai[j][3]);
+                const float2 cc = w.cf[l];
+                ao[j][0] = __builtin_fmaf(cc.x, w.gy.x, ao[j][0]);
+                ao[j][1] = __builtin_fmaf(cc.x, w.gy.y, ao[j][1]);
+                ao[j][2] = __builtin_fmaf(cc.x, w.gy.z, ao[j][2]);
+                ao[j][3] = __builtin_fmaf(cc.x, w.gy.w, ao[j][3]);
+                ai[j][0] = __builtin_fmaf(cc.y, w.xv.x, ai[j][0]);
+                ai[j][1] = __builtin_fmaf(cc.y, w.xv.y, ai[j][1]);
+                ai[j][2] = __builtin_fmaf(cc.y, w.xv.z, ai[j][2]);
+                ai[j][3] = __builtin_fmaf(cc.y, w.xv.w, ai[j][3]);
             }
+        };
+        // Sorted token indices 64 at a time (one per lane), then one token per step with the
+        // next one's loads in flight.
+        for (int64_t q0 = p0; q0 < p1; q0 += 64) {
+            const int nb = int(std::min<int64_t>(64, p1 - q0));
+            const int32_t mine = lane < nb ? perm[q0 + lane] : 0;
+            WTok a = fetch(__builtin_amdgcn_readlane(mine, 0));
+            int i = 0;
+            for (; i + 2 <= nb; i += 2) {
+                const WTok b = fetch(__builtin_amdgcn_readlane(mine, i + 1));
+                consume(a);
+                if (i + 2 < nb) a = fetch(__builtin_amdgcn_readlane(mine, i + 2));
+                consume(b);
+            }
+            if (i < nb) consume(a);
         }
+        // the last run of every level: complete, or it goes on into the next piece
 #pragma unroll
         for (int j = 0; j < LV; ++j) {
-            if (l0 + j > D) break;
-            if (cur[j] >= 0) {
-                const int64_t row = (int64_t(t) * N + cur[j]) * H;
-                flush_row(p.dw_out, row, col, active, ao[j]);
-                flush_row(p.dw_in, row, col, active, ai[j]);
+            const int l = l0 + j;
+            if (l > D) break;
+            const bool goes_on = next1 != 0 && int32_t(next1 >> (D - l)) - 1 == cur[j];
+            if (goes_on) {
+                put_part(p, t, k, l, (head >> j) & 1u ? 0 : 1, col, active, ao[j], ai[j]);
+            } else {
+                end_run(j, l);
             }
         }
+    }
+}
+
+// Run bounds of node n of tree t in the sorted order: [S, E).
+__device__ __forceinline__ void node_run(const BwdParams& p, int t, int64_t n, int l, int64_t* S, int64_t* E) {
+    const int D = p.depth;
+    const int64_t L = int64_t(1) << D;
+    const int64_t first = ((n + 1) << (D - l)) - L;  // its leaves, as bins of the level-D order
+    const int64_t last = ((n + 2) << (D - l)) - L - 1;
+    const int32_t* cnt = p.counts + t * L;
+    const int32_t* end = p.offs + t * L;  // after the scatter: one past each leaf's last position
+    *S = int64_t(end[first]) - cnt[first];
+    *E = end[last];
+}
+
+__device__ __forceinline__ int level_of(int64_t n) { return 63 - __builtin_clzll(uint64_t(n + 1)); }
+
+// Levels 0..top_levels-1 of every tree: one 1024-thread block per (tree, node,
+// slice); the 16 waves take every 16th piece sum (eight loads in flight) and
+// the wave sums are added in wave order through LDS.
+constexpr int FIX_BLOCK = 1024;
+
+__global__ __launch_bounds__(FIX_BLOCK) void bwd_fixup_top_kernel(BwdParams p, int top_levels) {
+    constexpr int WAVES = FIX_BLOCK / 64;
+    __shared__ float4 red[2][WAVES][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int H = p.hidden;
+    const int slices = (H + SLICE - 1) / SLICE;
+    const int64_t ntop = (int64_t(1) << top_levels) - 1;
+    const int64_t task = blockIdx.x;
+    const int s = int(task % slices);
+    const int64_t n = (task / slices) % ntop;
+    const int t = int(task / (slices * ntop));
+    const int l = level_of(n);
+    int64_t S, E;
+    node_run(p, t, n, l, &S, &E);
+    const int col = s * SLICE + lane * 4;
+    const bool active = col < H;
+    const int64_t row = (int64_t(t) * p.n_nodes + n) * H + col;
+    const float zero[4] = {0.f, 0.f, 0.f, 0.f};
+    if (S == E) {  // block-uniform
+        if (!p.accumulate && wave == 0) {
+            put_row(p.dw_out, row, active, false, zero);
+            put_row(p.dw_in, row, active, false, zero);
+        }
+        return;
+    }
+    const int64_t kS = S / p.piece, kE = (E - 1) / p.piece;
+    if (kS == kE) return;  // inside one piece: stored by the piece kernel
+    float4 so = make_float4(0.f, 0.f, 0.f, 0.f), si = so;
+    if (active) {
+        constexpr int U = 8;
+        for (int64_t k0 = kS + wave; k0 <= kE; k0 += int64_t(WAVES) * U) {
+            float4 vo[U], vi[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t k = k0 + int64_t(u) * WAVES;
+                vo[u] = vi[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (k <= kE) {
+                    const int slot = k == kS ? 1 : 0;
+                    if (p.dw_out) vo[u] = *reinterpret_cast<const float4*>(p.part + part_at(p, t, k, l, slot, 0) + col);
+                    if (p.dw_in) vi[u] = *reinterpret_cast<const float4*>(p.part + part_at(p, t, k, l, slot, 1) + col);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                so.x += vo[u].x; so.y += vo[u].y; so.z += vo[u].z; so.w += vo[u].w;
+                si.x += vi[u].x; si.y += vi[u].y; si.z += vi[u].z; si.w += vi[u].w;
+            }
+        }
+    }
+    red[0][wave][lane] = so;
+    red[1][wave][lane] = si;
+    __syncthreads();
+    if (wave == 0) {
+        float o[4] = {0.f, 0.f, 0.f, 0.f}, in[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < WAVES; ++w) {
+            const float4 a = red[0][w][lane], b = red[1][w][lane];
+            o[0] += a.x; o[1] += a.y; o[2] += a.z; o[3] += a.w;
+            in[0] += b.x; in[1] += b.y; in[2] += b.z; in[3] += b.w;
+        }
+        put_row(p.dw_out, row, active, p.accumulate, o);
+        put_row(p.dw_in, row, active, p.accumulate, in);
+    }
+}
+
+// Levels top_levels..D: one wave per (tree, node, slice), grid-stride; these
+// runs usually span one or two pieces.
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_fixup_kernel(BwdParams p, int top_levels) {
+    const int lane = threadIdx.x & 63;
+    const int T = p.n_trees, H = p.hidden;
+    const int64_t N = p.n_nodes;
+    const int64_t n0 = (int64_t(1) << top_levels) - 1;  // first node handled here
+    const int64_t nn = N - n0;
+    const int slices = (H + SLICE - 1) / SLICE;
+    const int64_t tasks = int64_t(T) * nn * slices;
+    const int64_t waves = int64_t(gridDim.x) * (BWD_BLOCK / 64);
+    for (int64_t w = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6); w < tasks; w += waves) {
+        const int s = int(w % slices);
+        const int64_t n = n0 + (w / slices) % nn;
+        const int t = int(w / (slices * nn));
+        const int l = level_of(n);
+        int64_t S, E;
+        node_run(p, t, n, l, &S, &E);
+        const int col = s * SLICE + lane * 4;
+        const bool active = col < H;
+        const int64_t row = (int64_t(t) * N + n) * H + col;
+        float o[4] = {0.f, 0.f, 0.f, 0.f}, in[4] = {0.f, 0.f, 0.f, 0.f};
+        if (S == E) {  // no token visits this node
+            if (!p.accumulate) {
+                put_row(p.dw_out, row, active, false, o);
+                put_row(p.dw_in, row, active, false, in);
+            }
+            continue;
+        }
+        const int64_t kS = S / p.piece, kE = (E - 1) / p.piece;
+        if (kS == kE) continue;  // inside one piece: stored by the piece kernel
+        for (int64_t k = kS; k <= kE && active; ++k) {
+            const int slot = k == kS ? 1 : 0;
+            if (p.dw_out) {
+                const float4 v = *reinterpret_cast<const float4*>(p.part + part_at(p, t, k, l, slot, 0) + col);
+                o[0] += v.x; o[1] += v.y; o[2] += v.z; o[3] += v.w;
+            }
+            if (p.dw_in) {
+                const float4 v = *reinterpret_cast<const float4*>(p.part + part_at(p, t, k, l, slot, 1) + col);
+                in[0] += v.x; in[1] += v.y; in[2] += v.z; in[3] += v.w;
+            }
+        }
+        put_row(p.dw_out, row, active, p.accumulate, o);
+        put_row(p.dw_in, row, active, p.accumulate, in);
     }
 }
 
@@ -389,17 +590,31 @@ int resident_blocks(const void* kernel, size_t lds) {
 
 }  // namespace
 
-size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees) {
+int32_t bwd_piece(int64_t n_tokens, int32_t n_trees) {
+    // about 1024 pieces over all trees (x 3 column slices at hidden 768: three
+    // waves per SIMD), at least 64 positions (one perm load per lane)
+    const int64_t want = (n_tokens * n_trees + 1023) / 1024;
+    return int32_t(std::max<int64_t>(64, (want + 63) / 64 * 64));
+}
+
+static int64_t bwd_pieces(int64_t n_tokens, int32_t piece) { return std::max<int64_t>(1, (n_tokens + piece - 1) / piece); }
+
+size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
     const size_t recs = size_t(n_tokens) * size_t(n_trees);
     const size_t bins = (size_t(1) << depth) * size_t(n_trees);
+    const size_t parts = size_t(n_trees) * size_t(bwd_pieces(n_tokens, bwd_piece(n_tokens, n_trees))) *
+                         size_t(depth + 1) * 4 * size_t(hidden);
     return align256(recs * size_t(depth + 1) * sizeof(float2)) + 2 * align256(bins * sizeof(int32_t)) +
-           align256(recs * sizeof(int32_t)) + align256(size_t(n_trees) * sizeof(int32_t));
+           align256(recs * sizeof(int32_t)) + align256(size_t(n_trees) * sizeof(int32_t)) +
+           align256(parts * sizeof(float));
 }
 
 void bwd_workspace_views(BwdParams& p, void* workspace) {
     char* w = static_cast<char*>(workspace);
     const size_t recs = size_t(p.n_tokens) * size_t(p.n_trees);
     const size_t bins = (size_t(1) << p.depth) * size_t(p.n_trees);
+    p.piece = bwd_piece(p.n_tokens, p.n_trees);
+    p.pieces = int32_t(bwd_pieces(p.n_tokens, p.piece));
     p.coef = reinterpret_cast<float2*>(w);
     w += align256(recs * size_t(p.depth + 1) * sizeof(float2));
     p.counts = reinterpret_cast<int32_t*>(w);
@@ -409,6 +624,8 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
     p.perm = reinterpret_cast<int32_t*>(w);
     w += align256(recs * sizeof(int32_t));
     p.total = reinterpret_cast<int32_t*>(w);
+    w += align256(size_t(p.n_trees) * sizeof(int32_t));
+    p.part = reinterpret_cast<float*>(w);
 }
 
 hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, int* status) {
@@ -422,36 +639,18 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         return hipSuccess;
     }
     void* args[] = {&p};
-    const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
-    const int64_t dw4 = p.n_trees * p.n_nodes * p.hidden / 4;
-    // zero the leaf counts, and dW unless accumulating (a fill kernel: no memset nodes)
-    {
-        const int64_t n4 = p.accumulate ? 0 : dw4;
-        const int64_t work = std::max<int64_t>(n4, p.need_dw ? bins : 0);
-        if (work > 0) {
-            const int grid = int(std::min<int64_t>((work + BWD_BLOCK - 1) / BWD_BLOCK, int64_t(dev.cu_count) * 8));
-            for (float* dw : {p.dw_in, p.dw_out}) {
-                if (!dw || p.accumulate) continue;
-                float* a = dw;
-                int64_t na = dw4;
-                int32_t* b = nullptr;
-                int64_t nb = 0;
-                void* fa[] = {&a, &na, &b, &nb};
-                const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_fill_kernel), dim3(grid),
-                                                     dim3(BWD_BLOCK), fa, 0, stream);
-                if (e != hipSuccess) return e;
-            }
-            if (p.need_dw) {
-                float* a = nullptr;
-                int64_t na = 0;
-                int32_t* b = p.counts;
-                int64_t nb = bins;
-                void* fa[] = {&a, &na, &b, &nb};
-                const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_fill_kernel), dim3(grid),
-                                                     dim3(BWD_BLOCK), fa, 0, stream);
-                if (e != hipSuccess) return e;
-            }
-        }
+    const int64_t cap = int64_t(dev.cu_count) * 8;
+    if (p.need_dw) {  // zero the leaf counts (a fill kernel: no memset nodes)
+        const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
+        float* a = nullptr;
+        int64_t na = 0;
+        int32_t* b = p.counts;
+        int64_t nb = bins;
+        void* fa[] = {&a, &na, &b, &nb};
+        const int grid = int(std::min<int64_t>((bins + BWD_BLOCK - 1) / BWD_BLOCK, cap));
+        const hipError_t e =
+            hipLaunchKernel(reinterpret_cast<const void*>(&bwd_fill_kernel), dim3(grid), dim3(BWD_BLOCK), fa, 0, stream);
+        if (e != hipSuccess) return e;
     }
     // token kernel
     {
@@ -479,23 +678,39 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
     if (e != hipSuccess) return e;
     {
         const int64_t n = p.n_tokens * p.n_trees;
-        const int grid = int(std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, int64_t(dev.cu_count) * 8));
+        const int grid = int(std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap));
         e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scatter_kernel), dim3(grid), dim3(BWD_BLOCK), args, 0,
                             stream);
         if (e != hipSuccess) return e;
     }
+    const int slices = (p.hidden + SLICE - 1) / SLICE;
     {
-        // about four waves per SIMD over all slices and trees
-        const int slices = (p.hidden + SLICE - 1) / SLICE;
-        const int64_t target = int64_t(dev.cu_count) * 16;
-        const int64_t chunks = std::max<int64_t>(1, target / (int64_t(slices) * p.n_trees));
-        p.chunk = int32_t(std::max<int64_t>(16, (p.n_tokens + chunks - 1) / chunks));
-        const int64_t waves = ((p.n_tokens + p.chunk - 1) / p.chunk) * slices * p.n_trees;
+        const int64_t waves = int64_t(p.pieces) * slices * p.n_trees;
         const int64_t grid = (waves + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64);
-        void* wargs[] = {&p};
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_weight_kernel), dim3(unsigned(grid)), dim3(BWD_BLOCK),
-                            wargs, 0, stream);
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_piece_kernel), dim3(unsigned(grid)), dim3(BWD_BLOCK),
+                            args, 0, stream);
         if (e != hipSuccess) return e;
+    }
+    {
+        // Levels whose runs span about eight pieces or more under uniform routing get a block
+        // per node; any routing is handled correctly by either kernel.
+        int top = 0;
+        while (top < p.depth + 1 && (int64_t(p.pieces) >> top) >= 8) ++top;
+        if (top > 0) {
+            const int64_t blocks = int64_t(p.n_trees) * ((int64_t(1) << top) - 1) * slices;
+            void* targs[] = {&p, &top};
+            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_fixup_top_kernel), dim3(unsigned(blocks)),
+                                dim3(FIX_BLOCK), targs, 0, stream);
+            if (e != hipSuccess) return e;
+        }
+        const int64_t tasks = int64_t(p.n_trees) * (p.n_nodes - ((int64_t(1) << top) - 1)) * slices;
+        if (tasks > 0) {
+            const int64_t grid = std::min<int64_t>((tasks + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64), cap * 4);
+            void* fargs[] = {&p, &top};
+            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_fixup_kernel), dim3(unsigned(grid)),
+                                dim3(BWD_BLOCK), fargs, 0, stream);
+            if (e != hipSuccess) return e;
+        }
     }
     return hipSuccess;
 }

@@ -80,12 +80,16 @@ struct BwdParams {
     int32_t* offs;           // [T, 2^D] first sorted position of each leaf, then the scatter cursor
     int32_t* perm;           // [T, B] token indices sorted by leaf
     int32_t* total;          // [T] valid (token, tree) pairs per tree
-    int32_t chunk;           // sorted tokens per wave in the weight kernel
+    float* part;             // [T, pieces, D+1, 2 slots, 2 matrices, H] run sums that cross pieces
+    int32_t piece;           // sorted positions per piece of the weight kernel
+    int32_t pieces;          // pieces per tree
     int32_t need_dw;         // dW_in or dW_out requested
 };
 
+// Sorted positions per piece of the backward's weight kernel (a multiple of 64).
+int32_t bwd_piece(int64_t n_tokens, int32_t n_trees);
 // Workspace of the backward; the views are carved by bwd_workspace_views.
-size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees);
+size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
 void bwd_workspace_views(BwdParams& p, void* workspace);
 
 constexpr int XCDS = 8;  // MI355X: 8 XCDs, workgroups dealt to them round-robin

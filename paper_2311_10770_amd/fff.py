@@ -98,7 +98,7 @@ def load_library(path: Path | str | None = None):
     lib.fff_describe_stack.restype = c_int
     lib.fff_backward.argtypes = [ctypes.POINTER(FffBackwardArgs)]
     lib.fff_backward.restype = c_int
-    lib.fff_backward_workspace_bytes.argtypes = [c_int64, c_int32, c_int32]
+    lib.fff_backward_workspace_bytes.argtypes = [c_int64, c_int32, c_int32, c_int32]
     lib.fff_backward_workspace_bytes.restype = c_size_t
     lib.fff_status_str.argtypes = [c_int]
     lib.fff_status_str.restype = c_char_p
@@ -294,8 +294,8 @@ def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str
 _BWD_WORKSPACES: dict = {}
 
 
-def backward_workspace_bytes(n_tokens: int, depth: int, n_trees: int) -> int:
-    return int(load_library().fff_backward_workspace_bytes(n_tokens, depth, n_trees))
+def backward_workspace_bytes(n_tokens: int, depth: int, n_trees: int, hidden: int) -> int:
+    return int(load_library().fff_backward_workspace_bytes(n_tokens, depth, n_trees, hidden))
 
 
 def backward(x, w_in, w_out, depth: int, n_trees: int, dy, leaves, logits, *, dx=None, dw_in=None, dw_out=None,
@@ -334,7 +334,7 @@ def backward(x, w_in, w_out, depth: int, n_trees: int, dy, leaves, logits, *, dx
     if dx is not None:
         _dev_tensor(dx, "dx", device)
     if (dw_in is not None or dw_out is not None) and workspace is None:
-        need = backward_workspace_bytes(B, depth, n_trees)
+        need = backward_workspace_bytes(B, depth, n_trees, H)
         ws = _BWD_WORKSPACES.get(device)
         if ws is None or ws.numel() < need:
             ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)

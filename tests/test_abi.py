@@ -201,9 +201,9 @@ def test_backward_invalid_arguments(lib, over):
 
 
 def test_backward_workspace_rules(lib):
-    need = lib.fff_backward_workspace_bytes(4, 3, 1)
-    assert need > 0 and lib.fff_backward_workspace_bytes(-1, 3, 1) == 0
-    assert lib.fff_backward_workspace_bytes(4, 25, 1) == 0
+    need = lib.fff_backward_workspace_bytes(4, 3, 1, 64)
+    assert need > 0 and lib.fff_backward_workspace_bytes(-1, 3, 1, 64) == 0
+    assert lib.fff_backward_workspace_bytes(4, 25, 1, 64) == 0 and lib.fff_backward_workspace_bytes(4, 3, 1, 0) == 0
     for over in (dict(workspace=None), dict(workspace_bytes=need - 1), dict(workspace=P * 256 + 16)):
         assert lib.fff_backward(ctypes.byref(bwd_args(**over))) == binding.FFF_ERR_WORKSPACE
     # dx only needs no workspace, and nothing requested or no tokens is a no-op
