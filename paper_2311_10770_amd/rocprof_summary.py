@@ -24,7 +24,7 @@ COPY_KERNEL = "copy_kernel"
 def kernel_source_hash() -> str:
     """Hash of the kernel sources: counter figures are void once these change."""
     h = hashlib.sha256()
-    for name in ("fff_kernels.hip", "fff_device.hpp"):
+    for name in ("fff_kernels.hip", "fff_backward.hip", "fff_common.hpp", "fff_device.hpp", "fff_internal.hpp"):
         p = PKG / "csrc" / name
         if p.exists():
             h.update(p.read_bytes())
