@@ -492,8 +492,8 @@ void format_plan(const fff::Plan& plan, const char* prefix, char* buf, size_t le
     int n = std::snprintf(buf, len, "%s%s<%s> lanes_per_token=%d lds_levels=%d", prefix, kinds[plan.kind],
                           plan.name, plan.lanes, plan.lds_levels);
     if (plan.kind == fff::KIND_GROUPED && n > 0 && size_t(n) < len)
-        n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d", plan.emit_lds_levels,
-                           plan.split_level);
+        n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d emit_lanes=%d",
+                           plan.emit_lds_levels, plan.split_level, plan.emit_lanes);
     for (int i = 0; i < plan.n_launch && n > 0 && size_t(n) < len; ++i)
         n += std::snprintf(buf + n, len - n, " | launch%d grid=%d block=%d lds_bytes=%zu", i, plan.launch[i].grid,
                            plan.launch[i].block, plan.launch[i].lds_bytes);

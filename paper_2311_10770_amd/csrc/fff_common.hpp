@@ -365,14 +365,6 @@ __device__ __forceinline__ uint32_t walk_tree(const XRegs<LANES, NV, XBF, WBF>& 
 template <int LANES, int NV, bool WBF, class LdsRowFn, class GlobalRowFn, class ActFn>
 __device__ __forceinline__ void emit_levels(float* acc, int KD, int D, LdsRowFn lds_row, GlobalRowFn global_row,
                                             ActFn act) {
-    for (int l = 0; l < KD; ++l) {
-        const uint4* r = lds_row(l);
-        uint4 w[NV];
-#pragma unroll
-        for (int c = 0; c < NV; ++c) w[c] = r[c * LANES];
-        axpy<NV, WBF>(acc, act(l), w);
-    }
-    if (KD > D) return;
     uint4 cur[NV], nxt[NV];
     float a_cur, a_nxt;
     auto load = [&](uint4* dst, float& a, int l) {
@@ -381,9 +373,20 @@ __device__ __forceinline__ void emit_levels(float* acc, int KD, int D, LdsRowFn 
         for (int c = 0; c < NV; ++c) dst[c] = r[c * LANES];
         a = act(l);
     };
+    // The first global row is in flight while the LDS levels are accumulated;
     // sched_barrier keeps each prefetch above the FMAs it is meant to overlap
     // (the scheduler would otherwise sink it to its use to save registers).
-    load(cur, a_cur, KD);
+    const bool global = KD <= D;
+    if (global) load(cur, a_cur, KD);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int l = 0; l < KD; ++l) {
+        const uint4* r = lds_row(l);
+        uint4 w[NV];
+#pragma unroll
+        for (int c = 0; c < NV; ++c) w[c] = r[c * LANES];
+        axpy<NV, WBF>(acc, act(l), w);
+    }
+    if (!global) return;
     for (int l = KD;; l += 2) {
         load(nxt, a_nxt, l + 1 <= D ? l + 1 : D);
         __builtin_amdgcn_sched_barrier(0);

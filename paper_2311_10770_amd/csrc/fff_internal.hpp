@@ -115,6 +115,7 @@ struct Plan {
     Launch launch[3];              // descent/generic: [0]; grouped: walk, scatter (optional), emit
     int n_launch = 0;
     int lanes = 0;                 // lanes per token
+    int emit_lanes = 0;            // lanes per token of the grouped emit
     int lds_levels = 0;            // descent, generic, grouped walk
     int emit_lds_levels = 0;       // grouped emit
     int split_level = 0;           // grouped mode

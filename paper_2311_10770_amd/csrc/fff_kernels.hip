@@ -209,11 +209,12 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
 
 constexpr int EMIT_SCAN_PER_THREAD = 4;
 
-// Subtree of a token at the split level k (tree 0), and the XCD that owns it.
-__device__ __forceinline__ int owner_xcd(const Params& p, int64_t tok) {
+// XCD owning the subtree of a token whose tree-0 leaf is `leaf`: its node at
+// the split level k, counted within the level, modulo the XCD count.
+__device__ __forceinline__ int owner_xcd(const Params& p, int32_t leaf) {
     const int k = p.split_level, D = p.depth;
-    const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * p.n_trees]) + 1;
-    const uint32_t bucket = (leaf1 >> (D - k)) - (1u << k);  // node at level k minus the level's first node
+    const uint32_t leaf1 = uint32_t(leaf) + 1;
+    const uint32_t bucket = (leaf1 >> (D - k)) - (1u << k);
     return int(bucket % XCDS);
 }
 
@@ -223,7 +224,8 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
     constexpr int WAVES = BLOCK / 64;
     constexpr int SCAN = BLOCK * EMIT_SCAN_PER_THREAD;
     extern __shared__ uint4 lds_out[];  // [T][Nk][ROWV] W_out rows of the top levels
-    __shared__ int32_t queue[SCAN];
+    __shared__ int32_t queue[SCAN];       // token
+    __shared__ int32_t queue_leaf[SCAN];  // its tree-0 leaf
     __shared__ int32_t queue_len;
 
     const int tid = threadIdx.x;
@@ -248,6 +250,16 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
     const int64_t b0 = local * chunk;
     const int64_t b1 = b0 + chunk < p.n_tokens ? b0 + chunk : p.n_tokens;
 
+    // What a token group needs before its first row: the token, its tree-0 leaf and
+    // tree-0 activations (one level per lane, broadcast when used).  Fetched one
+    // group ahead so that these loads are off the critical path.
+    struct GroupIn {
+        int64_t tok;
+        uint32_t leaf1;
+        bool valid;
+        LevelRegs<LANES> av;
+    };
+
     for (int64_t base = b0; base < b1; base += SCAN) {
         int count;
         if (affine) {
@@ -256,14 +268,18 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
 #pragma unroll
             for (int i = 0; i < EMIT_SCAN_PER_THREAD; ++i) {
                 const int64_t b = base + int64_t(i) * BLOCK + tid;
-                const bool take = b < b1 && owner_xcd(p, b) == xcd;
+                const int32_t leaf = b < b1 ? p.ws_leaf[b * T] : 0;
+                const bool take = b < b1 && owner_xcd(p, leaf) == xcd;
                 const uint64_t mask = __ballot(take);
                 const int before = __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32),
                                                               __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0));
                 int wbase = 0;
                 if (lane == 0 && mask) wbase = atomicAdd(&queue_len, __popcll(mask));
                 wbase = __builtin_amdgcn_readfirstlane(wbase);
-                if (take) queue[wbase + before] = int32_t(b);
+                if (take) {
+                    queue[wbase + before] = int32_t(b);
+                    queue_leaf[wbase + before] = leaf;
+                }
             }
             __syncthreads();
             count = queue_len;
@@ -272,27 +288,54 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
             count = int(b1 - base < SCAN ? b1 - base : SCAN);
         }
         const int groups = (count + S::TPW - 1) / S::TPW;
-        for (int g = wave; g < groups; g += WAVES) {
+        auto fetch = [&](int g) {
+            GroupIn in;
             const int idx_raw = g * S::TPW + sub;
-            const bool valid = idx_raw < count;
-            const int idx = valid ? idx_raw : count - 1;
-            const int64_t tok = affine ? int64_t(queue[idx]) : base + idx;
-            float acc[S::E];
+            in.valid = idx_raw < count;
+            const int idx = in.valid ? idx_raw : count - 1;
+            in.tok = affine ? int64_t(queue[idx]) : base + idx;
+            in.leaf1 = uint32_t(affine ? queue_leaf[idx] : p.ws_leaf[in.tok * T]) + 1;
+            const float* arec = p.ws_act + in.tok * T * (D + 1);
 #pragma unroll
-            for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
-            for (int t = 0; t < T; ++t) {
-                const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * T + t]) + 1;
-                const float* arec = p.ws_act + (tok * T + t) * (D + 1);  // one address per group
-                const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + int64_t(t) * N * S::ROWV + sl;
-                const uint4* lrows = lds_out + int64_t(t) * Nk * S::ROWV + sl;
-                emit_levels<LANES, NV, WBF>(
-                    acc, KD, D, [&](int l) { return lrows + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
-                    [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
-                    [&](int l) { return arec[l]; });
+            for (int r = 0; r < LevelRegs<LANES>::NR; ++r) {
+                const int l = r * LANES + sl;
+                in.av.v[r] = l <= D ? arec[l] : 0.0f;
             }
-            XRegs<LANES, NV, XBF, WBF> xr;
-            if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
-            if (valid) store_output<LANES, NV, WBF>(p, xr, acc, tok, sl);
+            return in;
+        };
+        if (wave < groups) {  // wave-uniform
+            GroupIn cur = fetch(wave);
+            for (int g = wave; g < groups; g += WAVES) {
+                GroupIn nxt = cur;
+                if (g + WAVES < groups) nxt = fetch(g + WAVES);
+                const int64_t tok = cur.tok;
+                float acc[S::E];
+#pragma unroll
+                for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
+                {
+                    const uint32_t leaf1 = cur.leaf1;
+                    const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + sl;
+                    const uint4* lrows = lds_out + sl;
+                    emit_levels<LANES, NV, WBF>(
+                        acc, KD, D, [&](int l) { return lrows + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                        [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                        [&](int l) { return cur.av.get(l, lane); });
+                }
+                for (int t = 1; t < T; ++t) {
+                    const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * T + t]) + 1;
+                    const float* arec = p.ws_act + (tok * T + t) * (D + 1);  // one address per group
+                    const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + int64_t(t) * N * S::ROWV + sl;
+                    const uint4* lrows = lds_out + int64_t(t) * Nk * S::ROWV + sl;
+                    emit_levels<LANES, NV, WBF>(
+                        acc, KD, D, [&](int l) { return lrows + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                        [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                        [&](int l) { return arec[l]; });
+                }
+                XRegs<LANES, NV, XBF, WBF> xr;
+                if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
+                if (cur.valid) store_output<LANES, NV, WBF>(p, xr, acc, tok, sl);
+                cur = nxt;
+            }
         }
         if (affine) __syncthreads();  // the queue is refilled next round
     }
@@ -498,6 +541,7 @@ struct Variant {
     int hidden;
     bool xbf, wbf;
     int lanes;
+    int emit_lanes;  // the emit has no cross-lane reduction: wider groups hold fewer registers per lane
     const void* descent;
     const void* walk;
     const void* emit;
@@ -510,31 +554,31 @@ struct Variant {
 };
 
 #define FFF_K(...) reinterpret_cast<const void*>(&__VA_ARGS__)
-#define FFF_VARIANT(H, XB, WB, L, NV)                                                                         \
+#define FFF_VARIANT(H, XB, WB, L, NV, EL, ENV)                                                                \
     Variant {                                                                                                 \
-        H, XB, WB, L, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                     \
-            FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<L, NV, XB, WB, BLOCK>),        \
+        H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
+            FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<L, NV, false, WB, BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
     }
 
 static const Variant kVariants[] = {
-    // H = 768 (BERT-base width)
-    FFF_VARIANT(768, true, true, 16, 6),
-    FFF_VARIANT(768, false, true, 16, 6),
-    FFF_VARIANT(768, false, false, 32, 6),
-    FFF_VARIANT(768, true, false, 32, 6),
+    // H = 768 (BERT-base width); the emit takes 32 (bf16 W) or 64 (fp32 W) lanes per token
+    FFF_VARIANT(768, true, true, 16, 6, 32, 3),
+    FFF_VARIANT(768, false, true, 16, 6, 32, 3),
+    FFF_VARIANT(768, false, false, 32, 6, 64, 3),
+    FFF_VARIANT(768, true, false, 32, 6, 64, 3),
     // H = 1024
-    FFF_VARIANT(1024, true, true, 16, 8),
-    FFF_VARIANT(1024, false, true, 16, 8),
-    FFF_VARIANT(1024, false, false, 32, 8),
-    FFF_VARIANT(1024, true, false, 32, 8),
+    FFF_VARIANT(1024, true, true, 16, 8, 32, 4),
+    FFF_VARIANT(1024, false, true, 16, 8, 32, 4),
+    FFF_VARIANT(1024, false, false, 32, 8, 64, 4),
+    FFF_VARIANT(1024, true, false, 32, 8, 64, 4),
     // H = 4096 (LLM width)
-    FFF_VARIANT(4096, true, true, 64, 8),
-    FFF_VARIANT(4096, false, true, 64, 8),
-    FFF_VARIANT(4096, false, false, 64, 16),
-    FFF_VARIANT(4096, true, false, 64, 16),
+    FFF_VARIANT(4096, true, true, 64, 8, 64, 8),
+    FFF_VARIANT(4096, false, true, 64, 8, 64, 8),
+    FFF_VARIANT(4096, false, false, 64, 16, 64, 16),
+    FFF_VARIANT(4096, true, false, 64, 16, 64, 16),
 };
 
 static const void* generic_kernel_for(bool xbf, bool wbf) {
@@ -660,7 +704,9 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         E.kernel = v->emit;
         E.block = BLOCK;
         E.lds_bytes = rows_lds_bytes(p, ke, 1);
-        int eg = resident_grid(dev, E.kernel, E.lds_bytes, want);
+        const int64_t egroups = token_groups(p, v->emit_lanes);
+        plan->emit_lanes = v->emit_lanes;
+        int eg = resident_grid(dev, E.kernel, E.lds_bytes, (egroups + BLOCK / 64 - 1) / (BLOCK / 64));
         if (split) eg = std::max(XCDS, eg / XCDS * XCDS);  // every XCD gets the same number of workgroups
         E.grid = eg;
         plan->emit_lds_levels = ke;
