@@ -72,6 +72,11 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * tokens grouped by their tree-0 node at a split level, each group's subtree
  * handled by the workgroups of one XCD so that its rows stay in that XCD's L2.
  * GENERIC: any hidden size, one wave per token.
+ * TILED: one tree, depth 5..16, hidden a multiple of 128: the walk drops each
+ * token into a bucket of its leaf, and the output rows of up to 16 tokens that
+ * share a leaf (hence all D+1 nodes) are accumulated as one dense product on
+ * MFMA (fp32); tokens past a full bucket take the per-token emit.  Needs the
+ * workspace of fff_workspace_bytes.
  * AUTO: GROUPED for single-tree layers with hidden <= 1024 when a large enough
  * workspace is passed, else DESCENT when a kernel is compiled for the hidden
  * size and types, else GENERIC. */
@@ -79,7 +84,8 @@ typedef enum {
     FFF_MODE_AUTO = 0,
     FFF_MODE_DESCENT = 1,
     FFF_MODE_GROUPED = 2,
-    FFF_MODE_GENERIC = 3
+    FFF_MODE_GENERIC = 3,
+    FFF_MODE_TILED = 4
 } fff_mode;
 
 /* What is written to y: FFF(u); y + FFF(u); or x + FFF(u) (the residual of a
@@ -146,9 +152,12 @@ typedef struct {
 
 int fff_forward_ex(const fff_args* a);
 
-/* Device scratch bytes GROUPED mode needs for n_tokens tokens: one fp32
- * activation per visited node and one int32 leaf per (token, tree).  The
- * split level (-1..depth) does not change it.  Returns 0 for invalid shapes. */
+/* Device scratch bytes GROUPED and TILED mode need for n_tokens tokens: one
+ * fp32 activation per visited node and one int32 leaf per (token, tree), plus
+ * for TILED the leaf buckets (int32 counts; token slots, a few times the mean
+ * tokens per leaf, each with its D+1 fp32 activations; a spill list).  The
+ * result covers both modes; the split level (-1..depth) does not change it.
+ * Returns 0 for invalid shapes. */
 size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,
                            int32_t split_level);
 

@@ -31,6 +31,13 @@ struct Params {
     float* ws_act;        // [B, T, D+1] activation of every visited node
     int32_t* ws_leaf;     // [B, T] leaf reached in each tree
     int32_t split_level;  // group tokens by their tree-0 node at this level; 0 = keep token order
+    // tiled mode: tokens bucketed by their tree-0 leaf during the walk
+    int32_t* bk_count;    // [2^D] tokens that reached each leaf
+    int32_t* bk_tok;      // [2^D, bk_cap] the first bk_cap of them, in arrival order
+    int32_t* bk_spill;    // [B] tokens that found their bucket full
+    int32_t* bk_nspill;   // [1] how many
+    float* bk_act;        // [2^D, bk_cap, D+1] activations of the bucketed tokens, by slot
+    int32_t bk_cap;
     // LayerNorm prologue (norm = 1): u = (x - mean) / sqrt(var + eps) * gamma + beta
     int32_t norm;
     float norm_eps;
@@ -101,7 +108,7 @@ struct DeviceInfo {
     size_t lds_per_cu = 0;     // bytes
 };
 
-enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4 };
+enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4, KIND_TILED = 5 };
 
 struct Launch {
     const void* kernel = nullptr;  // __global__ function handle
@@ -145,6 +152,8 @@ hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream
 
 // Grouped mode scratch size for a resolved split level (0 = no bucketing).
 size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t split_level);
+// Tiled mode scratch (grouped scratch plus the leaf buckets); 0 when the shape has no tiled mode.
+size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
 // Split level used when the caller asks for the default (0 in fff_args).
 int default_split_level(int32_t depth, int32_t n_trees);
 

@@ -32,10 +32,11 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <type_traits>
 
 namespace fff {
 
-enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3 };
+enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3, MODE_TILED = 4 };
 // status values mirrored from fff.h
 enum { ST_OK = 0, ST_INVALID = -1, ST_UNSUPPORTED = -2, ST_WORKSPACE = -3 };
 
@@ -192,12 +193,26 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
             const uint4* lrows = lds_in + int64_t(t) * Nk * S::ROWV + sl;
             LevelRegs<LANES> lv;
             const uint32_t leaf1 = walk_tree<LANES, NV, XR_BF, WBF>(xr, lrows, S::ROWV, win, KD, D, sl, lv);
+            float* rec = p.ws_act + (tok * T + t) * (D + 1);
+            if (p.bk_count && t == 0) {
+                // tiled mode: take the next slot of this leaf's bucket; the activations
+                // go to the slot, or to the token's record once the bucket is full
+                const int64_t bin = int64_t(leaf1) - (int64_t(1) << D);
+                int32_t pos = 0;
+                if (valid && sl == 0) pos = atomicAdd(&p.bk_count[bin], 1);
+                pos = __float_as_int(group_bcast<LANES>(__int_as_float(pos), lane, 0));
+                if (valid && pos < p.bk_cap) {
+                    rec = p.bk_act + (bin * p.bk_cap + pos) * (D + 1);
+                    if (sl == 0) p.bk_tok[bin * p.bk_cap + pos] = int32_t(tok);
+                } else if (valid && sl == 0) {
+                    p.bk_spill[atomicAdd(p.bk_nspill, 1)] = int32_t(tok);
+                }
+            }
             if (valid) {
-                const int64_t rec0 = (tok * T + t) * (D + 1);
 #pragma unroll
                 for (int r = 0; r < LevelRegs<LANES>::NR; ++r) {
                     const int l = r * LANES + sl;
-                    if (l <= D) p.ws_act[rec0 + l] = activation(lv.v[r], p.act);
+                    if (l <= D) rec[l] = activation(lv.v[r], p.act);
                 }
                 if (sl == 0) p.ws_leaf[tok * T + t] = int32_t(leaf1 - 1);
                 if (p.nodes_out || p.logits_out)
@@ -339,6 +354,233 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
         }
         if (affine) __syncthreads();  // the queue is refilled next round
     }
+}
+
+// ----------------------------------------------------------------------------
+// TILED: the output accumulation of tokens that share a leaf on MFMA
+// ----------------------------------------------------------------------------
+//
+// Tokens that reach the same leaf visit the same D+1 nodes, so for a tile of
+// up to 16 of them the output is a dense product
+//     Y[16 tokens, H] = A[16 tokens, D+1 levels] x W_out[path rows, H],
+// with A the tokens' activations.  v_mfma_f32_16x16x4_f32 takes four levels
+// per step: lane l supplies A[l%16][l/16] (token l%16, level 4s + l/16) and
+// B[l/16][l%16], and receives D[4(l/16)+r][l%16].  One workgroup takes one
+// leaf; its wave w takes the 128-column groups g = w, w + waves, ...  In group
+// g, MFMA column n of block j is output column 128 g + 8 n + j: lane n loads
+// the eight consecutive weights 128 g + 8n .. +7 of a row with one 16-byte
+// load (the sixteen lanes of a level read 256 contiguous bytes), keeps them in
+// registers for all of the leaf's tiles, and stores eight consecutive output
+// columns of four tokens (sixteen lanes write 256 contiguous bytes of a
+// token's row).  fp32 throughout (the weights are widened exactly); the MFMA
+// accumulates the products over levels in fp32.  Tokens whose bucket was full
+// (more than bk_cap reached one leaf) are handled by extra workgroups with the
+// per-token emit.
+
+constexpr int TILE_MAX_STEPS = 5;  // depth <= 16: at most 17 levels, five steps of four
+
+// Waves per tiled workgroup for hidden size h: one per 128-column group, at most 8
+// (larger workgroups would cap the registers of the spill path below 128).
+constexpr int tile_waves(int h) { return h / 128 < 8 ? h / 128 : 8; }
+
+template <bool WBF>
+__device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out) {
+    if constexpr (WBF) {
+        const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(w) + at);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            out[2 * j] = bf16_lo(word(v, j));
+            out[2 * j + 1] = bf16_hi(word(v, j));
+        }
+    } else {
+        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(w) + at);
+        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(w) + at + 4);
+        out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+        out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+    }
+}
+
+// Eight consecutive output columns of one token: combine (residual / accumulate) and store.
+__device__ __forceinline__ void tile_store8(const Params& p, int64_t tok, int64_t col, const float* v8) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = v8[i];
+    const int64_t at = tok * p.hidden + col;
+    if (p.out_mode == OUT_RESIDUAL) {
+        float xv[8];
+        if (p.x_bf16) tile_load8<true>(p.x, at, xv);
+        else tile_load8<false>(p.x, at, xv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += xv[i];
+    }
+    if (p.y_bf16) {
+        uint4* d = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p.y) + at);
+        if (p.out_mode == OUT_ACCUMULATE) {
+            const uint4 o = *d;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                v[2 * j] += bf16_lo(word(o, j));
+                v[2 * j + 1] += bf16_hi(word(o, j));
+            }
+        }
+        *d = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                        pack_bf16x2(v[6], v[7]));
+    } else {
+        float4* d = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.y) + at);
+        if (p.out_mode == OUT_ACCUMULATE) {
+            const float4 a = d[0], b = d[1];
+            v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+            v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+        }
+        d[0] = make_float4(v[0], v[1], v[2], v[3]);
+        d[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+}
+
+typedef float tile_v4f __attribute__((ext_vector_type(4)));
+
+// Grid: one workgroup per leaf (XCD-affine by the subtree at the split level),
+// then spill workgroups.  ELANES/ENV: the per-token emit layout for spilled tokens.
+template <int CB, bool XBF, bool WBF, int ELANES, int ENV>
+__global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
+    constexpr int H = 16 * CB;
+    static_assert(H % 128 == 0, "128-column groups");
+    constexpr int GROUPS = H / 128;
+    constexpr int WAVES = tile_waves(H);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int D = p.depth;
+    const int64_t L = int64_t(1) << D;
+
+    if (int(blockIdx.x) >= leaf_blocks) {
+        // spilled tokens: the per-token emit (all levels from global memory)
+        using S = Shape<ELANES, ENV, XBF, WBF>;
+        const int sl = lane % ELANES, sub = lane / ELANES;
+        const int64_t count = *p.bk_nspill;
+        const int64_t groups = (count + S::TPW - 1) / S::TPW;
+        const int64_t stride = int64_t(gridDim.x - leaf_blocks) * WAVES;
+        for (int64_t g = int64_t(blockIdx.x - leaf_blocks) * WAVES + wave; g < groups; g += stride) {
+            const int64_t idx_raw = g * S::TPW + sub;
+            const bool valid = idx_raw < count;
+            const int64_t tok = p.bk_spill[valid ? idx_raw : count - 1];
+            const uint32_t leaf1 = uint32_t(p.ws_leaf[tok]) + 1;
+            const float* arec = p.ws_act + tok * (D + 1);
+            const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + sl;
+            float acc[S::E];
+#pragma unroll
+            for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
+            emit_levels<ELANES, ENV, WBF>(
+                acc, 0, D, [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
+                [&](int l) { return arec[l]; });
+            XRegs<ELANES, ENV, XBF, WBF> xr;
+            if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
+            if (valid) store_output<ELANES, ENV, WBF>(p, xr, acc, tok, sl);
+        }
+        return;
+    }
+
+    // this workgroup's leaf: XCD x (blockIdx % 8) takes the subtrees at the split level that are x mod 8
+    int64_t leaf = blockIdx.x;
+    if (p.split_level > 0) {
+        const int64_t per = int64_t(1) << (D - p.split_level);  // leaves per subtree
+        const int64_t x = blockIdx.x % XCDS, lb = blockIdx.x / XCDS;
+        leaf = (x + XCDS * (lb / per)) * per + lb % per;
+    }
+    const int32_t cnt_all = p.bk_count[leaf];
+    const int cnt = cnt_all < p.bk_cap ? cnt_all : p.bk_cap;
+    if (cnt == 0) return;  // workgroup-uniform
+    const uint32_t leaf1 = uint32_t(leaf + L);
+    const int n = lane & 15, kq = lane >> 4;
+    const int steps = (D + 4) / 4;
+    const int cap = p.bk_cap;
+    const int32_t* bucket = p.bk_tok + leaf * cap;
+    const float* act = p.bk_act + leaf * int64_t(cap) * (D + 1);
+    // Operands of the tile at slot t0 for this lane: token id of slot t0 + n and
+    // its activations at levels 4s + kq.  Indices are clamped into the bucket so
+    // that every load is in bounds; out-of-range values are replaced by 0 / -1.
+    auto load_tile = [&](int t0, int32_t& tok, float* a) {
+        const int slot = t0 + n < cap ? t0 + n : cap - 1;
+        const bool in = t0 + n < cnt;
+        const int32_t tv = bucket[slot];
+#pragma unroll
+        for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+            const int lvl = 4 * s + kq;
+            float v = 0.0f;
+            if (s < steps) v = act[int64_t(slot) * (D + 1) + (lvl <= D ? lvl : D)];
+            a[s] = in && lvl <= D ? v : 0.0f;
+        }
+        tok = in ? tv : -1;
+    };
+    for (int g = wave; g < GROUPS; g += WAVES) {
+        const int64_t col = int64_t(g) * 128 + 8 * n;
+        // B operand: this lane's eight weights of the row at level 4s + kq (levels
+        // past D read row 0; their A is 0), kept as loaded for all of the leaf's tiles
+        using WRaw = typename std::conditional<WBF, uint4, float4[2]>::type;
+        WRaw w[TILE_MAX_STEPS];
+#pragma unroll
+        for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+            const int lvl = 4 * s + kq;
+            if (s < steps) {
+                const int64_t at = (lvl <= D ? int64_t(leaf1 >> (D - lvl)) - 1 : 0) * H + col;
+                if constexpr (WBF) {
+                    w[s] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w_out) + at);
+                } else {
+                    w[s][0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at);
+                    w[s][1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at + 4);
+                }
+            }
+        }
+        int32_t tok_c;
+        float a_c[TILE_MAX_STEPS];
+        load_tile(0, tok_c, a_c);
+        for (int t0 = 0; t0 < cnt; t0 += 16) {
+            int32_t tok_n;
+            float a_n[TILE_MAX_STEPS];
+            load_tile(t0 + 16, tok_n, a_n);  // next tile (all -1 / 0 past the count)
+            tile_v4f acc[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+                if (s < steps) {
+                    float b[8];
+                    if constexpr (WBF) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            b[2 * j] = bf16_lo(word(w[s], j));
+                            b[2 * j + 1] = bf16_hi(word(w[s], j));
+                        }
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            b[j] = fword(w[s][0], j);
+                            b[4 + j] = fword(w[s][1], j);
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_c[s], b[j], acc[j], 0, 0, 0);
+                }
+            }
+            // lane (n, kq) holds tokens 4 kq + r of the tile: their ids from the lanes that loaded them
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int32_t tok = __shfl(tok_c, 4 * kq + r, 64);
+                if (tok < 0) continue;
+                float v8[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
+                tile_store8(p, tok, col, v8);
+            }
+            tok_c = tok_n;
+#pragma unroll
+            for (int s = 0; s < TILE_MAX_STEPS; ++s) a_c[s] = a_n[s];
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* a, int64_t n) {
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) a[i] = 0;
 }
 
 // ----------------------------------------------------------------------------
@@ -545,6 +787,7 @@ struct Variant {
     const void* descent;
     const void* walk;
     const void* emit;
+    const void* tile;
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -558,6 +801,7 @@ struct Variant {
     Variant {                                                                                                 \
         H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
             FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
+            FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV>),                                                      \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<L, NV, false, WB, BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -642,6 +886,30 @@ size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees,
     return align256(recs * size_t(depth + 1) * sizeof(float)) + align256(recs * sizeof(int32_t));
 }
 
+// Tiled mode: one tree, depth 5..16, hidden a multiple of 128 (eight column blocks of 16 per load).
+static bool tiled_shape(int32_t depth, int32_t n_trees, int32_t hidden) {
+    return n_trees == 1 && depth >= 5 && depth <= 16 && hidden % 128 == 0;
+}
+
+// Bucket capacity: four times the mean tokens per leaf, at least one tile of 16, a multiple of 16.
+static int32_t tile_cap(int64_t n_tokens, int32_t depth) {
+    const int64_t leaves = int64_t(1) << depth;
+    const int64_t mean = (n_tokens + leaves - 1) / leaves;
+    return int32_t(std::max<int64_t>(16, (4 * mean + 15) / 16 * 16));
+}
+
+// Tiled workspace, in order: token records and leaves (as grouped; the records
+// are used by spilled tokens only), bucket counts + spill count, bucket token
+// ids, spill list, bucket activation records.
+size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
+    if (!tiled_shape(depth, n_trees, hidden)) return 0;
+    const size_t leaves = size_t(1) << depth;
+    const size_t cap = size_t(tile_cap(n_tokens, depth));
+    return grouped_workspace_bytes(n_tokens, depth, n_trees, 0) + align256((leaves + 1) * sizeof(int32_t)) +
+           align256(leaves * cap * sizeof(int32_t)) + align256(size_t(n_tokens) * sizeof(int32_t)) +
+           align256(leaves * cap * size_t(depth + 1) * sizeof(float));
+}
+
 static const Variant* find_variant(const Params& p) {
     for (const auto& c : kVariants)
         if (c.hidden == p.hidden && c.xbf == bool(p.x_bf16) && c.wbf == bool(p.w_bf16)) return &c;
@@ -654,7 +922,36 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
                  const DeviceInfo& dev, Plan* plan) {
     *plan = Plan{};
     const Variant* v = find_variant(p);
-    if ((mode == MODE_DESCENT || mode == MODE_GROUPED) && !v) return ST_UNSUPPORTED;
+    if ((mode == MODE_DESCENT || mode == MODE_GROUPED || mode == MODE_TILED) && !v) return ST_UNSUPPORTED;
+    if (mode == MODE_TILED) {
+        if (!tiled_shape(p.depth, p.n_trees, p.hidden)) return ST_UNSUPPORTED;
+        bool ok;
+        const int kw = pick_levels(p, lds_levels_req, 1, WALK_LDS_BUDGET, dev.lds_per_block, &ok);
+        if (!ok) return ST_UNSUPPORTED;
+        plan->kind = KIND_TILED;
+        plan->lanes = v->lanes;
+        plan->emit_lanes = v->emit_lanes;
+        plan->lds_levels = kw;
+        plan->split_level = std::min<int>(p.depth - 2, 5);  // subtrees of at least four leaves
+        plan->name = v->name;
+        const int64_t leaves = int64_t(1) << p.depth;
+        Launch& F = plan->launch[plan->n_launch++];
+        F.kernel = reinterpret_cast<const void*>(&fill_i32_kernel);
+        F.block = 256;
+        F.grid = int(std::min<int64_t>((leaves + 1 + 255) / 256, int64_t(dev.cu_count) * 4));
+        Launch& W = plan->launch[plan->n_launch++];
+        W.kernel = p.norm ? v->walk_norm : v->walk;
+        W.block = BLOCK;
+        W.lds_bytes = rows_lds_bytes(p, kw, 1);
+        W.grid = resident_grid(dev, W.kernel, W.lds_bytes,
+                               (token_groups(p, v->lanes) + BLOCK / 64 - 1) / (BLOCK / 64));
+        Launch& E = plan->launch[plan->n_launch++];
+        E.kernel = v->tile;
+        E.block = 64 * tile_waves(p.hidden);
+        // one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
+        E.grid = int(leaves) + dev.cu_count;
+        return ST_OK;
+    }
     if (mode == MODE_AUTO) {
         // Measured on MI355X: the two-kernel grouped path wins for single trees with 16/32-lane
         // tokens (hidden <= 1024); the fused kernel wins for multi-tree layers and 64-lane tokens.
@@ -764,6 +1061,42 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         q.ws_leaf = reinterpret_cast<int32_t*>(ws + align256(recs * size_t(p.depth + 1) * sizeof(float)));
         q.split_level = plan.split_level;
         (void)workspace_bytes;
+    }
+    if (plan.kind == KIND_TILED) {
+        const size_t recs = size_t(p.n_tokens);
+        const int64_t leaves = int64_t(1) << p.depth;
+        char* ws = static_cast<char*>(workspace);
+        q.ws_act = reinterpret_cast<float*>(ws);
+        ws += align256(recs * size_t(p.depth + 1) * sizeof(float));
+        q.ws_leaf = reinterpret_cast<int32_t*>(ws);
+        ws += align256(recs * sizeof(int32_t));
+        q.bk_count = reinterpret_cast<int32_t*>(ws);
+        q.bk_nspill = q.bk_count + leaves;
+        ws += align256((size_t(leaves) + 1) * sizeof(int32_t));
+        q.bk_cap = tile_cap(p.n_tokens, p.depth);
+        q.bk_tok = reinterpret_cast<int32_t*>(ws);
+        ws += align256(size_t(leaves) * size_t(q.bk_cap) * sizeof(int32_t));
+        q.bk_spill = reinterpret_cast<int32_t*>(ws);
+        ws += align256(recs * sizeof(int32_t));
+        q.bk_act = reinterpret_cast<float*>(ws);
+        q.split_level = plan.split_level;
+        (void)workspace_bytes;
+        int32_t* fa = q.bk_count;
+        int64_t fn = leaves + 1;
+        void* fargs[] = {&fa, &fn};
+        const Launch& F = plan.launch[0];
+        hipError_t e = hipLaunchKernel(F.kernel, dim3(F.grid), dim3(F.block), fargs, 0, stream);
+        if (e != hipSuccess) return e;
+        void* wargs[] = {&q};
+        const Launch& W = plan.launch[1];
+        e = hipLaunchKernel(W.kernel, dim3(W.grid), dim3(W.block), wargs, W.lds_bytes, stream);
+        if (e != hipSuccess) return e;
+        Params qt = q;
+        qt.bk_count = q.bk_count;  // read-only from here on
+        int leaf_blocks = int(leaves);
+        void* targs[] = {&qt, &leaf_blocks};
+        const Launch& E = plan.launch[2];
+        return hipLaunchKernel(E.kernel, dim3(E.grid), dim3(E.block), targs, 0, stream);
     }
     for (int i = 0; i < plan.n_launch; ++i) {
         const Launch& L = plan.launch[i];

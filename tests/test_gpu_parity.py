@@ -291,3 +291,69 @@ def test_errors_surface_as_exceptions(fff_lib):
         fff_lib.forward(xb, wi, wo, 3, 1, y=buf[768:].view(16, 768))  # y overlaps x without being x
     with pytest.raises(fff_lib.FffError):
         fff_lib.forward(x[:8], wi, wo, 3, 1, y=wi.view(-1)[:8 * 768].view(8, 768))  # y overlaps W_in
+
+
+# ----------------------------------------------------------------- tiled mode
+
+
+@pytest.mark.parametrize("xd,wd,yd", DTYPE_COMBOS)
+@pytest.mark.parametrize("H", [768, 1024, 4096])
+def test_tiled_dtype_combinations(fff_lib, xd, wd, yd, H):
+    depth = 7 if H == 4096 else 9
+    L = layer(190 + H, 1500, H, depth, 1, xd, wd)
+    check_layer(fff_lib, f"tiled {xd}/{wd}/{yd} H={H}", L, depth, 1, yd, mode="tiled")
+
+
+@pytest.mark.parametrize("B", [1, 7, 100, 2049, 30001])
+@pytest.mark.parametrize("depth", [5, 8, 11, 16])
+def test_tiled_ragged_and_depths(fff_lib, B, depth):
+    L = layer(200 + B + depth, B, 768, depth, 1, "bf16", "bf16")
+    check_layer(fff_lib, f"tiled B={B} D={depth}", L, depth, 1, "bf16", mode="tiled")
+
+
+@pytest.mark.parametrize("out", ["residual", "accumulate"])
+def test_tiled_output_modes(fff_lib, out):
+    L = layer(210, 3000, 768, 11, 1, "f32", "f32")
+    y0 = synth.make_x(211, 3000, 768, "f32")
+    got = run_fff(fff_lib, L, 11, 1, "f32", mode="tiled", out=out, y_init=y0 if out == "accumulate" else None)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 11, 1)
+    base = L["x"] if out == "residual" else y0
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 11, 1, ref, got["y"], got["nodes"], tol=1e-5,
+                         base_dev=base)
+
+
+def test_tiled_skewed_routing_spills(fff_lib):
+    """Clustered tokens crowd a few leaves: most of them overflow their bucket and take the spill path."""
+    B, H, D = 20000, 768, 11
+    x = synth.make_clustered_x(220, B, H, "bf16", n_centres=8)
+    wi, wo = synth.make_weights(220, H, D, 1, "bf16")
+    check_layer(fff_lib, "tiled clustered", {"x": x, "w_in": wi, "w_out": wo}, D, 1, "bf16", mode="tiled")
+
+
+def test_tiled_headline_full_size(fff_lib):
+    w = WORKLOADS["d11_h768_b65536_bf16"]
+    L = synth.make_layer(w.seed, w.n_tokens, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    check_layer(fff_lib, "tiled headline", L, w.depth, w.n_trees, w.y_dtype, mode="tiled")
+
+
+def test_tiled_with_layernorm(fff_lib):
+    L = layer(230, 5000, 768, 11, 1, "bf16", "bf16")
+    gamma, beta = synth.make_norm(230, 768)
+    x = fff_lib.from_numpy(L["x"], DEV)
+    wi, wo = fff_lib.from_numpy(L["w_in"], DEV), fff_lib.from_numpy(L["w_out"], DEV)
+    kw = dict(norm="layernorm", norm_eps=1e-5, norm_gamma=fff_lib.from_numpy(gamma, DEV),
+              norm_beta=fff_lib.from_numpy(beta, DEV), out="residual")
+    yt = fff_lib.forward(x, wi, wo, 11, 1, mode="tiled", y_dtype=torch.float32, **kw)
+    yg = fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", y_dtype=torch.float32, **kw)
+    torch.cuda.synchronize()
+    err = ((yt - yg).norm(dim=1) / (yg - x.float()).norm(dim=1)).max().item()
+    assert err < 1e-5, err
+
+
+def test_tiled_unsupported_shapes(fff_lib):
+    L = layer(240, 64, 768, 4, 1, "f32", "f32")  # depth below 5
+    with pytest.raises(fff_lib.FffError):
+        run_fff(fff_lib, L, 4, 1, "f32", mode="tiled")
+    L = layer(241, 64, 768, 6, 2, "f32", "f32")  # two trees
+    with pytest.raises(fff_lib.FffError):
+        run_fff(fff_lib, L, 6, 2, "f32", mode="tiled")
