@@ -72,11 +72,13 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * tokens grouped by their tree-0 node at a split level, each group's subtree
  * handled by the workgroups of one XCD so that its rows stay in that XCD's L2.
  * GENERIC: any hidden size, one wave per token.
- * TILED: one tree, depth 5..16, hidden a multiple of 128: the walk drops each
+ * TILED: one tree, depth 5..15, hidden a multiple of 128: the walk drops each
  * token into a bucket of its leaf, and the output rows of up to 16 tokens that
  * share a leaf (hence all D+1 nodes) are accumulated as one dense product on
- * MFMA (fp32); tokens past a full bucket take the per-token emit.  Needs the
- * workspace of fff_workspace_bytes.
+ * MFMA: fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
+ * activations split into bf16 parts (three parts: fp32 working accuracy; two,
+ * relative error about 2^-17, when y is a bf16 store).  Tokens past a full
+ * bucket take the per-token emit.  Needs the workspace of fff_workspace_bytes.
  * AUTO: GROUPED for single-tree layers with hidden <= 1024 when a large enough
  * workspace is passed, else DESCENT when a kernel is compiled for the hidden
  * size and types, else GENERIC. */

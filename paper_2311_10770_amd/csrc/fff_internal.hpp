@@ -36,7 +36,8 @@ struct Params {
     int32_t* bk_tok;      // [2^D, bk_cap] the first bk_cap of them, in arrival order
     int32_t* bk_spill;    // [B] tokens that found their bucket full
     int32_t* bk_nspill;   // [1] how many
-    float* bk_act;        // [2^D, bk_cap, D+1] activations of the bucketed tokens, by slot
+    float* bk_act;        // [2^D, bk_cap, TILE_REC] activations of the bucketed tokens, by slot
+    void* bk_junk;        // target of the stores of empty tile rows
     int32_t bk_cap;
     // LayerNorm prologue (norm = 1): u = (x - mean) / sqrt(var + eps) * gamma + beta
     int32_t norm;
@@ -100,6 +101,7 @@ size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int
 void bwd_workspace_views(BwdParams& p, void* workspace);
 
 constexpr int XCDS = 8;  // MI355X: 8 XCDs, workgroups dealt to them round-robin
+constexpr int TILE_REC = 16;  // floats per activation record of a bucketed token (tiled mode)
 
 struct DeviceInfo {
     int device = -1;

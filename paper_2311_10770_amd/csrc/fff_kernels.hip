@@ -202,7 +202,7 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
                 if (valid && sl == 0) pos = atomicAdd(&p.bk_count[bin], 1);
                 pos = __float_as_int(group_bcast<LANES>(__int_as_float(pos), lane, 0));
                 if (valid && pos < p.bk_cap) {
-                    rec = p.bk_act + (bin * p.bk_cap + pos) * (D + 1);
+                    rec = p.bk_act + (bin * p.bk_cap + pos) * TILE_REC;
                     if (sl == 0) p.bk_tok[bin * p.bk_cap + pos] = int32_t(tok);
                 } else if (valid && sl == 0) {
                     p.bk_spill[atomicAdd(p.bk_nspill, 1)] = int32_t(tok);
@@ -363,21 +363,33 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
 // Tokens that reach the same leaf visit the same D+1 nodes, so for a tile of
 // up to 16 of them the output is a dense product
 //     Y[16 tokens, H] = A[16 tokens, D+1 levels] x W_out[path rows, H],
-// with A the tokens' activations.  v_mfma_f32_16x16x4_f32 takes four levels
-// per step: lane l supplies A[l%16][l/16] (token l%16, level 4s + l/16) and
-// B[l/16][l%16], and receives D[4(l/16)+r][l%16].  One workgroup takes one
-// leaf; its wave w takes the 128-column groups g = w, w + waves, ...  In group
-// g, MFMA column n of block j is output column 128 g + 8 n + j: lane n loads
-// the eight consecutive weights 128 g + 8n .. +7 of a row with one 16-byte
-// load (the sixteen lanes of a level read 256 contiguous bytes), keeps them in
-// registers for all of the leaf's tiles, and stores eight consecutive output
-// columns of four tokens (sixteen lanes write 256 contiguous bytes of a
-// token's row).  fp32 throughout (the weights are widened exactly); the MFMA
-// accumulates the products over levels in fp32.  Tokens whose bucket was full
-// (more than bk_cap reached one leaf) are handled by extra workgroups with the
-// per-token emit.
+// with A the tokens' activations.  One workgroup takes one leaf; its wave w
+// takes the 128-column groups g = w, w + waves, ...  Every 16x16 MFMA used here
+// returns D[4(l/16)+r][l%16] to lane l, register r; in group g, MFMA column n of
+// block j is output column 128 g + 8 n + j, so a lane holds eight consecutive
+// output columns of four tokens and sixteen lanes write 256 contiguous bytes
+// of a token's row.
+//
+// bf16 weights: v_mfma_f32_16x16x32_bf16 takes 32 (level, part) products per
+// lane group.  Lane group q = l/16 covers levels 8(q%2) .. 8(q%2)+7; each
+// activation (fp32) is split into bf16 parts a = hi + mid + lo (each part the
+// rounded remainder of the previous ones, exact to fp32 working accuracy), and
+// group q supplies part q/2 in the first MFMA and part q/2 + 2 (lo, or zero)
+// in the second.  Two parts (hi + mid, relative error about 2^-17) are used
+// when y is stored in bf16, whose own rounding is 2^-9.  The B operand of
+// lane (n, q) for block j is the column 128 g + 8n + j of its eight path rows:
+// eight 16-byte row loads, transposed in registers once per leaf.  Products
+// of bf16 values are exact; the MFMA accumulates in fp32.
+//
+// fp32 weights: v_mfma_f32_16x16x4_f32, four levels per step: lane l supplies
+// A[l%16][l/16] (token l%16, level 4s + l/16) and the eight weights of its
+// level's row for blocks j = 0..7 from one 32-byte load.
+//
+// Activation records of bucketed tokens are TILE_REC floats apart (depth at
+// most 15).  Tokens whose bucket was full (more than bk_cap reached one leaf)
+// are handled by extra workgroups with the per-token emit.
 
-constexpr int TILE_MAX_STEPS = 5;  // depth <= 16: at most 17 levels, five steps of four
+constexpr int TILE_MAX_STEPS = 4;  // fp32 weights: depth <= 15, at most 16 levels, four steps of four
 
 // Waves per tiled workgroup for hidden size h: one per 128-column group, at most 8
 // (larger workgroups would cap the registers of the spill path below 128).
@@ -400,22 +412,34 @@ __device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out
     }
 }
 
-// Eight consecutive output columns of one token: combine (residual / accumulate) and store.
-__device__ __forceinline__ void tile_store8(const Params& p, int64_t tok, int64_t col, const float* v8) {
+// Output forms of the tile kernel: any (out mode and y type read at run time),
+// or a plain store of bf16 / fp32 y fixed at compile time.  With the form fixed,
+// every path through a tile issues the same memory operations, so the compiler
+// can wait for the prefetched operands without draining the stores.
+enum { TILE_Y_ANY = 0, TILE_Y_STORE_BF16 = 1, TILE_Y_STORE_F32 = 2 };
+
+// Bytes of the junk area that stores of empty tile rows are sent to: one
+// 32-byte slot per lane of 128 wave slots.
+constexpr size_t TILE_JUNK_BYTES = 128 * 64 * 32;
+
+// Eight consecutive output columns of one token: combine (residual / accumulate)
+// and store.  xs / yd point at the eight elements of x and y (or at junk).
+template <int YM, bool XBF>
+__device__ __forceinline__ void tile_store8(const Params& p, const void* xs, void* yd, const float* v8) {
+    const int om = YM == TILE_Y_ANY ? p.out_mode : OUT_STORE;
+    const bool ybf = YM == TILE_Y_ANY ? bool(p.y_bf16) : YM == TILE_Y_STORE_BF16;
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = v8[i];
-    const int64_t at = tok * p.hidden + col;
-    if (p.out_mode == OUT_RESIDUAL) {
+    if (om == OUT_RESIDUAL) {
         float xv[8];
-        if (p.x_bf16) tile_load8<true>(p.x, at, xv);
-        else tile_load8<false>(p.x, at, xv);
+        tile_load8<XBF>(xs, 0, xv);
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] += xv[i];
     }
-    if (p.y_bf16) {
-        uint4* d = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p.y) + at);
-        if (p.out_mode == OUT_ACCUMULATE) {
+    if (ybf) {
+        uint4* d = reinterpret_cast<uint4*>(yd);
+        if (om == OUT_ACCUMULATE) {
             const uint4 o = *d;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -426,8 +450,8 @@ __device__ __forceinline__ void tile_store8(const Params& p, int64_t tok, int64_
         *d = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                         pack_bf16x2(v[6], v[7]));
     } else {
-        float4* d = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.y) + at);
-        if (p.out_mode == OUT_ACCUMULATE) {
+        float4* d = reinterpret_cast<float4*>(yd);
+        if (om == OUT_ACCUMULATE) {
             const float4 a = d[0], b = d[1];
             v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
             v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
@@ -440,8 +464,9 @@ __device__ __forceinline__ void tile_store8(const Params& p, int64_t tok, int64_
 typedef float tile_v4f __attribute__((ext_vector_type(4)));
 
 // Grid: one workgroup per leaf (XCD-affine by the subtree at the split level),
-// then spill workgroups.  ELANES/ENV: the per-token emit layout for spilled tokens.
-template <int CB, bool XBF, bool WBF, int ELANES, int ENV>
+// then spill workgroups.  ELANES/ENV: the per-token emit layout for spilled
+// tokens; YM: the output form.
+template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int YM>
 __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
     constexpr int H = 16 * CB;
     static_assert(H % 128 == 0, "128-column groups");
@@ -492,89 +517,176 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     if (cnt == 0) return;  // workgroup-uniform
     const uint32_t leaf1 = uint32_t(leaf + L);
     const int n = lane & 15, kq = lane >> 4;
-    const int steps = (D + 4) / 4;
     const int cap = p.bk_cap;
     const int32_t* bucket = p.bk_tok + leaf * cap;
-    const float* act = p.bk_act + leaf * int64_t(cap) * (D + 1);
-    // Operands of the tile at slot t0 for this lane: token id of slot t0 + n and
-    // its activations at levels 4s + kq.  Indices are clamped into the bucket so
-    // that every load is in bounds; out-of-range values are replaced by 0 / -1.
-    auto load_tile = [&](int t0, int32_t& tok, float* a) {
-        const int slot = t0 + n < cap ? t0 + n : cap - 1;
-        const bool in = t0 + n < cnt;
-        const int32_t tv = bucket[slot];
+    const float* act = p.bk_act + leaf * int64_t(cap) * TILE_REC;
+    constexpr int XSZ = XBF ? 2 : 4;
+    const int ysz = YM == TILE_Y_ANY ? (p.y_bf16 ? 2 : 4) : YM == TILE_Y_STORE_BF16 ? 2 : 4;
+    char* const junk = reinterpret_cast<char*>(p.bk_junk) + ((int64_t(blockIdx.x) * WAVES + wave) % 128 * 64 + lane) * 32;
+    // Every load below is in bounds and unconditional (slots and levels are
+    // clamped; values past the count or past D are replaced by 0 where used), so
+    // each path through a tile issues the same memory operations.
+
+    // stores of one tile's outputs: lane (n, kq) holds tokens 4 kq + r of the
+    // tile, whose ids come from the lanes that loaded them; empty rows go to junk
+    auto store_tile = [&](int32_t tok_a, const tile_v4f* acc, int64_t col) {
 #pragma unroll
-        for (int s = 0; s < TILE_MAX_STEPS; ++s) {
-            const int lvl = 4 * s + kq;
-            float v = 0.0f;
-            if (s < steps) v = act[int64_t(slot) * (D + 1) + (lvl <= D ? lvl : D)];
-            a[s] = in && lvl <= D ? v : 0.0f;
+        for (int r = 0; r < 4; ++r) {
+            const int32_t tok = __shfl(tok_a, 4 * kq + r, 64);
+            const int64_t e = int64_t(tok) * H + col;
+            void* yd = tok >= 0 ? reinterpret_cast<char*>(p.y) + e * ysz : junk;
+            const void* xs = tok >= 0 ? reinterpret_cast<const char*>(p.x) + e * XSZ : junk;
+            float v8[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
+            tile_store8<YM, XBF>(p, xs, yd, v8);
         }
-        tok = in ? tv : -1;
     };
-    for (int g = wave; g < GROUPS; g += WAVES) {
-        const int64_t col = int64_t(g) * 128 + 8 * n;
-        // B operand: this lane's eight weights of the row at level 4s + kq (levels
-        // past D read row 0; their A is 0), kept as loaded for all of the leaf's tiles
-        using WRaw = typename std::conditional<WBF, uint4, float4[2]>::type;
-        WRaw w[TILE_MAX_STEPS];
+
+    if constexpr (WBF) {
+        constexpr int PARTS = YM == TILE_Y_STORE_BF16 ? 2 : 3;
+        const int h = kq & 1, part = kq >> 1;
+        struct Raw {
+            int32_t tok;
+            float4 a0, a1;  // activations of levels 8h .. 8h+7
+        };
+        auto load_tile = [&](int t0, Raw& r) {
+            const int slot = t0 + n < cap ? t0 + n : cap - 1;
+            r.tok = bucket[slot];
+            const float4* rec = reinterpret_cast<const float4*>(act + int64_t(slot) * TILE_REC + 8 * h);
+            r.a0 = rec[0];
+            r.a1 = rec[1];
+        };
+        for (int g = wave; g < GROUPS; g += WAVES) {
+            const int64_t col = int64_t(g) * 128 + 8 * n;
+            // B operands: bj[j] holds column 128 g + 8n + j of the rows of levels 8h .. 8h+7
+            // (levels past D repeat the leaf row: their activations are 0)
+            uint4 bj[8];
+            {
+                uint4 row[8];
 #pragma unroll
-        for (int s = 0; s < TILE_MAX_STEPS; ++s) {
-            const int lvl = 4 * s + kq;
-            if (s < steps) {
-                const int64_t at = (lvl <= D ? int64_t(leaf1 >> (D - lvl)) - 1 : 0) * H + col;
-                if constexpr (WBF) {
-                    w[s] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w_out) + at);
-                } else {
-                    w[s][0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at);
-                    w[s][1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at + 4);
+                for (int i = 0; i < 8; ++i) {
+                    const int lvl = 8 * h + i <= D ? 8 * h + i : D;
+                    row[i] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w_out) +
+                                                             (int64_t(leaf1 >> (D - lvl)) - 1) * H + col);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    uint32_t w4[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t lo = word(row[2 * q], j / 2), hi = word(row[2 * q + 1], j / 2);
+                        w4[q] = (j & 1) ? (lo >> 16) | (hi & 0xffff0000u) : (lo & 0xffffu) | (hi << 16);
+                    }
+                    bj[j] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
                 }
             }
-        }
-        int32_t tok_c;
-        float a_c[TILE_MAX_STEPS];
-        load_tile(0, tok_c, a_c);
-        for (int t0 = 0; t0 < cnt; t0 += 16) {
-            int32_t tok_n;
-            float a_n[TILE_MAX_STEPS];
-            load_tile(t0 + 16, tok_n, a_n);  // next tile (all -1 / 0 past the count)
-            tile_v4f acc[8];
+            auto tile = [&](int t0, const Raw& cur) {
+                const bool in = t0 + n < cnt;
+                const int32_t tok_a = in ? cur.tok : -1;
+                // this lane's parts of its eight activations
+                float av[8] = {cur.a0.x, cur.a0.y, cur.a0.z, cur.a0.w, cur.a1.x, cur.a1.y, cur.a1.z, cur.a1.w};
+                uint32_t p0[4], p1[4];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+                for (int q = 0; q < 4; ++q) {
+                    const float x0 = in && 8 * h + 2 * q <= D ? av[2 * q] : 0.0f;
+                    const float x1 = in && 8 * h + 2 * q + 1 <= D ? av[2 * q + 1] : 0.0f;
+                    const uint32_t hi = pack_bf16x2(x0, x1);
+                    const float r0 = x0 - bf16_lo(hi), r1 = x1 - bf16_hi(hi);
+                    const uint32_t mid = pack_bf16x2(r0, r1);
+                    if constexpr (PARTS == 3) {
+                        const uint32_t lo = pack_bf16x2(r0 - bf16_lo(mid), r1 - bf16_hi(mid));
+                        p0[q] = part == 0 ? hi : mid;
+                        p1[q] = part == 0 ? lo : 0u;
+                    } else {
+                        p0[q] = part == 0 ? hi : mid;
+                    }
+                }
+                const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, make_uint4(p0[0], p0[1], p0[2], p0[3]));
+                tile_v4f acc[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8_t, bj[j]),
+                                                                     tile_v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                }
+                if constexpr (PARTS == 3) {
+                    const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, make_uint4(p1[0], p1[1], p1[2], p1[3]));
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8_t, bj[j]),
+                                                                         acc[j], 0, 0, 0);
+                }
+                store_tile(tok_a, acc, col);
+            };
+            // two operand sets in turn: the next tile's loads are in flight while
+            // this one runs, and no register copy makes the wait early
+            Raw r0, r1;
+            load_tile(0, r0);
+            for (int t0 = 0;;) {
+                load_tile(t0 + 16, r1);
+                tile(t0, r0);
+                if ((t0 += 16) >= cnt) break;
+                load_tile(t0 + 16, r0);
+                tile(t0, r1);
+                if ((t0 += 16) >= cnt) break;
+            }
+        }
+    } else {
+        const int steps = (D + 4) / 4;
+        // level of step s for this lane, clamped to D
+        int lvl_c[TILE_MAX_STEPS];
+#pragma unroll
+        for (int s = 0; s < TILE_MAX_STEPS; ++s) lvl_c[s] = 4 * s + kq <= D ? 4 * s + kq : D;
+        struct Raw {
+            int32_t tok;
+            float a[TILE_MAX_STEPS];
+        };
+        // token id of slot t0 + n and its activations at levels 4s + kq
+        auto load_tile = [&](int t0, Raw& r) {
+            const int slot = t0 + n < cap ? t0 + n : cap - 1;
+            r.tok = bucket[slot];
+            const float* rec = act + int64_t(slot) * TILE_REC;
+#pragma unroll
+            for (int s = 0; s < TILE_MAX_STEPS; ++s) r.a[s] = rec[lvl_c[s]];
+        };
+        for (int g = wave; g < GROUPS; g += WAVES) {
+            const int64_t col = int64_t(g) * 128 + 8 * n;
+            // B operand: this lane's eight weights of the row at level 4s + kq, kept
+            // as loaded for all of the leaf's tiles
+            float4 w[TILE_MAX_STEPS][2];
 #pragma unroll
             for (int s = 0; s < TILE_MAX_STEPS; ++s) {
-                if (s < steps) {
-                    float b[8];
-                    if constexpr (WBF) {
+                const int64_t at = (int64_t(leaf1 >> (D - lvl_c[s])) - 1) * H + col;
+                w[s][0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at);
+                w[s][1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at + 4);
+            }
+            auto tile = [&](int t0, const Raw& cur) {
+                const bool in = t0 + n < cnt;
+                const int32_t tok_a = in ? cur.tok : -1;
+                tile_v4f acc[8];
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            b[2 * j] = bf16_lo(word(w[s], j));
-                            b[2 * j + 1] = bf16_hi(word(w[s], j));
-                        }
-                    } else {
+                for (int j = 0; j < 8; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            b[j] = fword(w[s][0], j);
-                            b[4 + j] = fword(w[s][1], j);
-                        }
+                for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+                    if (s < steps) {
+                        const float a = in && 4 * s + kq <= D ? cur.a[s] : 0.0f;
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, fword(w[s][j / 4], j % 4), acc[j], 0, 0, 0);
                     }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_c[s], b[j], acc[j], 0, 0, 0);
                 }
+                store_tile(tok_a, acc, col);
+            };
+            Raw r0, r1;
+            load_tile(0, r0);
+            for (int t0 = 0;;) {
+                load_tile(t0 + 16, r1);
+                tile(t0, r0);
+                if ((t0 += 16) >= cnt) break;
+                load_tile(t0 + 16, r0);
+                tile(t0, r1);
+                if ((t0 += 16) >= cnt) break;
             }
-            // lane (n, kq) holds tokens 4 kq + r of the tile: their ids from the lanes that loaded them
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int32_t tok = __shfl(tok_c, 4 * kq + r, 64);
-                if (tok < 0) continue;
-                float v8[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
-                tile_store8(p, tok, col, v8);
-            }
-            tok_c = tok_n;
-#pragma unroll
-            for (int s = 0; s < TILE_MAX_STEPS; ++s) a_c[s] = a_n[s];
         }
     }
 }
@@ -787,7 +899,7 @@ struct Variant {
     const void* descent;
     const void* walk;
     const void* emit;
-    const void* tile;
+    const void* tile[3];  // indexed by TILE_Y_*
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -801,7 +913,9 @@ struct Variant {
     Variant {                                                                                                 \
         H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
             FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
-            FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV>),                                                      \
+            {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_ANY>),                                         \
+             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_BF16>),                                  \
+             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_F32>)},                                  \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<L, NV, false, WB, BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -886,9 +1000,9 @@ size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees,
     return align256(recs * size_t(depth + 1) * sizeof(float)) + align256(recs * sizeof(int32_t));
 }
 
-// Tiled mode: one tree, depth 5..16, hidden a multiple of 128 (eight column blocks of 16 per load).
+// Tiled mode: one tree, depth 5..15 (records of TILE_REC levels), hidden a multiple of 128.
 static bool tiled_shape(int32_t depth, int32_t n_trees, int32_t hidden) {
-    return n_trees == 1 && depth >= 5 && depth <= 16 && hidden % 128 == 0;
+    return n_trees == 1 && depth >= 5 && depth < TILE_REC && hidden % 128 == 0;
 }
 
 // Bucket capacity: four times the mean tokens per leaf, at least one tile of 16, a multiple of 16.
@@ -900,14 +1014,14 @@ static int32_t tile_cap(int64_t n_tokens, int32_t depth) {
 
 // Tiled workspace, in order: token records and leaves (as grouped; the records
 // are used by spilled tokens only), bucket counts + spill count, bucket token
-// ids, spill list, bucket activation records.
+// ids, spill list, bucket activation records, junk area for empty tile rows.
 size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
     if (!tiled_shape(depth, n_trees, hidden)) return 0;
     const size_t leaves = size_t(1) << depth;
     const size_t cap = size_t(tile_cap(n_tokens, depth));
     return grouped_workspace_bytes(n_tokens, depth, n_trees, 0) + align256((leaves + 1) * sizeof(int32_t)) +
            align256(leaves * cap * sizeof(int32_t)) + align256(size_t(n_tokens) * sizeof(int32_t)) +
-           align256(leaves * cap * size_t(depth + 1) * sizeof(float));
+           align256(leaves * cap * size_t(TILE_REC) * sizeof(float)) + TILE_JUNK_BYTES;
 }
 
 static const Variant* find_variant(const Params& p) {
@@ -946,7 +1060,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         W.grid = resident_grid(dev, W.kernel, W.lds_bytes,
                                (token_groups(p, v->lanes) + BLOCK / 64 - 1) / (BLOCK / 64));
         Launch& E = plan->launch[plan->n_launch++];
-        E.kernel = v->tile;
+        E.kernel = v->tile[p.out_mode != OUT_STORE ? TILE_Y_ANY : p.y_bf16 ? TILE_Y_STORE_BF16 : TILE_Y_STORE_F32];
         E.block = 64 * tile_waves(p.hidden);
         // one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
         E.grid = int(leaves) + dev.cu_count;
@@ -1079,6 +1193,8 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         q.bk_spill = reinterpret_cast<int32_t*>(ws);
         ws += align256(recs * sizeof(int32_t));
         q.bk_act = reinterpret_cast<float*>(ws);
+        ws += align256(size_t(leaves) * size_t(q.bk_cap) * size_t(TILE_REC) * sizeof(float));
+        q.bk_junk = ws;
         q.split_level = plan.split_level;
         (void)workspace_bytes;
         int32_t* fa = q.bk_count;

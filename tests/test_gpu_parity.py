@@ -305,7 +305,7 @@ def test_tiled_dtype_combinations(fff_lib, xd, wd, yd, H):
 
 
 @pytest.mark.parametrize("B", [1, 7, 100, 2049, 30001])
-@pytest.mark.parametrize("depth", [5, 8, 11, 16])
+@pytest.mark.parametrize("depth", [5, 8, 11, 15])
 def test_tiled_ragged_and_depths(fff_lib, B, depth):
     L = layer(200 + B + depth, B, 768, depth, 1, "bf16", "bf16")
     check_layer(fff_lib, f"tiled B={B} D={depth}", L, depth, 1, "bf16", mode="tiled")
@@ -357,3 +357,6 @@ def test_tiled_unsupported_shapes(fff_lib):
     L = layer(241, 64, 768, 6, 2, "f32", "f32")  # two trees
     with pytest.raises(fff_lib.FffError):
         run_fff(fff_lib, L, 6, 2, "f32", mode="tiled")
+    L = layer(242, 64, 768, 16, 1, "bf16", "bf16")  # depth above 15
+    with pytest.raises(fff_lib.FffError):
+        run_fff(fff_lib, L, 16, 1, "bf16", mode="tiled")
