@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None, help="a name from paper_2311_10770_amd.configs.WORKLOADS")
     ap.add_argument("--tokens", type=int, default=None, help="override the workload's token count")
-    ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "generic"])
+    ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "tiled", "generic"])
     ap.add_argument("--lds-levels", type=int, default=0)
     ap.add_argument("--norm", action="store_true", help="LayerNorm before every layer (gain/shift drawn per layer)")
     ap.add_argument("--backward", action="store_true",
@@ -187,7 +187,12 @@ def main():
             traffic = summ.get("hbm_bytes_per_launch")
         else:
             log(f"{tpath.name} was taken on other kernel sources: traffic unreported")
-    kernels = "walk_kernel + emit_kernel" if "grouped<" in plan else plan.split("<")[0].split()[-1] + "_kernel"
+    if "grouped<" in plan:
+        kernels = "walk_kernel + emit_kernel"
+    elif "tiled<" in plan:
+        kernels = "fill_i32_kernel + walk_kernel + tile_kernel"
+    else:
+        kernels = plan.split("<")[0].split()[-1] + "_kernel"
     if args.backward:
         kernels = "bwd_token_kernel + bwd_scan/scatter + bwd_weight_kernel"
     if plan.startswith("per-layer"):

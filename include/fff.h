@@ -79,9 +79,11 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * activations split into bf16 parts (three parts: fp32 working accuracy; two,
  * relative error about 2^-17, when y is a bf16 store).  Tokens past a full
  * bucket take the per-token emit.  Needs the workspace of fff_workspace_bytes.
- * AUTO: GROUPED for single-tree layers with hidden <= 1024 when a large enough
- * workspace is passed, else DESCENT when a kernel is compiled for the hidden
- * size and types, else GENERIC. */
+ * AUTO (from measurements on MI355X): for single-tree layers of at least 48M
+ * input elements (tokens x hidden) whose workspace is large enough, TILED at
+ * depth 9..15 with at least 8 tokens per leaf, else GROUPED at depth 11 or
+ * more; otherwise DESCENT when a kernel is compiled for the hidden size and
+ * types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,
     FFF_MODE_DESCENT = 1,

@@ -233,10 +233,8 @@ int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
     fff::DeviceInfo dev;
     rc = current_device_info(&dev);
     if (rc != FFF_OK) return rc;
-    const size_t need = fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
-    const bool have_ws = a->workspace && a->workspace_bytes >= need &&
-                         (reinterpret_cast<uintptr_t>(a->workspace) & 255u) == 0;
-    rc = fff::plan_forward(*p, a->mode, a->lds_levels, a->split_level, have_ws, dev, plan);
+    const size_t ws = a->workspace && (reinterpret_cast<uintptr_t>(a->workspace) & 255u) == 0 ? a->workspace_bytes : 0;
+    rc = fff::plan_forward(*p, a->mode, a->lds_levels, a->split_level, ws, dev, plan);
     if (rc != FFF_OK) return rc;
     if ((plan->kind == fff::KIND_GROUPED || plan->kind == fff::KIND_TILED) && a->n_tokens > 0)
         return check_workspace(a, plan->kind == fff::KIND_TILED);

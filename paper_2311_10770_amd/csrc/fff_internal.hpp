@@ -132,9 +132,10 @@ struct Plan {
 };
 
 // Fills *plan for a validated request; returns an fff_status value.
-// have_workspace: the caller passed a workspace big enough for grouped mode
-// (AUTO only picks grouped mode then).
-int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, bool have_workspace,
+// workspace_bytes: size of the 256-byte aligned workspace the caller passed (0
+// if none); AUTO picks the grouped or tiled path only when it covers that
+// path's scratch.
+int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
                  const DeviceInfo& dev, Plan* plan);
 
 // Enqueues the planned work on stream; returns the first failing HIP error.

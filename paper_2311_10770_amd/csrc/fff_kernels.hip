@@ -1032,10 +1032,25 @@ static const Variant* find_variant(const Params& p) {
 
 static int64_t token_groups(const Params& p, int lanes) { return (p.n_tokens + 64 / lanes - 1) / (64 / lanes); }
 
-int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, bool have_workspace,
+int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
                  const DeviceInfo& dev, Plan* plan) {
     *plan = Plan{};
     const Variant* v = find_variant(p);
+    if (mode == MODE_AUTO) {
+        // Measured on MI355X (hidden 768 / 1024 / 4096, depth 5..15, 4K..64K tokens, bf16 and
+        // fp32 weights): below about 48M input elements the fused descent kernel is fastest.
+        // Above it, single trees of depth 9..15 with at least 8 tokens per leaf run fastest
+        // leaf-tiled on MFMA, other single trees of depth 11 or more grouped by subtree.
+        const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
+        const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
+        const int64_t grouped_ws = int64_t(grouped_workspace_bytes(p.n_tokens, p.depth, p.n_trees, 0));
+        if (!v) mode = MODE_GENERIC;
+        else if (big && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
+                 p.n_tokens >= (int64_t(8) << p.depth))
+            mode = MODE_TILED;
+        else if (big && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws) mode = MODE_GROUPED;
+        else mode = MODE_DESCENT;
+    }
     if ((mode == MODE_DESCENT || mode == MODE_GROUPED || mode == MODE_TILED) && !v) return ST_UNSUPPORTED;
     if (mode == MODE_TILED) {
         if (!tiled_shape(p.depth, p.n_trees, p.hidden)) return ST_UNSUPPORTED;
@@ -1065,13 +1080,6 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         // one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
         E.grid = int(leaves) + dev.cu_count;
         return ST_OK;
-    }
-    if (mode == MODE_AUTO) {
-        // Measured on MI355X: the two-kernel grouped path wins for single trees with 16/32-lane
-        // tokens (hidden <= 1024); the fused kernel wins for multi-tree layers and 64-lane tokens.
-        if (!v) mode = MODE_GENERIC;
-        else if (have_workspace && p.n_trees == 1 && v->lanes < 64 && p.depth >= 3) mode = MODE_GROUPED;
-        else mode = MODE_DESCENT;
     }
 
     if (mode == MODE_DESCENT) {

@@ -271,7 +271,7 @@ def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
     of x's dtype; y may be x itself).  ``layers``: sequence of (W_in, W_out[, gamma[, beta]])."""
     if y is None:
         y = torch.empty_like(x)
-    if kw.get("mode", "auto") in ("grouped", 2) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", 0, 2, 4) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     with torch.cuda.device(x.device):
@@ -282,7 +282,7 @@ def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
 def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str:
     if y is None:
         y = torch.empty_like(x)
-    if kw.get("mode", "auto") in ("grouped", 2) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", 0, 2, 4) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     buf = ctypes.create_string_buffer(512)

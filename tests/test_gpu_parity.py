@@ -153,12 +153,14 @@ def test_grouped_out_modes_and_skewed_routing(fff_lib):
 def test_grouped_workspace_errors(fff_lib):
     L = layer(200, 512, 768, 11, 1, "bf16", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
-    need = fff_lib.workspace_bytes(512, 11, 1, 768)
-    assert need >= 512 * 12 * 4 + 512 * 4
-    small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
-    with pytest.raises(fff_lib.FffError) as e:
-        fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", workspace=small)
-    assert e.value.status == fff_lib.fff.FFF_ERR_WORKSPACE
+    need = fff_lib.workspace_bytes(512, 11, 1, 768)  # covers grouped and tiled mode
+    grouped_need = 512 * 12 * 4 + 512 * 4  # activation records and leaves, each a multiple of 256 bytes
+    assert need > grouped_need
+    for mode, n in (("grouped", grouped_need), ("tiled", need)):
+        small = torch.empty(n - 256, dtype=torch.uint8, device=DEV)
+        with pytest.raises(fff_lib.FffError) as e:
+            fff_lib.forward(x, wi, wo, 11, 1, mode=mode, workspace=small)
+        assert e.value.status == fff_lib.fff.FFF_ERR_WORKSPACE
     big = torch.empty(need + 4096, dtype=torch.uint8, device=DEV)
     with pytest.raises(fff_lib.FffError) as e:
         fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", workspace=big[16:])  # misaligned
@@ -265,8 +267,14 @@ def test_guard_bands_untouched(fff_lib, yd, mode):
 def test_describe_names_the_kernel(fff_lib):
     L = layer(140, 64, 768, 11, 1, "bf16", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
-    d = fff_lib.describe(x, wi, wo, 11, 1)  # auto with the binding's workspace: grouped for one tree
-    assert d.startswith("grouped<"), d
+    d = fff_lib.describe(x, wi, wo, 11, 1)  # auto, small batch: the fused kernel
+    assert d.startswith("descent<"), d
+    # auto with the binding's workspace at 64K tokens: leaf tiles at 32 tokens per leaf,
+    # subtree grouping at 4 per leaf (planning only: nothing is launched)
+    xb = torch.zeros((65536, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, wi, wo, 11, 1).startswith("tiled<")
+    w14 = torch.zeros((1, (1 << 15) - 1, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, w14, w14, 14, 1).startswith("grouped<")
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="descent")
     assert d.startswith("descent<") and "lds_levels=" in d
     wi4 = fff_lib.from_numpy(np.concatenate([L["w_in"]] * 4), DEV)
