@@ -887,7 +887,8 @@ __global__ __launch_bounds__(GENERIC_BLOCK) void generic_kernel(Params p) {
 
 constexpr int BLOCK = 256;
 constexpr size_t DESCENT_LDS_BUDGET = 32 * 1024;  // per 256-thread block: keeps 4-5 blocks per CU
-constexpr size_t WALK_LDS_BUDGET = 24 * 1024;     // the walk kernel runs at 6-8 waves per SIMD
+constexpr int WALK_BLOCK = 512;                     // walk workgroups: twice the rows in LDS per wave
+constexpr size_t WALK_LDS_BUDGET = 48 * 1024;     // per 512-thread walk block: three blocks per CU
 constexpr size_t EMIT_LDS_BUDGET = 32 * 1024;
 constexpr int GENERIC_MAX_PAIRS = 2048;
 
@@ -912,12 +913,12 @@ struct Variant {
 #define FFF_VARIANT(H, XB, WB, L, NV, EL, ENV)                                                                \
     Variant {                                                                                                 \
         H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
-            FFF_K(walk_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
+            FFF_K(walk_kernel<L, NV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
             {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_ANY>),                                         \
              FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_BF16>),                                  \
              FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_F32>)},                                  \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
-            FFF_K(walk_kernel<L, NV, false, WB, BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
+            FFF_K(walk_kernel<L, NV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
     }
 
@@ -982,8 +983,8 @@ static int pick_levels(const Params& p, int req, int matrices, size_t budget, si
     return k;
 }
 
-static int resident_grid(const DeviceInfo& dev, const void* kernel, size_t lds, int64_t want) {
-    const int64_t resident = int64_t(dev.cu_count) * blocks_per_cu(dev.device, kernel, BLOCK, lds);
+static int resident_grid(const DeviceInfo& dev, const void* kernel, size_t lds, int64_t want, int block = BLOCK) {
+    const int64_t resident = int64_t(dev.cu_count) * blocks_per_cu(dev.device, kernel, block, lds);
     return int(std::max<int64_t>(1, std::min(want, resident)));
 }
 
@@ -1070,10 +1071,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         F.grid = int(std::min<int64_t>((leaves + 1 + 255) / 256, int64_t(dev.cu_count) * 4));
         Launch& W = plan->launch[plan->n_launch++];
         W.kernel = p.norm ? v->walk_norm : v->walk;
-        W.block = BLOCK;
+        W.block = WALK_BLOCK;
         W.lds_bytes = rows_lds_bytes(p, kw, 1);
         W.grid = resident_grid(dev, W.kernel, W.lds_bytes,
-                               (token_groups(p, v->lanes) + BLOCK / 64 - 1) / (BLOCK / 64));
+                               (token_groups(p, v->lanes) + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64), WALK_BLOCK);
         Launch& E = plan->launch[plan->n_launch++];
         E.kernel = v->tile[p.out_mode != OUT_STORE ? TILE_Y_ANY : p.y_bf16 ? TILE_Y_STORE_BF16 : TILE_Y_STORE_F32];
         E.block = 64 * tile_waves(p.hidden);
@@ -1113,12 +1114,12 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         plan->split_level = split;
         plan->name = v->name;
         const int64_t groups = token_groups(p, v->lanes);
-        const int64_t want = (groups + BLOCK / 64 - 1) / (BLOCK / 64);
+        const int64_t want = (groups + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64);
         Launch& W = plan->launch[plan->n_launch++];
         W.kernel = p.norm ? v->walk_norm : v->walk;
-        W.block = BLOCK;
+        W.block = WALK_BLOCK;
         W.lds_bytes = rows_lds_bytes(p, kw, 1);
-        W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want);
+        W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want, WALK_BLOCK);
         Launch& E = plan->launch[plan->n_launch++];
         E.kernel = v->emit;
         E.block = BLOCK;
