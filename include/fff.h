@@ -77,7 +77,8 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * share a leaf (hence all D+1 nodes) are accumulated as one dense product on
  * MFMA: fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
  * activations split into bf16 parts (three parts: fp32 working accuracy; two,
- * relative error about 2^-17, when y is a bf16 store).  Tokens past a full
+ * relative error about 2^-17, when y is bf16 and either stored or the residual
+ * of bf16 x).  Tokens past a full
  * bucket take the per-token emit.  Needs the workspace of fff_workspace_bytes.
  * AUTO (from measurements on MI355X): for single-tree layers of at least 48M
  * input elements (tokens x hidden) whose workspace is large enough, TILED at

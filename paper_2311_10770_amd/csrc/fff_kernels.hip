@@ -413,10 +413,11 @@ __device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out
 }
 
 // Output forms of the tile kernel: any (out mode and y type read at run time),
-// or a plain store of bf16 / fp32 y fixed at compile time.  With the form fixed,
-// every path through a tile issues the same memory operations, so the compiler
-// can wait for the prefetched operands without draining the stores.
-enum { TILE_Y_ANY = 0, TILE_Y_STORE_BF16 = 1, TILE_Y_STORE_F32 = 2 };
+// a plain store of bf16 / fp32 y, or the residual y = x + FFF with y of x's
+// type, fixed at compile time.  With the form fixed, every path through a tile
+// issues the same memory operations, so the compiler can wait for the
+// prefetched operands without draining the stores.
+enum { TILE_Y_ANY = 0, TILE_Y_STORE_BF16 = 1, TILE_Y_STORE_F32 = 2, TILE_Y_RESIDUAL = 3 };
 
 // Bytes of the junk area that stores of empty tile rows are sent to: one
 // 32-byte slot per lane of 128 wave slots.
@@ -426,8 +427,8 @@ constexpr size_t TILE_JUNK_BYTES = 128 * 64 * 32;
 // and store.  xs / yd point at the eight elements of x and y (or at junk).
 template <int YM, bool XBF>
 __device__ __forceinline__ void tile_store8(const Params& p, const void* xs, void* yd, const float* v8) {
-    const int om = YM == TILE_Y_ANY ? p.out_mode : OUT_STORE;
-    const bool ybf = YM == TILE_Y_ANY ? bool(p.y_bf16) : YM == TILE_Y_STORE_BF16;
+    const int om = YM == TILE_Y_ANY ? p.out_mode : YM == TILE_Y_RESIDUAL ? OUT_RESIDUAL : OUT_STORE;
+    const bool ybf = YM == TILE_Y_ANY ? bool(p.y_bf16) : YM == TILE_Y_RESIDUAL ? XBF : YM == TILE_Y_STORE_BF16;
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = v8[i];
@@ -521,7 +522,10 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     const int32_t* bucket = p.bk_tok + leaf * cap;
     const float* act = p.bk_act + leaf * int64_t(cap) * TILE_REC;
     constexpr int XSZ = XBF ? 2 : 4;
-    const int ysz = YM == TILE_Y_ANY ? (p.y_bf16 ? 2 : 4) : YM == TILE_Y_STORE_BF16 ? 2 : 4;
+    const int ysz = YM == TILE_Y_ANY         ? (p.y_bf16 ? 2 : 4)
+                    : YM == TILE_Y_RESIDUAL  ? (XBF ? 2 : 4)
+                    : YM == TILE_Y_STORE_BF16 ? 2
+                                              : 4;
     char* const junk = reinterpret_cast<char*>(p.bk_junk) + ((int64_t(blockIdx.x) * WAVES + wave) % 128 * 64 + lane) * 32;
     // Every load below is in bounds and unconditional (slots and levels are
     // clamped; values past the count or past D are replaced by 0 where used), so
@@ -544,7 +548,7 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     };
 
     if constexpr (WBF) {
-        constexpr int PARTS = YM == TILE_Y_STORE_BF16 ? 2 : 3;
+        constexpr int PARTS = YM == TILE_Y_STORE_BF16 || (YM == TILE_Y_RESIDUAL && XBF) ? 2 : 3;
         const int h = kq & 1, part = kq >> 1;
         struct Raw {
             int32_t tok;
@@ -900,7 +904,7 @@ struct Variant {
     const void* descent;
     const void* walk;
     const void* emit;
-    const void* tile[3];  // indexed by TILE_Y_*
+    const void* tile[4];  // indexed by TILE_Y_*
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -916,7 +920,8 @@ struct Variant {
             FFF_K(walk_kernel<L, NV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
             {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_ANY>),                                         \
              FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_BF16>),                                  \
-             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_F32>)},                                  \
+             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_F32>),                                   \
+             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_RESIDUAL>)},                                   \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<L, NV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -1076,7 +1081,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         W.grid = resident_grid(dev, W.kernel, W.lds_bytes,
                                (token_groups(p, v->lanes) + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64), WALK_BLOCK);
         Launch& E = plan->launch[plan->n_launch++];
-        E.kernel = v->tile[p.out_mode != OUT_STORE ? TILE_Y_ANY : p.y_bf16 ? TILE_Y_STORE_BF16 : TILE_Y_STORE_F32];
+        int form = TILE_Y_ANY;
+        if (p.out_mode == OUT_STORE) form = p.y_bf16 ? TILE_Y_STORE_BF16 : TILE_Y_STORE_F32;
+        else if (p.out_mode == OUT_RESIDUAL && p.y_bf16 == p.x_bf16) form = TILE_Y_RESIDUAL;
+        E.kernel = v->tile[form];
         E.block = 64 * tile_waves(p.hidden);
         // one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
         E.grid = int(leaves) + dev.cu_count;
