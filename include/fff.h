@@ -220,12 +220,15 @@ int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_laye
  * (x is the FFF input; a residual or a LayerNorm around the layer is the
  * caller's to differentiate).
  *
- * Work: a token kernel (dx and the per-visit pairs (a, dl)), a counting sort
- * of the tokens by leaf (so that every node's tokens form one run at every
- * level), a weight kernel that sums the runs of fixed pieces of the sorted
- * order in registers (a run inside one piece is stored directly), and a
- * fix-up kernel that adds the piece sums of runs crossing pieces in piece
- * order.  No atomics on dx or dW: results are deterministic.
+ * Work: a token kernel (dx and the per-visit pairs (a, dl)), a stable
+ * counting sort of the tokens by leaf (every node's tokens form one run at
+ * every level, in token order within a leaf), and the weight sums along that
+ * order: for depth <= 15 and hidden a multiple of 128 on MFMA, one workgroup
+ * per subtree accumulating the rows of its tokens' paths, with the rows above
+ * the subtrees added in subtree order by a fix-up; otherwise by fixed pieces
+ * of the sorted order summed in registers and a fix-up of the runs crossing
+ * pieces.  No atomics on dx or dW and every sum in a fixed order: the results
+ * are the same bits on every run.
  */
 typedef struct {
     const void* x;          /* [n_tokens, hidden] the layer's FFF input (x_dtype) */

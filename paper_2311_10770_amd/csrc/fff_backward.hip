@@ -12,7 +12,7 @@
 //    token, dy in registers; per level the two rows of the known path are
 //    gathered, da is reduced across the group, dx accumulates in registers;
 //    the pair (a, dl) of every visit is saved and the leaves are counted.
-// 2. bwd_scan_kernel + bwd_scatter_kernel: counting sort of the tokens by
+// 2. bwd_scan_kernel + bwd_rank/base/place_kernel: stable counting sort of the tokens by
 //    leaf.  Sorted by leaf, the tokens through any node form one contiguous
 //    run at every level (a node's leaves are a contiguous range).
 // 3. bwd_piece_kernel: the sorted order is cut into pieces of P positions;
@@ -35,6 +35,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 namespace fff {
 
@@ -44,6 +45,7 @@ enum { ST_OK_ = 0, ST_UNSUPPORTED_ = -2 };
 
 constexpr int BWD_BLOCK = 256;
 constexpr int SCAN_BLOCK = 1024;
+constexpr int RANK_BLOCK = 256;   // threads of the rank kernel; a chunk is 1..16 tokens per thread
 constexpr int SLICE = 256;       // columns per wave in the weight kernel (64 lanes x 4)
 constexpr int LV = 6;            // levels handled per pass of the piece kernel
 
@@ -260,8 +262,79 @@ __global__ __launch_bounds__(SCAN_BLOCK) void bwd_scan_kernel(BwdParams p) {
     if (tid == 0) p.total[t] = carry_s;
 }
 
-// Sorted position of every valid (token, tree): perm[t][offs[leaf]++] = token.
-__global__ __launch_bounds__(BWD_BLOCK) void bwd_scatter_kernel(BwdParams p) {
+// Stable placement of every valid (token, tree) in leaf order: within a leaf
+// the tokens keep their index order, so the sorted order, and every sum taken
+// along it, is the same on every run.  Tokens are cut into chunks of
+// RANK_BLOCK; a token's position is its leaf's start + the tokens of that leaf
+// in earlier chunks + its rank among the leaf's tokens earlier in its chunk.
+//
+// bwd_rank_kernel (block = one chunk of one tree): each token's rank within its
+// chunk and the chunk's count per leaf (hist[t][chunk][leaf], zero for absent
+// leaves).  The chunk's leaves sit in LDS; every token compares itself with all
+// of them.
+__global__ __launch_bounds__(RANK_BLOCK) void bwd_rank_kernel(BwdParams p) {
+    extern __shared__ int32_t bins[];  // [p.chunk]
+    const int t = blockIdx.y, T = p.n_trees, D = p.depth;
+    const int64_t L = int64_t(1) << D;
+    const int64_t chunk = blockIdx.x;
+    const int C = p.chunk;
+    const int tid = threadIdx.x;
+    for (int i = tid; i < C; i += RANK_BLOCK) {
+        const int64_t b = chunk * C + i;
+        int32_t bin = -1;
+        if (b < p.n_tokens) {
+            const int32_t leaf = p.leaves[b * T + t];
+            if (leaf_ok(leaf, D)) bin = int32_t(int64_t(leaf) - (L - 1));
+        }
+        bins[i] = bin;
+    }
+    int32_t* h = p.hist + (int64_t(t) * p.chunks + chunk) * L;
+    for (int64_t i = tid; i < L; i += RANK_BLOCK) h[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < C; i += RANK_BLOCK) {
+        const int64_t b = chunk * C + i;
+        const int32_t bin = bins[i];
+        int32_t rank = 0;
+        bool last = true;
+        for (int j = 0; j < C; ++j) {
+            const bool same = bins[j] == bin;
+            rank += same && j < i ? 1 : 0;
+            last = last && !(same && j > i);
+        }
+        if (b < p.n_tokens) p.rank[int64_t(t) * p.n_tokens + b] = rank;
+        if (bin >= 0 && last) h[bin] = rank + 1;
+    }
+}
+
+// bwd_base_kernel (one wave per (tree, leaf)): turns the chunk counts into the
+// first sorted position of the leaf's tokens in each chunk (an exclusive scan
+// over the chunks, 64 at a time), and leaves offs at one past the leaf's last
+// position.
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_base_kernel(BwdParams p) {
+    const int64_t L = int64_t(1) << p.depth;
+    const int lane = threadIdx.x & 63;
+    const int64_t i = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
+    if (i >= L * p.n_trees) return;  // wave-uniform
+    const int64_t t = i / L, leaf = i - t * L;
+    int32_t run = p.offs[i];
+    int32_t* h = p.hist + t * p.chunks * L + leaf;
+    for (int64_t c0 = 0; c0 < p.chunks; c0 += 64) {
+        const int64_t c = c0 + lane;
+        const int32_t n = c < p.chunks ? h[c * L] : 0;
+        int32_t inc = n;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t u = __shfl_up(inc, d, 64);
+            if (lane >= d) inc += u;
+        }
+        if (c < p.chunks) h[c * L] = run + inc - n;
+        run += __shfl(inc, 63, 64);
+    }
+    if (lane == 0) p.offs[i] = run;
+}
+
+// bwd_place_kernel: perm[t][position] = token.
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_place_kernel(BwdParams p) {
     const int T = p.n_trees, D = p.depth;
     const int64_t L = int64_t(1) << D;
     const int64_t n = p.n_tokens * T;
@@ -271,7 +344,7 @@ __global__ __launch_bounds__(BWD_BLOCK) void bwd_scatter_kernel(BwdParams p) {
         const int32_t leaf = p.leaves[i];
         if (!leaf_ok(leaf, D)) continue;
         const int64_t bin = int64_t(leaf) - (L - 1);
-        const int32_t pos = atomicAdd(&p.offs[t * L + bin], 1);
+        const int64_t pos = p.hist[(int64_t(t) * p.chunks + b / p.chunk) * L + bin] + p.rank[int64_t(t) * p.n_tokens + b];
         p.perm[int64_t(t) * p.n_tokens + pos] = int32_t(b);
     }
 }
@@ -567,6 +640,291 @@ __global__ __launch_bounds__(BWD_BLOCK) void bwd_fixup_kernel(BwdParams p, int t
 // planning
 // ---------------------------------------------------------------------------
 
+// ---------------------------------------------------------------------------
+// 3'. leaf-tiled weight kernel on MFMA (depth <= 15, hidden a multiple of 128)
+// ---------------------------------------------------------------------------
+//
+// One workgroup per subtree of 2^sub leaves (the subtree's root at level
+// k = D - sub), one wave per 128-column group g.  The subtree's tokens are taken
+// in sorted order, leaf by leaf, four per step of v_mfma_f32_16x16x4_f32: rows
+// are levels, the K dimension is the four tokens, and lane l supplies the pair
+// (a, dl) of token 4s + l/16 at level l%16 and that token's eight dy (x) values
+// at columns 128g + 8(l%16) .. +7 for the eight column blocks.  The
+// accumulators hold the sums for all D+1 nodes of the current path, lane l
+// receiving levels 4(l/16) .. +3 of its eight columns.  When a leaf is done the
+// rows of the nodes it completes (levels from the leaf up to the subtree root
+// whose last leaf it is) are stored and cleared; a node no token reached gets
+// a zero row.  The levels above the subtree root leave this subtree's sums in
+// part[] and are added in subtree order by bwd_wfix_kernel.  Every dW element
+// has one writer and the order of every sum is fixed.
+constexpr int WT_WAVES_MAX = 8;
+constexpr int WT_TOP_LEVELS = 9;   // subtrees hang at level min(D, 9)
+constexpr int WT_MAX_SUB = 6;      // depth <= 15: at most 2^6 leaves per subtree
+constexpr int WT_LDS_TOK = 4096;   // token ids of a subtree staged in LDS when they fit
+constexpr int FIXW_BLOCK = 1024;
+
+__device__ __forceinline__ void load8f(const void* base, bool bf, int64_t at, float* v) {
+    if (bf) {
+        const uint4 u = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + at);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = bf16_lo(word(u, j));
+            v[2 * j + 1] = bf16_hi(word(u, j));
+        }
+    } else {
+        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + at);
+        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + at + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+}
+
+// Eight fp32 values of a dW row: stored, or added to what is there.
+__device__ __forceinline__ void put8(float* dst, bool add, const float* v) {
+    float4* d = reinterpret_cast<float4*>(dst);
+    float4 a = make_float4(v[0], v[1], v[2], v[3]), b = make_float4(v[4], v[5], v[6], v[7]);
+    if (add) {
+        const float4 o0 = d[0], o1 = d[1];
+        a.x += o0.x; a.y += o0.y; a.z += o0.z; a.w += o0.w;
+        b.x += o1.x; b.y += o1.y; b.z += o1.z; b.w += o1.w;
+    }
+    d[0] = a;
+    d[1] = b;
+}
+
+template <bool XBF, bool DYBF>
+__global__ __launch_bounds__(64 * WT_WAVES_MAX) void bwd_wtile_kernel(BwdParams p, int sub) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, waves = blockDim.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int t = blockIdx.y, T = p.n_trees, D = p.depth;
+    const int64_t L = int64_t(1) << D, H = p.hidden, N = p.n_nodes;
+    const int k = D - sub;
+    const int64_t st = blockIdx.x;
+    const int64_t leaf0 = st << sub;
+    const int32_t* cnt = p.counts + t * L;
+    const int32_t* end = p.offs + t * L;  // after the placement: one past each leaf's last position
+    const int32_t* perm = p.perm + int64_t(t) * p.n_tokens;
+    float* dwo = p.dw_out ? p.dw_out + int64_t(t) * N * H : nullptr;
+    float* dwi = p.dw_in ? p.dw_in + int64_t(t) * N * H : nullptr;
+    const bool add = p.accumulate != 0;
+    const int lvl_a = n <= D ? n : D;  // this lane's level as A supplier (clamped; A is 0 past D)
+    // The subtree's tokens are one contiguous range of the sorted order: its
+    // leaves' counts and, when the range fits, its token ids are staged in LDS
+    // once for all waves.
+    __shared__ int32_t s_cnt[1 << WT_MAX_SUB];
+    __shared__ int32_t s_tok[WT_LDS_TOK];
+    const int nleaf = 1 << sub;
+    for (int i = threadIdx.x; i < nleaf; i += blockDim.x) s_cnt[i] = cnt[leaf0 + i];
+    const int64_t first = int64_t(end[leaf0]) - cnt[leaf0];
+    const int64_t range = int64_t(end[leaf0 + nleaf - 1]) - first;
+    const bool staged = range <= WT_LDS_TOK;  // workgroup-uniform
+    if (staged)
+        for (int64_t i = threadIdx.x; i < range; i += blockDim.x) s_tok[i] = perm[first + i];
+    __syncthreads();
+    for (int64_t g = wave; g < H / 128; g += waves) {
+        const int64_t col = g * 128 + 8 * n;
+        tile_v4f ao[8], ai[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) ao[j] = ai[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+        int64_t pos0 = first;  // sorted position of the current leaf's first token
+        for (int jl = 0; jl < nleaf; ++jl) {
+            const int64_t leaf = leaf0 + jl;
+            const int32_t c = s_cnt[jl];
+            {
+                const int32_t m = c;
+                // operands of step s0 for this lane: (a, dl) of token s0 + q at its level,
+                // and that token's eight dy and x values as stored (token clamped into the leaf)
+                struct Ops {
+                    float2 cf;
+                    typename std::conditional<DYBF, uint4, float4[2]>::type dy;
+                    typename std::conditional<XBF, uint4, float4[2]>::type x;
+                };
+                auto load_ops = [&](int32_t s0, Ops& o) {
+                    const int64_t pos = pos0 + (s0 + q < m ? s0 + q : 0);
+                    const int32_t tok = staged ? s_tok[pos - first] : perm[pos];
+                    o.cf = p.coef[(int64_t(tok) * T + t) * (D + 1) + lvl_a];
+                    const int64_t at = int64_t(tok) * H + col;
+                    if constexpr (DYBF) {
+                        o.dy = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.dy) + at);
+                    } else {
+                        o.dy[0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at);
+                        o.dy[1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at + 4);
+                    }
+                    if constexpr (XBF) {
+                        o.x = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.x) + at);
+                    } else {
+                        o.x[0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.x) + at);
+                        o.x[1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.x) + at + 4);
+                    }
+                };
+                auto val = [](const auto& v, int j) -> float {
+                    if constexpr (std::is_same<typename std::decay<decltype(v)>::type, uint4>::value)
+                        return (j & 1) ? bf16_hi(word(v, j >> 1)) : bf16_lo(word(v, j >> 1));
+                    else
+                        return fword(v[j >> 2], j & 3);
+                };
+                auto step = [&](int32_t s0, const Ops& o) {
+                    const bool in = s0 + q < m && n <= D;
+                    const float a = in ? o.cf.x : 0.0f, dl = in ? o.cf.y : 0.0f;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, val(o.dy, j), ao[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dl, val(o.x, j), ai[j], 0, 0, 0);
+                    }
+                };
+                if (m > 0) {
+                    // three operand sets in turn: two steps are in flight while one runs;
+                    // sched_barrier keeps each prefetch above the MFMAs it overlaps (the
+                    // scheduler would otherwise sink the loads to their use)
+                    Ops o0, o1, o2;
+                    load_ops(0, o0);
+                    load_ops(4, o1);
+                    for (int32_t s0 = 0;;) {
+                        load_ops(s0 + 8, o2);
+                        __builtin_amdgcn_sched_barrier(0);
+                        step(s0, o0);
+                        if ((s0 += 4) >= m) break;
+                        load_ops(s0 + 8, o0);
+                        __builtin_amdgcn_sched_barrier(0);
+                        step(s0, o1);
+                        if ((s0 += 4) >= m) break;
+                        load_ops(s0 + 8, o1);
+                        __builtin_amdgcn_sched_barrier(0);
+                        step(s0, o2);
+                        if ((s0 += 4) >= m) break;
+                    }
+                }
+            }
+            pos0 += c;
+            // rows this leaf completes: levels lv >= k whose node's last leaf this is
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int lv = 4 * q + r;
+                if (lv <= D && lv >= k && ((leaf + 1) & ((int64_t(1) << (D - lv)) - 1)) == 0) {
+                    const int64_t node = ((leaf + L) >> (D - lv)) - 1;
+                    float v[8];
+                    if (dwo) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] = ao[j][r];
+                        put8(dwo + node * H + col, add, v);
+                    }
+                    if (dwi) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] = ai[j][r];
+                        put8(dwi + node * H + col, add, v);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) ao[j][r] = ai[j][r] = 0.0f;
+                }
+            }
+        }
+        // levels above the subtree root: this subtree's sums for the fix-up
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int lv = 4 * q + r;
+            if (lv < k) {
+                float* dst = p.part + (((int64_t(t) << k) + st) * k + lv) * 2 * H + col;
+                float v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[j] = ao[j][r];
+                put8(dst, false, v);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[j] = ai[j][r];
+                put8(dst + H, false, v);
+            }
+        }
+    }
+}
+
+// Rows of the levels above the subtrees: node u at level lv < k sums the part[]
+// of its 2^(k-lv) subtrees in subtree order, four running sums (subtree j goes to
+// sum j % 4), then the sums added in order.  bwd_wfix_kernel: one wave per
+// (tree, node, matrix, 256-column slice) for the levels from k - WFIX_SPLIT on
+// (at most 2^WFIX_SPLIT subtrees each).  bwd_wfix_top_kernel: the levels above,
+// a 1024-thread block per task, wave w taking subtrees w, w+16, ...; the
+// sixteen wave sums are added in wave order.  Fixed order throughout.
+constexpr int WFIX_SPLIT = 5;
+
+__device__ __forceinline__ void wfix_task(const BwdParams& p, int k, int64_t task, int64_t node0, int64_t nodes,
+                                          int64_t* node, int* lv, int* mat, int64_t* c4, int* t) {
+    const int64_t slices = (int64_t(p.hidden) + 255) / 256;
+    int64_t b = task;
+    const int64_t slice = b % slices;
+    b /= slices;
+    *mat = int(b % 2);
+    b /= 2;
+    *node = node0 + b % nodes;
+    *t = int(b / nodes);
+    int l = 0;
+    while ((int64_t(2) << l) - 1 <= *node) ++l;  // node in [2^l - 1, 2^(l+1) - 1)
+    *lv = l;
+    *c4 = slice * 64;
+}
+
+__device__ __forceinline__ float4 wfix_sum(const BwdParams& p, int k, int t, int lv, int mat, int64_t node,
+                                           int64_t c4, int64_t j0, int64_t step) {
+    const int64_t u = node - ((int64_t(1) << lv) - 1);
+    const int64_t first = u << (k - lv), count = int64_t(1) << (k - lv);
+    const int64_t H = p.hidden;
+    float4 s[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    int i = 0;
+    for (int64_t j = j0; j < count; j += step, i = (i + 1) & 3) {
+        const float4 v =
+            reinterpret_cast<const float4*>(p.part + ((((int64_t(t) << k) + first + j) * k + lv) * 2 + mat) * H)[c4];
+        s[i].x += v.x; s[i].y += v.y; s[i].z += v.z; s[i].w += v.w;
+    }
+    float4 w = s[0];
+#pragma unroll
+    for (int q = 1; q < 4; ++q) { w.x += s[q].x; w.y += s[q].y; w.z += s[q].z; w.w += s[q].w; }
+    return w;
+}
+
+__device__ __forceinline__ void wfix_store(const BwdParams& p, int t, int mat, int64_t node, int64_t c4, float4 a) {
+    float* dw = mat == 0 ? p.dw_out : p.dw_in;
+    if (!dw) return;
+    float4* d = reinterpret_cast<float4*>(dw + (int64_t(t) * p.n_nodes + node) * p.hidden) + c4;
+    if (p.accumulate) {
+        const float4 o = *d;
+        a.x += o.x; a.y += o.y; a.z += o.z; a.w += o.w;
+    }
+    *d = a;
+}
+
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_wfix_kernel(BwdParams p, int k, int64_t node0, int64_t nodes) {
+    const int lane = threadIdx.x & 63;
+    const int64_t task = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
+    const int64_t slices = (int64_t(p.hidden) + 255) / 256;
+    if (task >= int64_t(p.n_trees) * nodes * 2 * slices) return;  // wave-uniform
+    int64_t node, c4;
+    int lv, mat, t;
+    wfix_task(p, k, task, node0, nodes, &node, &lv, &mat, &c4, &t);
+    c4 += lane;
+    if (c4 * 4 >= p.hidden) return;
+    wfix_store(p, t, mat, node, c4, wfix_sum(p, k, t, lv, mat, node, c4, 0, 1));
+}
+
+__global__ __launch_bounds__(FIXW_BLOCK) void bwd_wfix_top_kernel(BwdParams p, int k, int64_t nodes) {
+    __shared__ float4 red[FIXW_BLOCK / 64][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t node, c4;
+    int lv, mat, t;
+    wfix_task(p, k, blockIdx.x, 0, nodes, &node, &lv, &mat, &c4, &t);
+    c4 += lane;
+    const bool live = c4 * 4 < p.hidden;
+    red[wave][lane] = live ? wfix_sum(p, k, t, lv, mat, node, c4, wave, FIXW_BLOCK / 64) : make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+    if (wave == 0 && live) {
+        float4 a = red[0][lane];
+        for (int i = 1; i < FIXW_BLOCK / 64; ++i) {
+            const float4 v = red[i][lane];
+            a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
+        }
+        wfix_store(p, t, mat, node, c4, a);
+    }
+}
+
 struct BwdVariant {
     int hidden;
     bool wbf;
@@ -599,13 +957,36 @@ int32_t bwd_piece(int64_t n_tokens, int32_t n_trees) {
 
 static int64_t bwd_pieces(int64_t n_tokens, int32_t piece) { return std::max<int64_t>(1, (n_tokens + piece - 1) / piece); }
 
+// Tokens per chunk of the stable placement: one per rank-kernel thread, more (up to 16) once the
+// batch would need over 512 chunks, which bounds the [chunks, leaves] table.
+static int32_t bwd_chunk(int64_t n_tokens) {
+    const int64_t per = std::min<int64_t>(16, std::max<int64_t>(1, (n_tokens + RANK_BLOCK * 512 - 1) / (RANK_BLOCK * 512)));
+    return int32_t(RANK_BLOCK * per);
+}
+static int64_t bwd_chunks(int64_t n_tokens) {
+    const int64_t c = bwd_chunk(n_tokens);
+    return std::max<int64_t>(1, (n_tokens + c - 1) / c);
+}
+
+// The leaf-tiled weight kernel takes depth <= 15 (levels are the rows of a 16x16 MFMA) and
+// hidden a multiple of 128; it hangs its subtrees at level min(depth, WT_TOP_LEVELS).
+static bool wtile_shape(int32_t depth, int32_t hidden) { return depth <= 15 && hidden % 128 == 0; }
+static int wtile_k(int32_t depth) { return std::min<int32_t>(depth, WT_TOP_LEVELS); }
+
 size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
     const size_t recs = size_t(n_tokens) * size_t(n_trees);
     const size_t bins = (size_t(1) << depth) * size_t(n_trees);
-    const size_t parts = size_t(n_trees) * size_t(bwd_pieces(n_tokens, bwd_piece(n_tokens, n_trees))) *
-                         size_t(depth + 1) * 4 * size_t(hidden);
+    size_t parts;
+    if (wtile_shape(depth, hidden)) {
+        const int k = wtile_k(depth);
+        parts = size_t(n_trees) * (size_t(1) << k) * size_t(k) * 2 * size_t(hidden);
+    } else {
+        parts = size_t(n_trees) * size_t(bwd_pieces(n_tokens, bwd_piece(n_tokens, n_trees))) * size_t(depth + 1) *
+                4 * size_t(hidden);
+    }
     return align256(recs * size_t(depth + 1) * sizeof(float2)) + 2 * align256(bins * sizeof(int32_t)) +
            align256(recs * sizeof(int32_t)) + align256(size_t(n_trees) * sizeof(int32_t)) +
+           align256(recs * sizeof(int32_t)) + align256(bins * size_t(bwd_chunks(n_tokens)) * sizeof(int32_t)) +
            align256(parts * sizeof(float));
 }
 
@@ -625,6 +1006,12 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
     w += align256(recs * sizeof(int32_t));
     p.total = reinterpret_cast<int32_t*>(w);
     w += align256(size_t(p.n_trees) * sizeof(int32_t));
+    p.chunk = bwd_chunk(p.n_tokens);
+    p.chunks = bwd_chunks(p.n_tokens);
+    p.rank = reinterpret_cast<int32_t*>(w);
+    w += align256(recs * sizeof(int32_t));
+    p.hist = reinterpret_cast<int32_t*>(w);
+    w += align256(bins * size_t(p.chunks) * sizeof(int32_t));
     p.part = reinterpret_cast<float*>(w);
 }
 
@@ -676,12 +1063,52 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
     hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scan_kernel), dim3(p.n_trees), dim3(SCAN_BLOCK),
                                    args, 0, stream);
     if (e != hipSuccess) return e;
-    {
-        const int64_t n = p.n_tokens * p.n_trees;
-        const int grid = int(std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap));
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scatter_kernel), dim3(grid), dim3(BWD_BLOCK), args, 0,
+    {  // stable placement in leaf order
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_kernel), dim3(unsigned(p.chunks), p.n_trees),
+                            dim3(RANK_BLOCK), args, size_t(p.chunk) * sizeof(int32_t), stream);
+        if (e != hipSuccess) return e;
+        const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_base_kernel),
+                            dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), args, 0,
                             stream);
         if (e != hipSuccess) return e;
+        const int64_t n = p.n_tokens * p.n_trees;
+        const int grid = int(std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap));
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_place_kernel), dim3(grid), dim3(BWD_BLOCK), args, 0,
+                            stream);
+        if (e != hipSuccess) return e;
+    }
+    if (wtile_shape(p.depth, p.hidden)) {  // weight sums on MFMA, leaf by leaf
+        const int k = wtile_k(p.depth);
+        int sub = p.depth - k;
+        const void* kern = p.x_bf16 ? (p.dy_bf16 ? reinterpret_cast<const void*>(&bwd_wtile_kernel<true, true>)
+                                                 : reinterpret_cast<const void*>(&bwd_wtile_kernel<true, false>))
+                                    : (p.dy_bf16 ? reinterpret_cast<const void*>(&bwd_wtile_kernel<false, true>)
+                                                 : reinterpret_cast<const void*>(&bwd_wtile_kernel<false, false>));
+        const int waves = std::min(p.hidden / 128, WT_WAVES_MAX);
+        void* wargs[] = {&p, &sub};
+        e = hipLaunchKernel(kern, dim3(unsigned(int64_t(1) << k), p.n_trees), dim3(64 * waves), wargs, 0, stream);
+        if (e != hipSuccess) return e;
+        int kk = k;
+        const int64_t slices = (p.hidden + 255) / 256;
+        const int top = std::max(0, k - WFIX_SPLIT);  // levels 0 .. top-1 take the block kernel
+        int64_t top_nodes = (int64_t(1) << top) - 1;
+        if (top_nodes > 0) {
+            void* fargs[] = {&p, &kk, &top_nodes};
+            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_top_kernel),
+                                dim3(unsigned(int64_t(p.n_trees) * top_nodes * 2 * slices)), dim3(FIXW_BLOCK), fargs, 0,
+                                stream);
+            if (e != hipSuccess) return e;
+        }
+        int64_t rest = ((int64_t(1) << k) - 1) - top_nodes;
+        if (rest > 0) {
+            void* fargs[] = {&p, &kk, &top_nodes, &rest};
+            const int64_t waves = int64_t(p.n_trees) * rest * 2 * slices;
+            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_kernel),
+                                dim3(unsigned((waves + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), fargs,
+                                0, stream);
+        }
+        return e;
     }
     const int slices = (p.hidden + SLICE - 1) / SLICE;
     {

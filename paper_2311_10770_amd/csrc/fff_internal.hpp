@@ -88,6 +88,10 @@ struct BwdParams {
     int32_t* offs;           // [T, 2^D] first sorted position of each leaf, then the scatter cursor
     int32_t* perm;           // [T, B] token indices sorted by leaf
     int32_t* total;          // [T] valid (token, tree) pairs per tree
+    int32_t* rank;           // [T, B] rank of each token among its leaf's tokens earlier in its chunk
+    int32_t* hist;           // [T, chunks, 2^D] tokens per (chunk, leaf), then their first sorted position
+    int64_t chunks;          // token chunks of the stable placement
+    int32_t chunk;           // tokens per chunk
     float* part;             // [T, pieces, D+1, 2 slots, 2 matrices, H] run sums that cross pieces
     int32_t piece;           // sorted positions per piece of the weight kernel
     int32_t pieces;          // pieces per tree

@@ -462,8 +462,6 @@ __device__ __forceinline__ void tile_store8(const Params& p, const void* xs, voi
     }
 }
 
-typedef float tile_v4f __attribute__((ext_vector_type(4)));
-
 // Grid: one workgroup per leaf (XCD-affine by the subtree at the split level),
 // then spill workgroups.  ELANES/ENV: the per-token emit layout for spilled
 // tokens; YM: the output form.

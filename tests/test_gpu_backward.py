@@ -113,7 +113,8 @@ def test_bounded_generic_widths(fff_lib, H, wd):
     bounded_case(fff_lib, f"generic H={H}", L, 7, 3, synth.make_x(321, 500, H, "f32"))
 
 
-@pytest.mark.parametrize("B,D,T", [(1, 11, 1), (5, 3, 2), (257, 14, 1), (3000, 0, 64), (1000, 2, 300)])
+@pytest.mark.parametrize("B,D,T", [(1, 11, 1), (5, 3, 2), (257, 14, 1), (400, 15, 1), (300, 16, 1), (3000, 0, 64),
+                                   (1000, 2, 300)])
 def test_bounded_shapes(fff_lib, B, D, T):
     L = synth.make_layer(330 + B, B, 768, D, T, "bf16", "bf16")
     bounded_case(fff_lib, f"B={B} D={D} T={T}", L, D, T, synth.make_x(331, B, 768, "bf16"))
@@ -173,3 +174,29 @@ def test_headline_layer_full_size(fff_lib):
     bounded_case(fff_lib, "d11 65536 bf16", L, w.depth, w.n_trees, synth.make_x(w.seed + 100, w.n_tokens,
                                                                                    w.hidden, "bf16"),
                  path_from="device", dx_dtype="bf16")
+
+
+@pytest.mark.parametrize("B,H,D", [(6000, 768, 11), (5000, 1024, 9)])
+def test_bitwise_reproducible_with_skewed_and_one_hot_leaves(fff_lib, B, H, D):
+    """Two backward calls on the same inputs give the same bits (no atomics, stable leaf order, fixed
+    summation order), with clustered tokens (skewed leaves) and with every token on one path (a
+    single leaf holding the whole batch, more token ids than one workgroup stages in LDS)."""
+    for kind in ("clustered", "one path"):
+        if kind == "clustered":
+            x = synth.make_clustered_x(360 + H, B, H, "bf16")
+        else:
+            x = np.repeat(synth.make_x(361 + H, 1, H, "bf16"), B, axis=0)
+        wi, wo = synth.make_weights(360 + H, H, D, 1, "bf16")
+        L = {"x": x, "w_in": wi, "w_out": wo}
+        dy = synth.make_x(362 + H, B, H, "bf16")
+        fwd = oracle.forward(x, wi, wo, D, 1)
+        leaves = fwd["nodes"][:, :, D].astype(np.int32)
+        logits32 = fwd["logits"].astype(np.float32)
+        flush_print(f"[gpu] bwd twice {kind}: B={B} H={H} D={D}, largest leaf {np.bincount(leaves[:, 0]).max()}")
+        a = run_bwd(fff_lib, L, D, 1, dy, leaves, logits32)
+        b = run_bwd(fff_lib, L, D, 1, dy, leaves, logits32)
+        for k in ("dx", "dw_in", "dw_out"):
+            assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), (kind, k)
+        ref = oracle.backward(x, wi, wo, D, 1, dy, fwd["nodes"])
+        rep = parity.backward_check(x, wi, wo, D, 1, dy, fwd["nodes"], logits32, a, ref)
+        assert rep["ok"], (kind, rep["fail"])
