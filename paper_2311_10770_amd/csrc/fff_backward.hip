@@ -333,6 +333,23 @@ __global__ __launch_bounds__(BWD_BLOCK) void bwd_base_kernel(BwdParams p) {
     if (lane == 0) p.offs[i] = run;
 }
 
+// bwd_leafsum_kernel (one wave per (tree, leaf)): the leaf's token count, the
+// sum of its chunk counts (the fused path counts leaves here, not in a token
+// kernel).
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_leafsum_kernel(BwdParams p) {
+    const int64_t L = int64_t(1) << p.depth;
+    const int lane = threadIdx.x & 63;
+    const int64_t i = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
+    if (i >= L * p.n_trees) return;  // wave-uniform
+    const int64_t t = i / L, leaf = i - t * L;
+    const int32_t* h = p.hist + t * p.chunks * L + leaf;
+    int32_t sum = 0;
+    for (int64_t c = lane; c < p.chunks; c += 64) sum += h[c * L];
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) sum += __shfl_xor(sum, d, 64);
+    if (lane == 0) p.counts[i] = sum;
+}
+
 // bwd_place_kernel: perm[t][position] = token.
 __global__ __launch_bounds__(BWD_BLOCK) void bwd_place_kernel(BwdParams p) {
     const int T = p.n_trees, D = p.depth;
@@ -342,7 +359,18 @@ __global__ __launch_bounds__(BWD_BLOCK) void bwd_place_kernel(BwdParams p) {
         const int64_t b = i / T;
         const int t = int(i % T);
         const int32_t leaf = p.leaves[i];
-        if (!leaf_ok(leaf, D)) continue;
+        if (!leaf_ok(leaf, D)) {
+            if (p.fused) {  // no token kernel ran: count the pair and give the token a zero dx row
+                if (p.bad) atomicAdd(p.bad, 1);
+                if (p.dx && !p.accumulate) {
+                    for (int64_t c = 0; c < p.hidden; ++c) {
+                        if (p.dx_bf16) reinterpret_cast<uint16_t*>(p.dx)[b * p.hidden + c] = 0;
+                        else reinterpret_cast<float*>(p.dx)[b * p.hidden + c] = 0.0f;
+                    }
+                }
+            }
+            continue;
+        }
         const int64_t bin = int64_t(leaf) - (L - 1);
         const int64_t pos = p.hist[(int64_t(t) * p.chunks + b / p.chunk) * L + bin] + p.rank[int64_t(t) * p.n_tokens + b];
         p.perm[int64_t(t) * p.n_tokens + pos] = int32_t(b);
@@ -836,6 +864,262 @@ __global__ __launch_bounds__(64 * WT_WAVES_MAX) void bwd_wtile_kernel(BwdParams 
     }
 }
 
+// ---------------------------------------------------------------------------
+// 1'. fused leaf-tiled backward (bf16 W, one tree, depth <= 15, hidden 128..1024)
+// ---------------------------------------------------------------------------
+//
+// The tokens of a leaf share all D+1 rows, so after the stable sort the whole
+// backward of a tile of sixteen tokens is dense algebra over one path:
+//     da[16, D+1]  = dY[16, H] W_out[path]^T   (bf16 MFMA 16x16x32, K = columns)
+//     a, dl        = act(l), da act'(l)         (the forward's logits)
+//     dx[16, H]    = dL[16, D+1] W_in[path]     (bf16 MFMA on dl split into bf16 parts)
+//     dW_out[path] += a^T dY,  dW_in[path] += dL^T X   (fp32 MFMA 16x16x4, K = four tokens)
+// One workgroup per subtree as in bwd_wtile_kernel, one wave per 128-column
+// group.  Each wave's da is a partial sum over its columns; the partials are
+// added in wave order through LDS.  dy (as two operand layouts) and x are read
+// in leaf order, once per token; dx is written once.  The dW rows are stored
+// and the fix-up run exactly as in bwd_wtile_kernel.
+constexpr int FUSED_WAVES_MAX = 8;
+
+template <bool XBF, bool DYBF>
+__global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdParams p, int sub) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, waves = blockDim.x >> 6;
+    const int n = lane & 15, q = lane >> 4, h = q & 1, part = q >> 1;
+    const int D = p.depth;
+    const int64_t L = int64_t(1) << D, H = p.hidden;
+    const int k = D - sub;
+    const int64_t st = blockIdx.x;
+    const int64_t leaf0 = st << sub;
+    const int nleaf = 1 << sub;
+    const int32_t* cnt = p.counts;
+    const int32_t* end = p.offs;  // after the placement: one past each leaf's last position
+    const int32_t* perm = p.perm;
+    const bool add = p.accumulate != 0;
+    const int64_t col = int64_t(wave) * 128;  // this wave's column group (hidden / 128 == waves)
+    __shared__ int32_t s_cnt[1 << WT_MAX_SUB];
+    __shared__ int32_t s_tok[WT_LDS_TOK];
+    __shared__ float red[FUSED_WAVES_MAX][16][17];  // per-wave partial da [token][level]
+    __shared__ float s_a[16][17], s_dl[16][17];
+    __shared__ int32_t s_tt[16];
+    for (int i = threadIdx.x; i < nleaf; i += blockDim.x) s_cnt[i] = cnt[leaf0 + i];
+    const int64_t first = int64_t(end[leaf0]) - cnt[leaf0];
+    const int64_t range = int64_t(end[leaf0 + nleaf - 1]) - first;
+    const bool staged = range <= WT_LDS_TOK;  // workgroup-uniform
+    if (staged)
+        for (int64_t i = threadIdx.x; i < range; i += blockDim.x) s_tok[i] = perm[first + i];
+    __syncthreads();
+
+    const uint16_t* wout16 = reinterpret_cast<const uint16_t*>(p.w_out);
+    const uint16_t* win16 = reinterpret_cast<const uint16_t*>(p.w_in);
+    tile_v4f ao[8], ai[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ao[j] = ai[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+    int64_t pos0 = first;
+    for (int jl = 0; jl < nleaf; ++jl) {
+        const int64_t leaf = leaf0 + jl;
+        const uint32_t leaf1 = uint32_t(leaf + L);
+        const int32_t c = s_cnt[jl];
+        if (c > 0) {  // workgroup-uniform
+            // da B operand: lane (level n, q) holds W_out[node(n)][col + 32 s + 8 q .. +7]
+            uint4 wo[4];
+            {
+                const int lv = n <= D ? n : D;  // levels past D: any row (their da is not used)
+                const int64_t node = int64_t(leaf1 >> (D - lv)) - 1;
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    wo[s] = *reinterpret_cast<const uint4*>(wout16 + node * H + col + 32 * s + 8 * q);
+            }
+            // dx B operand: bj[j] = column col + 8n + j of the W_in rows of levels 8h .. 8h+7
+            uint4 bj[8];
+            {
+                uint4 row[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int lvl = 8 * h + i <= D ? 8 * h + i : D;
+                    row[i] = *reinterpret_cast<const uint4*>(win16 + (int64_t(leaf1 >> (D - lvl)) - 1) * H + col + 8 * n);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    uint32_t w4[4];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        const uint32_t lo = word(row[2 * qq], j / 2), hi = word(row[2 * qq + 1], j / 2);
+                        w4[qq] = (j & 1) ? (lo >> 16) | (hi & 0xffff0000u) : (lo & 0xffffu) | (hi << 16);
+                    }
+                    bj[j] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+                }
+            }
+            for (int32_t t0 = 0; t0 < c; t0 += 16) {
+                // the tile's token ids (-1 past the leaf's count)
+                if (threadIdx.x < 16) {
+                    const int32_t slot = t0 + int32_t(threadIdx.x);
+                    s_tt[threadIdx.x] = slot < c ? (staged ? s_tok[pos0 + slot - first] : perm[pos0 + slot]) : -1;
+                }
+                __syncthreads();
+                // 1. partial da over this wave's columns: A = dy of token m (lane (m, q))
+                {
+                    const int32_t tm = s_tt[n] >= 0 ? s_tt[n] : s_tt[0];  // lane (token n, q)
+                    tile_v4f da = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) {
+                        const int64_t at = int64_t(tm) * H + col + 32 * s + 8 * q;
+                        if constexpr (DYBF) {
+                            const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.dy) + at);
+                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, v),
+                                                                         __builtin_bit_cast(bf16x8_t, wo[s]), da, 0, 0, 0);
+                        } else {
+                            // fp32 dy: three bf16 parts (hi, mid, lo), each product exact
+                            const float4 u0 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at);
+                            const float4 u1 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at + 4);
+                            const float v[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+                            uint32_t ph[4], pm[4], pl[4];
+#pragma unroll
+                            for (int qq = 0; qq < 4; ++qq) {
+                                const float x0 = v[2 * qq], x1 = v[2 * qq + 1];
+                                ph[qq] = pack_bf16x2(x0, x1);
+                                const float r0 = x0 - bf16_lo(ph[qq]), r1 = x1 - bf16_hi(ph[qq]);
+                                pm[qq] = pack_bf16x2(r0, r1);
+                                pl[qq] = pack_bf16x2(r0 - bf16_lo(pm[qq]), r1 - bf16_hi(pm[qq]));
+                            }
+                            const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wo[s]);
+                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, make_uint4(ph[0], ph[1], ph[2], ph[3])), b, da, 0, 0, 0);
+                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, make_uint4(pm[0], pm[1], pm[2], pm[3])), b, da, 0, 0, 0);
+                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, make_uint4(pl[0], pl[1], pl[2], pl[3])), b, da, 0, 0, 0);
+                        }
+                    }
+                    // lane (level n, q) holds tokens 4q + r
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) red[wave][4 * q + r][n] = da[r];
+                }
+                __syncthreads();
+                // 2. a and dl of the tile's (token, level) pairs, the partials added in wave order
+                for (int i = threadIdx.x; i < 256; i += blockDim.x) {
+                    const int tt = i >> 4, lv = i & 15;
+                    float da = 0.0f;
+                    for (int w = 0; w < waves; ++w) da += red[w][tt][lv];
+                    const int32_t tok = s_tt[tt];
+                    float a = 0.0f, dl = 0.0f;
+                    if (tok >= 0 && lv <= D) {
+                        const float l = p.logits[int64_t(tok) * (D + 1) + lv];
+                        a = activation(l, p.act);
+                        dl = da * activation_grad(l, p.act);
+                    }
+                    s_a[tt][lv] = a;
+                    s_dl[tt][lv] = dl;
+                }
+                __syncthreads();
+                // 3. dx rows of the tile: A = parts of dl (token m, levels 8h .. 8h+7), B = bj
+                if (p.dx) {
+                    uint32_t p0[4], p1[4];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        const float x0 = s_dl[n][8 * h + 2 * qq], x1 = s_dl[n][8 * h + 2 * qq + 1];
+                        const uint32_t hi = pack_bf16x2(x0, x1);
+                        const float r0 = x0 - bf16_lo(hi), r1 = x1 - bf16_hi(hi);
+                        const uint32_t mid = pack_bf16x2(r0, r1);
+                        const uint32_t lo = pack_bf16x2(r0 - bf16_lo(mid), r1 - bf16_hi(mid));
+                        p0[qq] = part == 0 ? hi : mid;
+                        p1[qq] = part == 0 ? lo : 0u;
+                    }
+                    const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, make_uint4(p0[0], p0[1], p0[2], p0[3]));
+                    const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, make_uint4(p1[0], p1[1], p1[2], p1[3]));
+                    tile_v4f acc[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8_t, bj[j]),
+                                                                         tile_v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8_t, bj[j]), acc[j],
+                                                                         0, 0, 0);
+                    }
+                    // lane (n, q) holds tokens 4q + r, columns col + 8n + j
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int32_t tok = s_tt[4 * q + r];
+                        if (tok < 0) continue;
+                        float v[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] = acc[j][r];
+                        const int64_t at = int64_t(tok) * H + col + 8 * n;
+                        if (p.dx_bf16) {
+                            uint4* d = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p.dx) + at);
+                            if (add) {
+                                const uint4 o = *d;
+#pragma unroll
+                                for (int jj = 0; jj < 4; ++jj) {
+                                    v[2 * jj] += bf16_lo(word(o, jj));
+                                    v[2 * jj + 1] += bf16_hi(word(o, jj));
+                                }
+                            }
+                            *d = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                            pack_bf16x2(v[6], v[7]));
+                        } else {
+                            put8(reinterpret_cast<float*>(p.dx) + at, add, v);
+                        }
+                    }
+                }
+                // 4. dW sums, four tokens per step: A = a (dl) of token 4s + q at level n,
+                //    B = dy (x) of that token at columns col + 8n .. +7
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    const int32_t tok0 = s_tt[4 * s + q];
+                    const int32_t tok = tok0 >= 0 ? tok0 : s_tt[0];
+                    const float av = s_a[4 * s + q][n], dlv = s_dl[4 * s + q][n];
+                    const int64_t at = int64_t(tok) * H + col + 8 * n;
+                    float dy8[8], x8[8];
+                    load8f(p.dy, DYBF, at, dy8);
+                    load8f(p.x, XBF, at, x8);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, dy8[j], ao[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv, x8[j], ai[j], 0, 0, 0);
+                    }
+                }
+                __syncthreads();  // the next tile rewrites s_tt, red, s_a and s_dl
+            }
+        }
+        pos0 += c;
+        // rows this leaf completes (levels lv >= k whose node's last leaf this is)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int lv = 4 * q + r;
+            if (lv <= D && lv >= k && ((leaf + 1) & ((int64_t(1) << (D - lv)) - 1)) == 0) {
+                const int64_t node = ((leaf + L) >> (D - lv)) - 1;
+                float v[8];
+                if (p.dw_out) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) v[j] = ao[j][r];
+                    put8(p.dw_out + node * H + col + 8 * n, add, v);
+                }
+                if (p.dw_in) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) v[j] = ai[j][r];
+                    put8(p.dw_in + node * H + col + 8 * n, add, v);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) ao[j][r] = ai[j][r] = 0.0f;
+            }
+        }
+    }
+    // levels above the subtree root: this subtree's sums for the fix-up
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int lv = 4 * q + r;
+        if (lv < k) {
+            float* dst = p.part + ((st * k + lv) * 2) * H + col + 8 * n;
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = ao[j][r];
+            put8(dst, false, v);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = ai[j][r];
+            put8(dst + H, false, v);
+        }
+    }
+}
+
 // Rows of the levels above the subtrees: node u at level lv < k sums the part[]
 // of its 2^(k-lv) subtrees in subtree order, four running sums (subtree j goes to
 // sum j % 4), then the sums added in order.  bwd_wfix_kernel: one wave per
@@ -1015,6 +1299,57 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
     p.part = reinterpret_cast<float*>(w);
 }
 
+// The fix-up of the rows above the subtrees (levels 0 .. k-1) after bwd_wtile_kernel or
+// bwd_fused_kernel.
+static hipError_t launch_wfix(BwdParams& p, int k, hipStream_t stream) {
+    hipError_t e = hipSuccess;
+    int kk = k;
+    const int64_t slices = (p.hidden + 255) / 256;
+    const int top = std::max(0, k - WFIX_SPLIT);  // levels 0 .. top-1 take the block kernel
+    int64_t top_nodes = (int64_t(1) << top) - 1;
+    if (top_nodes > 0) {
+        void* fargs[] = {&p, &kk, &top_nodes};
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_top_kernel),
+                            dim3(unsigned(int64_t(p.n_trees) * top_nodes * 2 * slices)), dim3(FIXW_BLOCK), fargs, 0,
+                            stream);
+        if (e != hipSuccess) return e;
+    }
+    int64_t rest = ((int64_t(1) << k) - 1) - top_nodes;
+    if (rest > 0) {
+        void* fargs[] = {&p, &kk, &top_nodes, &rest};
+        const int64_t waves = int64_t(p.n_trees) * rest * 2 * slices;
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_kernel),
+                            dim3(unsigned((waves + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), fargs, 0,
+                            stream);
+    }
+    return e;
+}
+
+// The stable placement in leaf order (rank, [leaf sums], scan, base, place).
+static hipError_t launch_sort(BwdParams& p, bool count_leaves, const int64_t cap, hipStream_t stream) {
+    void* args[] = {&p};
+    const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_kernel), dim3(unsigned(p.chunks), p.n_trees),
+                                   dim3(RANK_BLOCK), args, size_t(p.chunk) * sizeof(int32_t), stream);
+    if (e != hipSuccess) return e;
+    if (count_leaves) {
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_leafsum_kernel),
+                            dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), args, 0,
+                            stream);
+        if (e != hipSuccess) return e;
+    }
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scan_kernel), dim3(p.n_trees), dim3(SCAN_BLOCK), args, 0,
+                        stream);
+    if (e != hipSuccess) return e;
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_base_kernel),
+                        dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), args, 0, stream);
+    if (e != hipSuccess) return e;
+    const int64_t n = p.n_tokens * p.n_trees;
+    const int grid = int(std::max<int64_t>(1, std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap)));
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bwd_place_kernel), dim3(grid), dim3(BWD_BLOCK), args, 0,
+                           stream);
+}
+
 hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, int* status) {
     *status = ST_OK_;
     const BwdVariant* v = nullptr;
@@ -1025,8 +1360,24 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         *status = ST_UNSUPPORTED_;
         return hipSuccess;
     }
-    void* args[] = {&p};
     const int64_t cap = int64_t(dev.cu_count) * 8;
+    // bf16 weights, one tree, depth <= 15, hidden 128..1024: the fused leaf-tiled backward
+    p.fused = p.need_dw && p.w_bf16 && p.n_trees == 1 && wtile_shape(p.depth, p.hidden) && p.hidden <= 1024;
+    if (p.fused) {
+        hipError_t e = launch_sort(p, true, cap, stream);
+        if (e != hipSuccess) return e;
+        const int k = wtile_k(p.depth);
+        int sub = p.depth - k;
+        const void* kern = p.x_bf16 ? (p.dy_bf16 ? reinterpret_cast<const void*>(&bwd_fused_kernel<true, true>)
+                                                 : reinterpret_cast<const void*>(&bwd_fused_kernel<true, false>))
+                                    : (p.dy_bf16 ? reinterpret_cast<const void*>(&bwd_fused_kernel<false, true>)
+                                                 : reinterpret_cast<const void*>(&bwd_fused_kernel<false, false>));
+        void* fargs[] = {&p, &sub};
+        e = hipLaunchKernel(kern, dim3(unsigned(int64_t(1) << k)), dim3(64 * (p.hidden / 128)), fargs, 0, stream);
+        if (e != hipSuccess) return e;
+        return launch_wfix(p, k, stream);
+    }
+    void* args[] = {&p};
     if (p.need_dw) {  // zero the leaf counts (a fill kernel: no memset nodes)
         const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
         float* a = nullptr;
@@ -1060,24 +1411,8 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         if (e != hipSuccess) return e;
     }
     if (!p.need_dw) return hipSuccess;
-    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scan_kernel), dim3(p.n_trees), dim3(SCAN_BLOCK),
-                                   args, 0, stream);
+    hipError_t e = launch_sort(p, false, cap, stream);
     if (e != hipSuccess) return e;
-    {  // stable placement in leaf order
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_kernel), dim3(unsigned(p.chunks), p.n_trees),
-                            dim3(RANK_BLOCK), args, size_t(p.chunk) * sizeof(int32_t), stream);
-        if (e != hipSuccess) return e;
-        const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_base_kernel),
-                            dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), args, 0,
-                            stream);
-        if (e != hipSuccess) return e;
-        const int64_t n = p.n_tokens * p.n_trees;
-        const int grid = int(std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap));
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_place_kernel), dim3(grid), dim3(BWD_BLOCK), args, 0,
-                            stream);
-        if (e != hipSuccess) return e;
-    }
     if (wtile_shape(p.depth, p.hidden)) {  // weight sums on MFMA, leaf by leaf
         const int k = wtile_k(p.depth);
         int sub = p.depth - k;
@@ -1089,26 +1424,7 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         void* wargs[] = {&p, &sub};
         e = hipLaunchKernel(kern, dim3(unsigned(int64_t(1) << k), p.n_trees), dim3(64 * waves), wargs, 0, stream);
         if (e != hipSuccess) return e;
-        int kk = k;
-        const int64_t slices = (p.hidden + 255) / 256;
-        const int top = std::max(0, k - WFIX_SPLIT);  // levels 0 .. top-1 take the block kernel
-        int64_t top_nodes = (int64_t(1) << top) - 1;
-        if (top_nodes > 0) {
-            void* fargs[] = {&p, &kk, &top_nodes};
-            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_top_kernel),
-                                dim3(unsigned(int64_t(p.n_trees) * top_nodes * 2 * slices)), dim3(FIXW_BLOCK), fargs, 0,
-                                stream);
-            if (e != hipSuccess) return e;
-        }
-        int64_t rest = ((int64_t(1) << k) - 1) - top_nodes;
-        if (rest > 0) {
-            void* fargs[] = {&p, &kk, &top_nodes, &rest};
-            const int64_t waves = int64_t(p.n_trees) * rest * 2 * slices;
-            e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_kernel),
-                                dim3(unsigned((waves + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), fargs,
-                                0, stream);
-        }
-        return e;
+        return launch_wfix(p, k, stream);
     }
     const int slices = (p.hidden + SLICE - 1) / SLICE;
     {

@@ -92,6 +92,7 @@ struct BwdParams {
     int32_t* hist;           // [T, chunks, 2^D] tokens per (chunk, leaf), then their first sorted position
     int64_t chunks;          // token chunks of the stable placement
     int32_t chunk;           // tokens per chunk
+    int32_t fused;           // the fused leaf-tiled path runs (no token kernel)
     float* part;             // [T, pieces, D+1, 2 slots, 2 matrices, H] run sums that cross pieces
     int32_t piece;           // sorted positions per piece of the weight kernel
     int32_t pieces;          // pieces per tree
