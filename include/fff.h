@@ -220,10 +220,14 @@ int fff_forward_stack(const fff_args* a, const fff_layer* layers, int32_t n_laye
  * (x is the FFF input; a residual or a LayerNorm around the layer is the
  * caller's to differentiate).
  *
- * Work: a token kernel (dx and the per-visit pairs (a, dl)), a stable
- * counting sort of the tokens by leaf (every node's tokens form one run at
- * every level, in token order within a leaf), and the weight sums along that
- * order: for depth <= 15 and hidden a multiple of 128 on MFMA, one workgroup
+ * Work: a stable counting sort of the tokens by leaf (every node's tokens
+ * form one run at every level, in token order within a leaf).  With bf16
+ * weights, one tree, depth <= 15 and hidden 128..1024, one fused kernel then
+ * takes each leaf's tokens sixteen at a time through the whole backward on
+ * MFMA (da, a and dl, dx, the dW sums of the leaf's path), followed by a
+ * fix-up of the rows above its subtrees.  Otherwise a token kernel forms dx
+ * and the per-visit pairs (a, dl) first, and the weight sums run along the
+ * sorted order: for depth <= 15 and hidden a multiple of 128 on MFMA, one workgroup
  * per subtree accumulating the rows of its tokens' paths, with the rows above
  * the subtrees added in subtree order by a fix-up; otherwise by fixed pieces
  * of the sorted order summed in registers and a fix-up of the runs crossing
