@@ -173,6 +173,9 @@ def main():
                    "name": w.name, "n_tokens": B, "hidden": w.hidden, "depth": w.depth, "n_trees": w.n_trees,
                    "layers": NL, "norm": bool(args.norm), "mode": args.mode, "plan": plan},
         "kernel_us": {"mean": t["mean_ms"] * 1e3, "min": t["min_ms"] * 1e3, "std": t["std_ms"] * 1e3},
+        "timing": f"value and ms_per_step: the {args.steps} timed steps back to back between one pair of HIP "
+                  f"events on the launch stream; kernel_us and roofline: a second pass of {args.steps} steps, each "
+                  f"between its own pair of events",
     }
 
     # Measured HBM bytes per launch from a committed counter summary, valid only while the
@@ -183,7 +186,7 @@ def main():
     tpath = Path(args.traffic) if args.traffic else ROOT / "profiles" / f"traffic_{w.name}_{args.mode}.json"
     if tpath.exists():
         summ = json.loads(tpath.read_text())
-        if summ.get("kernel_source_hash") == kernel_source_hash():
+        if summ.get("kernel_source_hash") == kernel_source_hash(args.backward):
             traffic = summ.get("hbm_bytes_per_launch")
         else:
             log(f"{tpath.name} was taken on other kernel sources: traffic unreported")

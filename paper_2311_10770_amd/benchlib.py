@@ -76,21 +76,33 @@ def copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
 
 
 def time_launches(fn, steps: int, warmup: int, stream):
-    """Mean per-launch time from per-launch event pairs on `stream`, and the whole timed region."""
+    """Two timed passes of `steps` calls on `stream` after `warmup` untimed ones.
+
+    region_ms: the first pass, the calls back to back between one pair of events
+    (a timing event between every call would leave the GPU idle for a few
+    microseconds per call; a serving loop has none).  mean/min/max/std_ms: the
+    second pass, every call between its own pair of events: the duration of one
+    call's kernels."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    region_ms = e0.elapsed_time(e1)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    t0 = time.perf_counter()
     for i in range(steps):
         starts[i].record(stream)
         fn()
         ends[i].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    region_ms = starts[0].elapsed_time(ends[-1])
     return {"mean_ms": sum(per) / steps, "min_ms": min(per), "max_ms": max(per),
             "std_ms": (sum((p - sum(per) / steps) ** 2 for p in per) / steps) ** 0.5,
             "region_ms": region_ms, "wall_s": wall}

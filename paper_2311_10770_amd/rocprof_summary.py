@@ -21,10 +21,12 @@ PKG = Path(__file__).resolve().parent
 COPY_KERNEL = "copy_kernel"
 
 
-def kernel_source_hash() -> str:
-    """Hash of the kernel sources: counter figures are void once these change."""
+def kernel_source_hash(backward: bool = False) -> str:
+    """Hash of the sources the forward (or backward) kernels are compiled from: counter figures
+    taken on them are void once these change."""
     h = hashlib.sha256()
-    for name in ("fff_kernels.hip", "fff_backward.hip", "fff_common.hpp", "fff_device.hpp", "fff_internal.hpp"):
+    main = "fff_backward.hip" if backward else "fff_kernels.hip"
+    for name in (main, "fff_common.hpp", "fff_device.hpp", "fff_internal.hpp"):
         p = PKG / "csrc" / name
         if p.exists():
             h.update(p.read_bytes())
@@ -52,7 +54,7 @@ def read_counter(path: Path, counter: str, kernel: str) -> list:
 
 def summarise(kernels: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int) -> dict:
     names = [k for k in kernels.split(",") if k]
-    out = {"kernels": names, "kernel_source_hash": kernel_source_hash()}
+    out = {"kernels": names, "kernel_source_hash": kernel_source_hash(any(k.startswith("bwd_") for k in names))}
     if stats:
         durs = [read_stats(stats, k) for k in names]
         out["duration"] = {"per_kernel": durs, "step_mean_us": sum(d["mean_us"] for d in durs)}
