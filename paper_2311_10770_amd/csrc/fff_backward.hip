@@ -707,6 +707,41 @@ __device__ __forceinline__ void load8f(const void* base, bool bf, int64_t at, fl
     }
 }
 
+// Eight consecutive elements of a bf16 (one 16-byte word) or fp32 (two words)
+// row, loaded raw so that a caller can issue every load of a tile at once and
+// convert at the point of use; to8f gives the same floats as load8f.
+template <bool BF>
+struct Raw8 {
+    uint4 w[BF ? 1 : 2];
+};
+template <bool BF>
+__device__ __forceinline__ Raw8<BF> raw8(const void* base, int64_t at) {
+    Raw8<BF> r;
+    if constexpr (BF) {
+        r.w[0] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + at);
+    } else {
+        r.w[0] = *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(base) + at);
+        r.w[1] = *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(base) + at + 4);
+    }
+    return r;
+}
+template <bool BF>
+__device__ __forceinline__ void to8f(const Raw8<BF>& r, float* v) {
+    if constexpr (BF) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = bf16_lo(word(r.w[0], j));
+            v[2 * j + 1] = bf16_hi(word(r.w[0], j));
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[j] = __uint_as_float(word(r.w[0], j));
+            v[4 + j] = __uint_as_float(word(r.w[1], j));
+        }
+    }
+}
+
 // Eight fp32 values of a dW row: stored, or added to what is there.
 __device__ __forceinline__ void put8(float* dst, bool add, const float* v) {
     float4* d = reinterpret_cast<float4*>(dst);
@@ -898,15 +933,24 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
     const int64_t col = int64_t(wave) * 128;  // this wave's column group (hidden / 128 == waves)
     __shared__ int32_t s_cnt[1 << WT_MAX_SUB];
     __shared__ int32_t s_tok[WT_LDS_TOK];
-    __shared__ float red[FUSED_WAVES_MAX][16][17];  // per-wave partial da [token][level]
-    __shared__ float s_a[16][17], s_dl[16][17];
-    __shared__ int32_t s_tt[16];
+    // Tables of one tile, in two buffers by tile parity: a wave may enter the next tile while others
+    // finish this one (it cannot get two tiles ahead: the next tile's first barrier needs everyone).
+    __shared__ float red[2][FUSED_WAVES_MAX][16][17];  // per-wave partial da [token][level]
+    __shared__ float s_a[2][16][17], s_dl[2][16][17];
+    // each wave's dy tile (16 tokens x its 128 columns, one padding word per row), written in the
+    // da operand layout and read back in the dW one: a transpose without a second read of dy
+    constexpr int DW = DYBF ? 1 : 2;  // 16-byte words per 8 columns of dy
+    __shared__ uint4 s_dy[FUSED_WAVES_MAX][16][16 * DW + 1];
     for (int i = threadIdx.x; i < nleaf; i += blockDim.x) s_cnt[i] = cnt[leaf0 + i];
     const int64_t first = int64_t(end[leaf0]) - cnt[leaf0];
-    const int64_t range = int64_t(end[leaf0 + nleaf - 1]) - first;
-    const bool staged = range <= WT_LDS_TOK;  // workgroup-uniform
-    if (staged)
-        for (int64_t i = threadIdx.x; i < range; i += blockDim.x) s_tok[i] = perm[first + i];
+    const int64_t last = end[leaf0 + nleaf - 1];
+    // s_tok holds the sorted token ids of positions win0 .. win0 + WT_LDS_TOK - 1 (clipped to the
+    // subtree); a tile past the window moves it (rare: a subtree with that many tokens)
+    int64_t win0 = first;
+    auto stage = [&]() {
+        for (int64_t i = threadIdx.x; i < WT_LDS_TOK && win0 + i < last; i += blockDim.x) s_tok[i] = perm[win0 + i];
+    };
+    stage();
     __syncthreads();
 
     const uint16_t* wout16 = reinterpret_cast<const uint16_t*>(p.w_out);
@@ -914,6 +958,7 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
     tile_v4f ao[8], ai[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) ao[j] = ai[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+    int par = 0;  // buffer of the current tile's tables
     int64_t pos0 = first;
     for (int jl = 0; jl < nleaf; ++jl) {
         const int64_t leaf = leaf0 + jl;
@@ -949,29 +994,63 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     bj[j] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
                 }
             }
-            for (int32_t t0 = 0; t0 < c; t0 += 16) {
-                // the tile's token ids (-1 past the leaf's count)
-                if (threadIdx.x < 16) {
-                    const int32_t slot = t0 + int32_t(threadIdx.x);
-                    s_tt[threadIdx.x] = slot < c ? (staged ? s_tok[pos0 + slot - first] : perm[pos0 + slot]) : -1;
+            for (int32_t t0 = 0; t0 < c; t0 += 16, par ^= 1) {
+                const int32_t m_cnt = c - t0 < 16 ? c - t0 : 16;
+                // token of tile row r (r < 16), -1 past the leaf's count: one read per lane (row n),
+                // then cross-lane reads; row 0 stands in for absent rows where a load needs an address
+                if (pos0 + t0 + 16 > win0 + WT_LDS_TOK) {  // workgroup-uniform
+                    // every wave has read the ids of the tiles before: it passed their barriers
+                    win0 = pos0 + t0;
+                    stage();
+                    __syncthreads();
                 }
-                __syncthreads();
-                // 1. partial da over this wave's columns: A = dy of token m (lane (m, q))
+                const int32_t tv = n < m_cnt ? s_tok[pos0 + t0 - win0 + n] : -1;
+                auto row_tok = [&](int r) -> int32_t { return __shfl(tv, r, 64); };
+                const int32_t tk0 = row_tok(0);
+                auto valid = [&](int32_t t) -> int32_t { return t >= 0 ? t : tk0; };
+                int32_t t4[4];
+#pragma unroll
+                for (int s = 0; s < 4; ++s) t4[s] = row_tok(4 * s + q);  // dW rows: token 4s + q
+                constexpr int LG = 256 / 64;  // (token, level) entries per thread at one wave
+                int32_t tl[LG];
+#pragma unroll
+                for (int e = 0; e < LG; ++e) tl[e] = row_tok(((int(threadIdx.x) + e * int(blockDim.x)) >> 4) & 15);
+                // every global read of the tile, issued together: dy rows in the da operand layout
+                // (token n, columns col + 32s + 8q), dy and x rows in the dW layout (token 4s + q,
+                // columns col + 8n) and the logits
+                Raw8<DYBF> dyA[4];
+                Raw8<XBF> xB[4];
+                constexpr bool EARLY_X = XBF && DYBF;
+                auto load_x = [&]() {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) xB[s] = raw8<XBF>(p.x, int64_t(valid(t4[s])) * H + col + 8 * n);
+                };
                 {
-                    const int32_t tm = s_tt[n] >= 0 ? s_tt[n] : s_tt[0];  // lane (token n, q)
+                    const int64_t ra = int64_t(valid(tv)) * H + col + 8 * q;
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) dyA[s] = raw8<DYBF>(p.dy, ra + 32 * s);
+                }
+                float lg[LG];
+#pragma unroll
+                for (int e = 0; e < LG; ++e) {
+                    const int i = int(threadIdx.x) + e * int(blockDim.x);
+                    const int lv = i & 15;
+                    lg[e] = 0.0f;
+                    if (i < 256 && tl[e] >= 0 && lv <= D) lg[e] = p.logits[int64_t(tl[e]) * (D + 1) + lv];
+                }
+                // 1. partial da over this wave's columns: A = dy of token n (lane (n, q))
+                {
                     tile_v4f da = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int s = 0; s < 4; ++s) {
-                        const int64_t at = int64_t(tm) * H + col + 32 * s + 8 * q;
+                        const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wo[s]);
                         if constexpr (DYBF) {
-                            const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.dy) + at);
-                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, v),
-                                                                         __builtin_bit_cast(bf16x8_t, wo[s]), da, 0, 0, 0);
+                            da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, dyA[s].w[0]), b, da,
+                                                                         0, 0, 0);
                         } else {
                             // fp32 dy: three bf16 parts (hi, mid, lo), each product exact
-                            const float4 u0 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at);
-                            const float4 u1 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.dy) + at + 4);
-                            const float v[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+                            float v[8];
+                            to8f<DYBF>(dyA[s], v);
                             uint32_t ph[4], pm[4], pl[4];
 #pragma unroll
                             for (int qq = 0; qq < 4; ++qq) {
@@ -981,7 +1060,6 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                                 pm[qq] = pack_bf16x2(r0, r1);
                                 pl[qq] = pack_bf16x2(r0 - bf16_lo(pm[qq]), r1 - bf16_hi(pm[qq]));
                             }
-                            const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wo[s]);
                             da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                                 __builtin_bit_cast(bf16x8_t, make_uint4(ph[0], ph[1], ph[2], ph[3])), b, da, 0, 0, 0);
                             da = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -990,33 +1068,42 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                                 __builtin_bit_cast(bf16x8_t, make_uint4(pl[0], pl[1], pl[2], pl[3])), b, da, 0, 0, 0);
                         }
                     }
+                    // x rows of the dW sums (bf16 x and dy: in flight during the reduction and dx; otherwise
+                    // after dx, for registers); dy to the transpose
+                    if constexpr (EARLY_X) load_x();
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+#pragma unroll
+                        for (int w = 0; w < DW; ++w) s_dy[wave][n][(4 * s + q) * DW + w] = dyA[s].w[w];
                     // lane (level n, q) holds tokens 4q + r
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) red[wave][4 * q + r][n] = da[r];
+                    for (int r = 0; r < 4; ++r) red[par][wave][4 * q + r][n] = da[r];
                 }
                 __syncthreads();
                 // 2. a and dl of the tile's (token, level) pairs, the partials added in wave order
-                for (int i = threadIdx.x; i < 256; i += blockDim.x) {
-                    const int tt = i >> 4, lv = i & 15;
-                    float da = 0.0f;
-                    for (int w = 0; w < waves; ++w) da += red[w][tt][lv];
-                    const int32_t tok = s_tt[tt];
-                    float a = 0.0f, dl = 0.0f;
-                    if (tok >= 0 && lv <= D) {
-                        const float l = p.logits[int64_t(tok) * (D + 1) + lv];
-                        a = activation(l, p.act);
-                        dl = da * activation_grad(l, p.act);
+#pragma unroll
+                for (int e = 0; e < LG; ++e) {
+                    const int i = int(threadIdx.x) + e * int(blockDim.x);
+                    if (i < 256) {
+                        const int tt = i >> 4, lv = i & 15;
+                        float da = 0.0f;
+                        for (int w = 0; w < waves; ++w) da += red[par][w][tt][lv];
+                        float a = 0.0f, dl = 0.0f;
+                        if (tt < m_cnt && lv <= D) {
+                            a = activation(lg[e], p.act);
+                            dl = da * activation_grad(lg[e], p.act);
+                        }
+                        s_a[par][tt][lv] = a;
+                        s_dl[par][tt][lv] = dl;
                     }
-                    s_a[tt][lv] = a;
-                    s_dl[tt][lv] = dl;
                 }
                 __syncthreads();
-                // 3. dx rows of the tile: A = parts of dl (token m, levels 8h .. 8h+7), B = bj
+                // 3. dx rows of the tile: A = parts of dl (token n, levels 8h .. 8h+7), B = bj
                 if (p.dx) {
                     uint32_t p0[4], p1[4];
 #pragma unroll
                     for (int qq = 0; qq < 4; ++qq) {
-                        const float x0 = s_dl[n][8 * h + 2 * qq], x1 = s_dl[n][8 * h + 2 * qq + 1];
+                        const float x0 = s_dl[par][n][8 * h + 2 * qq], x1 = s_dl[par][n][8 * h + 2 * qq + 1];
                         const uint32_t hi = pack_bf16x2(x0, x1);
                         const float r0 = x0 - bf16_lo(hi), r1 = x1 - bf16_hi(hi);
                         const uint32_t mid = pack_bf16x2(r0, r1);
@@ -1037,7 +1124,7 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     // lane (n, q) holds tokens 4q + r, columns col + 8n + j
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const int32_t tok = s_tt[4 * q + r];
+                        const int32_t tok = row_tok(4 * q + r);  // dx rows: token 4q + r
                         if (tok < 0) continue;
                         float v[8];
 #pragma unroll
@@ -1061,23 +1148,23 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     }
                 }
                 // 4. dW sums, four tokens per step: A = a (dl) of token 4s + q at level n,
-                //    B = dy (x) of that token at columns col + 8n .. +7
+                //    B = dy (x) of that token at columns col + 8n .. +7 (absent tokens have a = dl = 0)
+                if constexpr (!EARLY_X) load_x();
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    const int32_t tok0 = s_tt[4 * s + q];
-                    const int32_t tok = tok0 >= 0 ? tok0 : s_tt[0];
-                    const float av = s_a[4 * s + q][n], dlv = s_dl[4 * s + q][n];
-                    const int64_t at = int64_t(tok) * H + col + 8 * n;
+                    const float av = s_a[par][4 * s + q][n], dlv = s_dl[par][4 * s + q][n];
+                    Raw8<DYBF> dyB;
+#pragma unroll
+                    for (int w = 0; w < DW; ++w) dyB.w[w] = s_dy[wave][4 * s + q][n * DW + w];
                     float dy8[8], x8[8];
-                    load8f(p.dy, DYBF, at, dy8);
-                    load8f(p.x, XBF, at, x8);
+                    to8f<DYBF>(dyB, dy8);
+                    to8f<XBF>(xB[s], x8);
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
                         ao[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, dy8[j], ao[j], 0, 0, 0);
                         ai[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv, x8[j], ai[j], 0, 0, 0);
                     }
                 }
-                __syncthreads();  // the next tile rewrites s_tt, red, s_a and s_dl
             }
         }
         pos0 += c;
