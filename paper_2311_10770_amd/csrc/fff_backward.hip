@@ -915,6 +915,9 @@ __global__ __launch_bounds__(64 * WT_WAVES_MAX) void bwd_wtile_kernel(BwdParams 
 // in leaf order, once per token; dx is written once.  The dW rows are stored
 // and the fix-up run exactly as in bwd_wtile_kernel.
 constexpr int FUSED_WAVES_MAX = 8;
+// two 32-bit words that may alias any LDS data (read back from tables written as uint16_t)
+typedef uint32_t lds_u32x2_base __attribute__((ext_vector_type(2)));
+typedef lds_u32x2_base __attribute__((may_alias)) lds_u32x2;
 
 template <bool XBF, bool DYBF>
 __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdParams p, int sub) {
@@ -936,11 +939,28 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
     // Tables of one tile, in two buffers by tile parity: a wave may enter the next tile while others
     // finish this one (it cannot get two tiles ahead: the next tile's first barrier needs everyone).
     __shared__ float red[2][FUSED_WAVES_MAX][16][17];  // per-wave partial da [token][level]
-    __shared__ float s_a[2][16][17], s_dl[2][16][17];
-    // each wave's dy tile (16 tokens x its 128 columns, one padding word per row), written in the
-    // da operand layout and read back in the dW one: a transpose without a second read of dy
+    // bf16 x and dy: the dW sums on bf16 MFMA (K = tokens), with a and dl level-major; otherwise
+    // on fp32 MFMA, with a token-major.  dl token-major for dx in both.
+    constexpr bool BF4 = XBF && DYBF;
+    __shared__ float s_a[2][BF4 ? 1 : 16][17], s_dl[2][16][17];
+    __shared__ float s_aT[2][BF4 ? 16 : 1][20], s_dlT[2][BF4 ? 16 : 1][20];
+    // Each wave's dy tile (and, with BF4, x tile) read back in another layout: a transpose without
+    // a second read.  BF4: dy then x, each [column slot][16 tokens] bf16, column c of the wave at
+    // slot (c % 8) * 16 + c / 8, so that a 16-column MFMA tile is 16 consecutive slots.
+    // Otherwise dy [token][column] with one padding word per row.
     constexpr int DW = DYBF ? 1 : 2;  // 16-byte words per 8 columns of dy
-    __shared__ uint4 s_dy[FUSED_WAVES_MAX][16][16 * DW + 1];
+    constexpr int DY_WORDS = BF4 ? 2 * 128 * 16 * 2 / 16 : 16 * (16 * DW + 1);
+    __shared__ uint4 s_dy[FUSED_WAVES_MAX][DY_WORDS];
+    uint16_t* const t16 = reinterpret_cast<uint16_t*>(&s_dy[wave][0]);  // BF4: dy^T, then x^T at 2048
+    // BF4: a row tile (token n of the tile, columns col + 32s + 8q .. +7) into a transposed table
+    auto put_t = [&](int base, const uint4& v, int s, bool keep) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t u = keep ? word(v, w) : 0u;
+            t16[base + ((2 * w) * 16 + 4 * s + q) * 16 + n] = uint16_t(u & 0xffffu);
+            t16[base + ((2 * w + 1) * 16 + 4 * s + q) * 16 + n] = uint16_t(u >> 16);
+        }
+    };
     for (int i = threadIdx.x; i < nleaf; i += blockDim.x) s_cnt[i] = cnt[leaf0 + i];
     const int64_t first = int64_t(end[leaf0]) - cnt[leaf0];
     const int64_t last = end[leaf0 + nleaf - 1];
@@ -1019,11 +1039,13 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                 // (token n, columns col + 32s + 8q), dy and x rows in the dW layout (token 4s + q,
                 // columns col + 8n) and the logits
                 Raw8<DYBF> dyA[4];
-                Raw8<XBF> xB[4];
+                Raw8<XBF> xB[4];  // BF4: the da operand layout; otherwise the dW one
                 constexpr bool EARLY_X = XBF && DYBF;
                 auto load_x = [&]() {
 #pragma unroll
-                    for (int s = 0; s < 4; ++s) xB[s] = raw8<XBF>(p.x, int64_t(valid(t4[s])) * H + col + 8 * n);
+                    for (int s = 0; s < 4; ++s)
+                        xB[s] = BF4 ? raw8<XBF>(p.x, int64_t(valid(tv)) * H + col + 8 * q + 32 * s)
+                                    : raw8<XBF>(p.x, int64_t(valid(t4[s])) * H + col + 8 * n);
                 };
                 {
                     const int64_t ra = int64_t(valid(tv)) * H + col + 8 * q;
@@ -1071,10 +1093,15 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     // x rows of the dW sums (bf16 x and dy: in flight during the reduction and dx; otherwise
                     // after dx, for registers); dy to the transpose
                     if constexpr (EARLY_X) load_x();
+                    if constexpr (BF4) {
 #pragma unroll
-                    for (int s = 0; s < 4; ++s)
+                        for (int s = 0; s < 4; ++s) put_t(0, dyA[s].w[0], s, n < m_cnt);
+                    } else {
 #pragma unroll
-                        for (int w = 0; w < DW; ++w) s_dy[wave][n][(4 * s + q) * DW + w] = dyA[s].w[w];
+                        for (int s = 0; s < 4; ++s)
+#pragma unroll
+                            for (int w = 0; w < DW; ++w) s_dy[wave][n * (16 * DW + 1) + (4 * s + q) * DW + w] = dyA[s].w[w];
+                    }
                     // lane (level n, q) holds tokens 4q + r
 #pragma unroll
                     for (int r = 0; r < 4; ++r) red[par][wave][4 * q + r][n] = da[r];
@@ -1093,7 +1120,12 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                             a = activation(lg[e], p.act);
                             dl = da * activation_grad(lg[e], p.act);
                         }
-                        s_a[par][tt][lv] = a;
+                        if constexpr (BF4) {
+                            s_aT[par][lv][tt] = a;
+                            s_dlT[par][lv][tt] = dl;
+                        } else {
+                            s_a[par][tt][lv] = a;
+                        }
                         s_dl[par][tt][lv] = dl;
                     }
                 }
@@ -1147,22 +1179,66 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                         }
                     }
                 }
-                // 4. dW sums, four tokens per step: A = a (dl) of token 4s + q at level n,
-                //    B = dy (x) of that token at columns col + 8n .. +7 (absent tokens have a = dl = 0)
-                if constexpr (!EARLY_X) load_x();
+                if constexpr (BF4) {
+                    // 4. dW sums on bf16 MFMA: K-slots 2i, 2i+1 of lane group q hold token 4q + i, A = the
+                    //    hi and mid bf16 parts of a (dl) in one product and the lo part and zero in a
+                    //    second, B = dy (x) of the token in both slots; every product is exact.  Output
+                    //    tile j, lane (n, q): levels 4q + r, column col + 8n + j.
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const float av = s_a[par][4 * s + q][n], dlv = s_dl[par][4 * s + q][n];
-                    Raw8<DYBF> dyB;
+                    for (int s = 0; s < 4; ++s) put_t(2048, xB[s].w[0], s, n < m_cnt);
+                    auto split = [](const float4& v, uint4& a1, uint4& a2) {
+                        uint32_t w1[4], w2[4];
 #pragma unroll
-                    for (int w = 0; w < DW; ++w) dyB.w[w] = s_dy[wave][4 * s + q][n * DW + w];
-                    float dy8[8], x8[8];
-                    to8f<DYBF>(dyB, dy8);
-                    to8f<XBF>(xB[s], x8);
+                        for (int i = 0; i < 4; ++i) {
+                            const float f = fword(v, i);
+                            const uint32_t hi = f32_to_bf16(f);
+                            const float r = f - bf16_to_f32(uint16_t(hi));
+                            const uint32_t mid = f32_to_bf16(r);
+                            const uint32_t lo = f32_to_bf16(r - bf16_to_f32(uint16_t(mid)));
+                            w1[i] = hi | (mid << 16);
+                            w2[i] = lo;
+                        }
+                        a1 = make_uint4(w1[0], w1[1], w1[2], w1[3]);
+                        a2 = make_uint4(w2[0], w2[1], w2[2], w2[3]);
+                    };
+                    uint4 aa1, aa2, ad1, ad2;
+                    split(*reinterpret_cast<const float4*>(&s_aT[par][n][4 * q]), aa1, aa2);
+                    split(*reinterpret_cast<const float4*>(&s_dlT[par][n][4 * q]), ad1, ad2);
+                    // four bf16 of a table row (read as a may_alias type: the table is written as uint16_t
+                    // with no barrier in between) -> each twice
+                    auto dup = [&](int at) {
+                        const lds_u32x2 u = *reinterpret_cast<const lds_u32x2*>(t16 + at);
+                        return make_uint4((u.x & 0xffffu) | (u.x << 16), (u.x >> 16) | (u.x & 0xffff0000u),
+                                          (u.y & 0xffffu) | (u.y << 16), (u.y >> 16) | (u.y & 0xffff0000u));
+                    };
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, dy8[j], ao[j], 0, 0, 0);
-                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv, x8[j], ai[j], 0, 0, 0);
+                        const int at = ((16 * j + n) * 16 + 4 * q);
+                        const bf16x8_t bd = __builtin_bit_cast(bf16x8_t, dup(at));
+                        const bf16x8_t bx = __builtin_bit_cast(bf16x8_t, dup(2048 + at));
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aa1), bd, ao[j], 0, 0, 0);
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aa2), bd, ao[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ad1), bx, ai[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ad2), bx, ai[j], 0, 0, 0);
+                    }
+                } else {
+                    // 4. dW sums on fp32 MFMA, four tokens per step: A = a (dl) of token 4s + q at level n,
+                    //    B = dy (x) of that token at columns col + 8n .. +7 (absent tokens have a = dl = 0)
+                    if constexpr (!EARLY_X) load_x();
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) {
+                        const float av = s_a[par][4 * s + q][n], dlv = s_dl[par][4 * s + q][n];
+                        Raw8<DYBF> dyB;
+#pragma unroll
+                        for (int w = 0; w < DW; ++w) dyB.w[w] = s_dy[wave][(4 * s + q) * (16 * DW + 1) + n * DW + w];
+                        float dy8[8], x8[8];
+                        to8f<DYBF>(dyB, dy8);
+                        to8f<XBF>(xB[s], x8);
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            ao[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, dy8[j], ao[j], 0, 0, 0);
+                            ai[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(dlv, x8[j], ai[j], 0, 0, 0);
+                        }
                     }
                 }
             }
@@ -1240,11 +1316,24 @@ __device__ __forceinline__ float4 wfix_sum(const BwdParams& p, int k, int t, int
     float4 s[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) s[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    // eight loads in flight, then their sums in subtree order
+    constexpr int BATCH = 8;
     int i = 0;
-    for (int64_t j = j0; j < count; j += step, i = (i + 1) & 3) {
-        const float4 v =
-            reinterpret_cast<const float4*>(p.part + ((((int64_t(t) << k) + first + j) * k + lv) * 2 + mat) * H)[c4];
-        s[i].x += v.x; s[i].y += v.y; s[i].z += v.z; s[i].w += v.w;
+    for (int64_t j = j0; j < count; j += BATCH * step) {
+        float4 v[BATCH];
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            const int64_t jj = j + b * step;
+            v[b] = jj < count ? reinterpret_cast<const float4*>(
+                                    p.part + ((((int64_t(t) << k) + first + jj) * k + lv) * 2 + mat) * H)[c4]
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+            if (j + b * step >= count) break;
+            s[i].x += v[b].x; s[i].y += v[b].y; s[i].z += v[b].z; s[i].w += v[b].w;
+            i = (i + 1) & 3;
+        }
     }
     float4 w = s[0];
 #pragma unroll
