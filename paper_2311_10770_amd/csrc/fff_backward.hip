@@ -683,13 +683,12 @@ __global__ __launch_bounds__(BWD_BLOCK) void bwd_fixup_kernel(BwdParams p, int t
 // rows of the nodes it completes (levels from the leaf up to the subtree root
 // whose last leaf it is) are stored and cleared; a node no token reached gets
 // a zero row.  The levels above the subtree root leave this subtree's sums in
-// part[] and are added in subtree order by bwd_wfix_kernel.  Every dW element
+// part[] and are added in a fixed order by bwd_wsum_kernel.  Every dW element
 // has one writer and the order of every sum is fixed.
 constexpr int WT_WAVES_MAX = 8;
 constexpr int WT_TOP_LEVELS = 9;   // subtrees hang at level min(D, 9)
 constexpr int WT_MAX_SUB = 6;      // depth <= 15: at most 2^6 leaves per subtree
 constexpr int WT_LDS_TOK = 4096;   // token ids of a subtree staged in LDS when they fit
-constexpr int FIXW_BLOCK = 1024;
 
 __device__ __forceinline__ void load8f(const void* base, bool bf, int64_t at, float* v) {
     if (bf) {
@@ -1283,105 +1282,64 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
     }
 }
 
-// Rows of the levels above the subtrees: node u at level lv < k sums the part[]
-// of its 2^(k-lv) subtrees in subtree order, four running sums (subtree j goes to
-// sum j % 4), then the sums added in order.  bwd_wfix_kernel: one wave per
-// (tree, node, matrix, 256-column slice) for the levels from k - WFIX_SPLIT on
-// (at most 2^WFIX_SPLIT subtrees each).  bwd_wfix_top_kernel: the levels above,
-// a 1024-thread block per task, wave w taking subtrees w, w+16, ...; the
-// sixteen wave sums are added in wave order.  Fixed order throughout.
-constexpr int WFIX_SPLIT = 5;
+// Rows of the levels above the subtrees (lv < k): node u at level lv sums the
+// part[] of its 2^(k-lv) subtrees.  One block per (tree, level, matrix,
+// 16-column slice); thread (column c, group g) owns subtrees g*per .. g*per +
+// per - 1 (G = min(64, 2^k) groups of per = 2^k / G <= 8 subtrees) and loads
+// them at once.  A node inside one group is summed there in subtree order; a
+// node spanning several groups adds its groups' sums in group order through
+// LDS.  The order is fixed, so the rows are the same on every run.
+constexpr int WSUM_GROUPS = 64;
+constexpr int WSUM_BLOCK = 16 * WSUM_GROUPS;
+static_assert((1 << WT_TOP_LEVELS) <= 8 * WSUM_GROUPS, "a group holds at most eight subtrees");
 
-__device__ __forceinline__ void wfix_task(const BwdParams& p, int k, int64_t task, int64_t node0, int64_t nodes,
-                                          int64_t* node, int* lv, int* mat, int64_t* c4, int* t) {
-    const int64_t slices = (int64_t(p.hidden) + 255) / 256;
-    int64_t b = task;
-    const int64_t slice = b % slices;
-    b /= slices;
-    *mat = int(b % 2);
-    b /= 2;
-    *node = node0 + b % nodes;
-    *t = int(b / nodes);
-    int l = 0;
-    while ((int64_t(2) << l) - 1 <= *node) ++l;  // node in [2^l - 1, 2^(l+1) - 1)
-    *lv = l;
-    *c4 = slice * 64;
-}
-
-__device__ __forceinline__ float4 wfix_sum(const BwdParams& p, int k, int t, int lv, int mat, int64_t node,
-                                           int64_t c4, int64_t j0, int64_t step) {
-    const int64_t u = node - ((int64_t(1) << lv) - 1);
-    const int64_t first = u << (k - lv), count = int64_t(1) << (k - lv);
-    const int64_t H = p.hidden;
-    float4 s[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) s[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    // eight loads in flight, then their sums in subtree order
-    constexpr int BATCH = 8;
-    int i = 0;
-    for (int64_t j = j0; j < count; j += BATCH * step) {
-        float4 v[BATCH];
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b) {
-            const int64_t jj = j + b * step;
-            v[b] = jj < count ? reinterpret_cast<const float4*>(
-                                    p.part + ((((int64_t(t) << k) + first + jj) * k + lv) * 2 + mat) * H)[c4]
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b) {
-            if (j + b * step >= count) break;
-            s[i].x += v[b].x; s[i].y += v[b].y; s[i].z += v[b].z; s[i].w += v[b].w;
-            i = (i + 1) & 3;
-        }
-    }
-    float4 w = s[0];
-#pragma unroll
-    for (int q = 1; q < 4; ++q) { w.x += s[q].x; w.y += s[q].y; w.z += s[q].z; w.w += s[q].w; }
-    return w;
-}
-
-__device__ __forceinline__ void wfix_store(const BwdParams& p, int t, int mat, int64_t node, int64_t c4, float4 a) {
+__global__ __launch_bounds__(WSUM_BLOCK) void bwd_wsum_kernel(BwdParams p, int k) {
+    __shared__ float red[WSUM_GROUPS][17];
+    const int c = threadIdx.x & 15, g = threadIdx.x >> 4;
+    const int64_t H = p.hidden, slices = H / 16;
+    const int64_t slice = blockIdx.x % slices;
+    const int mat = int((blockIdx.x / slices) % 2);
+    const int lv = int(blockIdx.x / (2 * slices));  // < k
+    const int64_t col = slice * 16 + c;
+    const int t = blockIdx.y;
+    const int64_t S = int64_t(1) << k;
+    const int G = S < WSUM_GROUPS ? int(S) : WSUM_GROUPS;
+    const int per = int(S / G);
+    const int span = 1 << (k - lv);  // subtrees under a node of this level
     float* dw = mat == 0 ? p.dw_out : p.dw_in;
-    if (!dw) return;
-    float4* d = reinterpret_cast<float4*>(dw + (int64_t(t) * p.n_nodes + node) * p.hidden) + c4;
-    if (p.accumulate) {
-        const float4 o = *d;
-        a.x += o.x; a.y += o.y; a.z += o.z; a.w += o.w;
+    auto store = [&](int64_t u, float v) {  // node u of the level
+        if (!dw) return;
+        float* d = dw + (int64_t(t) * p.n_nodes + ((int64_t(1) << lv) - 1) + u) * H + col;
+        *d = p.accumulate ? *d + v : v;
+    };
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t st = int64_t(g) * per + j;
+        v[j] = g < G && j < per ? p.part[((((int64_t(t) << k) + st) * k + lv) * 2 + mat) * H + col] : 0.0f;
     }
-    *d = a;
-}
-
-__global__ __launch_bounds__(BWD_BLOCK) void bwd_wfix_kernel(BwdParams p, int k, int64_t node0, int64_t nodes) {
-    const int lane = threadIdx.x & 63;
-    const int64_t task = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
-    const int64_t slices = (int64_t(p.hidden) + 255) / 256;
-    if (task >= int64_t(p.n_trees) * nodes * 2 * slices) return;  // wave-uniform
-    int64_t node, c4;
-    int lv, mat, t;
-    wfix_task(p, k, task, node0, nodes, &node, &lv, &mat, &c4, &t);
-    c4 += lane;
-    if (c4 * 4 >= p.hidden) return;
-    wfix_store(p, t, mat, node, c4, wfix_sum(p, k, t, lv, mat, node, c4, 0, 1));
-}
-
-__global__ __launch_bounds__(FIXW_BLOCK) void bwd_wfix_top_kernel(BwdParams p, int k, int64_t nodes) {
-    __shared__ float4 red[FIXW_BLOCK / 64][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int64_t node, c4;
-    int lv, mat, t;
-    wfix_task(p, k, blockIdx.x, 0, nodes, &node, &lv, &mat, &c4, &t);
-    c4 += lane;
-    const bool live = c4 * 4 < p.hidden;
-    red[wave][lane] = live ? wfix_sum(p, k, t, lv, mat, node, c4, wave, FIXW_BLOCK / 64) : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (span <= per) {  // block-uniform
+        if (g < G)
+            for (int j0 = 0; j0 < per; j0 += span) {
+                float sum = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (j >= j0 && j < j0 + span) sum += v[j];
+                store((int64_t(g) * per + j0) >> (k - lv), sum);
+            }
+        return;
+    }
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (j < per) sum += v[j];
+    red[g][c] = sum;
     __syncthreads();
-    if (wave == 0 && live) {
-        float4 a = red[0][lane];
-        for (int i = 1; i < FIXW_BLOCK / 64; ++i) {
-            const float4 v = red[i][lane];
-            a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
-        }
-        wfix_store(p, t, mat, node, c4, a);
+    const int ng = span / per;  // groups per node
+    if (g < G && g % ng == 0) {
+        float tot = 0.0f;
+        for (int i = 0; i < ng; ++i) tot += red[g + i][c];
+        store((int64_t(g) * per) >> (k - lv), tot);
     }
 }
 
@@ -1477,28 +1435,13 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
 
 // The fix-up of the rows above the subtrees (levels 0 .. k-1) after bwd_wtile_kernel or
 // bwd_fused_kernel.
-static hipError_t launch_wfix(BwdParams& p, int k, hipStream_t stream) {
-    hipError_t e = hipSuccess;
+static hipError_t launch_wsum(BwdParams& p, int k, hipStream_t stream) {
+    if (k <= 0) return hipSuccess;
     int kk = k;
-    const int64_t slices = (p.hidden + 255) / 256;
-    const int top = std::max(0, k - WFIX_SPLIT);  // levels 0 .. top-1 take the block kernel
-    int64_t top_nodes = (int64_t(1) << top) - 1;
-    if (top_nodes > 0) {
-        void* fargs[] = {&p, &kk, &top_nodes};
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_top_kernel),
-                            dim3(unsigned(int64_t(p.n_trees) * top_nodes * 2 * slices)), dim3(FIXW_BLOCK), fargs, 0,
-                            stream);
-        if (e != hipSuccess) return e;
-    }
-    int64_t rest = ((int64_t(1) << k) - 1) - top_nodes;
-    if (rest > 0) {
-        void* fargs[] = {&p, &kk, &top_nodes, &rest};
-        const int64_t waves = int64_t(p.n_trees) * rest * 2 * slices;
-        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wfix_kernel),
-                            dim3(unsigned((waves + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), fargs, 0,
-                            stream);
-    }
-    return e;
+    void* fargs[] = {&p, &kk};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wsum_kernel),
+                           dim3(unsigned(int64_t(k) * 2 * (p.hidden / 16)), unsigned(p.n_trees)), dim3(WSUM_BLOCK), fargs,
+                           0, stream);
 }
 
 // The stable placement in leaf order (rank, [leaf sums], scan, base, place).
@@ -1551,7 +1494,7 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         void* fargs[] = {&p, &sub};
         e = hipLaunchKernel(kern, dim3(unsigned(int64_t(1) << k)), dim3(64 * (p.hidden / 128)), fargs, 0, stream);
         if (e != hipSuccess) return e;
-        return launch_wfix(p, k, stream);
+        return launch_wsum(p, k, stream);
     }
     void* args[] = {&p};
     if (p.need_dw) {  // zero the leaf counts (a fill kernel: no memset nodes)
@@ -1600,7 +1543,7 @@ hipError_t run_backward(BwdParams p, const DeviceInfo& dev, hipStream_t stream, 
         void* wargs[] = {&p, &sub};
         e = hipLaunchKernel(kern, dim3(unsigned(int64_t(1) << k), p.n_trees), dim3(64 * waves), wargs, 0, stream);
         if (e != hipSuccess) return e;
-        return launch_wfix(p, k, stream);
+        return launch_wsum(p, k, stream);
     }
     const int slices = (p.hidden + SLICE - 1) / SLICE;
     {
