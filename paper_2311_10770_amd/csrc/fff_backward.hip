@@ -306,6 +306,54 @@ __global__ __launch_bounds__(RANK_BLOCK) void bwd_rank_kernel(BwdParams p) {
     }
 }
 
+// bwd_rank_wave_kernel: the same outputs for chunks of RANKW_BLOCK tokens, one
+// per thread, when the chunk's leaf counters fit in LDS (depth <=
+// RANKW_MAX_DEPTH).  A wave finds the lanes holding its leaf with depth + 1
+// ballots (one per bit of the leaf, one for validity); a token's rank is the
+// count of its leaf in the chunk's earlier waves plus its matching lanes below
+// it.  The waves take their turn in order: a wave reads its leaves' counters,
+// then the last lane of each leaf group adds the group's size.
+constexpr int RANKW_BLOCK = 1024;
+constexpr int RANKW_MAX_DEPTH = 14;  // 16384 counters: 64 KB of LDS
+
+__global__ __launch_bounds__(RANKW_BLOCK) void bwd_rank_wave_kernel(BwdParams p) {
+    extern __shared__ int32_t cnt_l[];  // [2^depth]
+    const int t = blockIdx.y, T = p.n_trees, D = p.depth;
+    const int64_t L = int64_t(1) << D;
+    const int64_t chunk = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int64_t i = tid; i < L; i += RANKW_BLOCK) cnt_l[i] = 0;
+    const int64_t b = chunk * RANKW_BLOCK + tid;
+    int32_t bin = -1;
+    if (b < p.n_tokens) {
+        const int32_t leaf = p.leaves[b * T + t];
+        if (leaf_ok(leaf, D)) bin = int32_t(int64_t(leaf) - (L - 1));
+    }
+    // key: the bin, or L for no bin; lanes with equal keys
+    const uint32_t key = bin >= 0 ? uint32_t(bin) : uint32_t(L);
+    uint64_t same = ~uint64_t(0);
+    for (int i = 0; i <= D; ++i) {
+        const bool bit = (key >> i) & 1u;
+        const uint64_t m = __ballot(bit);
+        same &= bit ? m : ~m;
+    }
+    const int below = __popcll(same & ((uint64_t(1) << lane) - 1));
+    const bool leader = lane == 63 || (same >> (lane + 1)) == 0;  // last lane of its group
+    int32_t rank = 0;
+    __syncthreads();  // counters zeroed
+    for (int w = 0; w < RANKW_BLOCK / 64; ++w) {
+        if (wave == w && bin >= 0) {
+            const int32_t base = cnt_l[bin];
+            rank = base + below;
+            if (leader) cnt_l[bin] = base + __popcll(same);
+        }
+        __syncthreads();
+    }
+    if (b < p.n_tokens) p.rank[int64_t(t) * p.n_tokens + b] = rank;
+    int32_t* h = p.hist + (int64_t(t) * p.chunks + chunk) * L;
+    for (int64_t i = tid; i < L; i += RANKW_BLOCK) h[i] = cnt_l[i];
+}
+
 // bwd_base_kernel (one wave per (tree, leaf)): turns the chunk counts into the
 // first sorted position of the leaf's tokens in each chunk (an exclusive scan
 // over the chunks, 64 at a time), and leaves offs at one past the leaf's last
@@ -1377,12 +1425,15 @@ static int64_t bwd_pieces(int64_t n_tokens, int32_t piece) { return std::max<int
 
 // Tokens per chunk of the stable placement: one per rank-kernel thread, more (up to 16) once the
 // batch would need over 512 chunks, which bounds the [chunks, leaves] table.
-static int32_t bwd_chunk(int64_t n_tokens) {
+// Tokens per chunk of the stable sort: RANKW_BLOCK with the ballot rank kernel (its leaf
+// counters in LDS), else RANK_BLOCK x 1..16 for the compare-all rank kernel.
+static int32_t bwd_chunk(int64_t n_tokens, int32_t depth) {
+    if (depth <= RANKW_MAX_DEPTH) return RANKW_BLOCK;
     const int64_t per = std::min<int64_t>(16, std::max<int64_t>(1, (n_tokens + RANK_BLOCK * 512 - 1) / (RANK_BLOCK * 512)));
     return int32_t(RANK_BLOCK * per);
 }
-static int64_t bwd_chunks(int64_t n_tokens) {
-    const int64_t c = bwd_chunk(n_tokens);
+static int64_t bwd_chunks(int64_t n_tokens, int32_t depth) {
+    const int64_t c = bwd_chunk(n_tokens, depth);
     return std::max<int64_t>(1, (n_tokens + c - 1) / c);
 }
 
@@ -1404,7 +1455,7 @@ size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int
     }
     return align256(recs * size_t(depth + 1) * sizeof(float2)) + 2 * align256(bins * sizeof(int32_t)) +
            align256(recs * sizeof(int32_t)) + align256(size_t(n_trees) * sizeof(int32_t)) +
-           align256(recs * sizeof(int32_t)) + align256(bins * size_t(bwd_chunks(n_tokens)) * sizeof(int32_t)) +
+           align256(recs * sizeof(int32_t)) + align256(bins * size_t(bwd_chunks(n_tokens, depth)) * sizeof(int32_t)) +
            align256(parts * sizeof(float));
 }
 
@@ -1424,8 +1475,8 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
     w += align256(recs * sizeof(int32_t));
     p.total = reinterpret_cast<int32_t*>(w);
     w += align256(size_t(p.n_trees) * sizeof(int32_t));
-    p.chunk = bwd_chunk(p.n_tokens);
-    p.chunks = bwd_chunks(p.n_tokens);
+    p.chunk = bwd_chunk(p.n_tokens, p.depth);
+    p.chunks = bwd_chunks(p.n_tokens, p.depth);
     p.rank = reinterpret_cast<int32_t*>(w);
     w += align256(recs * sizeof(int32_t));
     p.hist = reinterpret_cast<int32_t*>(w);
@@ -1448,8 +1499,12 @@ static hipError_t launch_wsum(BwdParams& p, int k, hipStream_t stream) {
 static hipError_t launch_sort(BwdParams& p, bool count_leaves, const int64_t cap, hipStream_t stream) {
     void* args[] = {&p};
     const int64_t bins = (int64_t(1) << p.depth) * p.n_trees;
-    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_kernel), dim3(unsigned(p.chunks), p.n_trees),
-                                   dim3(RANK_BLOCK), args, size_t(p.chunk) * sizeof(int32_t), stream);
+    hipError_t e =
+        p.depth <= RANKW_MAX_DEPTH
+            ? hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_wave_kernel), dim3(unsigned(p.chunks), p.n_trees),
+                              dim3(RANKW_BLOCK), args, size_t(bins / p.n_trees) * sizeof(int32_t), stream)
+            : hipLaunchKernel(reinterpret_cast<const void*>(&bwd_rank_kernel), dim3(unsigned(p.chunks), p.n_trees),
+                              dim3(RANK_BLOCK), args, size_t(p.chunk) * sizeof(int32_t), stream);
     if (e != hipSuccess) return e;
     if (count_leaves) {
         e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_leafsum_kernel),
