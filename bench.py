@@ -126,7 +126,11 @@ def main():
         nn_ = (1 << (w.depth + 1)) - 1
         dwi = torch.empty((w.n_trees, nn_, w.hidden), dtype=torch.float32, device=dev)
         dwo = torch.empty_like(dwi)
-        plan = "backward: token kernel + counting sort by leaf + weight kernel"
+        fused = (w.n_trees == 1 and w.w_dtype == "bf16" and w.depth <= 15 and w.hidden % 128 == 0
+                 and w.hidden <= 1024)
+        plan = ("backward: stable sort by leaf (rank, leaf sums, scan, base, place) + fused leaf-tiled kernel "
+                "(da, dx, dW on MFMA per 16-token tile) + sums of the rows above the subtrees" if fused else
+                "backward: token kernel + stable sort by leaf + weight kernel + fix-up sums")
 
         def step():
             fff.backward(x, wi, wo, w.depth, w.n_trees, dy, leaves, logits_rec, dx=dx, dw_in=dwi, dw_out=dwo,
@@ -196,15 +200,30 @@ def main():
         kernels = "fill_i32_kernel + walk_kernel + tile_kernel"
     else:
         kernels = plan.split("<")[0].split()[-1] + "_kernel"
-    if args.backward:
-        kernels = "bwd_token_kernel + bwd_scan/scatter + bwd_weight_kernel"
     if plan.startswith("per-layer"):
         kernels = f"{NL} launches of {kernels}"
-    out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
-                       "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x {B} "
-                                f"tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, HIP "
-                                f"events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
+    if args.backward:
+        # compulsory HBM bytes of one backward: x, dy and dx rows, the forward's records (logits and
+        # leaf per token and tree), both weight matrices read and both fp32 dW matrices written
+        sz = {"bf16": 2, "f32": 4}
+        per_tok = w.hidden * (2 * sz[w.x_dtype] + sz[w.y_dtype]) + 4 * w.n_trees * (w.depth + 2)
+        bwd_bytes = B * per_tok + w.n_trees * w.nodes * w.hidden * 2 * (sz[w.w_dtype] + 4)
+        kernels = ("bwd_rank_wave_kernel + bwd_leafsum_kernel + bwd_scan_kernel + bwd_base_kernel + "
+                   "bwd_place_kernel + bwd_fused_kernel + bwd_wsum_kernel" if fused else
+                   "bwd_token_kernel + sort kernels + bwd_wtile_kernel / bwd_piece_kernel + fix-up")
+        bach = bwd_bytes / (t["mean_ms"] / 1e3) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": bach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": bach / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
+                           "basis": f"compulsory bytes of one backward = {B} tokens x {per_tok} B (x, dy, dx rows, "
+                                    f"logits and leaf) + {w.n_trees * w.nodes * w.hidden * 2 * (sz[w.w_dtype] + 4)} B "
+                                    f"(W read, fp32 dW written), over the mean time of one call ({kernels}, HIP "
+                                    f"events on the launch stream)"}
+    else:
+        out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
+                           "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x "
+                                    f"{B} tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, "
+                                    f"HIP events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
     flops = w.flops_per_token() * B * NL * (2 if args.backward else 1)  # backward: dot + axpy + two row updates
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
