@@ -962,9 +962,22 @@ __global__ __launch_bounds__(64 * WT_WAVES_MAX) void bwd_wtile_kernel(BwdParams 
 // in leaf order, once per token; dx is written once.  The dW rows are stored
 // and the fix-up run exactly as in bwd_wtile_kernel.
 constexpr int FUSED_WAVES_MAX = 8;
-// two 32-bit words that may alias any LDS data (read back from tables written as uint16_t)
-typedef uint32_t lds_u32x2_base __attribute__((ext_vector_type(2)));
-typedef lds_u32x2_base __attribute__((may_alias)) lds_u32x2;
+// 16 bytes of an LDS table written as uint16_t, read through a may_alias type
+typedef uint32_t lds_u32x4_base __attribute__((ext_vector_type(4)));
+typedef lds_u32x4_base __attribute__((may_alias)) lds_u32x4;
+__device__ __forceinline__ uint4 lds_u4(const uint16_t* p) {
+    const lds_u32x4 v = *reinterpret_cast<const lds_u32x4*>(p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+// v = hi + mid + lo with bf16 parts, each the round-to-nearest of what the parts before leave
+__device__ __forceinline__ void split3(float v, uint16_t* out) {
+    const uint16_t hi = f32_to_bf16(v);
+    const float r = v - bf16_to_f32(hi);
+    const uint16_t mid = f32_to_bf16(r);
+    out[0] = hi;
+    out[1] = mid;
+    out[2] = f32_to_bf16(r - bf16_to_f32(mid));
+}
 
 template <bool XBF, bool DYBF>
 __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdParams p, int sub) {
@@ -989,8 +1002,18 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
     // bf16 x and dy: the dW sums on bf16 MFMA (K = tokens), with a and dl level-major; otherwise
     // on fp32 MFMA, with a token-major.  dl token-major for dx in both.
     constexpr bool BF4 = XBF && DYBF;
-    __shared__ float s_a[2][BF4 ? 1 : 16][17], s_dl[2][16][17];
-    __shared__ float s_aT[2][BF4 ? 16 : 1][20], s_dlT[2][BF4 ? 16 : 1][20];
+    __shared__ float s_a[2][BF4 ? 1 : 16][17], s_dl[2][BF4 ? 1 : 16][17];
+    // a and dl as three bf16 parts (hi, mid, lo; hi + mid + lo = the fp32 value to fp32 precision):
+    // dl token-major for dx ([part][token][level]); BF4: a and dl level-major for the dW sums
+    __shared__ __align__(16) uint16_t s_dlQ[2][3][16][16];
+    __shared__ __align__(16) uint16_t s_aP[2][BF4 ? 3 : 1][16][16], s_dlP[2][BF4 ? 3 : 1][16][16];
+    // the tile's (token, level) entries go to the waves that have a SIMD to themselves when the
+    // workgroup has 5..7 waves (waves w and w + 4 share one), else to all waves
+    const bool shared_simd = waves > 4 && waves < 8;
+    const int aw0 = shared_simd ? waves - 4 : 0;
+    const int a_threads = ((shared_simd ? 4 : waves) - aw0) * 64;
+    const int a_tid = int(threadIdx.x) - aw0 * 64;  // takes entries a_tid + e a_threads if in [0, a_threads)
+    const bool a_live = a_tid >= 0 && a_tid < a_threads;
     // Each wave's dy tile (and, with BF4, x tile) read back in another layout: a transpose without
     // a second read.  BF4: dy then x, each [column slot][16 tokens] bf16, column c of the wave at
     // slot (c % 8) * 16 + c / 8, so that a 16-column MFMA tile is 16 consecutive slots.
@@ -1081,7 +1104,7 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                 constexpr int LG = 256 / 64;  // (token, level) entries per thread at one wave
                 int32_t tl[LG];
 #pragma unroll
-                for (int e = 0; e < LG; ++e) tl[e] = row_tok(((int(threadIdx.x) + e * int(blockDim.x)) >> 4) & 15);
+                for (int e = 0; e < LG; ++e) tl[e] = row_tok(((a_tid + e * a_threads) >> 4) & 15);
                 // every global read of the tile, issued together: dy rows in the da operand layout
                 // (token n, columns col + 32s + 8q), dy and x rows in the dW layout (token 4s + q,
                 // columns col + 8n) and the logits
@@ -1102,10 +1125,10 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                 float lg[LG];
 #pragma unroll
                 for (int e = 0; e < LG; ++e) {
-                    const int i = int(threadIdx.x) + e * int(blockDim.x);
+                    const int i = a_tid + e * a_threads;
                     const int lv = i & 15;
                     lg[e] = 0.0f;
-                    if (i < 256 && tl[e] >= 0 && lv <= D) lg[e] = p.logits[int64_t(tl[e]) * (D + 1) + lv];
+                    if (a_live && i < 256 && tl[e] >= 0 && lv <= D) lg[e] = p.logits[int64_t(tl[e]) * (D + 1) + lv];
                 }
                 // 1. partial da over this wave's columns: A = dy of token n (lane (n, q))
                 {
@@ -1157,8 +1180,8 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                 // 2. a and dl of the tile's (token, level) pairs, the partials added in wave order
 #pragma unroll
                 for (int e = 0; e < LG; ++e) {
-                    const int i = int(threadIdx.x) + e * int(blockDim.x);
-                    if (i < 256) {
+                    const int i = a_tid + e * a_threads;
+                    if (a_live && i < 256) {
                         const int tt = i >> 4, lv = i & 15;
                         float da = 0.0f;
                         for (int w = 0; w < waves; ++w) da += red[par][w][tt][lv];
@@ -1167,31 +1190,31 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                             a = activation(lg[e], p.act);
                             dl = da * activation_grad(lg[e], p.act);
                         }
+                        uint16_t dp[3];
+                        split3(dl, dp);
+#pragma unroll
+                        for (int r = 0; r < 3; ++r) s_dlQ[par][r][tt][lv] = dp[r];
                         if constexpr (BF4) {
-                            s_aT[par][lv][tt] = a;
-                            s_dlT[par][lv][tt] = dl;
+                            uint16_t ap[3];
+                            split3(a, ap);
+#pragma unroll
+                            for (int r = 0; r < 3; ++r) {
+                                s_aP[par][r][lv][tt] = ap[r];
+                                s_dlP[par][r][lv][tt] = dp[r];
+                            }
                         } else {
                             s_a[par][tt][lv] = a;
+                            s_dl[par][tt][lv] = dl;
                         }
-                        s_dl[par][tt][lv] = dl;
                     }
                 }
                 __syncthreads();
                 // 3. dx rows of the tile: A = parts of dl (token n, levels 8h .. 8h+7), B = bj
                 if (p.dx) {
-                    uint32_t p0[4], p1[4];
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) {
-                        const float x0 = s_dl[par][n][8 * h + 2 * qq], x1 = s_dl[par][n][8 * h + 2 * qq + 1];
-                        const uint32_t hi = pack_bf16x2(x0, x1);
-                        const float r0 = x0 - bf16_lo(hi), r1 = x1 - bf16_hi(hi);
-                        const uint32_t mid = pack_bf16x2(r0, r1);
-                        const uint32_t lo = pack_bf16x2(r0 - bf16_lo(mid), r1 - bf16_hi(mid));
-                        p0[qq] = part == 0 ? hi : mid;
-                        p1[qq] = part == 0 ? lo : 0u;
-                    }
-                    const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, make_uint4(p0[0], p0[1], p0[2], p0[3]));
-                    const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, make_uint4(p1[0], p1[1], p1[2], p1[3]));
+                    // lane (token n, q): part (q / 2 ? mid : hi) of dl at levels 8h .. 8h+7, then lo or zero
+                    const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, lds_u4(&s_dlQ[par][part][n][8 * h]));
+                    const bf16x8_t a1 = __builtin_bit_cast(
+                        bf16x8_t, part == 0 ? lds_u4(&s_dlQ[par][2][n][8 * h]) : make_uint4(0u, 0u, 0u, 0u));
                     tile_v4f acc[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
@@ -1233,40 +1256,23 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     //    tile j, lane (n, q): levels 4q + r, column col + 8n + j.
 #pragma unroll
                     for (int s = 0; s < 4; ++s) put_t(2048, xB[s].w[0], s, n < m_cnt);
-                    auto split = [](const float4& v, uint4& a1, uint4& a2) {
-                        uint32_t w1[4], w2[4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float f = fword(v, i);
-                            const uint32_t hi = f32_to_bf16(f);
-                            const float r = f - bf16_to_f32(uint16_t(hi));
-                            const uint32_t mid = f32_to_bf16(r);
-                            const uint32_t lo = f32_to_bf16(r - bf16_to_f32(uint16_t(mid)));
-                            w1[i] = hi | (mid << 16);
-                            w2[i] = lo;
-                        }
-                        a1 = make_uint4(w1[0], w1[1], w1[2], w1[3]);
-                        a2 = make_uint4(w2[0], w2[1], w2[2], w2[3]);
-                    };
-                    uint4 aa1, aa2, ad1, ad2;
-                    split(*reinterpret_cast<const float4*>(&s_aT[par][n][4 * q]), aa1, aa2);
-                    split(*reinterpret_cast<const float4*>(&s_dlT[par][n][4 * q]), ad1, ad2);
-                    // four bf16 of a table row (read as a may_alias type: the table is written as uint16_t
-                    // with no barrier in between) -> each twice
-                    auto dup = [&](int at) {
-                        const lds_u32x2 u = *reinterpret_cast<const lds_u32x2*>(t16 + at);
-                        return make_uint4((u.x & 0xffffu) | (u.x << 16), (u.x >> 16) | (u.x & 0xffff0000u),
-                                          (u.y & 0xffffu) | (u.y << 16), (u.y >> 16) | (u.y & 0xffff0000u));
-                    };
+                    // A, lane (level n, q): part (q / 2 ? mid : hi) of a (dl) for tokens 8(q % 2) .. +7, then
+                    // their lo part (q < 2) or zero; B: dy (x) of the same tokens at the tile's column
+                    const int half = q & 1;
+                    const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+                    const bf16x8_t aa1 = __builtin_bit_cast(bf16x8_t, lds_u4(&s_aP[par][part][n][8 * half]));
+                    const bf16x8_t aa2 = __builtin_bit_cast(bf16x8_t, part == 0 ? lds_u4(&s_aP[par][2][n][8 * half]) : z4);
+                    const bf16x8_t ad1 = __builtin_bit_cast(bf16x8_t, lds_u4(&s_dlP[par][part][n][8 * half]));
+                    const bf16x8_t ad2 = __builtin_bit_cast(bf16x8_t, part == 0 ? lds_u4(&s_dlP[par][2][n][8 * half]) : z4);
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        const int at = ((16 * j + n) * 16 + 4 * q);
-                        const bf16x8_t bd = __builtin_bit_cast(bf16x8_t, dup(at));
-                        const bf16x8_t bx = __builtin_bit_cast(bf16x8_t, dup(2048 + at));
-                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aa1), bd, ao[j], 0, 0, 0);
-                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, aa2), bd, ao[j], 0, 0, 0);
-                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ad1), bx, ai[j], 0, 0, 0);
-                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ad2), bx, ai[j], 0, 0, 0);
+                        const int at = (16 * j + n) * 16 + 8 * half;
+                        const bf16x8_t bd = __builtin_bit_cast(bf16x8_t, lds_u4(t16 + at));
+                        const bf16x8_t bx = __builtin_bit_cast(bf16x8_t, lds_u4(t16 + 2048 + at));
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa1, bd, ao[j], 0, 0, 0);
+                        ao[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa2, bd, ao[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad1, bx, ai[j], 0, 0, 0);
+                        ai[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad2, bx, ai[j], 0, 0, 0);
                     }
                 } else {
                     // 4. dW sums on fp32 MFMA, four tokens per step: A = a (dl) of token 4s + q at level n,
