@@ -224,6 +224,10 @@ def main():
                            "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x "
                                     f"{B} tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, "
                                     f"HIP events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
+    if traffic:
+        # the measured HBM bytes (counter summary) over the same mean call time
+        out["roofline"]["traffic_gbs"] = traffic / (t["mean_ms"] / 1e3) / 1e9
+        out["roofline"]["traffic_frac"] = out["roofline"]["traffic_gbs"] / HBM_PEAK_GBS
     flops = w.flops_per_token() * B * NL * (2 if args.backward else 1)  # backward: dot + axpy + two row updates
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
