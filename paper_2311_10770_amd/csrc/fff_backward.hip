@@ -962,6 +962,10 @@ __global__ __launch_bounds__(64 * WT_WAVES_MAX) void bwd_wtile_kernel(BwdParams 
 // in leaf order, once per token; dx is written once.  The dW rows are stored
 // and the fix-up run exactly as in bwd_wtile_kernel.
 constexpr int FUSED_WAVES_MAX = 8;
+// Stores of dx rows past a tile's count (or with no dx requested) go to a junk area, 32 bytes per
+// lane, so that every path through a tile issues the same vector memory operations and the
+// compiler's waits for earlier loads count exactly the operations after them.
+constexpr size_t BWD_JUNK_BYTES = 64 * 32;
 // 16 bytes of an LDS table written as uint16_t, read through a may_alias type
 typedef uint32_t lds_u32x4_base __attribute__((ext_vector_type(4)));
 typedef lds_u32x4_base __attribute__((may_alias)) lds_u32x4;
@@ -1049,6 +1053,33 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
 #pragma unroll
     for (int j = 0; j < 8; ++j) ao[j] = ai[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
     int par = 0;  // buffer of the current tile's tables
+    // Software pipeline over the subtree's tiles (16 sorted positions of one leaf each): during a
+    // tile, the token ids, dy rows (da operand layout) and logits of the positions that follow it
+    // are fetched.  The next tile's positions are contiguous with this one (empty leaves have
+    // none); rows past its count belong to a later leaf, are fetched all the same and are masked
+    // where used.  Every load is unconditional (clamped ids and levels) and every dx store has a
+    // target (junk for absent rows), so the waits for these loads do not wait for later stores.
+    constexpr int LG = 256 / 64;  // (token, level) entries per thread at one wave
+    int32_t tvN = -1;
+    Raw8<DYBF> dyN[4];
+    float lgN[LG];
+    auto prefetch = [&](int64_t P) {  // P < last, workgroup-uniform; s_tok covers P .. min(P + 15, last - 1)
+        tvN = P + n < last ? s_tok[P + n - win0] : -1;
+        const int32_t t0n = __shfl(tvN, 0, 64);
+        const int64_t ra = int64_t(tvN >= 0 ? tvN : t0n) * H + col + 8 * q;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) dyN[s] = raw8<DYBF>(p.dy, ra + 32 * s);
+#pragma unroll
+        for (int e = 0; e < LG; ++e) {
+            const int i = a_tid + e * a_threads;
+            const int32_t tok = __shfl(tvN, (i >> 4) & 15, 64);
+            const int lv = (i & 15) <= D ? (i & 15) : D;
+            lgN[e] = p.logits[int64_t(tok >= 0 ? tok : t0n) * (D + 1) + lv];
+        }
+    };
+    // bf16 x and dy: fetched one tile ahead; otherwise (more registers per row) at the tile's start
+    constexpr bool PIPE = BF4;
+    if (PIPE && first < last) prefetch(first);
     int64_t pos0 = first;
     for (int jl = 0; jl < nleaf; ++jl) {
         const int64_t leaf = leaf0 + jl;
@@ -1086,29 +1117,29 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
             }
             for (int32_t t0 = 0; t0 < c; t0 += 16, par ^= 1) {
                 const int32_t m_cnt = c - t0 < 16 ? c - t0 : 16;
-                // token of tile row r (r < 16), -1 past the leaf's count: one read per lane (row n),
-                // then cross-lane reads; row 0 stands in for absent rows where a load needs an address
-                if (pos0 + t0 + 16 > win0 + WT_LDS_TOK) {  // workgroup-uniform
+                // the window of staged ids covers this tile and the next one
+                if (pos0 + t0 + 32 > win0 + WT_LDS_TOK) {  // workgroup-uniform
                     // every wave has read the ids of the tiles before: it passed their barriers
                     win0 = pos0 + t0;
                     stage();
                     __syncthreads();
                 }
-                const int32_t tv = n < m_cnt ? s_tok[pos0 + t0 - win0 + n] : -1;
+                // token of tile row r (r < 16), -1 past the leaf's count: row n in lane (n, q), the
+                // others by cross-lane reads; row 0 stands in for absent rows where a load needs an address
+                if constexpr (!PIPE) prefetch(pos0 + t0);
+                const int32_t tv = n < m_cnt ? tvN : -1;
+                Raw8<DYBF> dyA[4];
+#pragma unroll
+                for (int s = 0; s < 4; ++s) dyA[s] = dyN[s];
+                float lg[LG];
+#pragma unroll
+                for (int e = 0; e < LG; ++e) lg[e] = lgN[e];
                 auto row_tok = [&](int r) -> int32_t { return __shfl(tv, r, 64); };
                 const int32_t tk0 = row_tok(0);
                 auto valid = [&](int32_t t) -> int32_t { return t >= 0 ? t : tk0; };
                 int32_t t4[4];
 #pragma unroll
                 for (int s = 0; s < 4; ++s) t4[s] = row_tok(4 * s + q);  // dW rows: token 4s + q
-                constexpr int LG = 256 / 64;  // (token, level) entries per thread at one wave
-                int32_t tl[LG];
-#pragma unroll
-                for (int e = 0; e < LG; ++e) tl[e] = row_tok(((a_tid + e * a_threads) >> 4) & 15);
-                // every global read of the tile, issued together: dy rows in the da operand layout
-                // (token n, columns col + 32s + 8q), dy and x rows in the dW layout (token 4s + q,
-                // columns col + 8n) and the logits
-                Raw8<DYBF> dyA[4];
                 Raw8<XBF> xB[4];  // BF4: the da operand layout; otherwise the dW one
                 constexpr bool EARLY_X = XBF && DYBF;
                 auto load_x = [&]() {
@@ -1117,19 +1148,6 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                         xB[s] = BF4 ? raw8<XBF>(p.x, int64_t(valid(tv)) * H + col + 8 * q + 32 * s)
                                     : raw8<XBF>(p.x, int64_t(valid(t4[s])) * H + col + 8 * n);
                 };
-                {
-                    const int64_t ra = int64_t(valid(tv)) * H + col + 8 * q;
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) dyA[s] = raw8<DYBF>(p.dy, ra + 32 * s);
-                }
-                float lg[LG];
-#pragma unroll
-                for (int e = 0; e < LG; ++e) {
-                    const int i = a_tid + e * a_threads;
-                    const int lv = i & 15;
-                    lg[e] = 0.0f;
-                    if (a_live && i < 256 && tl[e] >= 0 && lv <= D) lg[e] = p.logits[int64_t(tl[e]) * (D + 1) + lv];
-                }
                 // 1. partial da over this wave's columns: A = dy of token n (lane (n, q))
                 {
                     tile_v4f da = {0.f, 0.f, 0.f, 0.f};
@@ -1163,6 +1181,12 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     // x rows of the dW sums (bf16 x and dy: in flight during the reduction and dx; otherwise
                     // after dx, for registers); dy to the transpose
                     if constexpr (EARLY_X) load_x();
+                    if constexpr (PIPE) {
+                        // after the subtree's last tile: the last position again (unused), so that the
+                        // number of loads issued here does not depend on the path
+                        const int64_t nxt = pos0 + (t0 + 16 < c ? t0 + 16 : c);
+                        prefetch(nxt < last ? nxt : last - 1);
+                    }
                     if constexpr (BF4) {
 #pragma unroll
                         for (int s = 0; s < 4; ++s) put_t(0, dyA[s].w[0], s, n < m_cnt);
@@ -1170,7 +1194,9 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
 #pragma unroll
                         for (int s = 0; s < 4; ++s)
 #pragma unroll
-                            for (int w = 0; w < DW; ++w) s_dy[wave][n * (16 * DW + 1) + (4 * s + q) * DW + w] = dyA[s].w[w];
+                            for (int w = 0; w < DW; ++w)
+                                s_dy[wave][n * (16 * DW + 1) + (4 * s + q) * DW + w] =
+                                    n < m_cnt ? dyA[s].w[w] : make_uint4(0u, 0u, 0u, 0u);
                     }
                     // lane (level n, q) holds tokens 4q + r
 #pragma unroll
@@ -1209,8 +1235,15 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     }
                 }
                 __syncthreads();
+                // BF4: x of the tile to its transposed table now, before the dx stores: a wait for the x
+                // loads after the stores would wait for the stores too (the vector memory counter
+                // retires in order)
+                if constexpr (BF4) {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) put_t(2048, xB[s].w[0], s, n < m_cnt);
+                }
                 // 3. dx rows of the tile: A = parts of dl (token n, levels 8h .. 8h+7), B = bj
-                if (p.dx) {
+                {
                     // lane (token n, q): part (q / 2 ? mid : hi) of dl at levels 8h .. 8h+7, then lo or zero
                     const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, lds_u4(&s_dlQ[par][part][n][8 * h]));
                     const bf16x8_t a1 = __builtin_bit_cast(
@@ -1227,13 +1260,15 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int32_t tok = row_tok(4 * q + r);  // dx rows: token 4q + r
-                        if (tok < 0) continue;
+                        const bool real = tok >= 0 && p.dx != nullptr;
                         float v[8];
 #pragma unroll
                         for (int j = 0; j < 8; ++j) v[j] = acc[j][r];
-                        const int64_t at = int64_t(tok) * H + col + 8 * n;
+                        const int64_t at = int64_t(real ? tok : 0) * H + col + 8 * n;
+                        char* const jk = p.junk + lane * 32;
                         if (p.dx_bf16) {
-                            uint4* d = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p.dx) + at);
+                            uint4* d = real ? reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p.dx) + at)
+                                            : reinterpret_cast<uint4*>(jk);
                             if (add) {
                                 const uint4 o = *d;
 #pragma unroll
@@ -1245,7 +1280,7 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                             *d = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                             pack_bf16x2(v[6], v[7]));
                         } else {
-                            put8(reinterpret_cast<float*>(p.dx) + at, add, v);
+                            put8(real ? reinterpret_cast<float*>(p.dx) + at : reinterpret_cast<float*>(jk), add, v);
                         }
                     }
                 }
@@ -1254,8 +1289,6 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
                     //    hi and mid bf16 parts of a (dl) in one product and the lo part and zero in a
                     //    second, B = dy (x) of the token in both slots; every product is exact.  Output
                     //    tile j, lane (n, q): levels 4q + r, column col + 8n + j.
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) put_t(2048, xB[s].w[0], s, n < m_cnt);
                     // A, lane (level n, q): part (q / 2 ? mid : hi) of a (dl) for tokens 8(q % 2) .. +7, then
                     // their lo part (q < 2) or zero; B: dy (x) of the same tokens at the tile's column
                     const int half = q & 1;
@@ -1462,7 +1495,7 @@ size_t bwd_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int
     return align256(recs * size_t(depth + 1) * sizeof(float2)) + 2 * align256(bins * sizeof(int32_t)) +
            align256(recs * sizeof(int32_t)) + align256(size_t(n_trees) * sizeof(int32_t)) +
            align256(recs * sizeof(int32_t)) + align256(bins * size_t(bwd_chunks(n_tokens, depth)) * sizeof(int32_t)) +
-           align256(parts * sizeof(float));
+           align256(BWD_JUNK_BYTES) + align256(parts * sizeof(float));
 }
 
 void bwd_workspace_views(BwdParams& p, void* workspace) {
@@ -1487,6 +1520,8 @@ void bwd_workspace_views(BwdParams& p, void* workspace) {
     w += align256(recs * sizeof(int32_t));
     p.hist = reinterpret_cast<int32_t*>(w);
     w += align256(bins * size_t(p.chunks) * sizeof(int32_t));
+    p.junk = w;
+    w += align256(BWD_JUNK_BYTES);
     p.part = reinterpret_cast<float*>(w);
 }
 

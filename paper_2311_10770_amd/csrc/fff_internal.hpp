@@ -94,6 +94,7 @@ struct BwdParams {
     int32_t chunk;           // tokens per chunk
     int32_t fused;           // the fused leaf-tiled path runs (no token kernel)
     float* part;             // [T, pieces, D+1, 2 slots, 2 matrices, H] run sums that cross pieces
+    char* junk;              // BWD_JUNK_BYTES the fused kernel sends the stores of absent dx rows to
     int32_t piece;           // sorted positions per piece of the weight kernel
     int32_t pieces;          // pieces per tree
     int32_t need_dw;         // dW_in or dW_out requested
