@@ -200,3 +200,50 @@ def test_bitwise_reproducible_with_skewed_and_one_hot_leaves(fff_lib, B, H, D):
         ref = oracle.backward(x, wi, wo, D, 1, dy, fwd["nodes"])
         rep = parity.backward_check(x, wi, wo, D, 1, dy, fwd["nodes"], logits32, a, ref)
         assert rep["ok"], (kind, rep["fail"])
+
+
+@pytest.mark.parametrize("xd,dyd,H", [("bf16", "f32", 640), ("f32", "bf16", 128), ("bf16", "bf16", 256)])
+def test_fused_types_and_widths(fff_lib, xd, dyd, H):
+    """The fused leaf-tiled path (one tree, bf16 W, hidden a multiple of 128 up to 1024) with the x / dy
+    type pairs and workgroup sizes the other cases leave out: 5 waves (three of them alone on a SIMD
+    compute the tile's activations), 1 wave and 2 waves."""
+    D = 9
+    L = synth.make_layer(370 + H, 900, H, D, 1, xd, "bf16")
+    bounded_case(fff_lib, f"fused {xd}/{dyd} H={H}", L, D, 1, synth.make_x(371 + H, 900, H, dyd))
+
+
+def test_fused_accumulate_dw_only_and_bad_leaves(fff_lib):
+    """On the fused path: accumulation doubles every output, dW alone (no dx requested) equals the dW
+    of a full call bit for bit, and out-of-range leaves are counted and get zero dx rows while the
+    other tokens match the oracle."""
+    B, H, D = 3000, 768, 10
+    L = synth.make_layer(380, B, H, D, 1, "bf16", "bf16")
+    dy = synth.make_x(381, B, H, "bf16")
+    fwd = oracle.forward(L["x"], L["w_in"], L["w_out"], D, 1)
+    leaves, lg = fwd["nodes"][:, :, D].astype(np.int32), fwd["logits"].astype(np.float32)
+    first = run_bwd(fff_lib, L, D, 1, dy, leaves, lg)
+    both = run_bwd(fff_lib, L, D, 1, dy, leaves, lg, accumulate=True, init=first)
+    assert np.array_equal(both["dx"], first["dx"] * 2)  # x + x is exact
+    for k in ("dw_in", "dw_out"):
+        assert np.abs(both[k] - 2 * first[k]).max() <= 1e-5 * np.abs(first[k]).max(), k
+    _, dwi, dwo = fff_lib.backward(dev(fff_lib, L["x"]), dev(fff_lib, L["w_in"]), dev(fff_lib, L["w_out"]), D, 1,
+                                   dev(fff_lib, dy), dev(fff_lib, leaves), dev(fff_lib, lg), act="gelu",
+                                   want=("dw_in", "dw_out"))
+    torch.cuda.synchronize()
+    assert np.array_equal(fff_lib.to_numpy(dwi).view(np.uint32), first["dw_in"].view(np.uint32))
+    assert np.array_equal(fff_lib.to_numpy(dwo).view(np.uint32), first["dw_out"].view(np.uint32))
+    bad_rows = [0, 17, 1500, B - 1]
+    bad_leaves = leaves.copy()
+    for i, b in enumerate(bad_rows):
+        bad_leaves[b, 0] = [-1, 5, 2 ** (D + 1) - 1, 2 ** 30][i]
+    bad = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got = run_bwd(fff_lib, L, D, 1, dy, bad_leaves, lg, bad=bad)
+    assert int(bad.item()) == len(bad_rows)
+    assert not got["dx"][bad_rows].any()
+    keep = np.ones(B, dtype=bool)
+    keep[bad_rows] = False
+    ref = oracle.backward(L["x"][keep], L["w_in"], L["w_out"], D, 1, dy[keep], fwd["nodes"][keep])
+    for k in ("dx", "dw_in", "dw_out"):
+        g = got[k][keep] if k == "dx" else got[k]
+        err = np.abs(g - ref[k]).max()
+        assert err <= 1e-5 * np.abs(ref[k]).max(), (k, err)
