@@ -1371,61 +1371,70 @@ __global__ __launch_bounds__(64 * FUSED_WAVES_MAX) void bwd_fused_kernel(BwdPara
 
 // Rows of the levels above the subtrees (lv < k): node u at level lv sums the
 // part[] of its 2^(k-lv) subtrees.  One block per (tree, level, matrix,
-// 16-column slice); thread (column c, group g) owns subtrees g*per .. g*per +
-// per - 1 (G = min(64, 2^k) groups of per = 2^k / G <= 8 subtrees) and loads
-// them at once.  A node inside one group is summed there in subtree order; a
-// node spanning several groups adds its groups' sums in group order through
-// LDS.  The order is fixed, so the rows are the same on every run.
+// 64-column slice); thread (column quad c, group g) owns four columns and
+// subtrees g*per .. g*per + per - 1 (G = min(64, 2^k) groups of per = 2^k / G
+// <= 8 subtrees) and loads them at once, 16 bytes per subtree.  A node inside
+// one group is summed there in subtree order; a node spanning several groups
+// adds its groups' sums in group order through LDS.  The order is fixed, so
+// the rows are the same on every run.
 constexpr int WSUM_GROUPS = 64;
-constexpr int WSUM_BLOCK = 16 * WSUM_GROUPS;
+constexpr int WSUM_QUADS = 16;  // column quads per block: 64 columns
+constexpr int WSUM_BLOCK = WSUM_QUADS * WSUM_GROUPS;
 static_assert((1 << WT_TOP_LEVELS) <= 8 * WSUM_GROUPS, "a group holds at most eight subtrees");
 
+__device__ __forceinline__ float4 add4(float4 a, const float4& b) {
+    a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    return a;
+}
+
 __global__ __launch_bounds__(WSUM_BLOCK) void bwd_wsum_kernel(BwdParams p, int k) {
-    __shared__ float red[WSUM_GROUPS][17];
-    const int c = threadIdx.x & 15, g = threadIdx.x >> 4;
-    const int64_t H = p.hidden, slices = H / 16;
+    __shared__ float4 red[WSUM_GROUPS][WSUM_QUADS + 1];
+    const int c = threadIdx.x % WSUM_QUADS, g = threadIdx.x / WSUM_QUADS;
+    const int64_t H = p.hidden, slices = H / (4 * WSUM_QUADS);
     const int64_t slice = blockIdx.x % slices;
     const int mat = int((blockIdx.x / slices) % 2);
     const int lv = int(blockIdx.x / (2 * slices));  // < k
-    const int64_t col = slice * 16 + c;
+    const int64_t col = (slice * WSUM_QUADS + c) * 4;
     const int t = blockIdx.y;
     const int64_t S = int64_t(1) << k;
     const int G = S < WSUM_GROUPS ? int(S) : WSUM_GROUPS;
     const int per = int(S / G);
     const int span = 1 << (k - lv);  // subtrees under a node of this level
     float* dw = mat == 0 ? p.dw_out : p.dw_in;
-    auto store = [&](int64_t u, float v) {  // node u of the level
+    auto store = [&](int64_t u, float4 v) {  // node u of the level
         if (!dw) return;
-        float* d = dw + (int64_t(t) * p.n_nodes + ((int64_t(1) << lv) - 1) + u) * H + col;
-        *d = p.accumulate ? *d + v : v;
+        float4* d = reinterpret_cast<float4*>(dw + (int64_t(t) * p.n_nodes + ((int64_t(1) << lv) - 1) + u) * H + col);
+        *d = p.accumulate ? add4(v, *d) : v;
     };
-    float v[8];
+    float4 v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int64_t st = int64_t(g) * per + j;
-        v[j] = g < G && j < per ? p.part[((((int64_t(t) << k) + st) * k + lv) * 2 + mat) * H + col] : 0.0f;
+        v[j] = g < G && j < per
+                   ? *reinterpret_cast<const float4*>(p.part + ((((int64_t(t) << k) + st) * k + lv) * 2 + mat) * H + col)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (span <= per) {  // block-uniform
         if (g < G)
             for (int j0 = 0; j0 < per; j0 += span) {
-                float sum = 0.0f;
+                float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
-                    if (j >= j0 && j < j0 + span) sum += v[j];
+                    if (j >= j0 && j < j0 + span) sum = add4(sum, v[j]);
                 store((int64_t(g) * per + j0) >> (k - lv), sum);
             }
         return;
     }
-    float sum = 0.0f;
+    float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-        if (j < per) sum += v[j];
+        if (j < per) sum = add4(sum, v[j]);
     red[g][c] = sum;
     __syncthreads();
     const int ng = span / per;  // groups per node
     if (g < G && g % ng == 0) {
-        float tot = 0.0f;
-        for (int i = 0; i < ng; ++i) tot += red[g + i][c];
+        float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int i = 0; i < ng; ++i) tot = add4(tot, red[g + i][c]);
         store((int64_t(g) * per) >> (k - lv), tot);
     }
 }
@@ -1532,8 +1541,8 @@ static hipError_t launch_wsum(BwdParams& p, int k, hipStream_t stream) {
     int kk = k;
     void* fargs[] = {&p, &kk};
     return hipLaunchKernel(reinterpret_cast<const void*>(&bwd_wsum_kernel),
-                           dim3(unsigned(int64_t(k) * 2 * (p.hidden / 16)), unsigned(p.n_trees)), dim3(WSUM_BLOCK), fargs,
-                           0, stream);
+                           dim3(unsigned(int64_t(k) * 2 * (p.hidden / (4 * WSUM_QUADS))), unsigned(p.n_trees)),
+                           dim3(WSUM_BLOCK), fargs, 0, stream);
 }
 
 // The stable placement in leaf order (rank, [leaf sums], scan, base, place).
