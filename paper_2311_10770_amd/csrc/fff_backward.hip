@@ -357,14 +357,32 @@ __global__ __launch_bounds__(RANKW_BLOCK) void bwd_rank_wave_kernel(BwdParams p)
 // bwd_base_kernel (one wave per (tree, leaf)): turns the chunk counts into the
 // first sorted position of the leaf's tokens in each chunk (an exclusive scan
 // over the chunks, 64 at a time), and leaves offs at one past the leaf's last
-// position.
-__global__ __launch_bounds__(BWD_BLOCK) void bwd_base_kernel(BwdParams p) {
+// position.  The leaf's first position comes from offs (bwd_scan_kernel), or
+// with self_scan (one tree, at most BASE_SELF_SCAN_LEAVES leaves) from the
+// block itself: the sum of the counts of all earlier leaves (integer sums, so
+// any order gives the same value), which saves the scan kernel's launch.
+constexpr int BASE_SELF_SCAN_LEAVES = 4096;
+
+__global__ __launch_bounds__(BWD_BLOCK) void bwd_base_kernel(BwdParams p, int self_scan) {
     const int64_t L = int64_t(1) << p.depth;
-    const int lane = threadIdx.x & 63;
-    const int64_t i = int64_t(blockIdx.x) * (BWD_BLOCK / 64) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t i0 = int64_t(blockIdx.x) * (BWD_BLOCK / 64);
+    const int64_t i = i0 + wave;
+    int32_t run = 0;
+    if (self_scan) {  // block-uniform
+        __shared__ int32_t part[BWD_BLOCK / 64];
+        int32_t sum = 0;
+        for (int64_t j = threadIdx.x; j < i0 && j < L; j += BWD_BLOCK) sum += p.counts[j];
+#pragma unroll
+        for (int d = 32; d > 0; d >>= 1) sum += __shfl_xor(sum, d, 64);
+        if (lane == 0) part[wave] = sum;
+        __syncthreads();
+        for (int w = 0; w < BWD_BLOCK / 64; ++w) run += part[w];
+        for (int w = 0; w < wave; ++w) run += i0 + w < L ? p.counts[i0 + w] : 0;
+    }
     if (i >= L * p.n_trees) return;  // wave-uniform
     const int64_t t = i / L, leaf = i - t * L;
-    int32_t run = p.offs[i];
+    if (!self_scan) run = p.offs[i];
     int32_t* h = p.hist + t * p.chunks * L + leaf;
     for (int64_t c0 = 0; c0 < p.chunks; c0 += 64) {
         const int64_t c = c0 + lane;
@@ -1562,11 +1580,17 @@ static hipError_t launch_sort(BwdParams& p, bool count_leaves, const int64_t cap
                             stream);
         if (e != hipSuccess) return e;
     }
-    e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scan_kernel), dim3(p.n_trees), dim3(SCAN_BLOCK), args, 0,
-                        stream);
-    if (e != hipSuccess) return e;
+    // the fused path (leaf counts from bwd_leafsum_kernel, one tree) with few leaves: the base
+    // kernel finds each leaf's start itself; otherwise the scan kernel (which also gives the total)
+    int self_scan = count_leaves && p.n_trees == 1 && bins <= BASE_SELF_SCAN_LEAVES;
+    if (!self_scan) {
+        e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_scan_kernel), dim3(p.n_trees), dim3(SCAN_BLOCK), args,
+                            0, stream);
+        if (e != hipSuccess) return e;
+    }
+    void* bargs[] = {&p, &self_scan};
     e = hipLaunchKernel(reinterpret_cast<const void*>(&bwd_base_kernel),
-                        dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), args, 0, stream);
+                        dim3(unsigned((bins + BWD_BLOCK / 64 - 1) / (BWD_BLOCK / 64))), dim3(BWD_BLOCK), bargs, 0, stream);
     if (e != hipSuccess) return e;
     const int64_t n = p.n_tokens * p.n_trees;
     const int grid = int(std::max<int64_t>(1, std::min<int64_t>((n + BWD_BLOCK - 1) / BWD_BLOCK, cap)));
