@@ -80,17 +80,32 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * relative error about 2^-17, when y is bf16 and either stored or the residual
  * of bf16 x).  Tokens past a full
  * bucket take the per-token emit.  Needs the workspace of fff_workspace_bytes.
- * AUTO (from measurements on MI355X): for single-tree layers of at least 48M
- * input elements (tokens x hidden) whose workspace is large enough, TILED at
- * depth 9..15 with at least 8 tokens per leaf, else GROUPED at depth 11 or
- * more; otherwise DESCENT when a kernel is compiled for the hidden size and
- * types, else GENERIC. */
+ * MASKED: bf16 x and W, or fp32 x, W and y; depth <= 7, no LayerNorm (a
+ * residual needs y of x's type): the layer as two dense products around the
+ * walk, for shallow trees
+ * where a token uses a large share of the nodes (at depth 0 the layer is the
+ * dense feedforward): the logits of all nodes as one bf16 GEMM with fp32
+ * accumulation (hipBLASLt, MFMA), the walk of Algorithm 1 over them per
+ * (token, tree) with the visited nodes' activations split into bf16 parts
+ * (two when y is bf16, three otherwise) and zeros elsewhere, then the output
+ * as a second GEMM against W_out repeated once per part.  With fp32 x, W and
+ * y both GEMMs are fp32 and the activations go in whole.  Needs the
+ * workspace of fff_workspace_bytes (logits, parts, the repeated W_out and
+ * hipBLASLt's scratch).
+ * AUTO (from measurements on MI355X): MASKED at depth <= 5 (bf16 x and W) or
+ * <= 4 (fp32) with at least 8 trees or 4096 tokens when the workspace covers
+ * it; for
+ * single-tree layers of at least 48M input elements (tokens x hidden) whose
+ * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
+ * leaf, else GROUPED at depth 11 or more; otherwise DESCENT when a kernel is
+ * compiled for the hidden size and types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,
     FFF_MODE_DESCENT = 1,
     FFF_MODE_GROUPED = 2,
     FFF_MODE_GENERIC = 3,
-    FFF_MODE_TILED = 4
+    FFF_MODE_TILED = 4,
+    FFF_MODE_MASKED = 5
 } fff_mode;
 
 /* What is written to y: FFF(u); y + FFF(u); or x + FFF(u) (the residual of a
@@ -157,11 +172,13 @@ typedef struct {
 
 int fff_forward_ex(const fff_args* a);
 
-/* Device scratch bytes GROUPED and TILED mode need for n_tokens tokens: one
- * fp32 activation per visited node and one int32 leaf per (token, tree), plus
- * for TILED the leaf buckets (int32 counts; token slots, a few times the mean
- * tokens per leaf, each with its D+1 fp32 activations; a spill list).  The
- * result covers both modes; the split level (-1..depth) does not change it.
+/* Device scratch bytes GROUPED, TILED and MASKED mode need for n_tokens
+ * tokens: one fp32 activation per visited node and one int32 leaf per (token,
+ * tree), plus for TILED the leaf buckets (int32 counts; token slots, a few
+ * times the mean tokens per leaf, each with its D+1 fp32 activations; a spill
+ * list), and at depth <= 7 MASKED's logits of every node (fp32), their bf16
+ * parts, W_out repeated three times and 32 MiB of GEMM scratch.  The result
+ * covers every mode; the split level (-1..depth) does not change it.
  * Returns 0 for invalid shapes. */
 size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,
                            int32_t split_level);

@@ -116,7 +116,7 @@ int validate_shapes(const fff_args* a, int64_t rec_layers, fff::Params* p, int64
     for (int dt : {a->x_dtype, a->w_dtype, a->y_dtype})
         if (dt != FFF_F32 && dt != FFF_BF16) return FFF_ERR_INVALID_ARG;
     if (a->act < FFF_ACT_GELU_ERF || a->act > FFF_ACT_IDENTITY) return FFF_ERR_INVALID_ARG;
-    if (a->mode < FFF_MODE_AUTO || a->mode > FFF_MODE_TILED) return FFF_ERR_INVALID_ARG;
+    if (a->mode < FFF_MODE_AUTO || a->mode > FFF_MODE_MASKED) return FFF_ERR_INVALID_ARG;
     if (a->out_mode < FFF_OUT_STORE || a->out_mode > FFF_OUT_RESIDUAL) return FFF_ERR_INVALID_ARG;
     if (a->lds_levels < -1 || a->lds_levels > kMaxDepth + 1) return FFF_ERR_INVALID_ARG;
     if (a->split_level < -1 || a->split_level > a->depth) return FFF_ERR_INVALID_ARG;
@@ -207,9 +207,10 @@ int validate(const fff_args* a, fff::Params* p) {
 
 // Workspace checks for a grouped plan: present, big enough, 256-byte aligned,
 // and disjoint from every tensor the kernels read or write.
-int check_workspace(const fff_args* a, bool tiled) {
-    const size_t need = tiled ? fff::tiled_workspace_bytes(a->n_tokens, a->depth, a->n_trees, a->hidden)
-                              : fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
+int check_workspace(const fff_args* a, int kind) {
+    const size_t need = kind == fff::KIND_TILED  ? fff::tiled_workspace_bytes(a->n_tokens, a->depth, a->n_trees, a->hidden)
+                        : kind == fff::KIND_MASKED ? fff::masked_workspace_bytes(a->n_tokens, a->depth, a->n_trees, a->hidden)
+                                                   : fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
     if (!a->workspace || a->workspace_bytes < need || (reinterpret_cast<uintptr_t>(a->workspace) & 255u))
         return FFF_ERR_WORKSPACE;
     const int64_t wsb = int64_t(need);
@@ -236,8 +237,9 @@ int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
     const size_t ws = a->workspace && (reinterpret_cast<uintptr_t>(a->workspace) & 255u) == 0 ? a->workspace_bytes : 0;
     rc = fff::plan_forward(*p, a->mode, a->lds_levels, a->split_level, ws, dev, plan);
     if (rc != FFF_OK) return rc;
-    if ((plan->kind == fff::KIND_GROUPED || plan->kind == fff::KIND_TILED) && a->n_tokens > 0)
-        return check_workspace(a, plan->kind == fff::KIND_TILED);
+    if ((plan->kind == fff::KIND_GROUPED || plan->kind == fff::KIND_TILED || plan->kind == fff::KIND_MASKED) &&
+        a->n_tokens > 0)
+        return check_workspace(a, plan->kind);
     return FFF_OK;
 }
 
@@ -482,14 +484,15 @@ FFF_EXPORT size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n
     if (n_tokens < 0 || depth < 0 || depth > kMaxDepth || n_trees < 1 || hidden < 1 || split_level < -1 ||
         split_level > depth)
         return 0;
-    return std::max(fff::grouped_workspace_bytes(n_tokens, depth, n_trees, split_level),
-                    fff::tiled_workspace_bytes(n_tokens, depth, n_trees, hidden));
+    return std::max({fff::grouped_workspace_bytes(n_tokens, depth, n_trees, split_level),
+                     fff::tiled_workspace_bytes(n_tokens, depth, n_trees, hidden),
+                     fff::masked_workspace_bytes(n_tokens, depth, n_trees, hidden)});
 }
 
 namespace {
 void format_plan(const fff::Plan& plan, const char* prefix, char* buf, size_t len) {
     if (!buf || !len) return;
-    static const char* kinds[] = {"none", "descent", "generic", "grouped", "stack", "tiled"};
+    static const char* kinds[] = {"none", "descent", "generic", "grouped", "stack", "tiled", "masked"};
     int n = std::snprintf(buf, len, "%s%s<%s> lanes_per_token=%d lds_levels=%d", prefix, kinds[plan.kind],
                           plan.name, plan.lanes, plan.lds_levels);
     if ((plan.kind == fff::KIND_GROUPED || plan.kind == fff::KIND_TILED) && n > 0 && size_t(n) < len)

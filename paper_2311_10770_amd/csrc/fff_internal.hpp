@@ -116,7 +116,9 @@ struct DeviceInfo {
     size_t lds_per_cu = 0;     // bytes
 };
 
-enum KernelKind { KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4, KIND_TILED = 5 };
+enum KernelKind {
+    KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4, KIND_TILED = 5, KIND_MASKED = 6
+};
 
 struct Launch {
     const void* kernel = nullptr;  // __global__ function handle
@@ -165,5 +167,22 @@ size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees,
 size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
 // Split level used when the caller asks for the default (0 in fff_args).
 int default_split_level(int32_t depth, int32_t n_trees);
+
+// Masked mode (two dense products around the walk, fff_masked.hip): the deepest tree it takes,
+// and where AUTO picks it: depth at most MASKED_AUTO_DEPTH (bf16 x and W) or
+// MASKED_AUTO_DEPTH_F32 (fp32 x, W and y), with at least MASKED_AUTO_TREES trees or
+// MASKED_AUTO_TOKENS tokens.
+constexpr int MASKED_MAX_DEPTH = 7;
+constexpr int MASKED_AUTO_DEPTH = 5;
+constexpr int MASKED_AUTO_DEPTH_F32 = 4;
+constexpr int MASKED_AUTO_TREES = 8;
+constexpr int64_t MASKED_AUTO_TOKENS = 4096;
+// Whether a validated request can run masked (types, depth, no LayerNorm, residual types).
+bool masked_shape(const Params& p);
+// Masked mode scratch (logits, split activations, repeated W_out, hipBLASLt's scratch); 0 past
+// MASKED_MAX_DEPTH.
+size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
+// Enqueues the masked forward on stream (hipErrorNotSupported when hipBLASLt has no algorithm).
+hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream);
 
 }  // namespace fff

@@ -36,7 +36,7 @@
 
 namespace fff {
 
-enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3, MODE_TILED = 4 };
+enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3, MODE_TILED = 4, MODE_MASKED = 5 };
 // status values mirrored from fff.h
 enum { ST_OK = 0, ST_INVALID = -1, ST_UNSUPPORTED = -2, ST_WORKSPACE = -3 };
 
@@ -1048,12 +1048,27 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
         const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
         const int64_t grouped_ws = int64_t(grouped_workspace_bytes(p.n_tokens, p.depth, p.n_trees, 0));
-        if (!v) mode = MODE_GENERIC;
+        const int64_t masked_ws = int64_t(masked_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
+        // Shallow layers run fastest as dense products: a token uses (D+1)/(2^(D+1)-1) of the
+        // nodes, at least 9.5 % at depth <= 5, where bf16 MFMA products beat the walk (from 2048
+        // tokens on for the Table 1 shapes); fp32 products (about 125 TFLOP/s against the walk's
+        // 16) win down to 16 % (depth <= 4).
+        if (masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
+            (p.n_tokens >= MASKED_AUTO_TOKENS || p.n_trees >= MASKED_AUTO_TREES) && int64_t(workspace_bytes) >= masked_ws)
+            mode = MODE_MASKED;
+        else if (!v) mode = MODE_GENERIC;
         else if (big && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
                  p.n_tokens >= (int64_t(8) << p.depth))
             mode = MODE_TILED;
         else if (big && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws) mode = MODE_GROUPED;
         else mode = MODE_DESCENT;
+    }
+    if (mode == MODE_MASKED) {
+        if (!masked_shape(p)) return ST_UNSUPPORTED;
+        plan->kind = KIND_MASKED;
+        plan->name = !p.w_bf16 ? "fp32 GEMMs"
+                     : p.y_bf16 ? "bf16 GEMMs, activations in 2 parts" : "bf16 GEMMs, activations in 3 parts";
+        return ST_OK;
     }
     if ((mode == MODE_DESCENT || mode == MODE_GROUPED || mode == MODE_TILED) && !v) return ST_UNSUPPORTED;
     if (mode == MODE_TILED) {
@@ -1181,6 +1196,7 @@ hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream
 
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream) {
+    if (plan.kind == KIND_MASKED) return run_masked(p, workspace, stream);
     Params q = p;
     q.lds_levels = plan.lds_levels;
     if (plan.kind == KIND_GROUPED) {

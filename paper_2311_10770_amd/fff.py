@@ -18,7 +18,7 @@ LIB_PATH = Path(__file__).resolve().with_name("libfff.so")
 FFF_OK, FFF_ERR_INVALID_ARG, FFF_ERR_UNSUPPORTED, FFF_ERR_WORKSPACE, FFF_ERR_HIP = 0, -1, -2, -3, -4
 FFF_F32, FFF_BF16 = 0, 1
 ACTS = {"gelu": 0, "gelu_erf": 0, "gelu_tanh": 1, "identity": 2}
-MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3, "tiled": 4}
+MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3, "tiled": 4, "masked": 5}
 OUTS = {"store": 0, "accumulate": 1, "residual": 2}
 NORMS = {None: 0, "none": 0, "layernorm": 1}
 _TORCH_DT = {torch.float32: FFF_F32, torch.bfloat16: FFF_BF16}
@@ -232,7 +232,7 @@ def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=Non
     given (calls that may overlap on different streams must pass their own)."""
     if y is None:
         y = torch.empty(x.shape, dtype=y_dtype or x.dtype, device=x.device)
-    if kw.get("mode", "auto") in ("grouped", "auto", "tiled", 0, 2, 4) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("grouped", "auto", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     lib = load_library()
@@ -271,7 +271,7 @@ def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
     of x's dtype; y may be x itself).  ``layers``: sequence of (W_in, W_out[, gamma[, beta]])."""
     if y is None:
         y = torch.empty_like(x)
-    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", 0, 2, 4) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     with torch.cuda.device(x.device):
@@ -282,7 +282,7 @@ def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
 def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str:
     if y is None:
         y = torch.empty_like(x)
-    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", 0, 2, 4) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("auto", "grouped", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     buf = ctypes.create_string_buffer(512)
@@ -379,7 +379,7 @@ def describe(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, **kw) -> str:
     if y is None:
         y = torch.empty(x.shape, dtype=kw.pop("y_dtype", None) or x.dtype, device=x.device)
     kw.pop("y_dtype", None)
-    if kw.get("mode", "auto") in ("grouped", "auto", "tiled", 0, 2, 4) and kw.get("workspace") is None:
+    if kw.get("mode", "auto") in ("grouped", "auto", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     buf = ctypes.create_string_buffer(512)

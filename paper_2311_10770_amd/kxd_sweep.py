@@ -32,6 +32,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--shapes", default="", help="comma list of KxD to run, e.g. 1x11,4x9 (default: all)")
+    ap.add_argument("--mode", default="auto", choices=sorted(fff.MODES), help="plan to time (default: AUTO)")
     args = ap.parse_args()
 
     fff.load_library()
@@ -52,8 +53,13 @@ def main():
         wo = fff.from_numpy(L["w_out"], dev)
         y = torch.empty((B, w.hidden), dtype=torch.bfloat16 if w.y_dtype == "bf16" else torch.float32,
                         device=dev)
-        plan = fff.describe(x, wi, wo, d, k, y)
-        t = benchlib.time_launches(lambda: fff.forward(x, wi, wo, d, k, y), args.steps, args.warmup, stream)
+        try:
+            plan = fff.describe(x, wi, wo, d, k, y, mode=args.mode)
+        except fff.FffError as e:
+            log(f"{k}x{d}: mode {args.mode} not available ({e})")
+            continue
+        t = benchlib.time_launches(lambda: fff.forward(x, wi, wo, d, k, y, mode=args.mode), args.steps, args.warmup,
+                                   stream)
         us = t["mean_ms"] * 1e3
         n_t, n_i = k * w.nodes, k * (d + 1)
         row = {"shape": f"{k}x{d}", "K": k, "D": d, "N_T": n_t, "N_I": n_i, "N_I_over_N_T": n_i / n_t,

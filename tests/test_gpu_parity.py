@@ -368,3 +368,76 @@ def test_tiled_unsupported_shapes(fff_lib):
     L = layer(242, 64, 768, 16, 1, "bf16", "bf16")  # depth above 15
     with pytest.raises(fff_lib.FffError):
         run_fff(fff_lib, L, 16, 1, "bf16", mode="tiled")
+
+
+# ----------------------------------------------------- MASKED (dense products)
+
+
+@pytest.mark.parametrize("yd", ["bf16", "f32"])
+@pytest.mark.parametrize("k,d,B", [(3072, 0, 131), (1536, 1, 64), (512, 2, 131), (64, 5, 257), (16, 7, 100),
+                                   (1, 3, 5)])
+def test_masked_shapes(fff_lib, k, d, B, yd):
+    """The masked mode (logit GEMM, walk over the logits, output GEMM on split activations) against
+    the oracle for shallow KxD shapes, ragged batches and both output types."""
+    L = layer(400 + d + k, B, 768, d, k, "bf16", "bf16")
+    check_layer(fff_lib, f"masked {k}x{d} B={B} y={yd}", L, d, k, yd, mode="masked")
+
+
+@pytest.mark.parametrize("k,d,B", [(3072, 0, 67), (512, 2, 131), (64, 5, 257), (16, 7, 100), (1, 3, 5)])
+def test_masked_f32_shapes(fff_lib, k, d, B):
+    """fp32 x, W and y: both products are fp32 GEMMs and the activations go in whole."""
+    L = layer(440 + d + k, B, 768, d, k, "f32", "f32")
+    check_layer(fff_lib, f"masked f32 {k}x{d} B={B}", L, d, k, "f32", mode="masked")
+
+
+@pytest.mark.parametrize("out", ["residual", "accumulate"])
+def test_masked_f32_output_modes(fff_lib, out):
+    L = layer(450, 300, 768, 2, 16, "f32", "f32")
+    y0 = synth.make_x(451, 300, 768, "f32")
+    got = run_fff(fff_lib, L, 2, 16, "f32", mode="masked", out=out, y_init=y0 if out == "accumulate" else None)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 2, 16)
+    base = L["x"] if out == "residual" else y0
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 2, 16, ref, got["y"], got["nodes"], tol=1e-5,
+                         base_dev=base)
+
+
+@pytest.mark.parametrize("out", ["residual", "accumulate"])
+def test_masked_output_modes(fff_lib, out):
+    L = layer(420, 1000, 768, 3, 32, "bf16", "bf16")
+    y0 = synth.make_x(421, 1000, 768, "bf16")
+    got = run_fff(fff_lib, L, 3, 32, "bf16", mode="masked", out=out, y_init=y0 if out == "accumulate" else None)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 3, 32)
+    base = L["x"] if out == "residual" else y0
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 3, 32, ref, got["y"], got["nodes"], tol=2e-2,
+                         base_dev=base)
+
+
+def test_masked_mode_limits_and_auto(fff_lib):
+    """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it for layers of
+    depth <= 5 (bf16) or <= 4 (fp32) with at least 8 trees or 4096 tokens (planning only)."""
+    L = layer(430, 64, 768, 3, 8, "f32", "bf16")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x, wi, wo, 3, 8, mode="masked")  # fp32 x, bf16 W
+    L = layer(431, 64, 768, 3, 8, "f32", "f32")
+    x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x, wi, wo, 3, 8, torch.empty((64, 768), dtype=torch.bfloat16, device=DEV),
+                        mode="masked")  # fp32 x and W, bf16 y
+    w8 = torch.zeros((1, (1 << 9) - 1, 768), dtype=torch.bfloat16, device=DEV)
+    xb = torch.zeros((4096, 768), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(xb[:64], w8, w8, 8, 1, mode="masked")  # depth 8
+    w3 = torch.zeros((64, 15, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, w3, w3, 3, 64).startswith("masked<")
+    assert fff_lib.describe(xb[:512], w3, w3, 3, 64).startswith("masked<")  # 64 trees
+    w1 = torch.zeros((1, 15, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, w1, w1, 3, 1).startswith("masked<")  # 4096 tokens
+    assert not fff_lib.describe(xb[:512], w1, w1, 3, 1).startswith("masked<")
+    w6 = torch.zeros((8, 127, 768), dtype=torch.bfloat16, device=DEV)
+    assert not fff_lib.describe(xb, w6, w6, 6, 8).startswith("masked<")  # depth 6: the walk
+    xf = torch.zeros((4096, 768), dtype=torch.float32, device=DEV)
+    w4 = torch.zeros((1, 31, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf, w4, w4, 4, 1).startswith("masked<fp32")  # fp32, depth 4
+    w5 = torch.zeros((1, 63, 768), dtype=torch.float32, device=DEV)
+    assert not fff_lib.describe(xf, w5, w5, 5, 1).startswith("masked<")  # fp32, depth 5: the walk
