@@ -375,7 +375,7 @@ def test_tiled_unsupported_shapes(fff_lib):
 
 @pytest.mark.parametrize("yd", ["bf16", "f32"])
 @pytest.mark.parametrize("k,d,B", [(3072, 0, 131), (1536, 1, 64), (512, 2, 131), (64, 5, 257), (16, 7, 100),
-                                   (1, 3, 5)])
+                                   (1, 3, 5), (3, 4, 50), (200, 5, 33)])
 def test_masked_shapes(fff_lib, k, d, B, yd):
     """The masked mode (logit GEMM, walk over the logits, output GEMM on split activations) against
     the oracle for shallow KxD shapes, ragged batches and both output types."""
@@ -383,9 +383,11 @@ def test_masked_shapes(fff_lib, k, d, B, yd):
     check_layer(fff_lib, f"masked {k}x{d} B={B} y={yd}", L, d, k, yd, mode="masked")
 
 
-@pytest.mark.parametrize("k,d,B", [(3072, 0, 67), (512, 2, 131), (64, 5, 257), (16, 7, 100), (1, 3, 5)])
+@pytest.mark.parametrize("k,d,B", [(3072, 0, 67), (512, 2, 131), (64, 5, 257), (16, 7, 100), (1, 3, 5), (3, 4, 50),
+                                   (200, 5, 33)])
 def test_masked_f32_shapes(fff_lib, k, d, B):
-    """fp32 x, W and y: both products are fp32 GEMMs and the activations go in whole."""
+    """fp32 x, W and y: both products are fp32 GEMMs and the activations go in whole.  N_T = 15 and
+    93 take padded rows; 200 trees of depth 5 (N_T = 12600) the selection for rows wider than LDS."""
     L = layer(440 + d + k, B, 768, d, k, "f32", "f32")
     check_layer(fff_lib, f"masked f32 {k}x{d} B={B}", L, d, k, "f32", mode="masked")
 
