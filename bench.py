@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--backward", action="store_true",
                     help="time the hard-routed backward (dx, dW_in, dW_out from the forward's records) instead")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cold-reps", type=int, default=20,
+                    help="calls timed cold (a 1 GiB write before each evicts W from L2 and MALL); 0: skip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall budget of the oracle timing")
     ap.add_argument("--traffic", default=None,
@@ -228,6 +230,14 @@ def main():
         # the measured HBM bytes (counter summary) over the same mean call time
         out["roofline"]["traffic_gbs"] = traffic / (t["mean_ms"] / 1e3) / 1e9
         out["roofline"]["traffic_frac"] = out["roofline"]["traffic_gbs"] / HBM_PEAK_GBS
+    if args.cold_reps:
+        tc = benchlib.time_cold(step, args.cold_reps, stream)
+        out["cold"] = {"kernel_us": {"mean": tc["mean_ms"] * 1e3, "min": tc["min_ms"] * 1e3,
+                                     "std": tc["std_ms"] * 1e3},
+                       "tokens_per_s": B / (tc["mean_ms"] / 1e3),
+                       "timing": f"{args.cold_reps} calls, each after a 1 GiB write that evicts the weights from "
+                                 f"L2 and MALL, each between its own pair of HIP events"}
+        log(f"cold: {tc['mean_ms'] * 1e3:.1f} us per call (warm {t['mean_ms'] * 1e3:.1f})")
     flops = w.flops_per_token() * B * NL * (2 if args.backward else 1)  # backward: dot + axpy + two row updates
     out["alu"] = {"achieved_tflops": flops / (t["mean_ms"] / 1e3) / 1e12, "peak_tflops_fp32_vector": 157.3}
 
@@ -270,6 +280,10 @@ def main():
                         "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
                         "rel_err_vs_fp32_torch": rel,
                         "torch_unfused_ms": unfused_ms, "speedup_fff_over_torch_unfused": unfused_ms / ms}
+        if args.cold_reps:
+            tdc = benchlib.time_cold(dense_step, args.cold_reps, stream)
+            out["dense"]["cold_ms"] = tdc["mean_ms"]
+            out["dense"]["speedup_fff_over_dense_cold"] = tdc["mean_ms"] / out["cold"]["kernel_us"]["mean"] * 1e3
         dense.close()
         log(f"dense (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x "
             f"(rel err {rel:.1e}); torch unfused {unfused_ms * 1e3:.1f} us")

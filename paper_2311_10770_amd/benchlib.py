@@ -106,3 +106,25 @@ def time_launches(fn, steps: int, warmup: int, stream):
     return {"mean_ms": sum(per) / steps, "min_ms": min(per), "max_ms": max(per),
             "std_ms": (sum((p - sum(per) / steps) ** 2 for p in per) / steps) ** 0.5,
             "region_ms": region_ms, "wall_s": wall}
+
+
+def time_cold(fn, reps: int, stream, flush_bytes: int = 1 << 30):
+    """Cold-cache timing: before each call a `flush_bytes` write (1 GiB: more than the 256 MB
+    MALL and the eight 4 MB L2s together) evicts the weights; only the call sits between its
+    pair of events on `stream`.  Returns mean/min/std_ms over `reps` calls."""
+    scratch = torch.empty(flush_bytes, dtype=torch.uint8, device=torch.device("cuda", torch.cuda.current_device()))
+    fn()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    with torch.cuda.stream(stream):
+        for i in range(reps):
+            scratch.fill_(i & 0xFF)
+            starts[i].record(stream)
+            fn()
+            ends[i].record(stream)
+    torch.cuda.synchronize()
+    per = [a.elapsed_time(b) for a, b in zip(starts, ends)]
+    mean = sum(per) / reps
+    del scratch
+    return {"mean_ms": mean, "min_ms": min(per), "std_ms": (sum((q - mean) ** 2 for q in per) / reps) ** 0.5}
