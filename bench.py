@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None, help="a name from paper_2311_10770_amd.configs.WORKLOADS")
     ap.add_argument("--tokens", type=int, default=None, help="override the workload's token count")
-    ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "tiled", "generic"])
+    ap.add_argument("--mode", default="auto", choices=["auto", "descent", "grouped", "tiled", "generic", "masked", "subtree"])
     ap.add_argument("--lds-levels", type=int, default=0)
     ap.add_argument("--norm", action="store_true", help="LayerNorm before every layer (gain/shift drawn per layer)")
     ap.add_argument("--backward", action="store_true",

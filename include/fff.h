@@ -92,7 +92,16 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * y both GEMMs are fp32 and the activations go in whole.  Needs the
  * workspace of fff_workspace_bytes (logits, parts, the repeated W_out and
  * hipBLASLt's scratch).
- * AUTO (from measurements on MI355X): MASKED at depth <= 5 (bf16 x and W) or
+ * SUBTREE: hidden 768, 1024 or 4096 (any supported types), no LayerNorm; for
+ * a few tokens, where the walk's D+1 dependent row loads are the time: one
+ * workgroup of 1024 threads (512 for fp32 x with bf16 W at hidden >= 1024)
+ * per token computes the logits of every node of a 3- to 6-level subtree
+ * (64, 32 or 16 lanes per dot product) in one step and descends through
+ * them in LDS, then loads the path's W_out rows together.  Reads up to 63/6
+ * times the W_in rows of a walk.
+ * AUTO (from measurements on MI355X): SUBTREE at depth >= 8 while the W_in
+ * rows its steps read stay within 16 MiB (up to about 85 tokens at hidden 768
+ * in bf16, 34 at 4096); MASKED at depth <= 5 (bf16 x and W) or
  * <= 4 (fp32) with at least 8 trees or 4096 tokens when the workspace covers
  * it; for
  * single-tree layers of at least 48M input elements (tokens x hidden) whose
@@ -105,7 +114,8 @@ typedef enum {
     FFF_MODE_GROUPED = 2,
     FFF_MODE_GENERIC = 3,
     FFF_MODE_TILED = 4,
-    FFF_MODE_MASKED = 5
+    FFF_MODE_MASKED = 5,
+    FFF_MODE_SUBTREE = 6
 } fff_mode;
 
 /* What is written to y: FFF(u); y + FFF(u); or x + FFF(u) (the residual of a

@@ -116,7 +116,7 @@ int validate_shapes(const fff_args* a, int64_t rec_layers, fff::Params* p, int64
     for (int dt : {a->x_dtype, a->w_dtype, a->y_dtype})
         if (dt != FFF_F32 && dt != FFF_BF16) return FFF_ERR_INVALID_ARG;
     if (a->act < FFF_ACT_GELU_ERF || a->act > FFF_ACT_IDENTITY) return FFF_ERR_INVALID_ARG;
-    if (a->mode < FFF_MODE_AUTO || a->mode > FFF_MODE_MASKED) return FFF_ERR_INVALID_ARG;
+    if (a->mode < FFF_MODE_AUTO || a->mode > FFF_MODE_SUBTREE) return FFF_ERR_INVALID_ARG;
     if (a->out_mode < FFF_OUT_STORE || a->out_mode > FFF_OUT_RESIDUAL) return FFF_ERR_INVALID_ARG;
     if (a->lds_levels < -1 || a->lds_levels > kMaxDepth + 1) return FFF_ERR_INVALID_ARG;
     if (a->split_level < -1 || a->split_level > a->depth) return FFF_ERR_INVALID_ARG;
@@ -492,9 +492,11 @@ FFF_EXPORT size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n
 namespace {
 void format_plan(const fff::Plan& plan, const char* prefix, char* buf, size_t len) {
     if (!buf || !len) return;
-    static const char* kinds[] = {"none", "descent", "generic", "grouped", "stack", "tiled", "masked"};
+    static const char* kinds[] = {"none", "descent", "generic", "grouped", "stack", "tiled", "masked", "subtree"};
     int n = std::snprintf(buf, len, "%s%s<%s> lanes_per_token=%d lds_levels=%d", prefix, kinds[plan.kind],
                           plan.name, plan.lanes, plan.lds_levels);
+    if (plan.kind == fff::KIND_SUBTREE && n > 0 && size_t(n) < len)
+        n += std::snprintf(buf + n, len - n, " levels_per_step=%d", plan.split_level);
     if ((plan.kind == fff::KIND_GROUPED || plan.kind == fff::KIND_TILED) && n > 0 && size_t(n) < len)
         n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d emit_lanes=%d",
                            plan.emit_lds_levels, plan.split_level, plan.emit_lanes);

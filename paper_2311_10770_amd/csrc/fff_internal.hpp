@@ -117,7 +117,8 @@ struct DeviceInfo {
 };
 
 enum KernelKind {
-    KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4, KIND_TILED = 5, KIND_MASKED = 6
+    KIND_NONE = 0, KIND_DESCENT = 1, KIND_GENERIC = 2, KIND_GROUPED = 3, KIND_STACK = 4, KIND_TILED = 5, KIND_MASKED = 6,
+    KIND_SUBTREE = 7
 };
 
 struct Launch {
@@ -184,5 +185,20 @@ bool masked_shape(const Params& p);
 size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
 // Enqueues the masked forward on stream (hipErrorNotSupported when hipBLASLt has no algorithm).
 hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream);
+
+// Subtree mode (fff_subtree.hip): a workgroup per token evaluates whole subtrees of logits per
+// step.  AUTO takes it for trees of depth at least SUBTREE_AUTO_DEPTH when the W_in rows its
+// steps read come to at most SUBTREE_AUTO_BYTES (about 85 tokens at H = 768 in bf16, 34 at
+// H = 4096).
+constexpr int SUBTREE_AUTO_DEPTH = 8;
+constexpr int64_t SUBTREE_AUTO_BYTES = int64_t(16) << 20;
+bool subtree_auto(const Params& p);
+// Whether a validated request has a subtree kernel (hidden size and types; no LayerNorm).
+bool subtree_shape(const Params& p);
+int subtree_span(const Params& p);          // levels per step
+const char* subtree_name(const Params& p);
+int subtree_block(const Params& p);          // threads per workgroup
+int subtree_grid(const Params& p, int cu_count);
+hipError_t run_subtree(const Params& p, int grid, hipStream_t stream);
 
 }  // namespace fff

@@ -36,7 +36,8 @@
 
 namespace fff {
 
-enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3, MODE_TILED = 4, MODE_MASKED = 5 };
+enum { MODE_AUTO = 0, MODE_DESCENT = 1, MODE_GROUPED = 2, MODE_GENERIC = 3, MODE_TILED = 4, MODE_MASKED = 5,
+       MODE_SUBTREE = 6 };
 // status values mirrored from fff.h
 enum { ST_OK = 0, ST_INVALID = -1, ST_UNSUPPORTED = -2, ST_WORKSPACE = -3 };
 
@@ -1053,7 +1054,11 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         // nodes, at least 9.5 % at depth <= 5, where bf16 MFMA products beat the walk (from 2048
         // tokens on for the Table 1 shapes); fp32 products (about 125 TFLOP/s against the walk's
         // 16) win down to 16 % (depth <= 4).
-        if (masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
+        // A few tokens of a deep tree wait on the chain of dependent row loads: whole subtrees of
+        // logits per memory round trip shorten it.
+        if (subtree_auto(p))
+            mode = MODE_SUBTREE;
+        else if (masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
             (p.n_tokens >= MASKED_AUTO_TOKENS || p.n_trees >= MASKED_AUTO_TREES) && int64_t(workspace_bytes) >= masked_ws)
             mode = MODE_MASKED;
         else if (!v) mode = MODE_GENERIC;
@@ -1062,6 +1067,17 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
             mode = MODE_TILED;
         else if (big && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws) mode = MODE_GROUPED;
         else mode = MODE_DESCENT;
+    }
+    if (mode == MODE_SUBTREE) {
+        if (!subtree_shape(p)) return ST_UNSUPPORTED;
+        plan->kind = KIND_SUBTREE;
+        plan->name = subtree_name(p);
+        plan->lanes = subtree_block(p);  // a workgroup per token
+        plan->split_level = subtree_span(p);
+        Launch& L = plan->launch[plan->n_launch++];
+        L.block = subtree_block(p);
+        L.grid = subtree_grid(p, dev.cu_count);
+        return ST_OK;
     }
     if (mode == MODE_MASKED) {
         if (!masked_shape(p)) return ST_UNSUPPORTED;
@@ -1197,6 +1213,7 @@ hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream) {
     if (plan.kind == KIND_MASKED) return run_masked(p, workspace, stream);
+    if (plan.kind == KIND_SUBTREE) return run_subtree(p, plan.launch[0].grid, stream);
     Params q = p;
     q.lds_levels = plan.lds_levels;
     if (plan.kind == KIND_GROUPED) {

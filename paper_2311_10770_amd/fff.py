@@ -18,7 +18,7 @@ LIB_PATH = Path(__file__).resolve().with_name("libfff.so")
 FFF_OK, FFF_ERR_INVALID_ARG, FFF_ERR_UNSUPPORTED, FFF_ERR_WORKSPACE, FFF_ERR_HIP = 0, -1, -2, -3, -4
 FFF_F32, FFF_BF16 = 0, 1
 ACTS = {"gelu": 0, "gelu_erf": 0, "gelu_tanh": 1, "identity": 2}
-MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3, "tiled": 4, "masked": 5}
+MODES = {"auto": 0, "descent": 1, "grouped": 2, "generic": 3, "tiled": 4, "masked": 5, "subtree": 6}
 OUTS = {"store": 0, "accumulate": 1, "residual": 2}
 NORMS = {None: 0, "none": 0, "layernorm": 1}
 _TORCH_DT = {torch.float32: FFF_F32, torch.bfloat16: FFF_BF16}

@@ -267,7 +267,10 @@ def test_guard_bands_untouched(fff_lib, yd, mode):
 def test_describe_names_the_kernel(fff_lib):
     L = layer(140, 64, 768, 11, 1, "bf16", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
-    d = fff_lib.describe(x, wi, wo, 11, 1)  # auto, small batch: the fused kernel
+    d = fff_lib.describe(x, wi, wo, 11, 1)  # auto, 64 tokens: a workgroup per token
+    assert d.startswith("subtree<"), d
+    xm = torch.zeros((1024, 768), dtype=torch.bfloat16, device=DEV)
+    d = fff_lib.describe(xm, wi, wo, 11, 1)  # auto, 1024 tokens: the fused kernel
     assert d.startswith("descent<"), d
     # auto with the binding's workspace at 64K tokens: leaf tiles at 32 tokens per leaf,
     # subtree grouping at 4 per leaf (planning only: nothing is launched)
@@ -443,3 +446,72 @@ def test_masked_mode_limits_and_auto(fff_lib):
     assert fff_lib.describe(xf, w4, w4, 4, 1).startswith("masked<fp32")  # fp32, depth 4
     w5 = torch.zeros((1, 63, 768), dtype=torch.float32, device=DEV)
     assert not fff_lib.describe(xf, w5, w5, 5, 1).startswith("masked<")  # fp32, depth 5: the walk
+
+
+# ----------------------------------------------------- SUBTREE (a workgroup per token)
+
+
+@pytest.mark.parametrize("H,d,k,B,xd,wd,yd", [
+    (768, 11, 1, 5, "bf16", "bf16", "bf16"),     # 16-lane dots, 6 levels per step: 2 steps
+    (768, 0, 1, 3, "bf16", "bf16", "f32"),       # one level
+    (768, 3, 2, 7, "f32", "bf16", "f32"),        # one partial step, two trees
+    (768, 12, 1, 4, "bf16", "f32", "bf16"),      # 32-lane dots, 5 levels per step
+    (1024, 9, 3, 6, "f32", "f32", "f32"),
+    (1024, 10, 1, 9, "f32", "bf16", "f32"),      # 512-thread workgroups, 5 levels per step
+    (4096, 13, 1, 3, "bf16", "bf16", "bf16"),    # 64-lane dots, 4 levels per step (last step 2)
+    (4096, 7, 1, 2, "f32", "bf16", "f32"),       # 512-thread workgroups, 3 levels per step
+    (4096, 6, 2, 2, "f32", "f32", "f32"),
+])
+def test_subtree_shapes(fff_lib, H, d, k, B, xd, wd, yd):
+    """SUBTREE mode (whole subtrees of logits per step) against the oracle, with the records."""
+    L = layer(500 + H + d + k, B, H, d, k, xd, wd)
+    check_layer(fff_lib, f"subtree H={H} {k}x{d} B={B} {xd}/{wd}/{yd}", L, d, k, yd, mode="subtree")
+
+
+def test_subtree_many_tokens(fff_lib):
+    """More tokens than workgroups: each workgroup loops over tokens."""
+    L = layer(530, 1500, 768, 4, 1, "bf16", "bf16")
+    check_layer(fff_lib, "subtree B=1500", L, 4, 1, "bf16", mode="subtree")
+
+
+@pytest.mark.parametrize("out", ["residual", "accumulate"])
+@pytest.mark.parametrize("xd,wd", [("bf16", "bf16"), ("f32", "f32")])
+def test_subtree_output_modes(fff_lib, out, xd, wd):
+    """y = x + FFF(x) and y += FFF(x).  A bf16 y holds the rounding of the whole sum, whose error
+    scales with the base, not with FFF(x): there every element must lie within one bf16 spacing of
+    the fp64 total plus the fp32 bar on FFF(x)."""
+    B = 33
+    L = layer(540, B, 768, 9, 2, xd, wd)
+    y0 = synth.make_x(541, B, 768, xd)
+    got = run_fff(fff_lib, L, 9, 2, xd, mode="subtree", out=out, y_init=y0 if out == "accumulate" else None)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 9, 2)
+    base = L["x"] if out == "residual" else y0
+    bf16 = xd == "bf16"
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 9, 2, ref, got["y"], got["nodes"],
+                         tol=1.0 if bf16 else 1e-5, base_dev=base)
+    if bf16:
+        same = (got["nodes"] == ref["nodes"]).reshape(B, -1).all(axis=1)
+        total = parity.widen(base) + ref["y"]
+        ex = parity.bf16_total_excess(got["y"][same], total[same], ref["y"][same], 1e-5)
+        assert ex <= 1.0, f"bf16 {out} output {ex:.2f}x past its bound"
+
+
+def test_subtree_auto_and_limits(fff_lib):
+    """AUTO takes SUBTREE at depth >= 8 while its W_in reads stay within 16 MiB: 86 tokens at
+    H = 768 in bf16 (2 steps of 63 rows of 1536 bytes each), 34 at H = 4096 (4 steps of 15 rows of
+    8 KiB); no LayerNorm, no other widths."""
+    xb = torch.zeros((100, 768), dtype=torch.bfloat16, device=DEV)
+    w11 = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb[:86], w11, w11, 11, 1).startswith("subtree<")
+    assert fff_lib.describe(xb[:1], w11, w11, 11, 1).startswith("subtree<")
+    assert not fff_lib.describe(xb[:87], w11, w11, 11, 1).startswith("subtree<")
+    w7 = torch.zeros((1, 255, 768), dtype=torch.bfloat16, device=DEV)
+    assert not fff_lib.describe(xb[:8], w7, w7, 7, 1).startswith("subtree<")  # depth 7
+    x4 = torch.zeros((40, 4096), dtype=torch.bfloat16, device=DEV)
+    w12 = torch.zeros((1, (1 << 13) - 1, 4096), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(x4[:34], w12, w12, 12, 1).startswith("subtree<")
+    assert not fff_lib.describe(x4[:35], w12, w12, 12, 1).startswith("subtree<")
+    x5 = torch.zeros((4, 640), dtype=torch.bfloat16, device=DEV)
+    w5 = torch.zeros((1, 63, 640), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(fff_lib.FffError):
+        fff_lib.forward(x5, w5, w5, 5, 1, mode="subtree")  # no kernel for hidden 640
