@@ -130,7 +130,7 @@ def main():
         dwo = torch.empty_like(dwi)
         fused = (w.n_trees == 1 and w.w_dtype == "bf16" and w.depth <= 15 and w.hidden % 128 == 0
                  and w.hidden <= 1024)
-        plan = ("backward: stable sort by leaf (rank, leaf sums, scan, base, place) + fused leaf-tiled kernel "
+        plan = ("backward: stable sort by leaf (rank, leaf sums, base, place) + fused leaf-tiled kernel "
                 "(da, dx, dW on MFMA per 16-token tile) + sums of the rows above the subtrees" if fused else
                 "backward: token kernel + stable sort by leaf + weight kernel + fix-up sums")
 
@@ -189,7 +189,8 @@ def main():
     from paper_2311_10770_amd.rocprof_summary import kernel_source_hash
 
     traffic = None
-    tpath = Path(args.traffic) if args.traffic else ROOT / "profiles" / f"traffic_{w.name}_{args.mode}.json"
+    tname = f"traffic_{w.name}_{args.mode}{'_backward' if args.backward else ''}.json"
+    tpath = Path(args.traffic) if args.traffic else ROOT / "profiles" / tname
     if tpath.exists():
         summ = json.loads(tpath.read_text())
         if summ.get("kernel_source_hash") == kernel_source_hash(args.backward):
@@ -210,8 +211,8 @@ def main():
         sz = {"bf16": 2, "f32": 4}
         per_tok = w.hidden * (2 * sz[w.x_dtype] + sz[w.y_dtype]) + 4 * w.n_trees * (w.depth + 2)
         bwd_bytes = B * per_tok + w.n_trees * w.nodes * w.hidden * 2 * (sz[w.w_dtype] + 4)
-        kernels = ("bwd_rank_wave_kernel + bwd_leafsum_kernel + bwd_scan_kernel + bwd_base_kernel + "
-                   "bwd_place_kernel + bwd_fused_kernel + bwd_wsum_kernel" if fused else
+        kernels = ("bwd_rank_wave_kernel + bwd_leafsum_kernel + bwd_base_kernel (+ bwd_scan_kernel past 4096 "
+                   "leaves) + bwd_place_kernel + bwd_fused_kernel + bwd_wsum_kernel" if fused else
                    "bwd_token_kernel + sort kernels + bwd_wtile_kernel / bwd_piece_kernel + fix-up")
         bach = bwd_bytes / (t["mean_ms"] / 1e3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": bach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
