@@ -33,6 +33,19 @@ if str(ROOT) not in sys.path:
 HBM_PEAK_GBS = 8000.0
 
 
+def host_cpu() -> str:
+    """Host CPU model and logical CPU count, from /proc/cpuinfo."""
+    model, count = "unknown", 0
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                count += 1
+    except OSError:
+        pass
+    return f"{model} ({count} logical CPUs)"
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -316,10 +329,20 @@ def main():
             if time.perf_counter() - t0 >= args.cpu_seconds:
                 break
         el = time.perf_counter() - t0
+        # the same oracle on one thread over a tenth of the sample, for the per-core rate
+        n1 = max(1, n // 10)
+        t1 = time.perf_counter()
+        if NL == 1 and not args.norm:
+            oracle.forward(L["x"][:n1], layers_np[0]["w_in"], layers_np[0]["w_out"], w.depth, w.n_trees,
+                           records=False, threads=1)
+        else:
+            oracle.stack(L["x"][:n1], layers_np, w.depth, w.n_trees, w.y_dtype, norm_eps=eps, threads=1)
+        el1 = time.perf_counter() - t1
         out["cpu_baseline"] = {"value": done / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
                                "sample": f"first {n} tokens of the same batch, repeated {done // n}x over "
-                                         f"{el:.1f}s wall, fp64 C oracle on {threads} host threads"}
-        log(f"cpu oracle: {done / el:.0f} tok/s on {threads} threads")
+                                         f"{el:.1f}s wall, fp64 C oracle on {threads} host threads",
+                               "single_thread_value": n1 / el1, "host": host_cpu()}
+        log(f"cpu oracle: {done / el:.0f} tok/s on {threads} threads, {n1 / el1:.0f} on one")
         if not args.no_check:
             # the last layer, on the device's own input to it, against the oracle's block
             nodes = torch.empty((NL, B, w.n_trees, w.depth + 1), dtype=torch.int32, device=dev)

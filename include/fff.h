@@ -91,7 +91,10 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * as a second GEMM against W_out repeated once per part.  With fp32 x, W and
  * y both GEMMs are fp32 and the activations go in whole.  Needs the
  * workspace of fff_workspace_bytes (logits, parts, the repeated W_out and
- * hipBLASLt's scratch).
+ * hipBLASLt's scratch).  The first call for a shape times hipBLASLt's first
+ * eight candidate algorithms per product on the stream and keeps the fastest
+ * (that call synchronizes the device; under graph capture the heuristic's
+ * first candidate is used instead).
  * SUBTREE: hidden 768, 1024 or 4096 (any supported types), no LayerNorm; for
  * a few tokens, where the walk's D+1 dependent row loads are the time: one
  * workgroup of 1024 threads (512 for fp32 x with bf16 W at hidden >= 1024)
