@@ -107,9 +107,10 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * in bf16, 34 at 4096); MASKED at depth <= 5 (bf16 x and W) or
  * <= 4 (fp32) with at least 8 trees or 4096 tokens when the workspace covers
  * it; for
- * single-tree layers of at least 48M input elements (tokens x hidden) whose
- * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
- * leaf, else GROUPED at depth 11 or more; otherwise DESCENT when a kernel is
+ * single-tree layers whose workspace is large enough, TILED at depth 9..15
+ * with at least 16 tokens per leaf and 16M input elements (tokens x hidden),
+ * or 8 tokens per leaf and 48M elements; else, from 48M elements, GROUPED at
+ * depth 11 or more; otherwise DESCENT when a kernel is
  * compiled for the hidden size and types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,

@@ -1043,9 +1043,12 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     const Variant* v = find_variant(p);
     if (mode == MODE_AUTO) {
         // Measured on MI355X (hidden 768 / 1024 / 4096, depth 5..15, 4K..64K tokens, bf16 and
-        // fp32 weights): below about 48M input elements the fused descent kernel is fastest.
-        // Above it, single trees of depth 9..15 with at least 8 tokens per leaf run fastest
-        // leaf-tiled on MFMA, other single trees of depth 11 or more grouped by subtree.
+        // fp32 weights): below about 48M input elements the fused descent kernel is fastest,
+        // except for single trees of depth 9..15 with at least 16 tokens per leaf and 16M
+        // elements (depth 11 at 32768 tokens: 54 against 64 us in bf16, 104 against 132 in
+        // fp32), which run fastest leaf-tiled on MFMA.  Above it, single trees of depth 9..15
+        // with at least 8 tokens per leaf run leaf-tiled, other single trees of depth 11 or more
+        // grouped by subtree.
         const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
         const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
         const int64_t grouped_ws = int64_t(grouped_workspace_bytes(p.n_tokens, p.depth, p.n_trees, 0));
@@ -1062,8 +1065,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
             (p.n_tokens >= MASKED_AUTO_TOKENS || p.n_trees >= MASKED_AUTO_TREES) && int64_t(workspace_bytes) >= masked_ws)
             mode = MODE_MASKED;
         else if (!v) mode = MODE_GENERIC;
-        else if (big && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
-                 p.n_tokens >= (int64_t(8) << p.depth))
+        else if (tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
+                 ((big && p.n_tokens >= (int64_t(8) << p.depth)) ||
+                  (p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(16) << 20) &&
+                   p.n_tokens >= (int64_t(16) << p.depth))))
             mode = MODE_TILED;
         else if (big && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws) mode = MODE_GROUPED;
         else mode = MODE_DESCENT;

@@ -276,6 +276,8 @@ def test_describe_names_the_kernel(fff_lib):
     # subtree grouping at 4 per leaf (planning only: nothing is launched)
     xb = torch.zeros((65536, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb, wi, wo, 11, 1).startswith("tiled<")
+    assert fff_lib.describe(xb[:32768], wi, wo, 11, 1).startswith("tiled<")  # 16 per leaf, 25M elements
+    assert fff_lib.describe(xb[:16384], wi, wo, 11, 1).startswith("descent<")  # 8 per leaf, 12.6M
     w14 = torch.zeros((1, (1 << 15) - 1, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb, w14, w14, 14, 1).startswith("grouped<")
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="descent")
