@@ -80,7 +80,7 @@ def good_args(**over):
 
 @pytest.mark.parametrize("over", [
     dict(n_tokens=-1), dict(hidden=0), dict(depth=-1), dict(depth=25), dict(n_trees=0),
-    dict(x_dtype=2), dict(w_dtype=-1), dict(y_dtype=5), dict(act=3), dict(mode=9), dict(out_mode=3),
+    dict(x_dtype=2), dict(w_dtype=-1), dict(y_dtype=5), dict(act=3), dict(mode=9), dict(mode=7), dict(mode=-1), dict(out_mode=3),
     dict(lds_levels=-2), dict(split_level=4), dict(split_level=-2),
     dict(x=None), dict(W_in=None), dict(W_out=None), dict(y=None),
     dict(x=P + 4), dict(y=P * 64 + 8), dict(W_in=P * 16 + 2),
@@ -212,3 +212,10 @@ def test_backward_workspace_rules(lib):
     a = bwd_args(dx=None, dW_in=None, dW_out=None)
     assert lib.fff_backward(ctypes.byref(a)) == binding.FFF_OK
     assert lib.fff_backward(None) == binding.FFF_ERR_INVALID_ARG
+
+
+def test_binding_modes_match_header():
+    """The binding's mode names carry the header's fff_mode values, one for one."""
+    text = HEADER.read_text()
+    enum = {m.lower(): int(v) for m, v in re.findall(r"FFF_MODE_([A-Z]+)\s*=\s*(\d+)", text)}
+    assert enum == binding.MODES
