@@ -183,7 +183,15 @@ def test_activation_variants(fff_lib):
     check_layer(fff_lib, "identity", L, 9, 1, "f32", act="identity")
 
 
-@pytest.mark.parametrize("H,mode", [(768, "descent"), (40, "generic")])
+@pytest.mark.parametrize("act", ["gelu_tanh", "identity"])
+def test_activation_variants_masked_and_subtree(fff_lib, act):
+    L = layer(81, 300, 768, 3, 16, "bf16", "bf16")
+    check_layer(fff_lib, f"masked {act}", L, 3, 16, "f32", act=act, mode="masked")
+    L = layer(82, 40, 768, 9, 2, "f32", "f32")
+    check_layer(fff_lib, f"subtree {act}", L, 9, 2, "f32", act=act, mode="subtree")
+
+
+@pytest.mark.parametrize("H,mode", [(768, "descent"), (40, "generic"), (768, "subtree"), (768, "masked")])
 def test_small_integers_identity_bit_exact_with_ties(fff_lib, H, mode):
     """Identity activation on small integers: every value is an exact integer, so the device
     must match the oracle bit for bit, including logits of exactly zero (they go left)."""
