@@ -54,7 +54,7 @@ extern "C" {
 typedef enum {
     FFF_OK = 0,
     FFF_ERR_INVALID_ARG = -1, /* a null pointer, bad size, bad enum, misalignment or x/y overlap */
-    FFF_ERR_UNSUPPORTED = -2, /* valid request this build has no kernel for */
+    FFF_ERR_UNSUPPORTED = -2, /* valid request the library has no kernel for */
     FFF_ERR_WORKSPACE = -3,   /* grouped mode without enough workspace */
     FFF_ERR_HIP = -4          /* a HIP runtime call failed */
 } fff_status;
