@@ -102,15 +102,15 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * (64, 32 or 16 lanes per dot product) in one step and descends through
  * them in LDS, then loads the path's W_out rows together.  Reads up to 63/6
  * times the W_in rows of a walk.
- * AUTO (from measurements on MI355X): SUBTREE at depth >= 8 while the W_in
- * rows its steps read stay within 16 MiB (up to about 85 tokens at hidden 768
- * in bf16, 34 at 4096); MASKED at depth <= 5 (bf16 x and W) or
- * <= 4 (fp32) with at least 8 trees or 4096 tokens when the workspace covers
- * it; for
- * single-tree layers whose workspace is large enough, TILED at depth 9..15
- * with at least 16 tokens per leaf and 16M input elements (tokens x hidden),
- * or 8 tokens per leaf and 48M elements; else, from 48M elements, GROUPED at
- * depth 11 or more; otherwise DESCENT when a kernel is
+ * AUTO (from measurements on MI355X): SUBTREE for at most 4 trees of depth
+ * >= 5 and 256 token-tree pairs (32 at hidden 4096); MASKED at depth <= 5
+ * (bf16 x and W) or <= 4 (fp32) for 16 trees or more, or 8 trees and 16384
+ * tokens, when the workspace covers it; for single-tree layers whose
+ * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
+ * leaf and 48M input elements (tokens x hidden), or 16 tokens per leaf and
+ * 16M elements (fp32 W, or depth >= 10); else GROUPED at depth 11 or more
+ * from 48M elements, or from 16384 tokens with fp32 W or 24M elements;
+ * otherwise DESCENT when a kernel is
  * compiled for the hidden size and types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,

@@ -171,13 +171,14 @@ int default_split_level(int32_t depth, int32_t n_trees);
 
 // Masked mode (two dense products around the walk, fff_masked.hip): the deepest tree it takes,
 // and where AUTO picks it: depth at most MASKED_AUTO_DEPTH (bf16 x and W) or
-// MASKED_AUTO_DEPTH_F32 (fp32 x, W and y), with at least MASKED_AUTO_TREES trees or
-// MASKED_AUTO_TOKENS tokens.
+// MASKED_AUTO_DEPTH_F32 (fp32 x, W and y), with at least MASKED_AUTO_TREES trees, or half as
+// many and MASKED_AUTO_TOKENS tokens (its two GEMMs and the selection cost about 35 us at any
+// size, which fewer trees do not win back).
 constexpr int MASKED_MAX_DEPTH = 7;
 constexpr int MASKED_AUTO_DEPTH = 5;
 constexpr int MASKED_AUTO_DEPTH_F32 = 4;
-constexpr int MASKED_AUTO_TREES = 8;
-constexpr int64_t MASKED_AUTO_TOKENS = 4096;
+constexpr int MASKED_AUTO_TREES = 16;
+constexpr int64_t MASKED_AUTO_TOKENS = 16384;
 // Whether a validated request can run masked (types, depth, no LayerNorm, residual types).
 bool masked_shape(const Params& p);
 // Masked mode scratch (logits, split activations, repeated W_out, hipBLASLt's scratch); 0 past
@@ -187,11 +188,13 @@ size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, 
 hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream);
 
 // Subtree mode (fff_subtree.hip): a workgroup per token evaluates whole subtrees of logits per
-// step.  AUTO takes it for trees of depth at least SUBTREE_AUTO_DEPTH when the W_in rows its
-// steps read come to at most SUBTREE_AUTO_BYTES (about 85 tokens at H = 768 in bf16, 34 at
-// H = 4096).
-constexpr int SUBTREE_AUTO_DEPTH = 8;
-constexpr int64_t SUBTREE_AUTO_BYTES = int64_t(16) << 20;
+// step.  AUTO takes it for at most SUBTREE_AUTO_TREES trees of depth at least SUBTREE_AUTO_DEPTH
+// while tokens x trees stay within SUBTREE_AUTO_PAIRS (SUBTREE_AUTO_PAIRS_WIDE at hidden sizes
+// above 1024, where a step's rows are four times longer).
+constexpr int SUBTREE_AUTO_DEPTH = 5;
+constexpr int SUBTREE_AUTO_TREES = 4;
+constexpr int64_t SUBTREE_AUTO_PAIRS = 256;
+constexpr int64_t SUBTREE_AUTO_PAIRS_WIDE = 32;
 bool subtree_auto(const Params& p);
 // Whether a validated request has a subtree kernel (hidden size and types; no LayerNorm).
 bool subtree_shape(const Params& p);

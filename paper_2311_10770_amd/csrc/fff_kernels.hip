@@ -1042,35 +1042,43 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     *plan = Plan{};
     const Variant* v = find_variant(p);
     if (mode == MODE_AUTO) {
-        // Measured on MI355X (hidden 768 / 1024 / 4096, depth 5..15, 4K..64K tokens, bf16 and
-        // fp32 weights): below about 48M input elements the fused descent kernel is fastest,
-        // except for single trees of depth 9..15 with at least 16 tokens per leaf and 16M
-        // elements (depth 11 at 32768 tokens: 54 against 64 us in bf16, 104 against 132 in
-        // fp32), which run fastest leaf-tiled on MFMA.  Above it, single trees of depth 9..15
-        // with at least 8 tokens per leaf run leaf-tiled, other single trees of depth 11 or more
-        // grouped by subtree.
+        // Measured on MI355X (hidden 768 / 1024 / 4096, depth 2..15, 256..128K tokens, 1..3072
+        // trees, bf16 and fp32 weights):
+        // * at most 4 trees of depth >= 5 and 256 token-tree pairs (32 at hidden 4096): a
+        //   workgroup per token evaluating whole subtrees (depth 11, 256 tokens: 10.5 against
+        //   12.3 us);
+        // * shallow layers with many trees as dense products (masked; see its constants);
+        // * single trees of depth 9..15 leaf-tiled on MFMA with at least 8 tokens per leaf from
+        //   48M input elements, or 16 per leaf from 16M (fp32 weights, or depth >= 10: depth 11 at
+        //   32768 tokens 52 against 60 us in bf16; at depth 9 in bf16 the fused kernel stays ahead);
+        // * other single trees of depth >= 11 grouped by subtree from 48M elements, or from 16384
+        //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16;
+        // * else the fused descent kernel.
         const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
         const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
         const int64_t grouped_ws = int64_t(grouped_workspace_bytes(p.n_tokens, p.depth, p.n_trees, 0));
         const int64_t masked_ws = int64_t(masked_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
-        // Shallow layers run fastest as dense products: a token uses (D+1)/(2^(D+1)-1) of the
-        // nodes, at least 9.5 % at depth <= 5, where bf16 MFMA products beat the walk (from 2048
-        // tokens on for the Table 1 shapes); fp32 products (about 125 TFLOP/s against the walk's
-        // 16) win down to 16 % (depth <= 4).
-        // A few tokens of a deep tree wait on the chain of dependent row loads: whole subtrees of
-        // logits per memory round trip shorten it.
+        // Shallow layers: a token uses (D+1)/(2^(D+1)-1) of the nodes, at least 9.5 % at depth
+        // <= 5, where bf16 MFMA products beat the walk; fp32 products (about 125 TFLOP/s against
+        // the walk's 16) win down to 16 % (depth <= 4).
+        const int64_t elems = p.n_tokens * int64_t(p.hidden);
+        const bool one = p.n_trees == 1;
         if (subtree_auto(p))
             mode = MODE_SUBTREE;
         else if (masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
-            (p.n_tokens >= MASKED_AUTO_TOKENS || p.n_trees >= MASKED_AUTO_TREES) && int64_t(workspace_bytes) >= masked_ws)
+                 (p.n_trees >= MASKED_AUTO_TREES ||
+                  (p.n_trees >= MASKED_AUTO_TREES / 2 && p.n_tokens >= MASKED_AUTO_TOKENS)) &&
+                 int64_t(workspace_bytes) >= masked_ws)
             mode = MODE_MASKED;
         else if (!v) mode = MODE_GENERIC;
         else if (tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
                  ((big && p.n_tokens >= (int64_t(8) << p.depth)) ||
-                  (p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(16) << 20) &&
-                   p.n_tokens >= (int64_t(16) << p.depth))))
+                  (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth) &&
+                   (!p.w_bf16 || p.depth >= 10))))
             mode = MODE_TILED;
-        else if (big && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws) mode = MODE_GROUPED;
+        else if (one && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws &&
+                 (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20)))))
+            mode = MODE_GROUPED;
         else mode = MODE_DESCENT;
     }
     if (mode == MODE_SUBTREE) {

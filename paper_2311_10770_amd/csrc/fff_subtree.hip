@@ -228,12 +228,8 @@ const char* subtree_name(const Params& p) {
 }
 
 bool subtree_auto(const Params& p) {
-    const SubtreeVariant* v = find_subtree(p);
-    if (!v || p.norm || p.depth < SUBTREE_AUTO_DEPTH) return false;
-    // W_in bytes the subtree steps read: steps x (2^span - 1) rows per tree and token
-    const int64_t steps = (p.depth + v->span) / v->span;
-    const int64_t row = int64_t(p.hidden) * (p.w_bf16 ? 2 : 4);
-    return p.n_tokens * p.n_trees * steps * ((int64_t(1) << v->span) - 1) * row <= SUBTREE_AUTO_BYTES;
+    if (!subtree_shape(p) || p.depth < SUBTREE_AUTO_DEPTH || p.n_trees > SUBTREE_AUTO_TREES) return false;
+    return p.n_tokens * p.n_trees <= (p.hidden <= 1024 ? SUBTREE_AUTO_PAIRS : SUBTREE_AUTO_PAIRS_WIDE);
 }
 
 int subtree_block(const Params& p) {

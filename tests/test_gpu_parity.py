@@ -280,6 +280,12 @@ def test_describe_names_the_kernel(fff_lib):
     xm = torch.zeros((1024, 768), dtype=torch.bfloat16, device=DEV)
     d = fff_lib.describe(xm, wi, wo, 11, 1)  # auto, 1024 tokens: the fused kernel
     assert d.startswith("descent<"), d
+    xf = torch.zeros((16384, 768), dtype=torch.float32, device=DEV)
+    wf = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf, wf, wf, 11, 1).startswith("grouped<")  # fp32, 16384 tokens
+    w9 = torch.zeros((1, (1 << 10) - 1, 768), dtype=torch.bfloat16, device=DEV)
+    xb9 = torch.zeros((32768, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb9, w9, w9, 9, 1).startswith("descent<")  # bf16 depth 9, 32768 tokens
     # auto with the binding's workspace at 64K tokens: leaf tiles at 32 tokens per leaf,
     # subtree grouping at 4 per leaf (planning only: nothing is launched)
     xb = torch.zeros((65536, 768), dtype=torch.bfloat16, device=DEV)
@@ -291,7 +297,8 @@ def test_describe_names_the_kernel(fff_lib):
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="descent")
     assert d.startswith("descent<") and "lds_levels=" in d
     wi4 = fff_lib.from_numpy(np.concatenate([L["w_in"]] * 4), DEV)
-    assert fff_lib.describe(x, wi4, wi4, 11, 4).startswith("descent<")  # several trees: fused kernel
+    assert fff_lib.describe(xm, wi4, wi4, 11, 4).startswith("descent<")  # several trees: fused kernel
+    assert fff_lib.describe(x, wi4, wi4, 11, 4).startswith("subtree<")  # 64 tokens x 4 trees
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="generic")
     assert d.startswith("generic")
     d = fff_lib.describe(x, wi, wo, 11, 1, mode="grouped")
@@ -428,8 +435,8 @@ def test_masked_output_modes(fff_lib, out):
 
 
 def test_masked_mode_limits_and_auto(fff_lib):
-    """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it for layers of
-    depth <= 5 (bf16) or <= 4 (fp32) with at least 8 trees or 4096 tokens (planning only)."""
+    """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it at depth <= 5
+    (bf16) or <= 4 (fp32) for 16 trees or more, or 8 and 16384 tokens (planning only)."""
     L = layer(430, 64, 768, 3, 8, "f32", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
     with pytest.raises(fff_lib.FffError):
@@ -440,22 +447,23 @@ def test_masked_mode_limits_and_auto(fff_lib):
         fff_lib.forward(x, wi, wo, 3, 8, torch.empty((64, 768), dtype=torch.bfloat16, device=DEV),
                         mode="masked")  # fp32 x and W, bf16 y
     w8 = torch.zeros((1, (1 << 9) - 1, 768), dtype=torch.bfloat16, device=DEV)
-    xb = torch.zeros((4096, 768), dtype=torch.bfloat16, device=DEV)
+    xb = torch.zeros((16384, 768), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(fff_lib.FffError):
         fff_lib.forward(xb[:64], w8, w8, 8, 1, mode="masked")  # depth 8
-    w3 = torch.zeros((64, 15, 768), dtype=torch.bfloat16, device=DEV)
-    assert fff_lib.describe(xb, w3, w3, 3, 64).startswith("masked<")
-    assert fff_lib.describe(xb[:512], w3, w3, 3, 64).startswith("masked<")  # 64 trees
+    w16 = torch.zeros((16, 15, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb[:512], w16, w16, 3, 16).startswith("masked<")  # 16 trees
+    w8t = torch.zeros((8, 15, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, w8t, w8t, 3, 8).startswith("masked<")  # 8 trees, 16384 tokens
+    assert not fff_lib.describe(xb[:8192], w8t, w8t, 3, 8).startswith("masked<")  # 8 trees, 8192 tokens
     w1 = torch.zeros((1, 15, 768), dtype=torch.bfloat16, device=DEV)
-    assert fff_lib.describe(xb, w1, w1, 3, 1).startswith("masked<")  # 4096 tokens
-    assert not fff_lib.describe(xb[:512], w1, w1, 3, 1).startswith("masked<")
-    w6 = torch.zeros((8, 127, 768), dtype=torch.bfloat16, device=DEV)
-    assert not fff_lib.describe(xb, w6, w6, 6, 8).startswith("masked<")  # depth 6: the walk
+    assert fff_lib.describe(xb, w1, w1, 3, 1).startswith("descent<")  # one tree: the walk
+    w6 = torch.zeros((16, 127, 768), dtype=torch.bfloat16, device=DEV)
+    assert not fff_lib.describe(xb[:4096], w6, w6, 6, 16).startswith("masked<")  # depth 6: the walk
     xf = torch.zeros((4096, 768), dtype=torch.float32, device=DEV)
-    w4 = torch.zeros((1, 31, 768), dtype=torch.float32, device=DEV)
-    assert fff_lib.describe(xf, w4, w4, 4, 1).startswith("masked<fp32")  # fp32, depth 4
-    w5 = torch.zeros((1, 63, 768), dtype=torch.float32, device=DEV)
-    assert not fff_lib.describe(xf, w5, w5, 5, 1).startswith("masked<")  # fp32, depth 5: the walk
+    w4 = torch.zeros((16, 31, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf, w4, w4, 4, 16).startswith("masked<fp32")  # fp32, depth 4
+    w5 = torch.zeros((16, 63, 768), dtype=torch.float32, device=DEV)
+    assert not fff_lib.describe(xf, w5, w5, 5, 16).startswith("masked<")  # fp32, depth 5: the walk
 
 
 # ----------------------------------------------------- SUBTREE (a workgroup per token)
@@ -507,21 +515,25 @@ def test_subtree_output_modes(fff_lib, out, xd, wd):
 
 
 def test_subtree_auto_and_limits(fff_lib):
-    """AUTO takes SUBTREE at depth >= 8 while its W_in reads stay within 16 MiB: 86 tokens at
-    H = 768 in bf16 (2 steps of 63 rows of 1536 bytes each), 34 at H = 4096 (4 steps of 15 rows of
-    8 KiB); no LayerNorm, no other widths."""
-    xb = torch.zeros((100, 768), dtype=torch.bfloat16, device=DEV)
+    """AUTO takes SUBTREE for at most 4 trees of depth >= 5 and 256 token-tree pairs (32 at hidden
+    4096); no LayerNorm, no other widths."""
+    xb = torch.zeros((300, 768), dtype=torch.bfloat16, device=DEV)
     w11 = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.bfloat16, device=DEV)
-    assert fff_lib.describe(xb[:86], w11, w11, 11, 1).startswith("subtree<")
+    assert fff_lib.describe(xb[:256], w11, w11, 11, 1).startswith("subtree<")
     assert fff_lib.describe(xb[:1], w11, w11, 11, 1).startswith("subtree<")
-    assert not fff_lib.describe(xb[:87], w11, w11, 11, 1).startswith("subtree<")
-    w7 = torch.zeros((1, 255, 768), dtype=torch.bfloat16, device=DEV)
-    assert not fff_lib.describe(xb[:8], w7, w7, 7, 1).startswith("subtree<")  # depth 7
+    assert not fff_lib.describe(xb[:257], w11, w11, 11, 1).startswith("subtree<")
+    w5 = torch.zeros((4, 63, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb[:64], w5, w5, 5, 4).startswith("subtree<")  # 4 trees x 64 tokens
+    assert not fff_lib.describe(xb[:65], w5, w5, 5, 4).startswith("subtree<")
+    w4 = torch.zeros((1, 31, 768), dtype=torch.bfloat16, device=DEV)
+    assert not fff_lib.describe(xb[:8], w4, w4, 4, 1).startswith("subtree<")  # depth 4
+    w5t = torch.zeros((5, 63, 768), dtype=torch.bfloat16, device=DEV)
+    assert not fff_lib.describe(xb[:8], w5t, w5t, 5, 5).startswith("subtree<")  # 5 trees
     x4 = torch.zeros((40, 4096), dtype=torch.bfloat16, device=DEV)
     w12 = torch.zeros((1, (1 << 13) - 1, 4096), dtype=torch.bfloat16, device=DEV)
-    assert fff_lib.describe(x4[:34], w12, w12, 12, 1).startswith("subtree<")
-    assert not fff_lib.describe(x4[:35], w12, w12, 12, 1).startswith("subtree<")
+    assert fff_lib.describe(x4[:32], w12, w12, 12, 1).startswith("subtree<")
+    assert not fff_lib.describe(x4[:33], w12, w12, 12, 1).startswith("subtree<")
     x5 = torch.zeros((4, 640), dtype=torch.bfloat16, device=DEV)
-    w5 = torch.zeros((1, 63, 640), dtype=torch.bfloat16, device=DEV)
+    w5w = torch.zeros((1, 63, 640), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(fff_lib.FffError):
-        fff_lib.forward(x5, w5, w5, 5, 1, mode="subtree")  # no kernel for hidden 640
+        fff_lib.forward(x5, w5w, w5w, 5, 1, mode="subtree")  # no kernel for hidden 640
