@@ -108,8 +108,9 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * tokens, when the workspace covers it; for single-tree layers whose
  * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
  * leaf and 48M input elements (tokens x hidden), or 16 tokens per leaf and
- * 16M elements (fp32 W, or depth >= 10); else GROUPED at depth 11 or more
- * from 48M elements, or from 16384 tokens with fp32 W or 24M elements;
+ * 16M elements (bf16 W at depth 9: from 96M elements); else GROUPED at depth
+ * 11 or more from 48M elements, or from 16384 tokens with fp32 W or 24M
+ * elements, and with fp32 W at depth 5 or more from 65536 tokens;
  * otherwise DESCENT when a kernel is
  * compiled for the hidden size and types, else GENERIC. */
 typedef enum {

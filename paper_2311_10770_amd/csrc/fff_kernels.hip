@@ -1049,10 +1049,11 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         //   12.3 us);
         // * shallow layers with many trees as dense products (masked; see its constants);
         // * single trees of depth 9..15 leaf-tiled on MFMA with at least 8 tokens per leaf from
-        //   48M input elements, or 16 per leaf from 16M (fp32 weights, or depth >= 10: depth 11 at
-        //   32768 tokens 52 against 60 us in bf16; at depth 9 in bf16 the fused kernel stays ahead);
-        // * other single trees of depth >= 11 grouped by subtree from 48M elements, or from 16384
-        //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16;
+        //   48M input elements, or 16 per leaf from 16M (depth 11 at 32768 tokens: 52 against
+        //   60 us in bf16); at depth 9 in bf16 only from 96M (the fused kernel stays ahead below);
+        // * other single trees grouped by subtree at depth >= 11 from 48M elements, or from 16384
+        //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16, and
+        //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
         // * else the fused descent kernel.
         const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
         const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
@@ -1072,12 +1073,13 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
             mode = MODE_MASKED;
         else if (!v) mode = MODE_GENERIC;
         else if (tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
+                 (!p.w_bf16 || p.depth >= 10 || elems >= (int64_t(96) << 20)) &&
                  ((big && p.n_tokens >= (int64_t(8) << p.depth)) ||
-                  (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth) &&
-                   (!p.w_bf16 || p.depth >= 10))))
+                  (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth))))
             mode = MODE_TILED;
-        else if (one && p.depth >= 11 && int64_t(workspace_bytes) >= grouped_ws &&
-                 (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20)))))
+        else if (one && int64_t(workspace_bytes) >= grouped_ws &&
+                 ((p.depth >= 11 && (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20))))) ||
+                  (!p.w_bf16 && p.depth >= 5 && p.n_tokens >= 65536)))
             mode = MODE_GROUPED;
         else mode = MODE_DESCENT;
     }

@@ -286,6 +286,14 @@ def test_describe_names_the_kernel(fff_lib):
     w9 = torch.zeros((1, (1 << 10) - 1, 768), dtype=torch.bfloat16, device=DEV)
     xb9 = torch.zeros((32768, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb9, w9, w9, 9, 1).startswith("descent<")  # bf16 depth 9, 32768 tokens
+    xb9 = torch.zeros((131072, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb9[:65536], w9, w9, 9, 1).startswith("descent<")  # 48M elements
+    assert fff_lib.describe(xb9, w9, w9, 9, 1).startswith("tiled<")  # 96M elements
+    del xb9
+    xf5 = torch.zeros((65536, 768), dtype=torch.float32, device=DEV)
+    wf5 = torch.zeros((1, 63, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf5, wf5, wf5, 5, 1).startswith("grouped<")  # fp32 depth 5, 65536 tokens
+    assert fff_lib.describe(xf5[:32768], wf5, wf5, 5, 1).startswith("descent<")
     # auto with the binding's workspace at 64K tokens: leaf tiles at 32 tokens per leaf,
     # subtree grouping at 4 per leaf (planning only: nothing is launched)
     xb = torch.zeros((65536, 768), dtype=torch.bfloat16, device=DEV)
