@@ -8,12 +8,20 @@ activations and weights.
 
 Prints ONE JSON line on stdout; progress goes to stderr.  Besides the
 throughput it reports:
-* roofline: gathered weight bytes per launch (one W_in and one W_out row per
-  visited node) over the kernel's mean launch time, against the 8 TB/s HBM
-  peak, plus measured HBM traffic when a counter summary is supplied;
+* roofline: the compulsory HBM bytes of one forward (x read once, y written
+  once, every weight row the batch touches read once) over the mean forward
+  time of the timed region, against the 8 TB/s HBM peak, with the HBM bytes
+  the counters measured (a committed rocprofv3 summary) beside them;
+* gathered: the weight bytes the walk and the emit read per token (one W_in
+  and one W_out row per visited node) over the same time -- served mostly by
+  LDS, L2 and MALL, so this rate exceeds the HBM peak;
+* valu_only: the same layer through the vector-ALU plan (grouped or fused
+  descent, no matrix cores) when the default plan uses MFMA;
 * dense: a dense 768 -> 3072 -> 768 GELU feedforward on the same tokens
-  (bf16 hipBLASLt GEMMs with the GELU fused into the first GEMM's epilogue,
-  fastest heuristic candidate), and the speedup over it;
+  (hipBLASLt GEMMs with the GELU fused into the first GEMM's epilogue,
+  fastest heuristic candidate; bf16, and fp32 for fp32 workloads), its
+  achieved rate against the MFMA peak, and the speedups over it;
+* paper: the paper's own speedups, with the hardware they were measured on;
 * cpu_baseline: the fp64 CPU oracle on the host cores over a bounded sample,
   whose outputs are also compared with the device's for the same tokens.
 """
@@ -31,6 +39,22 @@ if str(ROOT) not in sys.path:
     sys.path.insert(0, str(ROOT))
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # dense MI355X peaks (no sparsity)
+
+# The paper's speedups of the FFF over a dense feedforward (Section 3.3, Table 2), with the
+# hardware and software they were measured on; context for the MI355X figures, not targets.
+PAPER_SPEEDUPS = {
+    "fff_cpu_level2_over_fastest_dense_cpu": {
+        "value": 78.0, "hardware": "Intel Core i7-6700HQ, Intel MKL 2023.2.0, 64-bit routines",
+        "what": "FFF through batched BLAS level-2 routines vs the fastest dense feedforward (level-3 GEMM)"},
+    "fff_pytorch_bmm_over_dense_same_primitive": {
+        "value": 39.45, "hardware": "NVIDIA RTX A6000, CUDA 11.7, PyTorch 2.0.1",
+        "what": "FFF through PyTorch batched matmul vs FF-4095 through the same primitive (the abstract's 40x)"},
+    "fff_pytorch_bmm_over_fastest_dense_gpu": {
+        "value": 3.15, "hardware": "NVIDIA RTX A6000, CUDA 11.7, PyTorch 2.0.1",
+        "what": "FFF through PyTorch batched matmul vs the fastest dense feedforward (native fused)"},
+    "theoretical_limit": {"value": 341.25, "hardware": "analytic", "what": "4095 neurons / 12 used per token"},
+}
 
 
 def host_cpu() -> str:
@@ -227,23 +251,33 @@ def main():
         kernels = ("bwd_rank_wave_kernel + bwd_leafsum_kernel + bwd_base_kernel (+ bwd_scan_kernel past 4096 "
                    "leaves) + bwd_place_kernel + bwd_fused_kernel + bwd_wsum_kernel" if fused else
                    "bwd_token_kernel + sort kernels + bwd_wtile_kernel / bwd_piece_kernel + fix-up")
-        bach = bwd_bytes / (t["mean_ms"] / 1e3) / 1e9
+        bach = bwd_bytes / (ms / 1e3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": bach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": bach / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
                            "basis": f"compulsory bytes of one backward = {B} tokens x {per_tok} B (x, dy, dx rows, "
                                     f"logits and leaf) + {w.n_trees * w.nodes * w.hidden * 2 * (sz[w.w_dtype] + 4)} B "
-                                    f"(W read, fp32 dW written), over the mean time of one call ({kernels}, HIP "
-                                    f"events on the launch stream)"}
+                                    f"(W read, fp32 dW written), over the mean backward time of the timed region "
+                                    f"(ms_per_step: back to back between one pair of HIP events on the launch "
+                                    f"stream; {kernels})"}
     else:
-        out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
-                           "basis": f"gathered weight bytes per forward = {w.gathered_bytes_per_token()} B/token x "
-                                    f"{B} tokens x {NL} layer(s), over the mean time of one forward call ({kernels}, "
-                                    f"HIP events on the launch stream); served by LDS/L2/MALL, not all from HBM"}
-    if traffic:
-        # the measured HBM bytes (counter summary) over the same mean call time
-        out["roofline"]["traffic_gbs"] = traffic / (t["mean_ms"] / 1e3) / 1e9
-        out["roofline"]["traffic_frac"] = out["roofline"]["traffic_gbs"] / HBM_PEAK_GBS
+        C = w.compulsory_bytes(B) * NL
+        cach = C / (ms / 1e3) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": cach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": cach / HBM_PEAK_GBS, "traffic": traffic, "kernels": kernels,
+                           "algorithmic_bytes": C,
+                           "traffic_over_algorithmic": (traffic / C) if traffic else None,
+                           "basis": f"compulsory HBM bytes of one forward C = B H (s_x + s_y) + T 2 H s_w "
+                                    f"sum_l 2^l (1 - (1 - 2^-l)^B) = {C / 1e6:.1f} MB ({NL} layer(s): x read once, y "
+                                    f"written once, every weight row the batch touches read once), over the mean "
+                                    f"forward time of the timed region (ms_per_step: {args.steps} forwards back to "
+                                    f"back between one pair of HIP events on the launch stream; {kernels})"}
+        out["gathered"] = {"bytes_per_forward": gathered, "gbs": gathered / (ms / 1e3) / 1e9,
+                           "over_hbm_peak": gathered / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                           "per_call_gbs": achieved,
+                           "basis": f"{w.gathered_bytes_per_token()} B per token (one W_in and one W_out row per "
+                                    f"visited node) x {B} tokens x {NL} layer(s), over ms_per_step (per_call_gbs: "
+                                    f"over the mean of calls each between their own events); served mostly by "
+                                    f"LDS, L2 and MALL, not HBM"}
     if args.cold_reps:
         tc = benchlib.time_cold(step, args.cold_reps, stream)
         out["cold"] = {"kernel_us": {"mean": tc["mean_ms"] * 1e3, "min": tc["min_ms"] * 1e3,
@@ -264,43 +298,75 @@ def main():
                         "persistent_plan": fff.describe_stack(x, dlayers, w.depth, w.n_trees, y, **kd)}
         log(f"persistent stack kernel: {tk['mean_ms'] * 1e3:.1f} us vs the planned step {t['mean_ms'] * 1e3:.1f} us")
 
+    if not args.backward and NL == 1 and ("tiled<" in plan or "masked<" in plan):
+        # the same layer without matrix cores: the grouped walk + emit (one tree) or the fused kernel
+        vmode = "grouped" if w.n_trees == 1 and w.depth >= 3 else "descent"
+        vkw = dict(kw, mode=vmode)
+        tv = benchlib.time_launches(lambda: fff.forward(x, wi, wo, w.depth, w.n_trees, y, **vkw, **layer_kw(0)),
+                                    args.steps, args.warmup, stream)
+        vms = tv["region_ms"] / args.steps
+        out["valu_only"] = {"mode": vmode, "ms_per_step": vms, "tokens_per_s": B / (vms / 1e3),
+                            "roofline_frac": w.compulsory_bytes(B) / (vms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                            "plan": fff.describe(x, wi, wo, w.depth, w.n_trees, y, **vkw, **layer_kw(0)),
+                            "why": "the default plan accumulates the outputs of tokens that share a leaf on "
+                                   "MFMA; this is the layer on the vector ALU alone"}
+        log(f"vector-ALU plan ({vmode}): {vms * 1e3:.1f} us/step, {B / (vms / 1e3) / 1e6:.1f} M tok/s")
+
     if not args.no_dense and not args.backward:
         H, F = w.hidden, 3072 if w.hidden == 768 else 4 * w.hidden
         g = torch.Generator(device="cpu").manual_seed(1234)
-        w1 = (torch.randn(F, H, generator=g) / H ** 0.5).to(dev, torch.bfloat16)
-        w2 = (torch.randn(H, F, generator=g) / F ** 0.5).to(dev, torch.bfloat16)
-        xb = x if x.dtype == torch.bfloat16 else x.to(torch.bfloat16)
-        dense = benchlib.DenseFF(xb, w1, w2)
+        w1_f = torch.randn(F, H, generator=g) / H ** 0.5
+        w2_f = torch.randn(H, F, generator=g) / F ** 0.5
+        out["dense"] = {}
+        dtypes = ["bf16"] + (["f32"] if w.x_dtype == "f32" else [])
+        for ddt in dtypes:
+            tdt = torch.bfloat16 if ddt == "bf16" else torch.float32
+            w1, w2 = w1_f.to(dev, tdt), w2_f.to(dev, tdt)
+            xb = x if x.dtype == tdt else x.to(tdt)
+            dense = benchlib.DenseFF(xb, w1, w2)
 
-        def dense_step():  # one dense layer per FFF layer of the workload
-            for _ in range(NL):
-                dense()
+            def dense_step():  # one dense layer per FFF layer of the workload
+                for _ in range(NL):
+                    dense()
 
-        nd = max(20, args.steps // 2)
-        td = benchlib.time_launches(dense_step, nd, 10, stream)
-        dense_ms = td["region_ms"] / nd
-        # sanity: the fused-epilogue GEMMs compute the dense layer (tanh- vs erf-GELU differ slightly)
-        ref = torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb[:1024].float(),
-                                         w1.float())), w2.float())
-        rel = float((dense.y[:1024].float() - ref).norm() / ref.norm())
+            nd = max(20, args.steps // 2)
+            td = benchlib.time_launches(dense_step, nd, 10, stream)
+            dense_ms = td["region_ms"] / nd
+            # sanity: the fused-epilogue GEMMs compute the dense layer (tanh- vs erf-GELU differ slightly)
+            ref = torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(
+                xb[:1024].float(), w1.float())), w2.float())
+            rel = float((dense.y[:1024].float() - ref).norm() / ref.norm())
+            dflops = dense.flops * NL
+            peak = MFMA_PEAK_TFLOPS[ddt]
+            ach = dflops / (dense_ms / 1e3) / 1e12
+            d = {"what": f"{NL} x " * (NL > 1) + f"dense FF {H}->{F}->{H} on the same tokens, {ddt}: {dense.info}",
+                 "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
+                 "flops": dflops, "achieved_tflops": ach, "mfma_peak_tflops": peak, "frac_of_mfma_peak": ach / peak,
+                 "speedup_fff_over_dense_at_mfma_peak": (dflops / (peak * 1e12) * 1e3) / ms,
+                 "rel_err_vs_fp32_torch": rel}
+            if "valu_only" in out:
+                d["speedup_valu_only_over_dense"] = dense_ms / out["valu_only"]["ms_per_step"]
+            if ddt == "bf16":
+                def dense_unfused():
+                    for _ in range(NL):
+                        torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
 
-        def dense_unfused():
-            for _ in range(NL):
-                torch.nn.functional.linear(torch.nn.functional.gelu(torch.nn.functional.linear(xb, w1)), w2)
-
-        tu = benchlib.time_launches(dense_unfused, nd, 5, stream)
-        unfused_ms = tu["region_ms"] / nd
-        out["dense"] = {"what": f"{NL} x " * (NL > 1) + f"dense FF {H}->{F}->{H} on the same tokens, bf16: {dense.info}",
-                        "ms": dense_ms, "tokens_per_s": B / (dense_ms / 1e3), "speedup_fff_over_dense": dense_ms / ms,
-                        "rel_err_vs_fp32_torch": rel,
-                        "torch_unfused_ms": unfused_ms, "speedup_fff_over_torch_unfused": unfused_ms / ms}
-        if args.cold_reps:
-            tdc = benchlib.time_cold(dense_step, args.cold_reps, stream)
-            out["dense"]["cold_ms"] = tdc["mean_ms"]
-            out["dense"]["speedup_fff_over_dense_cold"] = tdc["mean_ms"] / out["cold"]["kernel_us"]["mean"] * 1e3
-        dense.close()
-        log(f"dense (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step -> speedup {dense_ms / ms:.2f}x "
-            f"(rel err {rel:.1e}); torch unfused {unfused_ms * 1e3:.1f} us")
+                tu = benchlib.time_launches(dense_unfused, nd, 5, stream)
+                d["torch_unfused_ms"] = tu["region_ms"] / nd
+                d["speedup_fff_over_torch_unfused"] = d["torch_unfused_ms"] / ms
+            if args.cold_reps and ddt == "bf16":
+                tdc = benchlib.time_cold(dense_step, args.cold_reps, stream)
+                d["cold_ms"] = tdc["mean_ms"]
+                d["speedup_fff_over_dense_cold"] = tdc["mean_ms"] / out["cold"]["kernel_us"]["mean"] * 1e3
+            dense.close()
+            out["dense"][ddt] = d
+            log(f"dense {ddt} (hipBLASLt, fused GELU): {dense_ms * 1e3:.1f} us/step ({ach:.0f} TFLOP/s, "
+                f"{ach / peak:.0%} of the MFMA peak) -> speedup {dense_ms / ms:.2f}x, "
+                f"{d['speedup_fff_over_dense_at_mfma_peak']:.2f}x against a dense layer at peak (rel err {rel:.1e})")
+        # the headline comparison: the dense layer in the workload's weight type
+        out["dense"]["speedup_fff_over_dense"] = out["dense"]["f32" if w.w_dtype == "f32" else "bf16"][
+            "speedup_fff_over_dense"]
+        out["paper"] = PAPER_SPEEDUPS
 
     if args.backward:
         args.no_cpu_baseline = True  # the backward's CPU leg and check live in the tests
@@ -371,7 +437,10 @@ def main():
             rep = parity.check(u, lay["w_in"], lay["w_out"], w.depth, w.n_trees, r, fff.to_numpy(y)[:n],
                                nodes[-1].cpu().numpy()[:n], tol=2e-2 if w.y_dtype == "bf16" else 1e-5, base_dev=base)
             out["cpu_baseline"]["check"] = {"tokens": n, "layer_checked": NL - 1, "ok": rep["ok"],
-                                            "max_normwise_err": rep["max_normwise_err"],
+                                            "max_normwise_err_raw": rep["max_normwise_err_raw"],
+                                            "n_conditioned": rep["n_conditioned"],
+                                            "n_ill_conditioned": rep["n_ill_conditioned"],
+                                            "bf16_elem_excess": rep.get("bf16_elem_excess"),
                                             "n_near_tie": rep["n_near_tie"],
                                             "n_path_divergent": rep["n_path_divergent"]}
             log("device vs oracle on the sample:", out["cpu_baseline"]["check"])

@@ -36,8 +36,11 @@
  *   - every argument check runs before any HIP call; on a non-zero return no
  *     device work has been enqueued, except FFF_ERR_HIP, which reports a
  *     failed HIP call (see fff_last_hip_error).
- *   - the library is reentrant; its only global state is a per-device
- *     property cache and the thread-local last HIP error.
+ *   - the library is reentrant.  Its global state: a per-device property
+ *     cache, a cache of occupancy queries per kernel, the thread-local last
+ *     HIP error, and for MASKED mode a per-device hipBLASLt handle with its
+ *     matrix descriptors per product shape (created on first use under a
+ *     mutex; they hold no results, and no call waits on the device).
  */
 #ifndef FFF_H_
 #define FFF_H_
@@ -78,8 +81,10 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * MFMA: fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
  * activations split into bf16 parts (three parts: fp32 working accuracy; two,
  * relative error about 2^-17, when y is bf16 and either stored or the residual
- * of bf16 x).  Tokens past a full
- * bucket take the per-token emit.  Needs the workspace of fff_workspace_bytes.
+ * of bf16 x).  When more tokens reach a leaf than its bucket holds, all of
+ * that leaf's tokens take the per-token emit instead, so the output bits do
+ * not depend on the order in which the walk filled the bucket's slots.  Needs
+ * the workspace of fff_workspace_bytes.
  * MASKED: bf16 x and W, or fp32 x, W and y; depth <= 7, no LayerNorm (a
  * residual needs y of x's type): the layer as two dense products around the
  * walk, for shallow trees
@@ -91,10 +96,9 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * as a second GEMM against W_out repeated once per part.  With fp32 x, W and
  * y both GEMMs are fp32 and the activations go in whole.  Needs the
  * workspace of fff_workspace_bytes (logits, parts, the repeated W_out and
- * hipBLASLt's scratch).  The first call for a shape times hipBLASLt's first
- * eight candidate algorithms per product on the stream and keeps the fastest
- * (that call synchronizes the device; under graph capture the heuristic's
- * first candidate is used instead).
+ * hipBLASLt's scratch).  Each product runs hipBLASLt's first heuristic
+ * algorithm for its shape: a fixed choice, so results do not depend on
+ * timing, and the call only enqueues work like every other mode.
  * SUBTREE: hidden 768, 1024 or 4096 (any supported types), no LayerNorm; for
  * a few tokens, where the walk's D+1 dependent row loads are the time: one
  * workgroup of 1024 threads (512 for fp32 x with bf16 W at hidden >= 1024)

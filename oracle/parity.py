@@ -11,30 +11,65 @@ Rules (paths first, then values):
    Any other difference fails.
 2. Counts.  ``n_near_tie`` = tokens with any flagged visit on the oracle
    path; ``n_path_divergent`` = tokens whose device path differs anywhere.
-3. Values.  Per token, ||y_dev - y_ref||_2 <= tol * ||y_ref||_2 + allowance,
-   with y_ref evaluated in fp64 along the DEVICE path.  The allowance is the
-   first-order effect of rounding the fp32 logits:
-       allowance = sum over visits of |act'(l)| * gamma * ||x|| ||W_in[n]|| ||W_out[n]||
-   where gamma * ||x|| ||W_in[n]|| bounds the error of an fp32 dot product
-   (gamma = 64 unit roundoffs covers a per-lane chain plus a cross-lane tree
-   of up to 64 terms).  It matters only when y itself is tiny next to the
-   terms that feed it -- e.g. a single visited node with a strongly negative
-   logit, where GELU's relative slope (about |l|) amplifies the logit's
-   absolute rounding -- and tokens that need it are counted
-   (``n_conditioned``).
+3. Values.  Per token, the raw normwise error
+       err_b = ||y_dev - y_ref||_2 / ||y_ref||_2 <= tol,
+   with y_ref evaluated in fp64 along the DEVICE path (tol = 1e-5 for fp32
+   outputs, 2e-2 for bf16 outputs; for a bf16 output that adds to a base --
+   residual or accumulate -- the error is taken on the stored total).
+4. The one exception: ILL-CONDITIONED tokens, i.e. cancellation.  y_b is a
+   sum over the visits v of act(l_v) W_out[n_v], and each logit l_v is itself
+   a sum, of the H products x_i W_in[n_v, i].  Perturbing every input element
+   and every product by a relative eps moves y_b by at most
+   eps * kappa_b * ||y_b|| (to first order), with the componentwise condition
+       kappa_b = sum_v (|act'(l_v)| S_v + |act(l_v)|) ||W_out[n_v]|| / ||y_b||,
+       S_v = sum_i |x_i W_in[n_v, i]|.
+   An fp32 evaluation that perturbs each input and product by no more than
+   one unit roundoff u = 2^-24 (a backward-stable one) can therefore only
+   promise u * kappa_b; when that exceeds the fp32 bar (kappa_b > KAPPA_MAX =
+   1e-5 / u, about 168) the bar is not attainable in fp32 and the token is
+   ill-conditioned.  kappa_b is large only under cancellation: a logit far
+   smaller than the magnitudes it sums (|l_v| << S_v; at depth 0 the output
+   is act(l) W_out[0], so a logit near 0 makes the whole output relatively
+   inaccurate) or an output far below the sum of its terms (||y_b|| <<
+   sum |act(l_v)| ||W_out[n_v]||).  Typical tokens of the depth-11, hidden-768
+   layer have kappa_b around 50.  Only ill-conditioned tokens may exceed tol,
+   and only by the first-order rounding bound of the fp32 arithmetic:
+       allowance_b = sum_v [ |act'(l_v)| g_dot S_v
+                             + (8 + l_v^2 + T(D+1) + 1) u |act(l_v)| ] ||W_out[n_v]||,
+   g_dot = max(64, H/16 + 8) u bounding an fp32 dot product split over at
+   least 16 lanes (a per-lane chain plus a reduction tree), 8 + l^2 the
+   activation's own rounding (erfc's condition number near -l/sqrt 2), and
+   T(D+1) + 1 the roundings of the output sum.  Tokens that used it are
+   counted (``n_conditioned``) and a check fails when there are more than
+   ``max_conditioned`` of them (0 unless the caller names a reason).
+5. bf16 outputs, elementwise: every stored element lies within one bf16
+   spacing of the fp64 value (base + y_ref) plus the fp32 bar 1e-5 ||y_ref||
+   (plus the allowance for ill-conditioned tokens).  Rounding an fp32 result
+   that meets the fp32 bar moves it by half a spacing at most (a whole one
+   where it crosses into the next binade), so any error beyond fp32
+   accumulation -- a dropped term, a coarser activation split -- shows.
 
-Elementwise relative error is meaningless near zero, hence the normwise
-form; the largest elementwise error scaled by ||y_ref||_inf is reported too.
+Elementwise relative error is meaningless near zero, hence the normwise form;
+the largest elementwise error scaled by ||y_ref||_inf is reported too.
 """
 from __future__ import annotations
 
 import math
 
 import numpy as np
+from scipy.special import erfc
 
 from . import DEFAULT_TIE_REL, eval_path
 
-DOT_GAMMA = 64 * 2.0 ** -24
+U32 = 2.0 ** -24          # fp32 unit roundoff
+FP32_BAR = 1e-5           # per-token normwise bar of an fp32 output
+KAPPA_MAX = FP32_BAR / U32
+
+
+def dot_gamma(hidden: int) -> float:
+    """First-order bound, in units of ||x|| ||w||, on the rounding of an fp32 dot product of length
+    hidden split over at least 16 lanes: a per-lane chain of hidden/16 terms plus a reduction tree."""
+    return max(64.0, hidden / 16.0 + 8.0) * U32
 
 
 def widen(a: np.ndarray) -> np.ndarray:
@@ -59,32 +94,104 @@ def row_norms(w: np.ndarray, chunk: int = 4096) -> np.ndarray:
     return out
 
 
+def _is_identity(act) -> bool:
+    return act in ("identity", 2)
+
+
+def _is_tanh(act) -> bool:
+    return act in ("gelu_tanh", 1)
+
+
+def act_values(z: np.ndarray, act) -> np.ndarray:
+    """act(z) in float64: GELU z Phi(z) = z/2 erfc(-z/sqrt 2), its tanh form, or the identity."""
+    z = np.asarray(z, dtype=np.float64)
+    if _is_identity(act):
+        return z.copy()
+    if _is_tanh(act):
+        u = math.sqrt(2.0 / math.pi) * (z + 0.044715 * z ** 3)
+        return z / (1.0 + np.exp(-2.0 * u))
+    return 0.5 * z * erfc(-z / math.sqrt(2.0))
+
+
 def act_slope(logits: np.ndarray, act) -> np.ndarray:
-    """|d act / d l| at the given logits (GELU: Phi(l) + l*phi(l); identity: 1)."""
-    if act in ("identity", 2):
-        return np.ones_like(logits)
-    erf = np.vectorize(math.erf, otypes=[float])
-    phi_cdf = 0.5 * (1.0 + erf(logits / math.sqrt(2.0)))
-    pdf = np.exp(-0.5 * logits * logits) / math.sqrt(2.0 * math.pi)
-    return np.abs(phi_cdf + logits * pdf)
+    """|d act / d l| at the given logits (GELU: Phi(l) + l phi(l); identity: 1)."""
+    z = np.asarray(logits, dtype=np.float64)
+    if _is_identity(act):
+        return np.ones_like(z)
+    if _is_tanh(act):
+        u = math.sqrt(2.0 / math.pi) * (z + 0.044715 * z ** 3)
+        s = 1.0 / (1.0 + np.exp(-2.0 * u))
+        sm = 1.0 / (1.0 + np.exp(2.0 * u))
+        return np.abs(s + 2.0 * z * s * sm * math.sqrt(2.0 / math.pi) * (1.0 + 3 * 0.044715 * z * z))
+    cdf = 0.5 * erfc(-z / math.sqrt(2.0))
+    pdf = np.exp(-0.5 * z * z) / math.sqrt(2.0 * math.pi)
+    return np.abs(cdf + z * pdf)
+
+
+def dot_magnitudes(x_rows, w_in, nodes, chunk: int = 2048) -> np.ndarray:
+    """S[b, t, l] = sum_i |x[b, i] W_in[t, nodes[b, t, l], i]|, float64 (chunked over tokens)."""
+    x_rows = np.asarray(x_rows)
+    B = x_rows.shape[0]
+    T = w_in.shape[0]
+    nodes = np.asarray(nodes).reshape(B, T, -1)
+    out = np.empty(nodes.shape)
+    for b0 in range(0, B, chunk):
+        xa = np.abs(widen(x_rows[b0:b0 + chunk]))
+        for t in range(T):
+            rows = np.abs(widen(w_in[t][nodes[b0:b0 + chunk, t]]))  # [b, D+1, H]
+            out[b0:b0 + chunk, t] = np.einsum("bh,blh->bl", xa, rows)
+    return out
+
+
+def conditioning(x_rows, w_in, w_out, depth: int, n_trees: int, nodes, logits, y_ref, act):
+    """Per token: kappa_b (rule 4) and the allowance of rule 4, both float64 [B]."""
+    B = y_ref.shape[0]
+    H = np.asarray(x_rows).shape[1]
+    nout = row_norms(w_out)
+    tidx = np.arange(n_trees)[None, :, None]
+    nodes = np.asarray(nodes).reshape(B, n_trees, depth + 1)
+    l = np.asarray(logits, dtype=np.float64).reshape(B, n_trees, depth + 1)
+    a = act_values(l, act)
+    s = act_slope(l, act)
+    S = dot_magnitudes(x_rows, w_in, nodes)
+    wo = nout[tidx, nodes]
+    ynorm = np.linalg.norm(y_ref, axis=1)
+    terms = ((s * S + np.abs(a)) * wo).reshape(B, -1).sum(axis=1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        kappa = np.where(ynorm > 0, terms / np.maximum(ynorm, 1e-300), np.where(terms > 0, np.inf, 0.0))
+    n_sum = n_trees * (depth + 1) + 1
+    allow = (s * dot_gamma(H) * S + (8.0 + l * l + n_sum) * U32 * np.abs(a)) * wo
+    return kappa, allow.reshape(B, -1).sum(axis=1)
+
+
+def bf16_spacing(r: np.ndarray) -> np.ndarray:
+    """Distance between consecutive bf16 values at |r|: 2^(e-8) for |r| in [2^(e-1), 2^e), floored at
+    the subnormal step 2^-133."""
+    _, e = np.frexp(np.asarray(r, dtype=np.float64))
+    return np.ldexp(1.0, np.maximum(e - 8, -133))
 
 
 def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nodes_dev=None,
           tol: float = 1e-5, act="gelu", tie_rel: float = DEFAULT_TIE_REL, rows=None,
-          base_dev=None, dot_gamma: float = DOT_GAMMA) -> dict:
-    """Compare device results with the oracle.
+          base_dev=None, max_conditioned: int = 0) -> dict:
+    """Compare device results with the oracle (rules in the module docstring).
 
     ``rows``: optional token indices the oracle output covers (sampled check);
     ``x`` and the device arrays are then indexed by it.  ``base_dev``: an
     optional [B,H] term the device added to FFF(x) (residual or accumulate),
     subtracted before comparing.
     """
+    y_is_bf16 = np.asarray(y_dev).dtype == np.uint16
     y_dev = widen(y_dev)
+    base = None
     if base_dev is not None:
-        y_dev = y_dev - widen(base_dev)
+        base = widen(base_dev)
+        y_dev = y_dev - base
     if rows is not None:
         rows = np.asarray(rows)
         y_dev = y_dev[rows]
+        if base is not None and base.shape[0] != y_dev.shape[0]:
+            base = base[rows]
         x_rows = np.asarray(x)[rows]
         if nodes_dev is not None:
             nodes_dev = np.asarray(nodes_dev)[rows]
@@ -141,34 +248,60 @@ def check(x, w_in, w_out, depth: int, n_trees: int, oracle_out: dict, y_dev, nod
                 nodes_ref[b] = nodes_dev[b]
                 logits_ref[b] = logits_path
 
-    diff = np.linalg.norm(y_dev - y_ref, axis=1)
-    ref = np.linalg.norm(y_ref, axis=1)
+    kappa, allowance = conditioning(x_rows, w_in, w_out, depth, n_trees, nodes_ref, logits_ref, y_ref, act)
+    ill = kappa > KAPPA_MAX
+    allowance = np.where(ill, allowance, 0.0)
+    # the compared quantity: the FFF output, or for a bf16 output on a base the stored total
+    on_total = y_is_bf16 and base is not None
+    cmp_dev = y_dev + base if on_total else y_dev
+    cmp_ref = y_ref + base if on_total else y_ref
+    diff = np.linalg.norm(cmp_dev - cmp_ref, axis=1)
+    ref = np.linalg.norm(cmp_ref, axis=1)
     err = diff / np.maximum(ref, 1e-30)
     err[(ref == 0) & (diff == 0)] = 0.0
-    # first-order allowance for fp32 logit rounding (see module docstring)
-    nin, nout = row_norms(w_in), row_norms(w_out)
-    tidx = np.arange(n_trees)[None, :, None]
-    xnorm = np.linalg.norm(widen(x_rows), axis=1)
-    terms = act_slope(logits_ref, act) * nin[tidx, nodes_ref] * nout[tidx, nodes_ref]
-    allowance = dot_gamma * xnorm * terms.reshape(B, -1).sum(axis=1)
-    conditioned = (err > tol) & (diff <= tol * ref + allowance)
+    conditioned = ill & (err > tol) & (diff <= tol * ref + allowance)
+    report["n_ill_conditioned"] = int(ill.sum())
+    report["max_kappa"] = float(kappa.max()) if B else 0.0
     report["n_conditioned"] = int(conditioned.sum())
     report["max_normwise_err_raw"] = float(err.max()) if B else 0.0
-    err = np.where(conditioned, 0.0, err)
+    skip = np.zeros(B, dtype=bool)
     if nodes_dev is None:
         # Without device paths a near-tie token may have branched the other way; skip those.
         skip = tie_or.reshape(B, -1).any(axis=1)
-        err = np.where(skip, 0.0, err)
         report["n_skipped_near_tie"] = int(skip.sum())
+    judged = np.where(conditioned | skip, 0.0, err)
     amax = np.max(np.abs(y_ref), axis=1)
     elem = np.max(np.abs(y_dev - y_ref), axis=1) / np.maximum(amax, 1e-30)
-    report["max_normwise_err"] = float(err.max()) if B else 0.0
-    report["max_elem_err_over_inf"] = float(elem.max()) if B else 0.0
-    bad = np.nonzero(err > tol)[0]
+    report["max_normwise_err"] = float(np.where(skip, 0.0, err).max()) if B else 0.0
+    report["max_elem_err_over_inf"] = float(np.where(skip, 0.0, elem).max()) if B else 0.0
+    bad = np.nonzero(judged > tol)[0]
     report["value_failures"] = [(int(b), float(err[b])) for b in bad[:20]]
     report["n_value_failures"] = int(bad.size)
-    report["ok"] = (not report["path_failures"]) and bad.size == 0
+    elem_ok = True
+    if y_is_bf16:
+        total_ref = y_ref + (base if base is not None else 0.0)
+        total_dev = y_dev + (base if base is not None else 0.0)
+        bound = bf16_spacing(total_ref) + (FP32_BAR * np.linalg.norm(y_ref, axis=1) + allowance)[:, None]
+        excess = np.max(np.abs(total_dev - total_ref) / bound, axis=1)
+        excess = np.where(skip, 0.0, excess)
+        report["bf16_elem_excess"] = float(excess.max()) if B else 0.0
+        ebad = np.nonzero(excess > 1.0)[0]
+        report["n_bf16_elem_failures"] = int(ebad.size)
+        report["bf16_elem_failures"] = [(int(b), float(excess[b])) for b in ebad[:20]]
+        elem_ok = ebad.size == 0
+    report["ok"] = ((not report["path_failures"]) and bad.size == 0 and elem_ok
+                    and report["n_conditioned"] <= max_conditioned)
     return report
+
+
+def summary(rep: dict) -> str:
+    """One line with the figures every parity check prints: raw error, conditioning counts, paths."""
+    s = (f"max normwise err {rep['max_normwise_err_raw']:.2e} (raw), conditioned {rep['n_conditioned']} "
+         f"of {rep['n_ill_conditioned']} ill-conditioned (max kappa {rep['max_kappa']:.1f}), "
+         f"near-tie {rep['n_near_tie']}, divergent {rep['n_path_divergent']}")
+    if "bf16_elem_excess" in rep:
+        s += f", bf16 elementwise excess {rep['bf16_elem_excess']:.2f}"
+    return s
 
 
 def assert_parity(*args, **kwargs) -> dict:
@@ -177,7 +310,8 @@ def assert_parity(*args, **kwargs) -> dict:
         raise AssertionError(
             f"parity failed: {len(rep['path_failures'])} path failures "
             f"(first: {rep['path_failures'][:3]}), {rep['n_value_failures']} value failures "
-            f"(first: {rep['value_failures'][:3]}), max normwise err {rep['max_normwise_err']:.3e}")
+            f"(first: {rep['value_failures'][:3]}), {rep.get('n_bf16_elem_failures', 0)} bf16 elementwise "
+            f"failures (first: {rep.get('bf16_elem_failures', [])[:3]}); {summary(rep)}")
     return rep
 
 
@@ -201,8 +335,6 @@ def bf16_total_excess(y_dev_bits: np.ndarray, total_ref: np.ndarray, fff_ref: np
     bound = spacing + tol * np.linalg.norm(np.asarray(fff_ref, dtype=np.float64), axis=1, keepdims=True)
     return float(np.max(np.abs(d - r) / bound))
 
-
-U32 = 2.0 ** -24  # fp32 unit roundoff
 
 
 def _act_grad_np(z, act):

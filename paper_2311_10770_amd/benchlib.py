@@ -19,8 +19,8 @@ def load():
         if not LIB_PATH.exists():
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2311_10770_amd.build`")
         lib = ctypes.CDLL(str(LIB_PATH))
-        lib.fffb_dense_ff_create.argtypes = [c_int64, c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
-                                             c_void_p, c_void_p]
+        lib.fffb_dense_ff_create.argtypes = [c_int64, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p,
+                                             c_void_p, c_void_p, c_void_p]
         lib.fffb_dense_ff_create.restype = c_void_p
         lib.fffb_dense_ff_info.argtypes = [c_void_p]
         lib.fffb_dense_ff_info.restype = c_char_p
@@ -39,18 +39,22 @@ def load():
 
 
 class DenseFF:
-    """y = GELU(x W1^T) W2^T in bf16 on hipBLASLt, GELU fused in the first GEMM's epilogue."""
+    """y = GELU(x W1^T) W2^T on hipBLASLt (x, W1 and W2 all bf16 or all fp32; fp32 accumulation),
+    GELU fused in the first GEMM's epilogue."""
 
     def __init__(self, x: torch.Tensor, w1: torch.Tensor, w2: torch.Tensor, stream=None):
         lib = load()
+        if not (x.dtype == w1.dtype == w2.dtype) or x.dtype not in (torch.bfloat16, torch.float32):
+            raise ValueError("x, W1 and W2 must all be bf16 or all fp32")
         self.x, self.w1, self.w2 = x, w1, w2
         B, H = x.shape
         F = w1.shape[0]
-        self.h = torch.empty((B, F), dtype=torch.bfloat16, device=x.device)
-        self.y = torch.empty((B, H), dtype=torch.bfloat16, device=x.device)
+        self.flops = 4 * B * H * F
+        self.h = torch.empty((B, F), dtype=x.dtype, device=x.device)
+        self.y = torch.empty((B, H), dtype=x.dtype, device=x.device)
         self.stream = (stream or torch.cuda.current_stream(x.device)).cuda_stream
-        self.handle = lib.fffb_dense_ff_create(B, H, F, x.data_ptr(), w1.data_ptr(), w2.data_ptr(),
-                                               self.h.data_ptr(), self.y.data_ptr(), self.stream)
+        self.handle = lib.fffb_dense_ff_create(B, H, F, int(x.dtype == torch.float32), x.data_ptr(), w1.data_ptr(),
+                                               w2.data_ptr(), self.h.data_ptr(), self.y.data_ptr(), self.stream)
         if not self.handle:
             raise RuntimeError("hipBLASLt dense FF setup failed")
         self.info = lib.fffb_dense_ff_info(self.handle).decode()

@@ -37,6 +37,19 @@ class Workload:
         """Weight bytes one token reads: one W_in row and one W_out row per visited node."""
         return self.n_trees * (self.depth + 1) * 2 * self.hidden * self.w_elem_bytes()
 
+    def act_elem_bytes(self) -> tuple:
+        return (2 if self.x_dtype == BF16 else 4), (2 if self.y_dtype == BF16 else 4)
+
+    def compulsory_bytes(self, n_tokens: int | None = None) -> float:
+        """HBM bytes one forward cannot avoid: x read once, y written once, and every weight row
+        the batch touches read once.  Under uniform routing level l has 2^l nodes, each reached
+        by some token with probability 1 - (1 - 2^-l)^B, and every reached node costs one W_in
+        and one W_out row."""
+        B = self.n_tokens if n_tokens is None else n_tokens
+        sx, sy = self.act_elem_bytes()
+        rows = sum(2.0 ** l * (1.0 - (1.0 - 2.0 ** -l) ** B) for l in range(self.depth + 1))
+        return B * self.hidden * (sx + sy) + self.n_trees * 2 * self.hidden * self.w_elem_bytes() * rows
+
     def flops_per_token(self) -> int:
         """Multiply-adds of the dot product and of the output accumulation, 2 flops each."""
         return 4 * self.hidden * self.n_trees * (self.depth + 1)

@@ -1,9 +1,9 @@
 // bench_helpers.hip -- benchmark-only helpers (libfffbench.so), not part of
 // the FFF library:
-//   * a dense feedforward y = GELU(x W1^T) W2^T on hipBLASLt (bf16 in/out,
-//     fp32 accumulate, MFMA), GELU fused into the first GEMM's epilogue, the
-//     fastest of the heuristic's candidate algorithms picked by timing --
-//     the dense layer the FFF is compared against;
+//   * a dense feedforward y = GELU(x W1^T) W2^T on hipBLASLt (bf16 in/out with
+//     fp32 accumulation, or fp32 throughout; MFMA), GELU fused into the first
+//     GEMM's epilogue, the fastest of the heuristic's candidate algorithms
+//     picked by timing -- the dense layer the FFF is compared against;
 //   * a plain vectorised copy kernel whose HBM counter readings calibrate the
 //     traffic measured for the FFF kernels.
 #include <hip/hip_runtime.h>
@@ -33,6 +33,7 @@ struct DenseFF {
     size_t ws_bytes = 0;
     int64_t tokens = 0;
     int hidden = 0, width = 0;
+    hipDataType dt = HIP_R_16BF;
     char info[256] = {0};
 };
 
@@ -52,10 +53,9 @@ bool make_gemm(DenseFF* ff, Gemm* g, uint64_t m, uint64_t n, uint64_t k, bool ge
         if (!lt_ok(hipblasLtMatmulDescSetAttribute(g->desc, HIPBLASLT_MATMUL_DESC_EPILOGUE, &ep, sizeof ep)))
             return false;
     }
-    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->a, HIP_R_16BF, k, m, k))) return false;
-    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->b, HIP_R_16BF, k, n, k))) return false;
-    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->d, HIP_R_16BF, m, n, m))) return false;
-    (void)ff;
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->a, ff->dt, k, m, k))) return false;
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->b, ff->dt, k, n, k))) return false;
+    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g->d, ff->dt, m, n, m))) return false;
     return true;
 }
 
@@ -185,11 +185,13 @@ FFFB_EXPORT void fffb_dense_ff_destroy(void* handle) {
     delete ff;
 }
 
-// Create a tuned dense FF for [tokens, hidden] -> [tokens, width] -> [tokens, hidden], bf16.
-// Buffers are used for tuning only (contents are overwritten).  Returns NULL on failure.
-FFFB_EXPORT void* fffb_dense_ff_create(int64_t tokens, int32_t hidden, int32_t width, const void* x, const void* w1,
-                                       const void* w2, void* h, void* y, void* stream) {
+// Create a tuned dense FF for [tokens, hidden] -> [tokens, width] -> [tokens, hidden]; every
+// tensor bf16 (f32 = 0) or fp32 (f32 = 1), fp32 accumulation.  Buffers are used for tuning only
+// (contents are overwritten).  Returns NULL on failure.
+FFFB_EXPORT void* fffb_dense_ff_create(int64_t tokens, int32_t hidden, int32_t width, int32_t f32, const void* x,
+                                       const void* w1, const void* w2, void* h, void* y, void* stream) {
     DenseFF* ff = new DenseFF();
+    ff->dt = f32 ? HIP_R_32F : HIP_R_16BF;
     ff->tokens = tokens;
     ff->hidden = hidden;
     ff->width = width;
@@ -204,8 +206,8 @@ FFFB_EXPORT void* fffb_dense_ff_create(int64_t tokens, int32_t hidden, int32_t w
         fffb_dense_ff_destroy(ff);
         return nullptr;
     }
-    std::snprintf(ff->info, sizeof ff->info, "hipBLASLt bf16, GELU epilogue; tuned gemm1 %.1f us, gemm2 %.1f us",
-                  t1 * 1e3f, t2 * 1e3f);
+    std::snprintf(ff->info, sizeof ff->info, "hipBLASLt %s, GELU epilogue; tuned gemm1 %.1f us, gemm2 %.1f us",
+                  f32 ? "fp32" : "bf16", t1 * 1e3f, t2 * 1e3f);
     return ff;
 }
 

@@ -477,19 +477,19 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     const int D = p.depth;
     const int64_t L = int64_t(1) << D;
 
-    if (int(blockIdx.x) >= leaf_blocks) {
-        // spilled tokens: the per-token emit (all levels from global memory)
+    // The per-token emit (all levels from global memory) of `count` tokens: token i is tok_of(i),
+    // its activations at rec_of(i); groups g = first, first + stride, ... of this wave.
+    auto emit_per_token = [&](int64_t count, int64_t first, int64_t stride, auto tok_of, auto rec_of) {
         using S = Shape<ELANES, ENV, XBF, WBF>;
         const int sl = lane % ELANES, sub = lane / ELANES;
-        const int64_t count = *p.bk_nspill;
         const int64_t groups = (count + S::TPW - 1) / S::TPW;
-        const int64_t stride = int64_t(gridDim.x - leaf_blocks) * WAVES;
-        for (int64_t g = int64_t(blockIdx.x - leaf_blocks) * WAVES + wave; g < groups; g += stride) {
+        for (int64_t g = first; g < groups; g += stride) {
             const int64_t idx_raw = g * S::TPW + sub;
             const bool valid = idx_raw < count;
-            const int64_t tok = p.bk_spill[valid ? idx_raw : count - 1];
+            const int64_t idx = valid ? idx_raw : count - 1;
+            const int64_t tok = tok_of(idx);
             const uint32_t leaf1 = uint32_t(p.ws_leaf[tok]) + 1;
-            const float* arec = p.ws_act + tok * (D + 1);
+            const float* arec = rec_of(idx);
             const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + sl;
             float acc[S::E];
 #pragma unroll
@@ -502,6 +502,13 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
             if (valid) store_output<ELANES, ENV, WBF>(p, xr, acc, tok, sl);
         }
+    };
+
+    if (int(blockIdx.x) >= leaf_blocks) {
+        // spilled tokens (their leaf overflowed): the per-token emit from their own records
+        emit_per_token(int64_t(*p.bk_nspill), int64_t(blockIdx.x - leaf_blocks) * WAVES + wave,
+                       int64_t(gridDim.x - leaf_blocks) * WAVES, [&](int64_t i) { return int64_t(p.bk_spill[i]); },
+                       [&](int64_t i) { return p.ws_act + int64_t(p.bk_spill[i]) * (D + 1); });
         return;
     }
 
@@ -513,13 +520,21 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
         leaf = (x + XCDS * (lb / per)) * per + lb % per;
     }
     const int32_t cnt_all = p.bk_count[leaf];
-    const int cnt = cnt_all < p.bk_cap ? cnt_all : p.bk_cap;
-    if (cnt == 0) return;  // workgroup-uniform
-    const uint32_t leaf1 = uint32_t(leaf + L);
-    const int n = lane & 15, kq = lane >> 4;
+    if (cnt_all == 0) return;  // workgroup-uniform
     const int cap = p.bk_cap;
     const int32_t* bucket = p.bk_tok + leaf * cap;
     const float* act = p.bk_act + leaf * int64_t(cap) * TILE_REC;
+    if (cnt_all > cap) {
+        // An overflowing leaf: which of its tokens found a slot depends on the order of the walk's
+        // atomics, so all of them take the per-token emit (these from their slots, the rest in the
+        // spill workgroups) and every token's output is the same bits on every run.
+        emit_per_token(int64_t(cap), wave, WAVES, [&](int64_t i) { return int64_t(bucket[i]); },
+                       [&](int64_t i) { return act + i * TILE_REC; });
+        return;
+    }
+    const int cnt = cnt_all;
+    const uint32_t leaf1 = uint32_t(leaf + L);
+    const int n = lane & 15, kq = lane >> 4;
     constexpr int XSZ = XBF ? 2 : 4;
     const int ysz = YM == TILE_Y_ANY         ? (p.y_bf16 ? 2 : 4)
                     : YM == TILE_Y_RESIDUAL  ? (XBF ? 2 : 4)

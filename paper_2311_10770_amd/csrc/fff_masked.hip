@@ -17,9 +17,9 @@
 //      residual come in through the C operand (beta = 1).
 // With fp32 x, W and y both products are fp32 GEMMs (full fp32 compute) and A
 // holds the activations whole.  The workspace holds L, A, the repeated W_out and
-// hipBLASLt's scratch.  On a product shape's first use (outside graph capture)
-// the heuristic's first eight algorithms are timed on the stream and the fastest
-// is kept (the call then synchronizes the device once).
+// hipBLASLt's scratch.  Each product runs the heuristic's first algorithm for
+// its shape: a fixed choice, so the call only enqueues work and its results do
+// not depend on timing.
 #include "fff_common.hpp"
 #include "fff_device.hpp"
 #include "fff_internal.hpp"
@@ -181,16 +181,13 @@ __global__ __launch_bounds__(256) void repeat_kernel(const uint4* __restrict__ s
 
 // ---------------------------------------------------------------- hipBLASLt
 
-constexpr int LT_CANDIDATES = 8;  // heuristic candidates timed on a product's first use
+constexpr int LT_CANDIDATES = 8;  // heuristic candidates asked for; the first usable one runs
 
 struct GemmEntry {
     hipblasLtMatmulDesc_t desc = nullptr;
     hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
-    hipblasLtMatmulAlgo_t algo{};            // in use: the heuristic's first, then the fastest timed
-    hipblasLtMatmulAlgo_t cand[LT_CANDIDATES];
-    int n_cand = 0;
+    hipblasLtMatmulAlgo_t algo{};            // the heuristic's first usable algorithm
     bool ok = false;
-    bool tuned = false;
 };
 
 struct LtState {
@@ -231,46 +228,12 @@ GemmEntry* get_gemm(LtState& st, int64_t m, int64_t n, int64_t k, bool transa, h
         hipblasLtMatmulAlgoGetHeuristic(st.handle, g.desc, g.a, g.b, g.c, g.c, pref, LT_CANDIDATES, res, &found);
     hipblasLtMatmulPreferenceDestroy(pref);
     if (!lt_ok(s)) return nullptr;
-    for (int i = 0; i < found && i < LT_CANDIDATES; ++i)
-        if (res[i].state == HIPBLAS_STATUS_SUCCESS && res[i].workspaceSize <= LT_WORKSPACE) g.cand[g.n_cand++] = res[i].algo;
-    if (g.n_cand == 0) return nullptr;
-    g.algo = g.cand[0];
-    g.ok = true;
-    return &g;
-}
-
-// Times every candidate of g (one warm-up and three timed runs each, HIP events on the stream)
-// through run(algo) and keeps the fastest; once per product shape.  Skipped while the stream is
-// being captured into a graph (the heuristic's first candidate stays), and on any timing error.
-template <class Run>
-void tune(GemmEntry& g, hipStream_t stream, Run run) {
-    if (g.tuned) return;
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;
-    g.tuned = true;
-    if (g.n_cand < 2) return;
-    hipEvent_t e0, e1;
-    if (hipEventCreate(&e0) != hipSuccess) return;
-    if (hipEventCreate(&e1) != hipSuccess) {
-        (void)hipEventDestroy(e0);
-        return;
-    }
-    float best = 0.0f;
-    int best_i = 0;
-    for (int i = 0; i < g.n_cand; ++i) {
-        bool ok = run(g.cand[i]);
-        ok = ok && hipEventRecord(e0, stream) == hipSuccess;
-        for (int r = 0; r < 3 && ok; ++r) ok = run(g.cand[i]);
-        ok = ok && hipEventRecord(e1, stream) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
-        float ms = 0.0f;
-        if (ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess && (i == 0 || ms < best)) {
-            best = ms;
-            best_i = i;
+    for (int i = 0; i < found && i < LT_CANDIDATES && !g.ok; ++i)
+        if (res[i].state == HIPBLAS_STATUS_SUCCESS && res[i].workspaceSize <= LT_WORKSPACE) {
+            g.algo = res[i].algo;
+            g.ok = true;
         }
-    }
-    (void)hipEventDestroy(e0);
-    (void)hipEventDestroy(e1);
-    g.algo = g.cand[best_i];
+    return g.ok ? &g : nullptr;
 }
 
 }  // namespace
@@ -289,9 +252,7 @@ size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, 
     if (depth > MASKED_MAX_DEPTH) return 0;
     const size_t ntq = size_t(padded_cols(((int64_t(1) << (depth + 1)) - 1) * n_trees));
     const int P = 3;  // the larger part count (fp32 y); three bf16 parts also cover one fp32 row
-    // the logit region also takes G2's output while its candidates are timed
-    const size_t lcols = std::max(ntq, size_t(hidden));
-    return align256(size_t(n_tokens) * lcols * sizeof(float)) + align256(size_t(n_tokens) * P * ntq * sizeof(uint16_t)) +
+    return align256(size_t(n_tokens) * ntq * sizeof(float)) + align256(size_t(n_tokens) * P * ntq * sizeof(uint16_t)) +
            align256(size_t(P) * ntq * size_t(hidden) * sizeof(uint16_t)) + LT_WORKSPACE;
 }
 
@@ -301,7 +262,7 @@ hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
     const int P = f32 ? 1 : masked_parts(p.y_bf16);
     char* ws = static_cast<char*>(workspace);
     float* L = reinterpret_cast<float*>(ws);  // [B, ntq]
-    ws += align256(size_t(B) * std::max<int64_t>(ntq, H) * sizeof(float));
+    ws += align256(size_t(B) * ntq * sizeof(float));
     void* A = ws;                             // bf16 [B, P, ntq] or fp32 [B, ntq]
     ws += align256(size_t(B) * 3 * ntq * sizeof(uint16_t));
     uint16_t* Wrep = reinterpret_cast<uint16_t*>(ws);  // bf16 [P, ntq, H]
@@ -329,7 +290,6 @@ hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
         return lt_ok(hipblasLtMatmul(st.handle, g1->desc, &one, p.w_in, g1->a, p.x, g1->b, &zero, L, g1->c, L,
                                      g1->c, &algo, lt_ws, LT_WORKSPACE, stream));
     };
-    tune(*g1, stream, run_g1);
     if (!run_g1(g1->algo)) return hipErrorLaunchFailure;
     if (!f32) {
         const int64_t n = NT * H / 8, np = ntq * H / 8;
@@ -359,14 +319,9 @@ hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // G2: y^T (column-major [H, B]) = Wrep^T (column-major [H, k2]) A^T, plus C (y or x); its
-    // candidates are timed into the logit region (free once the selection has run), beta = 0
+    // G2: y^T (column-major [H, B]) = Wrep^T (column-major [H, k2]) A^T, plus C (y or x)
     const void* C = p.out_mode == OUT_RESIDUAL ? p.x : p.y;
     const void* W2 = f32 ? p.w_out : static_cast<const void*>(Wrep);
-    tune(*g2, stream, [&](const hipblasLtMatmulAlgo_t& algo) {
-        return lt_ok(hipblasLtMatmul(st.handle, g2->desc, &one, W2, g2->a, A, g2->b, &zero, L, g2->c, L, g2->c, &algo,
-                                     lt_ws, LT_WORKSPACE, stream));
-    });
     if (!lt_ok(hipblasLtMatmul(st.handle, g2->desc, &one, W2, g2->a, A, g2->b, beta_on ? &one : &zero, C, g2->c, p.y,
                                g2->c, &g2->algo, lt_ws, LT_WORKSPACE, stream)))
         return hipErrorLaunchFailure;

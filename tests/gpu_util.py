@@ -40,7 +40,7 @@ def run_fff(fff, L: dict, depth: int, trees: int, y_dtype: str, *, record=True, 
 
 
 def check_layer(fff, name: str, L: dict, depth: int, trees: int, y_dtype: str, act="gelu", tol=None,
-                **kw) -> dict:
+                max_conditioned: int = 0, **kw) -> dict:
     w_dtype = "bf16" if L["w_in"].dtype == np.uint16 else "f32"
     tol = tol if tol is not None else tol_for(w_dtype, y_dtype)
     B, H = L["x"].shape
@@ -48,15 +48,14 @@ def check_layer(fff, name: str, L: dict, depth: int, trees: int, y_dtype: str, a
     got = run_fff(fff, L, depth, trees, y_dtype, act=act, **kw)
     ref = oracle.forward(L["x"], L["w_in"], L["w_out"], depth, trees, act=act)
     rep = parity.assert_parity(L["x"], L["w_in"], L["w_out"], depth, trees, ref, got["y"], got["nodes"],
-                               tol=tol, act=act)
+                               tol=tol, act=act, max_conditioned=max_conditioned)
     # logits recorded by the device agree with fp64 along its own path wherever paths agree
     same = (got["nodes"] == ref["nodes"])
     wmax = max(float(np.linalg.norm(parity.widen(L["w_in"][t]), axis=1).max()) for t in range(trees))
     scale = np.linalg.norm(parity.widen(L["x"]), axis=1)[:, None, None] * wmax
     lerr = np.abs(got["logits"] - ref["logits"]) / np.maximum(scale, 1e-30)
     assert np.all(lerr[same] < 1e-5), f"logit error {lerr[same].max():.2e}"
-    flush_print(f"[gpu] {name}: ok, max normwise err {rep['max_normwise_err']:.2e}, "
-                f"near-tie tokens {rep['n_near_tie']}, divergent {rep['n_path_divergent']}")
+    flush_print(f"[gpu] {name}: ok, {parity.summary(rep)}")
     return rep
 
 

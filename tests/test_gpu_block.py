@@ -49,20 +49,14 @@ def check_block(fff, name, x, wi, wo, depth, trees, y_dtype, *, norm, out, mode,
     u = ref["u"]
     nd = nodes.cpu().numpy()
     residual = out == "residual"
-    bf16_total = residual and y_dtype == "bf16"
-    tol = 1.0 if bf16_total else (2e-2 if y_dtype == "bf16" else 1e-5)
+    # a bf16 output that stores x + FFF(u) is judged on the stored total: normwise 2e-2 and, per
+    # element, one bf16 spacing of the fp64 total plus the fp32 bar on FFF(u)
+    tol = 2e-2 if y_dtype == "bf16" else 1e-5
     fff_only = {k: ref[k] for k in ("nodes", "logits", "near_tie")}
     fff_only["y"] = ref["fff"]
     rep = parity.assert_parity(u, wi, wo, depth, trees, fff_only, got, nd, tol=tol,
                                base_dev=x if residual else None)
-    if bf16_total:
-        # element-wise: within one bf16 spacing of the fp64 residual sum plus the FFF bar (tokens
-        # whose device path matches the oracle's)
-        same = (nd == ref["nodes"]).reshape(B, -1).all(axis=1)
-        ex = parity.bf16_total_excess(got[same], ref["y"][same], ref["fff"][same], 1e-5)
-        assert ex <= 1.0, f"bf16 residual output {ex:.2f}x past its bound"
-    flush_print(f"[gpu] {name}: ok, max normwise err {rep['max_normwise_err']:.2e}, divergent "
-                f"{rep['n_path_divergent']}")
+    flush_print(f"[gpu] {name}: ok, {parity.summary(rep)}")
     return got
 
 
@@ -243,11 +237,8 @@ def test_stack_layers_teacher_forced_against_oracle(fff_lib, xd, wd):
         fff_only = {k: ref[k] for k in ("nodes", "logits", "near_tie")}
         fff_only["y"] = ref["fff"]
         rep = parity.assert_parity(ref["u"], lay["w_in"], lay["w_out"], D, T, fff_only, got, nd,
-                                   tol=1.0 if xd == "bf16" else 1e-5, base_dev=cur)
-        if xd == "bf16":
-            same = (nd == ref["nodes"]).reshape(B, -1).all(axis=1)
-            assert parity.bf16_total_excess(got[same], ref["y"][same], ref["fff"][same], 1e-5) <= 1.0
-        flush_print(f"[gpu] layer {i}: ok, divergent {rep['n_path_divergent']}, err {rep['max_normwise_err']:.2e}")
+                                   tol=2e-2 if xd == "bf16" else 1e-5, base_dev=cur)
+        flush_print(f"[gpu] layer {i}: ok, {parity.summary(rep)}")
         cur = got
 
 

@@ -12,6 +12,7 @@ import oracle
 from oracle import parity
 from paper_2311_10770_amd import synth
 from paper_2311_10770_amd.configs import WORKLOADS
+from tests.conftest import flush_print
 from tests.gpu_util import DEV, TORCH_DT, check_layer, layer, run_fff, tol_for
 
 pytestmark = pytest.mark.gpu
@@ -93,8 +94,12 @@ def test_generic_hidden_sizes(fff_lib, H, wd):
 
 @pytest.mark.parametrize("depth,trees", [(0, 1), (0, 64), (1, 3), (11, 4), (14, 1), (2, 300)])
 def test_depth_and_tree_edges(fff_lib, depth, trees):
+    """Depth 0 with one tree is a single neuron, y = act(l) W_out[0]: a token whose logit nearly
+    cancels (|l| far below sum_i |x_i W_in[0, i]|) is ill-conditioned in the checker's sense and may
+    use its rounding allowance; everywhere else the raw 1e-5 bar holds."""
     L = layer(50 + depth, 300, 768, depth, trees, "f32", "f32")
-    check_layer(fff_lib, f"depth={depth} trees={trees}", L, depth, trees, "f32")
+    check_layer(fff_lib, f"depth={depth} trees={trees}", L, depth, trees, "f32",
+                max_conditioned=300 if (depth, trees) == (0, 1) else 0)
 
 
 @pytest.mark.parametrize("mode", ["descent", "generic", "grouped"])
@@ -191,22 +196,67 @@ def test_activation_variants_masked_and_subtree(fff_lib, act):
     check_layer(fff_lib, f"subtree {act}", L, 9, 2, "f32", act=act, mode="subtree")
 
 
-@pytest.mark.parametrize("H,mode", [(768, "descent"), (40, "generic"), (768, "subtree"), (768, "masked")])
-def test_small_integers_identity_bit_exact_with_ties(fff_lib, H, mode):
+@pytest.mark.parametrize("H,mode,T,wd", [(768, "descent", 2, "f32"), (40, "generic", 2, "f32"),
+                                         (768, "subtree", 2, "f32"), (768, "masked", 2, "f32"),
+                                         (768, "grouped", 2, "f32"), (768, "grouped", 1, "bf16"),
+                                         (768, "tiled", 1, "f32"), (768, "tiled", 1, "bf16")])
+def test_small_integers_identity_bit_exact_with_ties(fff_lib, H, mode, T, wd):
     """Identity activation on small integers: every value is an exact integer, so the device
-    must match the oracle bit for bit, including logits of exactly zero (they go left)."""
-    D, T, B = 6, 2, 300
+    must match the oracle bit for bit, including logits of exactly zero (they go left).  bf16
+    weights and x hold the same integers exactly; the leaf-tiled MFMA emit splits each integer
+    activation into bf16 parts that sum to it exactly."""
+    D, B = 6, 300
     L = synth.small_int_layer(9, B, H, D, T)
     for b in range(0, B, 5):  # exact zero at the root of tree 0
         w0 = L["w_in"][0, 0]
         i, j = np.nonzero(w0)[0][:2]
         L["x"][b] = 0
         L["x"][b, i], L["x"][b, j] = w0[j], -w0[i]
+    if wd == "bf16":
+        L = {k: synth.as_dtype(v, "bf16") for k, v in L.items()}
     got = run_fff(fff_lib, L, D, T, "f32", act="identity", mode=mode)
     ref = oracle.forward(L["x"], L["w_in"], L["w_out"], D, T, act="identity")
     assert np.array_equal(got["nodes"], ref["nodes"])
     assert np.array_equal(got["y"].astype(np.float64), ref["y"])
     assert np.all(got["nodes"][::5, 0, 1] == 1)
+
+
+def test_device_gelu_on_a_dense_grid(fff_lib):
+    """The device activation itself (P7): a depth-0 tree with W_in = W_out = e_0 and x[b, 0] = z_b
+    gives y[b] = act(z_b) e_0 exactly (the logit is z_b, the output a product by 1), so y[:, 0] is the
+    kernels' GELU on a grid of 36001 points in [-9, 9], compared with the fp64 GELU in units of the
+    fp32 unit roundoff u.  Exact form z/2 erfc(-z/sqrt 2): the argument is formed in fp32 (the
+    rounded constant and one product: relative error below 1.3 u), which erfc's condition number
+    (about z^2 + 1) magnifies; erfcf's own error is a few ulp (8 u) and the final product one more
+    rounding: bound (11 + 1.3 (z^2 + 1)) u.  Tanh form z / (1 + exp(-2v)), v = sqrt(2/pi)(z +
+    0.044715 z^3): v carries about 3 u of relative error, which exp magnifies by |2v|: bound
+    (11 + 6 |v|) u.  Between -3 and 3 both stay within a few ulp.  The other columns must be
+    exactly 0.  Both forms, through every mode with a depth-0 kernel."""
+    z = np.linspace(-9.0, 9.0, 36001).astype(np.float32)
+    H = 768
+    x = np.zeros((z.size, H), dtype=np.float32)
+    x[:, 0] = z
+    e0 = np.zeros((1, 1, H), dtype=np.float32)
+    e0[0, 0, 0] = 1.0
+    L = {"x": x, "w_in": e0, "w_out": e0.copy()}
+    zd = z.astype(np.float64)
+    for act in ("gelu", "gelu_tanh"):
+        want = parity.act_values(zd, act)
+        for mode in ("descent", "generic", "masked", "subtree"):
+            got = run_fff(fff_lib, L, 0, 1, "f32", act=act, mode=mode, record=False)["y"]
+            assert np.all(got[:, 1:] == 0.0), mode
+            err = np.abs(got[:, 0].astype(np.float64) - want)
+            if act == "gelu":
+                units = 11.0 + 1.3 * (zd * zd + 1.0)
+            else:
+                units = 11.0 + 6.0 * np.abs(np.sqrt(2.0 / np.pi) * (zd + 0.044715 * zd ** 3))
+            bound = units * 2.0 ** -24 * np.abs(want) + 1e-45
+            worst = int(np.argmax(err / bound))
+            assert np.all(err <= bound), f"{act} {mode}: z={zd[worst]} got {got[worst, 0]!r} want {want[worst]!r}"
+            mid = np.abs(zd) <= 3.0
+            ulps = float((err[mid] / (2.0 ** -23 * np.abs(want[mid]) + 1e-45)).max())
+            flush_print(f"[gpu] gelu grid {act} {mode}: max err/bound {float((err / bound).max()):.3f}, "
+                        f"max {ulps:.2f} ulp on [-3, 3]")
 
 
 def test_out_modes(fff_lib):
@@ -233,11 +283,28 @@ def test_plain_six_argument_entry_point(fff_lib):
 # ------------------------------------------------- determinism, streams, guards
 
 
-def test_deterministic(fff_lib):
-    L = layer(110, 20000, 768, 11, 1, "bf16", "bf16")
-    a = run_fff(fff_lib, L, 11, 1, "bf16")
-    b = run_fff(fff_lib, L, 11, 1, "bf16")
-    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
+@pytest.mark.parametrize("case", ["descent", "tiled_headline", "tiled_spills", "grouped"])
+def test_deterministic(fff_lib, case):
+    """Two runs give the same bits: the fused kernel, the leaf-tiled path at the headline size (its
+    bucket slots are taken by atomics in any order), the leaf-tiled path with clustered tokens that
+    overflow their buckets, and the grouped path."""
+    if case == "tiled_headline":
+        w = WORKLOADS["d11_h768_b65536_bf16"]
+        L = synth.make_layer(w.seed, w.n_tokens, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+        mode = "auto"
+        x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
+        assert fff_lib.describe(x, wi, wo, 11, 1).startswith("tiled<")
+    elif case == "tiled_spills":
+        x = synth.make_clustered_x(111, 20000, 768, "bf16", n_centres=8)
+        wi, wo = synth.make_weights(111, 768, 11, 1, "bf16")
+        L, mode = {"x": x, "w_in": wi, "w_out": wo}, "tiled"
+    else:
+        L, mode = layer(110, 20000, 768, 11, 1, "bf16", "bf16"), case
+    flush_print(f"[gpu] deterministic {case}")
+    runs = [run_fff(fff_lib, L, 11, 1, "bf16", mode=mode) for _ in range(3)]
+    for r in runs[1:]:
+        assert np.array_equal(runs[0]["y"], r["y"]) and np.array_equal(runs[0]["nodes"], r["nodes"])
+        assert np.array_equal(runs[0]["logits"], r["logits"])
 
 
 def test_non_default_stream(fff_lib):
@@ -253,9 +320,14 @@ def test_non_default_stream(fff_lib):
     parity.assert_parity(L["x"], L["w_in"], L["w_out"], 11, 1, ref, y.cpu().numpy(), None, tol=1e-5)
 
 
-@pytest.mark.parametrize("yd,mode", [("bf16", "descent"), ("f32", "descent"), ("f32", "generic")])
+@pytest.mark.parametrize("yd,mode", [("bf16", "descent"), ("f32", "descent"), ("f32", "generic"),
+                                     ("bf16", "tiled"), ("f32", "tiled"), ("bf16", "grouped"), ("f32", "grouped"),
+                                     ("bf16", "masked"), ("f32", "subtree")])
 def test_guard_bands_untouched(fff_lib, yd, mode):
-    B, H, D = 517, 768, 11
+    """No kernel writes outside y and the records: both are placed between bands of sentinels (the
+    masked mode at depth 5, the others at depth 11; 517 tokens, a ragged count)."""
+    B, H = 517, 768
+    D = 5 if mode == "masked" else 11
     L = layer(130, B, H, D, 1, "bf16", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
     pad = 4096
@@ -263,10 +335,13 @@ def test_guard_bands_untouched(fff_lib, yd, mode):
     y = buf[pad:pad + B * H].view(B, H)
     nbuf = torch.full((B * (D + 1) + 2 * pad,), -99, dtype=torch.int32, device=DEV)
     nodes = nbuf[pad:pad + B * (D + 1)]
-    fff_lib.forward(x, wi, wo, D, 1, y, nodes_out=nodes, mode=mode)
+    lbuf = torch.full((B * (D + 1) + 2 * pad,), 777.0, dtype=torch.float32, device=DEV)
+    logits = lbuf[pad:pad + B * (D + 1)]
+    fff_lib.forward(x, wi, wo, D, 1, y, nodes_out=nodes, logits_out=logits, mode=mode)
     torch.cuda.synchronize()
     assert torch.all(buf[:pad] == 12345.0) and torch.all(buf[-pad:] == 12345.0)
     assert torch.all(nbuf[:pad] == -99) and torch.all(nbuf[-pad:] == -99)
+    assert torch.all(lbuf[:pad] == 777.0) and torch.all(lbuf[-pad:] == 777.0)
     ref = oracle.forward(L["x"], L["w_in"], L["w_out"], D, 1)
     parity.assert_parity(L["x"], L["w_in"], L["w_out"], D, 1, ref, fff_lib.to_numpy(y), nodes.view(B, 1, D + 1)
                          .cpu().numpy(), tol=tol_for("bf16", yd))
@@ -372,18 +447,26 @@ def test_tiled_headline_full_size(fff_lib):
     check_layer(fff_lib, "tiled headline", L, w.depth, w.n_trees, w.y_dtype, mode="tiled")
 
 
-def test_tiled_with_layernorm(fff_lib):
-    L = layer(230, 5000, 768, 11, 1, "bf16", "bf16")
+@pytest.mark.parametrize("yd", ["f32", "bf16"])
+def test_tiled_with_layernorm(fff_lib, yd):
+    """The leaf-tiled path behind the LayerNorm prologue, with the residual: y = x + FFF(LN(x)),
+    against the oracle's block on the device's own paths."""
+    B = 5000
+    L = layer(230, B, 768, 11, 1, "bf16", "bf16")
     gamma, beta = synth.make_norm(230, 768)
     x = fff_lib.from_numpy(L["x"], DEV)
     wi, wo = fff_lib.from_numpy(L["w_in"], DEV), fff_lib.from_numpy(L["w_out"], DEV)
+    nodes = torch.empty((B, 1, 12), dtype=torch.int32, device=DEV)
     kw = dict(norm="layernorm", norm_eps=1e-5, norm_gamma=fff_lib.from_numpy(gamma, DEV),
-              norm_beta=fff_lib.from_numpy(beta, DEV), out="residual")
-    yt = fff_lib.forward(x, wi, wo, 11, 1, mode="tiled", y_dtype=torch.float32, **kw)
-    yg = fff_lib.forward(x, wi, wo, 11, 1, mode="grouped", y_dtype=torch.float32, **kw)
+              norm_beta=fff_lib.from_numpy(beta, DEV), out="residual", nodes_out=nodes)
+    assert fff_lib.describe(x, wi, wo, 11, 1, mode="tiled", **kw).startswith("tiled<")
+    y = fff_lib.forward(x, wi, wo, 11, 1, mode="tiled", y_dtype=TORCH_DT[yd], **kw)
     torch.cuda.synchronize()
-    err = ((yt - yg).norm(dim=1) / (yg - x.float()).norm(dim=1)).max().item()
-    assert err < 1e-5, err
+    ref = oracle.block(L["x"], L["w_in"], L["w_out"], 11, 1, norm={"gamma": gamma, "beta": beta, "eps": 1e-5})
+    fff_only = dict(ref, y=ref["fff"])
+    rep = parity.assert_parity(ref["u"], L["w_in"], L["w_out"], 11, 1, fff_only, fff_lib.to_numpy(y),
+                               nodes.cpu().numpy(), tol=tol_for("bf16", yd), base_dev=L["x"])
+    flush_print(f"[gpu] tiled + LayerNorm y={yd}: {parity.summary(rep)}")
 
 
 def test_tiled_unsupported_shapes(fff_lib):
@@ -512,14 +595,8 @@ def test_subtree_output_modes(fff_lib, out, xd, wd):
     got = run_fff(fff_lib, L, 9, 2, xd, mode="subtree", out=out, y_init=y0 if out == "accumulate" else None)
     ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 9, 2)
     base = L["x"] if out == "residual" else y0
-    bf16 = xd == "bf16"
     parity.assert_parity(L["x"], L["w_in"], L["w_out"], 9, 2, ref, got["y"], got["nodes"],
-                         tol=1.0 if bf16 else 1e-5, base_dev=base)
-    if bf16:
-        same = (got["nodes"] == ref["nodes"]).reshape(B, -1).all(axis=1)
-        total = parity.widen(base) + ref["y"]
-        ex = parity.bf16_total_excess(got["y"][same], total[same], ref["y"][same], 1e-5)
-        assert ex <= 1.0, f"bf16 {out} output {ex:.2f}x past its bound"
+                         tol=2e-2 if xd == "bf16" else 1e-5, base_dev=base)
 
 
 def test_subtree_auto_and_limits(fff_lib):
