@@ -191,6 +191,29 @@ typedef struct {
 
 int fff_forward_ex(const fff_args* a);
 
+/*
+ * fff_forward_static -- fff_forward_ex that allocates nothing, for callers that
+ * cannot allocate device memory during the call: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The scratch of the
+ * GROUPED and TILED plans is the library's own file-scope device array of
+ * FFF_STATIC_SCRATCH_BYTES (64 MiB; one per GPU, held until the process ends),
+ * looked up once per device; the call makes no hipMalloc, hipFree or other
+ * allocating call.  Rules beyond fff_forward_ex's:
+ *   - workspace must be NULL and workspace_bytes 0 (FFF_ERR_INVALID_ARG);
+ *   - MASKED is not available (FFF_ERR_UNSUPPORTED; AUTO never picks it here);
+ *   - AUTO picks GROUPED or TILED only when its scratch fits the array; an
+ *     explicit GROUPED or TILED whose scratch (fff_workspace_bytes for that
+ *     plan) exceeds FFF_STATIC_SCRATCH_BYTES returns FFF_ERR_WORKSPACE;
+ *   - every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (the kernels clear what must start at zero): calls that
+ *     overlap on one GPU -- concurrent streams or threads -- race and must be
+ *     serialised by the caller.
+ * At depth 11 (one tree) the tiled scratch fits up to 196608 tokens, three
+ * times the 65536-token batch.
+ */
+#define FFF_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int fff_forward_static(const fff_args* a);
+
 /* Device scratch bytes GROUPED, TILED and MASKED mode need for n_tokens
  * tokens: one fp32 activation per visited node and one int32 leaf per (token,
  * tree), plus for TILED the leaf buckets (int32 counts; token slots, a few

@@ -6,6 +6,6 @@ synthetic-input generators and the named workloads.
 """
 from .fff import (  # noqa: F401
     FffArgs, FffBackwardArgs, FffError, FffLayer, backward, backward_workspace_bytes, describe, describe_stack,
-    forward, forward_plain, forward_stack, from_numpy, load_library, make_args, status_str, to_numpy, version,
+    forward, forward_plain, forward_stack, forward_static, from_numpy, load_library, make_args, status_str, to_numpy, version,
     workspace_bytes,
 )

@@ -243,6 +243,36 @@ int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
     return FFF_OK;
 }
 
+// The entry point that allocates nothing: the plan's scratch is the library's
+// static device array.  No MASKED plan (its hipBLASLt handle allocates);
+// AUTO picks a scratch-using mode only when the array covers it.
+int forward_static(const fff_args* a) {
+    fff::Params p;
+    int rc = validate(a, &p);
+    if (rc != FFF_OK) return rc;
+    if (a->workspace || a->workspace_bytes) return FFF_ERR_INVALID_ARG;
+    if (a->n_tokens == 0) return FFF_OK;
+    fff::DeviceInfo dev;
+    rc = current_device_info(&dev);
+    if (rc != FFF_OK) return rc;
+    fff::Plan plan;
+    rc = fff::plan_forward(p, a->mode, a->lds_levels, a->split_level, fff::STATIC_SCRATCH_BYTES, dev, &plan, false);
+    if (rc != FFF_OK) return rc;
+    size_t need = 0;
+    if (plan.kind == fff::KIND_TILED) need = fff::tiled_workspace_bytes(a->n_tokens, a->depth, a->n_trees, a->hidden);
+    else if (plan.kind == fff::KIND_GROUPED) need = fff::grouped_workspace_bytes(a->n_tokens, a->depth, a->n_trees, 0);
+    if (need > fff::STATIC_SCRATCH_BYTES) return FFF_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if (need) {
+        const hipError_t e = fff::static_scratch(dev.device, &ws);
+        if (e != hipSuccess) return hip_fail(e);
+    }
+    const hipError_t e =
+        fff::run_forward(p, plan, ws, fff::STATIC_SCRATCH_BYTES, reinterpret_cast<hipStream_t>(a->hip_stream));
+    if (e != hipSuccess) return hip_fail(e);
+    return FFF_OK;
+}
+
 int forward_one(const fff_args* a) {
     fff::Params p;
     {
@@ -399,6 +429,8 @@ int validate_backward(const fff_backward_args* a, fff::BwdParams* p) {
 }  // namespace
 
 FFF_EXPORT int fff_forward_ex(const fff_args* a) { return forward_one(a); }
+
+FFF_EXPORT int fff_forward_static(const fff_args* a) { return forward_static(a); }
 
 FFF_EXPORT int fff_backward(const fff_backward_args* a) {
     fff::BwdParams p;

@@ -144,8 +144,16 @@ struct Plan {
 // workspace_bytes: size of the 256-byte aligned workspace the caller passed (0
 // if none); AUTO picks the grouped or tiled path only when it covers that
 // path's scratch.
+// masked_ok: whether MASKED may be planned (it creates a hipBLASLt handle on first use, so the
+// entry point that allocates nothing excludes it).
 int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
-                 const DeviceInfo& dev, Plan* plan);
+                 const DeviceInfo& dev, Plan* plan, bool masked_ok = true);
+
+// Scratch of the entry point that allocates nothing (fff_forward_static): a file-scope device
+// array of STATIC_SCRATCH_BYTES, one per GPU, held until the process ends.  Its device address
+// on `device` (the current device), looked up once per device.
+constexpr size_t STATIC_SCRATCH_BYTES = size_t(64) << 20;
+hipError_t static_scratch(int device, void** ptr);
 
 // Enqueues the planned work on stream; returns the first failing HIP error.
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,

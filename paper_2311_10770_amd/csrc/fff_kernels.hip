@@ -900,6 +900,34 @@ __global__ __launch_bounds__(GENERIC_BLOCK) void generic_kernel(Params p) {
 }
 
 // ----------------------------------------------------------------------------
+// the scratch of the entry point that allocates nothing
+// ----------------------------------------------------------------------------
+
+// One copy per GPU, zero at load and afterwards holding whatever the last call
+// left; the kernels clear what must start at zero (the bucket counts) on every
+// call.  In host code `scratch` names a host-side stand-in: only the address
+// from hipGetSymbolAddress may be handed to kernels.
+static __device__ __align__(256) unsigned char scratch[STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::once_flag g_scratch_once[kScratchDevices];
+void* g_scratch_ptr[kScratchDevices];
+hipError_t g_scratch_err[kScratchDevices];
+}  // namespace
+
+hipError_t static_scratch(int device, void** ptr) {
+    if (device < 0 || device >= kScratchDevices) return hipErrorInvalidDevice;
+    std::call_once(g_scratch_once[device], [&] {
+        void* p = nullptr;
+        g_scratch_err[device] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[device] = g_scratch_err[device] == hipSuccess ? p : nullptr;
+    });
+    *ptr = g_scratch_ptr[device];
+    return g_scratch_err[device];
+}
+
+// ----------------------------------------------------------------------------
 // planning
 // ----------------------------------------------------------------------------
 
@@ -1053,7 +1081,7 @@ static const Variant* find_variant(const Params& p) {
 static int64_t token_groups(const Params& p, int lanes) { return (p.n_tokens + 64 / lanes - 1) / (64 / lanes); }
 
 int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
-                 const DeviceInfo& dev, Plan* plan) {
+                 const DeviceInfo& dev, Plan* plan, bool masked_ok) {
     *plan = Plan{};
     const Variant* v = find_variant(p);
     if (mode == MODE_AUTO) {
@@ -1081,7 +1109,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         const bool one = p.n_trees == 1;
         if (subtree_auto(p))
             mode = MODE_SUBTREE;
-        else if (masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
+        else if (masked_ok && masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
                  (p.n_trees >= MASKED_AUTO_TREES ||
                   (p.n_trees >= MASKED_AUTO_TREES / 2 && p.n_tokens >= MASKED_AUTO_TOKENS)) &&
                  int64_t(workspace_bytes) >= masked_ws)
@@ -1110,7 +1138,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         return ST_OK;
     }
     if (mode == MODE_MASKED) {
-        if (!masked_shape(p)) return ST_UNSUPPORTED;
+        if (!masked_ok || !masked_shape(p)) return ST_UNSUPPORTED;
         plan->kind = KIND_MASKED;
         plan->name = !p.w_bf16 ? "fp32 GEMMs"
                      : p.y_bf16 ? "bf16 GEMMs, activations in 2 parts" : "bf16 GEMMs, activations in 3 parts";

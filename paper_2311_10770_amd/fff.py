@@ -68,7 +68,7 @@ class FffError(RuntimeError):
 
 _lib = None
 
-EXPORTS = ("fff_forward", "fff_forward_ex", "fff_workspace_bytes", "fff_describe", "fff_forward_stack",
+EXPORTS = ("fff_forward", "fff_forward_ex", "fff_forward_static", "fff_workspace_bytes", "fff_describe", "fff_forward_stack",
            "fff_describe_stack", "fff_backward", "fff_backward_workspace_bytes", "fff_status_str",
            "fff_last_hip_error", "fff_version")
 
@@ -87,6 +87,8 @@ def load_library(path: Path | str | None = None):
     lib.fff_forward.restype = c_int
     lib.fff_forward_ex.argtypes = [ctypes.POINTER(FffArgs)]
     lib.fff_forward_ex.restype = c_int
+    lib.fff_forward_static.argtypes = [ctypes.POINTER(FffArgs)]
+    lib.fff_forward_static.restype = c_int
     lib.fff_workspace_bytes.argtypes = [c_int64, c_int32, c_int32, c_int32, c_int32]
     lib.fff_workspace_bytes.restype = c_size_t
     lib.fff_describe.argtypes = [ctypes.POINTER(FffArgs), c_char_p, c_size_t]
@@ -238,6 +240,22 @@ def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=Non
     lib = load_library()
     with torch.cuda.device(x.device):
         _check(lib.fff_forward_ex(ctypes.byref(a)))
+    return y
+
+
+STATIC_SCRATCH_BYTES = 64 << 20  # FFF_STATIC_SCRATCH_BYTES
+
+
+def forward_static(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=None, **kw):
+    """FFF forward through ``fff_forward_static``: the library's own scratch, nothing allocated by
+    the call (y is allocated here if not given).  No ``workspace`` argument; MASKED unavailable."""
+    if "workspace" in kw:
+        raise ValueError("fff_forward_static takes no workspace")
+    if y is None:
+        y = torch.empty(x.shape, dtype=y_dtype or x.dtype, device=x.device)
+    a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
+    with torch.cuda.device(x.device):
+        _check(load_library().fff_forward_static(ctypes.byref(a)))
     return y
 
 
