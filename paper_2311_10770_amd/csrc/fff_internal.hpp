@@ -27,18 +27,22 @@ struct Params {
     int32_t act;
     int32_t out_mode;
     int32_t lds_levels;   // levels staged in LDS
+    int32_t walk_affine;  // walk kernel: each workgroup walks one tree, chosen by its XCD (T divides 8)
     // grouped mode: views into the caller's workspace
     float* ws_act;        // [B, T, D+1] activation of every visited node
     int32_t* ws_leaf;     // [B, T] leaf reached in each tree
     int32_t split_level;  // group tokens by their tree-0 node at this level; 0 = keep token order
-    // tiled mode: tokens bucketed by their tree-0 leaf during the walk
-    int32_t* bk_count;    // [2^D] tokens that reached each leaf
-    int32_t* bk_tok;      // [2^D, bk_cap] the first bk_cap of them, in arrival order
-    int32_t* bk_spill;    // [B] tokens that found their bucket full
-    int32_t* bk_nspill;   // [1] how many
-    float* bk_act;        // [2^D, bk_cap, TILE_REC] activations of the bucketed tokens, by slot
+    // tiled mode: tokens bucketed by their leaf in every tree during the walk
+    int32_t* bk_count;    // [T, 2^D] tokens that reached each leaf
+    int32_t* bk_tok;      // [T, 2^D, bk_cap] the first bk_cap of them, in arrival order
+    int32_t* bk_spill;    // [T, B] tokens that found their bucket full
+    int32_t* bk_nspill;   // [T] how many
+    float* bk_act;        // [T, 2^D, bk_cap, TILE_REC] activations of the bucketed tokens, by slot
     void* bk_junk;        // target of the stores of empty tile rows
     int32_t bk_cap;
+    int32_t tile_tree;    // the tree a tile launch accumulates
+    const void* tile_src; // [B, H] row the tile launch adds its result to (or null)
+    void* tile_dst;       // [B, H] row it writes
     // LayerNorm prologue (norm = 1): u = (x - mean) / sqrt(var + eps) * gamma + beta
     int32_t norm;
     float norm_eps;
@@ -130,13 +134,14 @@ struct Launch {
 
 struct Plan {
     int kind = KIND_NONE;
-    Launch launch[3];              // descent/generic: [0]; grouped: walk, scatter (optional), emit
+    Launch launch[3];              // descent/generic: [0]; grouped: walk, emit; tiled: fill, walk, tiles (one per tree)
     int n_launch = 0;
     int lanes = 0;                 // lanes per token
     int emit_lanes = 0;            // lanes per token of the grouped emit
     int lds_levels = 0;            // descent, generic, grouped walk
     int emit_lds_levels = 0;       // grouped emit
     int split_level = 0;           // grouped mode
+    int walk_affine = 0;           // grouped / tiled: one tree per walk workgroup, by XCD
     const char* name = "";
 };
 

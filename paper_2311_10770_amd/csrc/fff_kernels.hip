@@ -177,28 +177,37 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
     const int T = p.n_trees, D = p.depth, K = p.lds_levels;
     const int64_t N = p.n_nodes;
     const int Nk = (1 << K) - 1;
+    // Tree-affine walk (T divides the XCD count): the workgroups of XCD x walk tree x mod T for
+    // all tokens, so each XCD's L2 holds one tree's rows and LDS that tree's top levels; x is
+    // read once per tree.  Otherwise every workgroup walks all trees of its tokens.
+    const bool affine = p.walk_affine;
+    const int t_first = affine ? int(blockIdx.x % XCDS) % T : 0;
+    const int t_end = affine ? t_first + 1 : T;
+    const int64_t n_blk = affine ? int64_t(gridDim.x) / T : int64_t(gridDim.x);
+    const int64_t blk = affine ? int64_t(blockIdx.x / XCDS) * (XCDS / T) + (blockIdx.x % XCDS) / T : int64_t(blockIdx.x);
     if (K > 0) {
-        stage_rows<S::ROWV, BLOCK>(lds_in, p.w_in, T, N, Nk, S::ROWV, 0);
+        const void* src = static_cast<const char*>(p.w_in) + int64_t(t_first) * N * S::ROWV * 16;
+        stage_rows<S::ROWV, BLOCK>(lds_in, src, t_end - t_first, N, Nk, S::ROWV, 0);
         __syncthreads();
     }
     const int KD = K < D + 1 ? K : D + 1;
     const int64_t n_groups = (p.n_tokens + S::TPW - 1) / S::TPW;
-    for (int64_t g = int64_t(blockIdx.x) * WAVES + wave; g < n_groups; g += int64_t(gridDim.x) * WAVES) {
+    for (int64_t g = blk * WAVES + wave; g < n_groups; g += n_blk * WAVES) {
         const int64_t slot_raw = g * S::TPW + sub;
         const bool valid = slot_raw < p.n_tokens;
         const int64_t tok = valid ? slot_raw : p.n_tokens - 1;
         XIn<LANES, NV, XBF, WBF, NORM> xr;
         load_input<LANES, NV, XBF, WBF, NORM>(xr, p, tok, sl);
-        for (int t = 0; t < T; ++t) {
+        for (int t = t_first; t < t_end; ++t) {
             const uint4* win = reinterpret_cast<const uint4*>(p.w_in) + int64_t(t) * N * S::ROWV + sl;
-            const uint4* lrows = lds_in + int64_t(t) * Nk * S::ROWV + sl;
+            const uint4* lrows = lds_in + int64_t(t - t_first) * Nk * S::ROWV + sl;
             LevelRegs<LANES> lv;
             const uint32_t leaf1 = walk_tree<LANES, NV, XR_BF, WBF>(xr, lrows, S::ROWV, win, KD, D, sl, lv);
             float* rec = p.ws_act + (tok * T + t) * (D + 1);
-            if (p.bk_count && t == 0) {
-                // tiled mode: take the next slot of this leaf's bucket; the activations
-                // go to the slot, or to the token's record once the bucket is full
-                const int64_t bin = int64_t(leaf1) - (int64_t(1) << D);
+            if (p.bk_count) {
+                // tiled mode: take the next slot of the bucket of this tree's leaf; the
+                // activations go to the slot, or to the token's record once the bucket is full
+                const int64_t bin = int64_t(t) * (int64_t(1) << D) + int64_t(leaf1) - (int64_t(1) << D);
                 int32_t pos = 0;
                 if (valid && sl == 0) pos = atomicAdd(&p.bk_count[bin], 1);
                 pos = __float_as_int(group_bcast<LANES>(__int_as_float(pos), lane, 0));
@@ -206,7 +215,7 @@ __global__ __launch_bounds__(BLOCK) void walk_kernel(Params p) {
                     rec = p.bk_act + (bin * p.bk_cap + pos) * TILE_REC;
                     if (sl == 0) p.bk_tok[bin * p.bk_cap + pos] = int32_t(tok);
                 } else if (valid && sl == 0) {
-                    p.bk_spill[atomicAdd(p.bk_nspill, 1)] = int32_t(tok);
+                    p.bk_spill[int64_t(t) * p.n_tokens + atomicAdd(&p.bk_nspill[t], 1)] = int32_t(tok);
                 }
             }
             if (valid) {
@@ -413,60 +422,80 @@ __device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out
     }
 }
 
-// Output forms of the tile kernel: any (out mode and y type read at run time),
-// a plain store of bf16 / fp32 y, or the residual y = x + FFF with y of x's
-// type, fixed at compile time.  With the form fixed, every path through a tile
-// issues the same memory operations, so the compiler can wait for the
-// prefetched operands without draining the stores.
-enum { TILE_Y_ANY = 0, TILE_Y_STORE_BF16 = 1, TILE_Y_STORE_F32 = 2, TILE_Y_RESIDUAL = 3 };
+// Output forms of the tile kernel, fixed at compile time: the tile's result is
+// added to a source row (none; fp32; bf16) and written to a destination row
+// (fp32 or bf16).  One tree: the source is x (residual), y (accumulate) or
+// none, the destination y.  Several trees: the trees' tile launches run in tree
+// order, tree t adding its contribution to the running sum S left by tree t-1
+// (S is y itself when y is fp32, else an fp32 workspace), the last writing y,
+// so the sum over trees has a fixed order.  With the form fixed, every path
+// through a tile issues the same memory operations, so the compiler can wait
+// for the prefetched operands without draining the stores.
+enum { TSRC_NONE = 0, TSRC_F32 = 1, TSRC_BF16 = 2 };
 
 // Bytes of the junk area that stores of empty tile rows are sent to: one
 // 32-byte slot per lane of 128 wave slots.
 constexpr size_t TILE_JUNK_BYTES = 128 * 64 * 32;
 
-// Eight consecutive output columns of one token: combine (residual / accumulate)
-// and store.  xs / yd point at the eight elements of x and y (or at junk).
-template <int YM, bool XBF>
-__device__ __forceinline__ void tile_store8(const Params& p, const void* xs, void* yd, const float* v8) {
-    const int om = YM == TILE_Y_ANY ? p.out_mode : YM == TILE_Y_RESIDUAL ? OUT_RESIDUAL : OUT_STORE;
-    const bool ybf = YM == TILE_Y_ANY ? bool(p.y_bf16) : YM == TILE_Y_RESIDUAL ? XBF : YM == TILE_Y_STORE_BF16;
+// Eight consecutive output columns of one token: add the source and store.
+// src / dst point at the eight elements (or at junk).
+template <int SRC, bool DBF>
+__device__ __forceinline__ void tile_store8(const void* src, void* dst, const float* v8) {
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = v8[i];
-    if (om == OUT_RESIDUAL) {
-        float xv[8];
-        tile_load8<XBF>(xs, 0, xv);
+    if constexpr (SRC != TSRC_NONE) {
+        float b[8];
+        tile_load8<SRC == TSRC_BF16>(src, 0, b);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += xv[i];
+        for (int i = 0; i < 8; ++i) v[i] += b[i];
     }
-    if (ybf) {
-        uint4* d = reinterpret_cast<uint4*>(yd);
-        if (om == OUT_ACCUMULATE) {
-            const uint4 o = *d;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                v[2 * j] += bf16_lo(word(o, j));
-                v[2 * j + 1] += bf16_hi(word(o, j));
-            }
-        }
-        *d = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
-                        pack_bf16x2(v[6], v[7]));
+    if constexpr (DBF) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                    pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
     } else {
-        float4* d = reinterpret_cast<float4*>(yd);
-        if (om == OUT_ACCUMULATE) {
-            const float4 a = d[0], b = d[1];
-            v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
-            v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
-        }
+        float4* d = reinterpret_cast<float4*>(dst);
         d[0] = make_float4(v[0], v[1], v[2], v[3]);
         d[1] = make_float4(v[4], v[5], v[6], v[7]);
     }
 }
 
-// Grid: one workgroup per leaf (XCD-affine by the subtree at the split level),
-// then spill workgroups.  ELANES/ENV: the per-token emit layout for spilled
-// tokens; YM: the output form.
-template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int YM>
+// Final combine and store of one token's output slice in the per-token emit
+// layout (LANES lanes, NV vectors of EV elements): acc + source row, written to
+// the destination row.
+template <int LANES, int NV, bool WBF, int SRC, bool DBF>
+__device__ __forceinline__ void store_token_sd(const void* src, void* dst, float* acc, int64_t tok, int sl) {
+    constexpr int EV = WBF ? 8 : 4;
+    constexpr int H = LANES * NV * EV;
+#pragma unroll
+    for (int c = 0; c < NV; ++c) {
+        const int64_t e = tok * H + int64_t(c * LANES + sl) * EV;
+#pragma unroll
+        for (int q = 0; q < EV / 4; ++q) {
+            float v[4] = {acc[c * EV + 4 * q], acc[c * EV + 4 * q + 1], acc[c * EV + 4 * q + 2],
+                          acc[c * EV + 4 * q + 3]};
+            if constexpr (SRC == TSRC_F32) {
+                const float4 b = *reinterpret_cast<const float4*>(static_cast<const float*>(src) + e + 4 * q);
+                v[0] += b.x; v[1] += b.y; v[2] += b.z; v[3] += b.w;
+            } else if constexpr (SRC == TSRC_BF16) {
+                const uint2 b = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(src) + e + 4 * q);
+                v[0] += bf16_lo(b.x); v[1] += bf16_hi(b.x); v[2] += bf16_lo(b.y); v[3] += bf16_hi(b.y);
+            }
+            if constexpr (DBF)
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(dst) + e + 4 * q) =
+                    make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+            else
+                *reinterpret_cast<float4*>(static_cast<float*>(dst) + e + 4 * q) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+    }
+}
+
+// Tree p.tile_tree of the layer: grid of one workgroup per leaf (XCD-affine by
+// the subtree at the split level), then spill workgroups.  ELANES/ENV: the
+// per-token emit layout for tokens of overflowing leaves; SRC/DBF: the output
+// form (p.tile_src, p.tile_dst); P2: two bf16 parts of each activation (the
+// layer's output is bf16) instead of three.
+template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2>
 __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
     constexpr int H = 16 * CB;
     static_assert(H % 128 == 0, "128-column groups");
@@ -474,8 +503,10 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     constexpr int WAVES = tile_waves(H);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int D = p.depth;
+    const int D = p.depth, T = p.n_trees, tree = p.tile_tree;
     const int64_t L = int64_t(1) << D;
+    const int64_t N = p.n_nodes;
+    const void* const w_out = static_cast<const char*>(p.w_out) + int64_t(tree) * N * H * (WBF ? 2 : 4);
 
     // The per-token emit (all levels from global memory) of `count` tokens: token i is tok_of(i),
     // its activations at rec_of(i); groups g = first, first + stride, ... of this wave.
@@ -488,9 +519,9 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             const bool valid = idx_raw < count;
             const int64_t idx = valid ? idx_raw : count - 1;
             const int64_t tok = tok_of(idx);
-            const uint32_t leaf1 = uint32_t(p.ws_leaf[tok]) + 1;
+            const uint32_t leaf1 = uint32_t(p.ws_leaf[tok * T + tree]) + 1;
             const float* arec = rec_of(idx);
-            const uint4* wout = reinterpret_cast<const uint4*>(p.w_out) + sl;
+            const uint4* wout = reinterpret_cast<const uint4*>(w_out) + sl;
             float acc[S::E];
 #pragma unroll
             for (int e = 0; e < S::E; ++e) acc[e] = 0.0f;
@@ -498,17 +529,16 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
                 acc, 0, D, [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
                 [&](int l) { return wout + int64_t((leaf1 >> (D - l)) - 1) * S::ROWV; },
                 [&](int l) { return arec[l]; });
-            XRegs<ELANES, ENV, XBF, WBF> xr;
-            if (p.out_mode == OUT_RESIDUAL) xr.load(p.x, tok, sl);
-            if (valid) store_output<ELANES, ENV, WBF>(p, xr, acc, tok, sl);
+            if (valid) store_token_sd<ELANES, ENV, WBF, SRC, DBF>(p.tile_src, p.tile_dst, acc, tok, sl);
         }
     };
 
     if (int(blockIdx.x) >= leaf_blocks) {
         // spilled tokens (their leaf overflowed): the per-token emit from their own records
-        emit_per_token(int64_t(*p.bk_nspill), int64_t(blockIdx.x - leaf_blocks) * WAVES + wave,
-                       int64_t(gridDim.x - leaf_blocks) * WAVES, [&](int64_t i) { return int64_t(p.bk_spill[i]); },
-                       [&](int64_t i) { return p.ws_act + int64_t(p.bk_spill[i]) * (D + 1); });
+        const int32_t* spill = p.bk_spill + int64_t(tree) * p.n_tokens;
+        emit_per_token(int64_t(p.bk_nspill[tree]), int64_t(blockIdx.x - leaf_blocks) * WAVES + wave,
+                       int64_t(gridDim.x - leaf_blocks) * WAVES, [&](int64_t i) { return int64_t(spill[i]); },
+                       [&](int64_t i) { return p.ws_act + (int64_t(spill[i]) * T + tree) * (D + 1); });
         return;
     }
 
@@ -519,11 +549,12 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
         const int64_t x = blockIdx.x % XCDS, lb = blockIdx.x / XCDS;
         leaf = (x + XCDS * (lb / per)) * per + lb % per;
     }
-    const int32_t cnt_all = p.bk_count[leaf];
+    const int64_t bin = int64_t(tree) * L + leaf;
+    const int32_t cnt_all = p.bk_count[bin];
     if (cnt_all == 0) return;  // workgroup-uniform
     const int cap = p.bk_cap;
-    const int32_t* bucket = p.bk_tok + leaf * cap;
-    const float* act = p.bk_act + leaf * int64_t(cap) * TILE_REC;
+    const int32_t* bucket = p.bk_tok + bin * cap;
+    const float* act = p.bk_act + bin * int64_t(cap) * TILE_REC;
     if (cnt_all > cap) {
         // An overflowing leaf: which of its tokens found a slot depends on the order of the walk's
         // atomics, so all of them take the per-token emit (these from their slots, the rest in the
@@ -535,11 +566,8 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     const int cnt = cnt_all;
     const uint32_t leaf1 = uint32_t(leaf + L);
     const int n = lane & 15, kq = lane >> 4;
-    constexpr int XSZ = XBF ? 2 : 4;
-    const int ysz = YM == TILE_Y_ANY         ? (p.y_bf16 ? 2 : 4)
-                    : YM == TILE_Y_RESIDUAL  ? (XBF ? 2 : 4)
-                    : YM == TILE_Y_STORE_BF16 ? 2
-                                              : 4;
+    constexpr int SSZ = SRC == TSRC_BF16 ? 2 : 4;
+    constexpr int DSZ = DBF ? 2 : 4;
     char* const junk = reinterpret_cast<char*>(p.bk_junk) + ((int64_t(blockIdx.x) * WAVES + wave) % 128 * 64 + lane) * 32;
     // Every load below is in bounds and unconditional (slots and levels are
     // clamped; values past the count or past D are replaced by 0 where used), so
@@ -552,17 +580,17 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
         for (int r = 0; r < 4; ++r) {
             const int32_t tok = __shfl(tok_a, 4 * kq + r, 64);
             const int64_t e = int64_t(tok) * H + col;
-            void* yd = tok >= 0 ? reinterpret_cast<char*>(p.y) + e * ysz : junk;
-            const void* xs = tok >= 0 ? reinterpret_cast<const char*>(p.x) + e * XSZ : junk;
+            void* yd = tok >= 0 ? static_cast<char*>(p.tile_dst) + e * DSZ : junk;
+            const void* xs = tok >= 0 && SRC != TSRC_NONE ? static_cast<const char*>(p.tile_src) + e * SSZ : junk;
             float v8[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
-            tile_store8<YM, XBF>(p, xs, yd, v8);
+            tile_store8<SRC, DBF>(xs, yd, v8);
         }
     };
 
     if constexpr (WBF) {
-        constexpr int PARTS = YM == TILE_Y_STORE_BF16 || (YM == TILE_Y_RESIDUAL && XBF) ? 2 : 3;
+        constexpr int PARTS = P2 ? 2 : 3;
         const int h = kq & 1, part = kq >> 1;
         struct Raw {
             int32_t tok;
@@ -585,7 +613,7 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     const int lvl = 8 * h + i <= D ? 8 * h + i : D;
-                    row[i] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w_out) +
+                    row[i] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(w_out) +
                                                              (int64_t(leaf1 >> (D - lvl)) - 1) * H + col);
                 }
 #pragma unroll
@@ -675,8 +703,8 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 #pragma unroll
             for (int s = 0; s < TILE_MAX_STEPS; ++s) {
                 const int64_t at = (int64_t(leaf1 >> (D - lvl_c[s])) - 1) * H + col;
-                w[s][0] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at);
-                w[s][1] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.w_out) + at + 4);
+                w[s][0] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at);
+                w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + 4);
             }
             auto tile = [&](int t0, const Raw& cur) {
                 const bool in = t0 + n < cnt;
@@ -946,7 +974,7 @@ struct Variant {
     const void* descent;
     const void* walk;
     const void* emit;
-    const void* tile[4];  // indexed by TILE_Y_*
+    const void* tile[3][3];  // [source TSRC_*][form: fp32 dst 3 parts, fp32 dst 2 parts, bf16 dst 2 parts]
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -956,14 +984,16 @@ struct Variant {
 };
 
 #define FFF_K(...) reinterpret_cast<const void*>(&__VA_ARGS__)
+#define FFF_TILES(H, XB, WB, EL, ENV, SRC)                                                                    \
+    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false>),                                       \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true>),                                        \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true>)}
 #define FFF_VARIANT(H, XB, WB, L, NV, EL, ENV)                                                                \
     Variant {                                                                                                 \
         H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
             FFF_K(walk_kernel<L, NV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
-            {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_ANY>),                                         \
-             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_BF16>),                                  \
-             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_STORE_F32>),                                   \
-             FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, TILE_Y_RESIDUAL>)},                                   \
+            {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE), FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32),                \
+             FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16)},                                                       \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<L, NV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -1048,9 +1078,11 @@ size_t grouped_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees,
     return align256(recs * size_t(depth + 1) * sizeof(float)) + align256(recs * sizeof(int32_t));
 }
 
-// Tiled mode: one tree, depth 5..15 (records of TILE_REC levels), hidden a multiple of 128.
+// Tiled mode: up to TILE_MAX_TREES trees, depth 5..15 (records of TILE_REC levels), hidden a
+// multiple of 128.
+constexpr int TILE_MAX_TREES = 16;
 static bool tiled_shape(int32_t depth, int32_t n_trees, int32_t hidden) {
-    return n_trees == 1 && depth >= 5 && depth < TILE_REC && hidden % 128 == 0;
+    return n_trees >= 1 && n_trees <= TILE_MAX_TREES && depth >= 5 && depth < TILE_REC && hidden % 128 == 0;
 }
 
 // Bucket capacity: four times the mean tokens per leaf, at least one tile of 16, a multiple of 16.
@@ -1061,15 +1093,18 @@ static int32_t tile_cap(int64_t n_tokens, int32_t depth) {
 }
 
 // Tiled workspace, in order: token records and leaves (as grouped; the records
-// are used by spilled tokens only), bucket counts + spill count, bucket token
-// ids, spill list, bucket activation records, junk area for empty tile rows.
+// are used by spilled tokens only), bucket counts + spill counts, bucket token
+// ids, spill lists, bucket activation records, the junk area for empty tile
+// rows, and with several trees an fp32 [B, H] running sum (used when y is bf16).
 size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
     if (!tiled_shape(depth, n_trees, hidden)) return 0;
+    const size_t T = size_t(n_trees);
     const size_t leaves = size_t(1) << depth;
     const size_t cap = size_t(tile_cap(n_tokens, depth));
-    return grouped_workspace_bytes(n_tokens, depth, n_trees, 0) + align256((leaves + 1) * sizeof(int32_t)) +
-           align256(leaves * cap * sizeof(int32_t)) + align256(size_t(n_tokens) * sizeof(int32_t)) +
-           align256(leaves * cap * size_t(TILE_REC) * sizeof(float)) + TILE_JUNK_BYTES;
+    return grouped_workspace_bytes(n_tokens, depth, n_trees, 0) + align256(T * (leaves + 1) * sizeof(int32_t)) +
+           align256(T * leaves * cap * sizeof(int32_t)) + align256(T * size_t(n_tokens) * sizeof(int32_t)) +
+           align256(T * leaves * cap * size_t(TILE_REC) * sizeof(float)) + TILE_JUNK_BYTES +
+           (T > 1 ? align256(size_t(n_tokens) * size_t(hidden) * sizeof(float)) : 0);
 }
 
 static const Variant* find_variant(const Params& p) {
@@ -1079,6 +1114,47 @@ static const Variant* find_variant(const Params& p) {
 }
 
 static int64_t token_groups(const Params& p, int lanes) { return (p.n_tokens + 64 / lanes - 1) / (64 / lanes); }
+
+// What the layer adds its result to (see TSRC_*): x (residual), y (accumulate) or nothing.
+static int out_src_kind(const Params& p) {
+    if (p.out_mode == OUT_RESIDUAL) return p.x_bf16 ? TSRC_BF16 : TSRC_F32;
+    if (p.out_mode == OUT_ACCUMULATE) return p.y_bf16 ? TSRC_BF16 : TSRC_F32;
+    return TSRC_NONE;
+}
+
+// Output form of tree t's tile launch: the first tree adds the layer's source; later trees add
+// the fp32 running sum; the last writes y, the others the running sum (fp32).  Two activation
+// parts when the layer's output is bf16.
+static int tile_src_kind(const Params& p, int t) { return t > 0 ? int(TSRC_F32) : out_src_kind(p); }
+
+static const void* tile_kernel_for(const Variant& v, const Params& p, int t) {
+    const bool last = t == p.n_trees - 1;
+    const int form = last && p.y_bf16 ? 2 : p.y_bf16 ? 1 : 0;
+    return v.tile[tile_src_kind(p, t)][form];
+}
+
+// The walk launch of the grouped and tiled plans: with 2, 4 or 8 trees one tree per workgroup
+// (by XCD), whose top levels then get the whole LDS budget; otherwise every tree per token.
+static bool plan_walk(const Params& p, const Variant& v, int lds_levels_req, const DeviceInfo& dev, Plan* plan,
+                      Launch& W) {
+    const bool affine = p.n_trees > 1 && XCDS % p.n_trees == 0;
+    Params one = p;
+    if (affine) one.n_trees = 1;
+    bool ok;
+    const int kw = pick_levels(one, lds_levels_req, 1, WALK_LDS_BUDGET, dev.lds_per_block, &ok);
+    if (!ok) return false;
+    plan->lds_levels = kw;
+    plan->walk_affine = affine;
+    W.kernel = p.norm ? v.walk_norm : v.walk;
+    W.block = WALK_BLOCK;
+    W.lds_bytes = rows_lds_bytes(one, kw, 1);
+    const int64_t groups = token_groups(p, v.lanes) * (affine ? p.n_trees : 1);
+    int64_t want = (groups + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64);
+    if (affine) want = (want + XCDS - 1) / XCDS * XCDS;
+    W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want, WALK_BLOCK);
+    if (affine) W.grid = std::max(XCDS, W.grid / XCDS * XCDS);  // every tree gets the same XCDs' worth
+    return true;
+}
 
 int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
                  const DeviceInfo& dev, Plan* plan, bool masked_ok) {
@@ -1147,33 +1223,22 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     if ((mode == MODE_DESCENT || mode == MODE_GROUPED || mode == MODE_TILED) && !v) return ST_UNSUPPORTED;
     if (mode == MODE_TILED) {
         if (!tiled_shape(p.depth, p.n_trees, p.hidden)) return ST_UNSUPPORTED;
-        bool ok;
-        const int kw = pick_levels(p, lds_levels_req, 1, WALK_LDS_BUDGET, dev.lds_per_block, &ok);
-        if (!ok) return ST_UNSUPPORTED;
         plan->kind = KIND_TILED;
         plan->lanes = v->lanes;
         plan->emit_lanes = v->emit_lanes;
-        plan->lds_levels = kw;
         plan->split_level = std::min<int>(p.depth - 2, 5);  // subtrees of at least four leaves
         plan->name = v->name;
         const int64_t leaves = int64_t(1) << p.depth;
         Launch& F = plan->launch[plan->n_launch++];
         F.kernel = reinterpret_cast<const void*>(&fill_i32_kernel);
         F.block = 256;
-        F.grid = int(std::min<int64_t>((leaves + 1 + 255) / 256, int64_t(dev.cu_count) * 4));
+        F.grid = int(std::min<int64_t>((p.n_trees * (leaves + 1) + 255) / 256, int64_t(dev.cu_count) * 4));
         Launch& W = plan->launch[plan->n_launch++];
-        W.kernel = p.norm ? v->walk_norm : v->walk;
-        W.block = WALK_BLOCK;
-        W.lds_bytes = rows_lds_bytes(p, kw, 1);
-        W.grid = resident_grid(dev, W.kernel, W.lds_bytes,
-                               (token_groups(p, v->lanes) + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64), WALK_BLOCK);
+        if (!plan_walk(p, *v, lds_levels_req, dev, plan, W)) return ST_UNSUPPORTED;
         Launch& E = plan->launch[plan->n_launch++];
-        int form = TILE_Y_ANY;
-        if (p.out_mode == OUT_STORE) form = p.y_bf16 ? TILE_Y_STORE_BF16 : TILE_Y_STORE_F32;
-        else if (p.out_mode == OUT_RESIDUAL && p.y_bf16 == p.x_bf16) form = TILE_Y_RESIDUAL;
-        E.kernel = v->tile[form];
+        E.kernel = tile_kernel_for(*v, p, 0);  // the first tree's; run_forward picks each tree's form
         E.block = 64 * tile_waves(p.hidden);
-        // one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
+        // per tree: one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
         E.grid = int(leaves) + dev.cu_count;
         return ST_OK;
     }
@@ -1199,22 +1264,15 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         int split = split_level_req == 0 ? default_split_level(p.depth, p.n_trees) : split_level_req;
         if (split < 0) split = 0;
         if (split != 0 && (split < 3 || split > p.depth)) return ST_UNSUPPORTED;  // at least one subtree per XCD
-        bool ok_w, ok_e;
-        const int kw = pick_levels(p, lds_levels_req, 1, WALK_LDS_BUDGET, dev.lds_per_block, &ok_w);
+        bool ok_e;
         const int ke = pick_levels(p, lds_levels_req, 1, EMIT_LDS_BUDGET, dev.lds_per_block, &ok_e);
-        if (!ok_w || !ok_e) return ST_UNSUPPORTED;
+        if (!ok_e) return ST_UNSUPPORTED;
         plan->kind = KIND_GROUPED;
         plan->lanes = v->lanes;
-        plan->lds_levels = kw;
         plan->split_level = split;
         plan->name = v->name;
-        const int64_t groups = token_groups(p, v->lanes);
-        const int64_t want = (groups + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64);
         Launch& W = plan->launch[plan->n_launch++];
-        W.kernel = p.norm ? v->walk_norm : v->walk;
-        W.block = WALK_BLOCK;
-        W.lds_bytes = rows_lds_bytes(p, kw, 1);
-        W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want, WALK_BLOCK);
+        if (!plan_walk(p, *v, lds_levels_req, dev, plan, W)) return ST_UNSUPPORTED;
         Launch& E = plan->launch[plan->n_launch++];
         E.kernel = v->emit;
         E.block = BLOCK;
@@ -1274,6 +1332,7 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
     if (plan.kind == KIND_SUBTREE) return run_subtree(p, plan.launch[0].grid, stream);
     Params q = p;
     q.lds_levels = plan.lds_levels;
+    q.walk_affine = plan.walk_affine;
     if (plan.kind == KIND_GROUPED) {
         const size_t recs = size_t(p.n_tokens) * size_t(p.n_trees);
         char* ws = static_cast<char*>(workspace);
@@ -1283,7 +1342,8 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         (void)workspace_bytes;
     }
     if (plan.kind == KIND_TILED) {
-        const size_t recs = size_t(p.n_tokens);
+        const size_t T = size_t(p.n_trees);
+        const size_t recs = size_t(p.n_tokens) * T;
         const int64_t leaves = int64_t(1) << p.depth;
         char* ws = static_cast<char*>(workspace);
         q.ws_act = reinterpret_cast<float*>(ws);
@@ -1291,20 +1351,22 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         q.ws_leaf = reinterpret_cast<int32_t*>(ws);
         ws += align256(recs * sizeof(int32_t));
         q.bk_count = reinterpret_cast<int32_t*>(ws);
-        q.bk_nspill = q.bk_count + leaves;
-        ws += align256((size_t(leaves) + 1) * sizeof(int32_t));
+        q.bk_nspill = q.bk_count + T * leaves;
+        ws += align256(T * (size_t(leaves) + 1) * sizeof(int32_t));
         q.bk_cap = tile_cap(p.n_tokens, p.depth);
         q.bk_tok = reinterpret_cast<int32_t*>(ws);
-        ws += align256(size_t(leaves) * size_t(q.bk_cap) * sizeof(int32_t));
+        ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * sizeof(int32_t));
         q.bk_spill = reinterpret_cast<int32_t*>(ws);
-        ws += align256(recs * sizeof(int32_t));
+        ws += align256(T * size_t(p.n_tokens) * sizeof(int32_t));
         q.bk_act = reinterpret_cast<float*>(ws);
-        ws += align256(size_t(leaves) * size_t(q.bk_cap) * size_t(TILE_REC) * sizeof(float));
+        ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * size_t(TILE_REC) * sizeof(float));
         q.bk_junk = ws;
+        ws += TILE_JUNK_BYTES;
+        void* sum = p.y_bf16 && T > 1 ? static_cast<void*>(ws) : p.y;  // fp32 running sum over trees
         q.split_level = plan.split_level;
         (void)workspace_bytes;
         int32_t* fa = q.bk_count;
-        int64_t fn = leaves + 1;
+        int64_t fn = int64_t(T) * (leaves + 1);
         void* fargs[] = {&fa, &fn};
         const Launch& F = plan.launch[0];
         hipError_t e = hipLaunchKernel(F.kernel, dim3(F.grid), dim3(F.block), fargs, 0, stream);
@@ -1313,12 +1375,22 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         const Launch& W = plan.launch[1];
         e = hipLaunchKernel(W.kernel, dim3(W.grid), dim3(W.block), wargs, W.lds_bytes, stream);
         if (e != hipSuccess) return e;
-        Params qt = q;
-        qt.bk_count = q.bk_count;  // read-only from here on
-        int leaf_blocks = int(leaves);
-        void* targs[] = {&qt, &leaf_blocks};
+        const Variant* v = find_variant(p);
         const Launch& E = plan.launch[2];
-        return hipLaunchKernel(E.kernel, dim3(E.grid), dim3(E.block), targs, 0, stream);
+        int leaf_blocks = int(leaves);
+        const void* src0 = out_src_kind(p) == TSRC_NONE ? nullptr : p.out_mode == OUT_RESIDUAL ? p.x : p.y;
+        // trees in order: tree t adds its contribution to the running sum of trees 0..t-1 (a fixed
+        // order of the sum over trees, so the output bits do not depend on scheduling)
+        for (int t = 0; t < int(T); ++t) {
+            Params qt = q;
+            qt.tile_tree = t;
+            qt.tile_src = t > 0 ? sum : src0;
+            qt.tile_dst = t == int(T) - 1 ? p.y : sum;
+            void* targs[] = {&qt, &leaf_blocks};
+            e = hipLaunchKernel(tile_kernel_for(*v, p, t), dim3(E.grid), dim3(E.block), targs, 0, stream);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
     }
     for (int i = 0; i < plan.n_launch; ++i) {
         const Launch& L = plan.launch[i];

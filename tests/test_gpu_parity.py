@@ -469,13 +469,58 @@ def test_tiled_with_layernorm(fff_lib, yd):
     flush_print(f"[gpu] tiled + LayerNorm y={yd}: {parity.summary(rep)}")
 
 
+@pytest.mark.parametrize("name", ["4x9_h768_b16384_f32", "4x8_h768_b16384_f32"])
+def test_tiled_multi_tree_full_size(fff_lib, name):
+    """UltraFastBERT-4x9 and 4x8 at 16384 tokens through the leaf-tiled path: one tile pass per tree,
+    in tree order, each adding to the running sum of the trees before it."""
+    w = WORKLOADS[name]
+    L = synth.make_layer(w.seed, w.n_tokens, w.hidden, w.depth, w.n_trees, w.x_dtype, w.w_dtype)
+    check_layer(fff_lib, f"tiled {name}", L, w.depth, w.n_trees, w.y_dtype, mode="tiled")
+
+
+@pytest.mark.parametrize("T,D,B,xd,wd,yd", [(2, 11, 9000, "bf16", "bf16", "bf16"), (3, 7, 2500, "f32", "bf16", "f32"),
+                                          (16, 5, 3000, "bf16", "bf16", "f32"), (5, 6, 777, "f32", "f32", "bf16"),
+                                          (2, 9, 1, "bf16", "bf16", "bf16")])
+def test_tiled_multi_tree_shapes(fff_lib, T, D, B, xd, wd, yd):
+    """Several trees, both weight types, bf16 outputs (the running sum then lives in the workspace),
+    ragged and single-token batches."""
+    L = layer(250 + T + D, B, 768, D, T, xd, wd)
+    check_layer(fff_lib, f"tiled {T}x{D} B={B} {xd}/{wd}/{yd}", L, D, T, yd, mode="tiled")
+
+
+@pytest.mark.parametrize("out", ["residual", "accumulate"])
+@pytest.mark.parametrize("xd,yd", [("f32", "f32"), ("bf16", "bf16")])
+def test_tiled_multi_tree_output_modes(fff_lib, out, xd, yd):
+    B, T, D = 3000, 3, 9
+    L = layer(260, B, 768, D, T, xd, "bf16")
+    y0 = synth.make_x(261, B, 768, yd)
+    got = run_fff(fff_lib, L, D, T, yd, mode="tiled", out=out, y_init=y0 if out == "accumulate" else None)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], D, T)
+    base = L["x"] if out == "residual" else y0
+    rep = parity.assert_parity(L["x"], L["w_in"], L["w_out"], D, T, ref, got["y"], got["nodes"],
+                               tol=tol_for("bf16", yd), base_dev=base)
+    flush_print(f"[gpu] tiled {T}x{D} {out} {xd}/{yd}: {parity.summary(rep)}")
+
+
+def test_tiled_multi_tree_spills_deterministic(fff_lib):
+    """Clustered tokens overflow the buckets of every tree; two runs give the same bits."""
+    B, T, D = 12000, 2, 10
+    x = synth.make_clustered_x(270, B, 768, "bf16", n_centres=6)
+    wi, wo = synth.make_weights(270, 768, D, T, "bf16")
+    L = {"x": x, "w_in": wi, "w_out": wo}
+    check_layer(fff_lib, "tiled 2x10 clustered", L, D, T, "f32", mode="tiled")
+    a = run_fff(fff_lib, L, D, T, "f32", mode="tiled")
+    b = run_fff(fff_lib, L, D, T, "f32", mode="tiled")
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
+
+
 def test_tiled_unsupported_shapes(fff_lib):
     L = layer(240, 64, 768, 4, 1, "f32", "f32")  # depth below 5
     with pytest.raises(fff_lib.FffError):
         run_fff(fff_lib, L, 4, 1, "f32", mode="tiled")
-    L = layer(241, 64, 768, 6, 2, "f32", "f32")  # two trees
+    L = layer(241, 64, 768, 5, 17, "f32", "f32")  # more than 16 trees
     with pytest.raises(fff_lib.FffError):
-        run_fff(fff_lib, L, 6, 2, "f32", mode="tiled")
+        run_fff(fff_lib, L, 5, 17, "f32", mode="tiled")
     L = layer(242, 64, 768, 16, 1, "bf16", "bf16")  # depth above 15
     with pytest.raises(fff_lib.FffError):
         run_fff(fff_lib, L, 16, 1, "bf16", mode="tiled")
