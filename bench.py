@@ -87,6 +87,8 @@ def parse():
     ap.add_argument("--backward", action="store_true",
                     help="time the hard-routed backward (dx, dW_in, dW_out from the forward's records) instead")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-valu-only", action="store_true",
+                    help="skip timing the vector-ALU plan beside an MFMA plan (keeps a profile to one plan)")
     ap.add_argument("--cold-reps", type=int, default=20,
                     help="calls timed cold (a 1 GiB write before each evicts W from L2 and MALL); 0: skip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -298,7 +300,7 @@ def main():
                         "persistent_plan": fff.describe_stack(x, dlayers, w.depth, w.n_trees, y, **kd)}
         log(f"persistent stack kernel: {tk['mean_ms'] * 1e3:.1f} us vs the planned step {t['mean_ms'] * 1e3:.1f} us")
 
-    if not args.backward and NL == 1 and ("tiled<" in plan or "masked<" in plan):
+    if not args.backward and not args.no_valu_only and NL == 1 and ("tiled<" in plan or "masked<" in plan):
         # the same layer without matrix cores: the grouped walk + emit (one tree) or the fused kernel
         vmode = "grouped" if w.n_trees == 1 and w.depth >= 3 else "descent"
         vkw = dict(kw, mode=vmode)

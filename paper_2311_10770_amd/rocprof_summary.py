@@ -52,7 +52,11 @@ def read_counter(path: Path, counter: str, kernel: str) -> list:
     return vals
 
 
-def summarise(kernels: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int) -> dict:
+HBM_PEAK_GBS = 8000.0
+
+
+def summarise(kernels: str, stats: Path | None, fetch: Path | None, write: Path | None, copy_mb: int,
+              algorithmic: str | None = None) -> dict:
     names = [k for k in kernels.split(",") if k]
     out = {"kernels": names, "kernel_source_hash": kernel_source_hash(any(k.startswith("bwd_") for k in names))}
     if stats:
@@ -77,6 +81,27 @@ def summarise(kernels: str, stats: Path | None, fetch: Path | None, write: Path 
         total += step
     if fetch and write:
         out["hbm_bytes_per_launch"] = total
+    if algorithmic:
+        # per kernel: the bytes it cannot avoid (given), the bytes the counters saw, their ratio, and
+        # the algorithmic bytes over its mean duration against the 8 TB/s HBM peak
+        algo = [float(v) for v in algorithmic.split(",")]
+        if len(algo) != len(names):
+            raise ValueError("--algorithmic needs one byte count per --kernel name")
+        table = []
+        for i, k in enumerate(names):
+            row = {"kernel": k, "algorithmic_bytes": algo[i]}
+            if "FETCH_SIZE" in out and "WRITE_SIZE" in out:
+                cb = out["FETCH_SIZE"]["per_kernel"][k]["bytes_per_dispatch"] + \
+                    out["WRITE_SIZE"]["per_kernel"][k]["bytes_per_dispatch"]
+                row["counter_bytes"] = cb
+                row["counter_over_algorithmic"] = cb / algo[i] if algo[i] else None
+            if stats:
+                us = out["duration"]["per_kernel"][i]["mean_us"]
+                row["mean_us"] = us
+                row["algorithmic_gbs"] = algo[i] / (us * 1e-6) / 1e9
+                row["frac_of_hbm_peak"] = row["algorithmic_gbs"] / HBM_PEAK_GBS
+            table.append(row)
+        out["per_kernel_roofline"] = table
     return out
 
 
@@ -88,8 +113,10 @@ def main():
     ap.add_argument("--write", type=Path)
     ap.add_argument("--copy-mb", type=int, default=512)
     ap.add_argument("--out", type=Path)
+    ap.add_argument("--algorithmic", default=None,
+                    help="comma-separated algorithmic bytes per dispatch, one per --kernel name")
     a = ap.parse_args()
-    s = summarise(a.kernel, a.stats, a.fetch, a.write, a.copy_mb)
+    s = summarise(a.kernel, a.stats, a.fetch, a.write, a.copy_mb, a.algorithmic)
     text = json.dumps(s, indent=1)
     if a.out:
         a.out.write_text(text + "\n")
