@@ -667,3 +667,41 @@ def test_subtree_auto_and_limits(fff_lib):
     w5w = torch.zeros((1, 63, 640), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(fff_lib.FffError):
         fff_lib.forward(x5, w5w, w5w, 5, 1, mode="subtree")  # no kernel for hidden 640
+
+
+_MASKED_CHILD = r"""
+import hashlib, sys
+import torch
+sys.path.insert(0, sys.argv[1])
+import paper_2311_10770_amd as fff
+from paper_2311_10770_amd import synth
+fff.load_library()
+dev = torch.device("cuda:0")
+out = []
+for xd, yd, k, d in (("bf16", "bf16", 512, 2), ("bf16", "f32", 64, 5), ("f32", "f32", 128, 4)):
+    L = synth.make_layer(77, 4096, 768, d, k, xd, xd)
+    x, wi, wo = (fff.from_numpy(L[n], dev) for n in ("x", "w_in", "w_out"))
+    y = torch.empty((4096, 768), dtype=torch.bfloat16 if yd == "bf16" else torch.float32, device=dev)
+    fff.forward(x, wi, wo, d, k, y, mode="masked")
+    torch.cuda.synchronize()
+    out.append(hashlib.sha256(y.view(torch.uint8).cpu().numpy().tobytes()).hexdigest())
+print(" ".join(out))
+"""
+
+
+def test_masked_bits_do_not_depend_on_the_process():
+    """Masked mode's products run a fixed algorithm per shape (no timing-based choice), so two fresh
+    processes produce the same output bits."""
+    import subprocess
+    import sys
+
+    from tests.conftest import ROOT
+
+    runs = []
+    for i in range(2):
+        flush_print(f"[gpu] masked bits, fresh process {i}")
+        r = subprocess.run([sys.executable, "-c", _MASKED_CHILD, str(ROOT)], capture_output=True, text=True,
+                           timeout=300)
+        assert r.returncode == 0, r.stderr[-2000:]
+        runs.append(r.stdout.strip().splitlines()[-1])
+    assert runs[0] == runs[1], runs
