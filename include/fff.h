@@ -38,9 +38,8 @@
  *     failed HIP call (see fff_last_hip_error).
  *   - the library is reentrant.  Its global state: a per-device property
  *     cache, a cache of occupancy queries per kernel, the thread-local last
- *     HIP error, and for MASKED mode a per-device hipBLASLt handle with its
- *     matrix descriptors per product shape (created on first use under a
- *     mutex; they hold no results, and no call waits on the device).
+ *     HIP error, and the device address of fff_forward_static's scratch per
+ *     device.  No call waits on the device.
  */
 #ifndef FFF_H_
 #define FFF_H_
@@ -90,15 +89,15 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * walk, for shallow trees
  * where a token uses a large share of the nodes (at depth 0 the layer is the
  * dense feedforward): the logits of all nodes as one bf16 GEMM with fp32
- * accumulation (hipBLASLt, MFMA), the walk of Algorithm 1 over them per
- * (token, tree) with the visited nodes' activations split into bf16 parts
- * (two when y is bf16, three otherwise) and zeros elsewhere, then the output
- * as a second GEMM against W_out repeated once per part.  With fp32 x, W and
- * y both GEMMs are fp32 and the activations go in whole.  Needs the
- * workspace of fff_workspace_bytes (logits, parts, the repeated W_out and
- * hipBLASLt's scratch).  Each product runs hipBLASLt's first heuristic
- * algorithm for its shape: a fixed choice, so results do not depend on
- * timing, and the call only enqueues work like every other mode.
+ * accumulation (the library's own MFMA kernel), the walk of Algorithm 1 over
+ * them per (token, tree) with the visited nodes' activations split into bf16
+ * parts (two when y is bf16, three otherwise) and zeros elsewhere, then the
+ * output as a second GEMM against W_out transposed and repeated once per
+ * part.  With fp32 x, W and y both GEMMs are fp32 (fp32 MFMA) and the
+ * activations go in whole.  The products' kernel and tile shapes depend on
+ * the shapes and the device's CU count only, so the result bits do too.
+ * Needs the workspace of fff_workspace_bytes (logits, parts, the transposed
+ * W_out).
  * SUBTREE: hidden 768, 1024 or 4096 (any supported types), no LayerNorm; for
  * a few tokens, where the walk's D+1 dependent row loads are the time: one
  * workgroup of 1024 threads (512 for fp32 x with bf16 W at hidden >= 1024)
@@ -200,7 +199,8 @@ int fff_forward_ex(const fff_args* a);
  * looked up once per device; the call makes no hipMalloc, hipFree or other
  * allocating call.  Rules beyond fff_forward_ex's:
  *   - workspace must be NULL and workspace_bytes 0 (FFF_ERR_INVALID_ARG);
- *   - MASKED is not available (FFF_ERR_UNSUPPORTED; AUTO never picks it here);
+ *   - MASKED is not available (FFF_ERR_UNSUPPORTED; AUTO never picks it here:
+ *     its workspace is far larger than the array);
  *   - AUTO picks GROUPED or TILED only when its scratch fits the array; an
  *     explicit GROUPED or TILED whose scratch (fff_workspace_bytes for that
  *     plan) exceeds FFF_STATIC_SCRATCH_BYTES returns FFF_ERR_WORKSPACE;
@@ -219,7 +219,7 @@ int fff_forward_static(const fff_args* a);
  * tree), plus for TILED the leaf buckets (int32 counts; token slots, a few
  * times the mean tokens per leaf, each with its D+1 fp32 activations; a spill
  * list), and at depth <= 7 MASKED's logits of every node (fp32), their bf16
- * parts, W_out repeated three times and 32 MiB of GEMM scratch.  The result
+ * parts and W_out transposed and repeated three times.  The result
  * covers every mode; the split level (-1..depth) does not change it.
  * Returns 0 for invalid shapes. */
 size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,

@@ -30,8 +30,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-fvi
           f"-I{INCLUDE}", f"-I{CSRC}"] + DEVICE_FLAGS
 
 LIBS = {
-    "libfff.so": {"sources": ["fff_api.cpp", "fff_kernels.hip", "fff_backward.hip", "fff_masked.hip", "fff_subtree.hip"],
-                  "link": ["-L/opt/rocm/lib", "-lhipblaslt"]},
+    "libfff.so": {"sources": ["fff_api.cpp", "fff_kernels.hip", "fff_backward.hip", "fff_masked.hip", "fff_gemm.hip",
+                              "fff_subtree.hip"],
+                  "link": []},
     "libfffbench.so": {"sources": ["bench_helpers.hip"], "link": ["-L/opt/rocm/lib", "-lhipblaslt"]},
 }
 

@@ -244,7 +244,7 @@ int plan_for(const fff_args* a, fff::Params* p, fff::Plan* plan) {
 }
 
 // The entry point that allocates nothing: the plan's scratch is the library's
-// static device array.  No MASKED plan (its hipBLASLt handle allocates);
+// static device array.  No MASKED plan (its workspace is far larger than the array);
 // AUTO picks a scratch-using mode only when the array covers it.
 int forward_static(const fff_args* a) {
     fff::Params p;

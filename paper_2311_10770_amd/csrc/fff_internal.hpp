@@ -142,6 +142,7 @@ struct Plan {
     int emit_lds_levels = 0;       // grouped emit
     int split_level = 0;           // grouped mode
     int walk_affine = 0;           // grouped / tiled: one tree per walk workgroup, by XCD
+    int cu_count = 0;              // masked: compute units, for the products' tile choice
     const char* name = "";
 };
 
@@ -149,8 +150,8 @@ struct Plan {
 // workspace_bytes: size of the 256-byte aligned workspace the caller passed (0
 // if none); AUTO picks the grouped or tiled path only when it covers that
 // path's scratch.
-// masked_ok: whether MASKED may be planned (it creates a hipBLASLt handle on first use, so the
-// entry point that allocates nothing excludes it).
+// masked_ok: whether MASKED may be planned (the entry point that allocates nothing excludes it: its
+// workspace is far larger than that entry point's scratch).
 int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_req, size_t workspace_bytes,
                  const DeviceInfo& dev, Plan* plan, bool masked_ok = true);
 
@@ -194,11 +195,23 @@ constexpr int MASKED_AUTO_TREES = 16;
 constexpr int64_t MASKED_AUTO_TOKENS = 16384;
 // Whether a validated request can run masked (types, depth, no LayerNorm, residual types).
 bool masked_shape(const Params& p);
-// Masked mode scratch (logits, split activations, repeated W_out, hipBLASLt's scratch); 0 past
+// Masked mode scratch (logits, split activations, transposed and repeated W_out); 0 past
 // MASKED_MAX_DEPTH.
 size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden);
-// Enqueues the masked forward on stream (hipErrorNotSupported when hipBLASLt has no algorithm).
-hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream);
+// Enqueues the masked forward on stream.
+hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_t stream);
+
+// Dense products of MASKED mode on the matrix cores (fff_gemm.hip): C = A B^T with A [M, K] and
+// B [N, K] row-major (K-contiguous, leading dimensions lda / ldb in elements, 16-byte aligned rows,
+// K a multiple of 8 for bf16 or 4 for fp32), bf16 (bf16 = true) or fp32 inputs, fp32 accumulation.
+// out: GEMM_OUT_F32 stores C as fp32; GEMM_OUT_SRC_* add a source matrix (none, fp32, bf16; leading
+// dimension ldc like C, may be C itself) and store as bf16 (dst_bf16) or fp32.  fp32 inputs take
+// fp32 sources and destinations only.  cu_count: compute units of the device (tile choice).  The
+// kernel and tile shape depend on the shapes and cu_count only, so the result bits do too.
+enum { GEMM_OUT_F32 = 0, GEMM_OUT_SRC_NONE = 1, GEMM_OUT_SRC_F32 = 2, GEMM_OUT_SRC_BF16 = 3 };
+hipError_t gemm_nt(bool bf16, int out, bool dst_bf16, const void* A, const void* B, void* C, const void* src,
+                   int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int cu_count,
+                   hipStream_t stream);
 
 // Subtree mode (fff_subtree.hip): a workgroup per token evaluates whole subtrees of logits per
 // step.  AUTO takes it for at most SUBTREE_AUTO_TREES trees of depth at least SUBTREE_AUTO_DEPTH

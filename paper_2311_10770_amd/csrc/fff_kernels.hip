@@ -1216,6 +1216,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     if (mode == MODE_MASKED) {
         if (!masked_ok || !masked_shape(p)) return ST_UNSUPPORTED;
         plan->kind = KIND_MASKED;
+        plan->cu_count = dev.cu_count;
         plan->name = !p.w_bf16 ? "fp32 GEMMs"
                      : p.y_bf16 ? "bf16 GEMMs, activations in 2 parts" : "bf16 GEMMs, activations in 3 parts";
         return ST_OK;
@@ -1328,7 +1329,7 @@ hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream
 
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream) {
-    if (plan.kind == KIND_MASKED) return run_masked(p, workspace, stream);
+    if (plan.kind == KIND_MASKED) return run_masked(p, workspace, plan.cu_count, stream);
     if (plan.kind == KIND_SUBTREE) return run_subtree(p, plan.launch[0].grid, stream);
     Params q = p;
     q.lds_levels = plan.lds_levels;

@@ -3,35 +3,29 @@
 // token uses N_I = K (D+1) of the N_T = K (2^(D+1) - 1) neurons (Section 2.1,
 // Table 1); at depth 0 the layer is the dense feedforward, and for small D a
 // large share of each row is used, so the layer runs best as dense MFMA work:
-//   G1 (hipBLASLt, bf16 MFMA, fp32 accumulate): L[B, N_T] = x W_in^T, the logit
-//      of every node of every tree;
+//   G1 (fff_gemm.hip, bf16 MFMA, fp32 accumulate): L[B, N_T] = x W_in^T, the
+//      logit of every node of every tree;
 //   selection: per (token, tree) the walk of Algorithm 1 over those logits
 //      (left on a logit <= 0, as in the other modes), the activation of every
 //      visited node split into bf16 parts (P = 2 for a bf16 y, else 3: hi, mid,
 //      lo, each the rounding of what the earlier parts leave), zeros for the
 //      other nodes: A[B, P, N_T'], part p of node j at column p N_T' + j, with
 //      N_T' = N_T rounded up to 8 (zero padding) for 16-byte rows;
-//   G2: y = A [W_out; ...; W_out] (W_out repeated P times in the workspace,
-//      zero rows in the padding), so
-//      every product is exact and y is rounded once; accumulation and the
-//      residual come in through the C operand (beta = 1).
-// With fp32 x, W and y both products are fp32 GEMMs (full fp32 compute) and A
-// holds the activations whole.  The workspace holds L, A, the repeated W_out and
-// hipBLASLt's scratch.  Each product runs the heuristic's first algorithm for
-// its shape: a fixed choice, so the call only enqueues work and its results do
-// not depend on timing.
+//   G2: y = A [W_out; ...; W_out] against W_out transposed and repeated P times
+//      in the workspace (zero columns in the padding), so every product is
+//      exact and y is rounded once; accumulation and the residual are added in
+//      the product's store.
+// With fp32 x, W and y both products are fp32 (fp32 MFMA) and A holds the
+// activations whole.  The workspace holds L, A and the transposed W_out.
 #include "fff_common.hpp"
 #include "fff_device.hpp"
 #include "fff_internal.hpp"
 
 #include <hip/hip_runtime.h>
-#include <hipblaslt/hipblaslt.h>
 
 #include <algorithm>
 #include <cstdint>
-#include <map>
-#include <mutex>
-#include <tuple>
+#include <type_traits>
 
 namespace fff {
 
@@ -39,7 +33,6 @@ namespace {
 
 constexpr int SELECT_BLOCK = 256;
 constexpr int SELECT_LDS_COLS = 8192;  // widest logit row the staged selection keeps in LDS
-constexpr size_t LT_WORKSPACE = size_t(32) << 20;
 
 typedef uint2 __attribute__((may_alias)) lds_u2a;
 
@@ -47,9 +40,11 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 int masked_parts(bool y_bf16) { return y_bf16 ? 2 : 3; }
 
-// Columns of a row of L and of each part of A: N_T rounded up to 8, so that rows
-// and parts start on 32-byte boundaries (the padding columns of A are zeros).
-int64_t padded_cols(int64_t nt) { return (nt + 7) & ~int64_t(7); }
+// Columns of a row of L and of each part of A: N_T rounded up to 64, so that each
+// part is a whole number of the second product's K steps (64 bf16 or 32 fp32
+// elements) and rows and parts start on 128-byte boundaries (the padding columns
+// of A are zeros).
+int64_t padded_cols(int64_t nt) { return (nt + 63) & ~int64_t(63); }
 
 // Writes the values of columns [8 v, 8 v + 8) of token b's row of A: fp32 whole,
 // or bf16 parts (hi, mid[, lo]) at part stride ntq.
@@ -169,71 +164,30 @@ __global__ __launch_bounds__(SELECT_BLOCK) void select_paths_kernel(Params p, co
     }
 }
 
-// W_out [N_T, H] repeated: dst [reps][ntq][H], rows N_T..ntq-1 of each copy zero (16-byte vectors;
-// n = N_T H / 8 vectors of the source, np = ntq H / 8 per copy).
-__global__ __launch_bounds__(256) void repeat_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n,
-                                                     int64_t np, int reps) {
-    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < np; i += int64_t(gridDim.x) * 256) {
-        const uint4 v = i < n ? src[i] : make_uint4(0, 0, 0, 0);
-        for (int r = 0; r < reps; ++r) dst[int64_t(r) * np + i] = v;
+// W_out [N_T, H] transposed and repeated: dst [H][reps * ntq] with dst[n][r ntq + j] = W_out[j][n]
+// for j < N_T and 0 on the padding columns; bf16 (BF) or fp32 elements.  64 x 64 tiles through LDS
+// so that both the reads (along H) and the writes (along N_T) are contiguous.
+template <bool BF>
+__global__ __launch_bounds__(256) void transpose_repeat_kernel(const void* __restrict__ src, void* __restrict__ dst,
+                                                               int64_t nt, int64_t ntq, int64_t H, int reps) {
+    typedef typename std::conditional<BF, uint16_t, float>::type E;
+    __shared__ E tile[64][65];
+    const int64_t j0 = int64_t(blockIdx.x) * 64, n0 = int64_t(blockIdx.y) * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const E* s = static_cast<const E*>(src);
+    E* d = static_cast<E*>(dst);
+    for (int r = ty; r < 64; r += 4) {  // tile[j][n] = W_out[j0 + j][n0 + n]
+        const int64_t j = j0 + r, n = n0 + tx;
+        tile[r][tx] = j < nt && n < H ? s[j * H + n] : E(0);
     }
-}
-
-// ---------------------------------------------------------------- hipBLASLt
-
-constexpr int LT_CANDIDATES = 8;  // heuristic candidates asked for; the first usable one runs
-
-struct GemmEntry {
-    hipblasLtMatmulDesc_t desc = nullptr;
-    hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
-    hipblasLtMatmulAlgo_t algo{};            // the heuristic's first usable algorithm
-    bool ok = false;
-};
-
-struct LtState {
-    hipblasLtHandle_t handle = nullptr;
-    // (m, n, k, transa, input type, d type, ldb, ldc) -> descriptors and the heuristic's first algorithm
-    std::map<std::tuple<int64_t, int64_t, int64_t, int, int, int, int64_t, int64_t>, GemmEntry> gemms;
-};
-
-std::mutex g_lt_mutex;
-std::map<int, LtState> g_lt;  // per device
-
-bool lt_ok(hipblasStatus_t s) { return s == HIPBLAS_STATUS_SUCCESS; }
-
-// Column-major D[m, n] = op(A) B with A stored [k, m] (transa) or [m, k] (packed), B [k, n] with
-// leading dimension ldb, D (and C) with leading dimension ldc; inputs of type itype (bf16, or fp32
-// computed in full fp32), fp32 accumulation, D (and C) of type dtype.
-GemmEntry* get_gemm(LtState& st, int64_t m, int64_t n, int64_t k, bool transa, hipDataType itype, hipDataType dtype,
-                    int64_t ldb, int64_t ldc) {
-    const auto key = std::make_tuple(m, n, k, int(transa), int(itype), int(dtype), ldb, ldc);
-    auto it = st.gemms.find(key);
-    if (it != st.gemms.end()) return it->second.ok ? &it->second : nullptr;
-    GemmEntry& g = st.gemms[key];
-    if (!lt_ok(hipblasLtMatmulDescCreate(&g.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F))) return nullptr;
-    const hipblasOperation_t ta = transa ? HIPBLAS_OP_T : HIPBLAS_OP_N, tb = HIPBLAS_OP_N;
-    hipblasLtMatmulDescSetAttribute(g.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof ta);
-    hipblasLtMatmulDescSetAttribute(g.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof tb);
-    if (!lt_ok(transa ? hipblasLtMatrixLayoutCreate(&g.a, itype, k, m, k) : hipblasLtMatrixLayoutCreate(&g.a, itype, m, k, m)))
-        return nullptr;
-    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g.b, itype, k, n, ldb))) return nullptr;
-    if (!lt_ok(hipblasLtMatrixLayoutCreate(&g.c, dtype, m, n, ldc))) return nullptr;
-    hipblasLtMatmulPreference_t pref;
-    if (!lt_ok(hipblasLtMatmulPreferenceCreate(&pref))) return nullptr;
-    uint64_t ws = LT_WORKSPACE;
-    hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &ws, sizeof ws);
-    hipblasLtMatmulHeuristicResult_t res[LT_CANDIDATES];
-    int found = 0;
-    const hipblasStatus_t s =
-        hipblasLtMatmulAlgoGetHeuristic(st.handle, g.desc, g.a, g.b, g.c, g.c, pref, LT_CANDIDATES, res, &found);
-    hipblasLtMatmulPreferenceDestroy(pref);
-    if (!lt_ok(s)) return nullptr;
-    for (int i = 0; i < found && i < LT_CANDIDATES && !g.ok; ++i)
-        if (res[i].state == HIPBLAS_STATUS_SUCCESS && res[i].workspaceSize <= LT_WORKSPACE) {
-            g.algo = res[i].algo;
-            g.ok = true;
+    __syncthreads();
+    for (int r = ty; r < 64; r += 4) {  // dst[n0 + r][rep ntq + j0 + tx] = tile[tx][r]
+        const int64_t n = n0 + r, j = j0 + tx;
+        if (n < H && j < ntq) {
+            const E v = tile[tx][r];
+            for (int rep = 0; rep < reps; ++rep) d[n * (int64_t(reps) * ntq) + int64_t(rep) * ntq + j] = v;
         }
-    return g.ok ? &g : nullptr;
+    }
 }
 
 }  // namespace
@@ -253,10 +207,10 @@ size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, 
     const size_t ntq = size_t(padded_cols(((int64_t(1) << (depth + 1)) - 1) * n_trees));
     const int P = 3;  // the larger part count (fp32 y); three bf16 parts also cover one fp32 row
     return align256(size_t(n_tokens) * ntq * sizeof(float)) + align256(size_t(n_tokens) * P * ntq * sizeof(uint16_t)) +
-           align256(size_t(P) * ntq * size_t(hidden) * sizeof(uint16_t)) + LT_WORKSPACE;
+           align256(size_t(P) * ntq * size_t(hidden) * sizeof(uint16_t));
 }
 
-hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
+hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_t stream) {
     const int64_t B = p.n_tokens, H = p.hidden, NT = p.n_nodes * p.n_trees, ntq = padded_cols(NT);
     const bool f32 = !p.w_bf16;          // fp32 x, W and y: fp32 products, activations whole
     const int P = f32 ? 1 : masked_parts(p.y_bf16);
@@ -265,37 +219,17 @@ hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
     ws += align256(size_t(B) * ntq * sizeof(float));
     void* A = ws;                             // bf16 [B, P, ntq] or fp32 [B, ntq]
     ws += align256(size_t(B) * 3 * ntq * sizeof(uint16_t));
-    uint16_t* Wrep = reinterpret_cast<uint16_t*>(ws);  // bf16 [P, ntq, H]
-    ws += align256(size_t(3) * ntq * H * sizeof(uint16_t));
-    void* lt_ws = ws;
+    void* WT = ws;                            // bf16 [H, P ntq] or fp32 [H, ntq]: W_out transposed
 
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    // G1: L = x W_in^T (logits of every node; the padding columns are not written)
+    hipError_t e = gemm_nt(!f32, GEMM_OUT_F32, false, p.x, p.w_in, L, nullptr, B, NT, H, H, H, ntq, cu_count, stream);
     if (e != hipSuccess) return e;
-    std::lock_guard<std::mutex> lock(g_lt_mutex);
-    LtState& st = g_lt[dev];
-    if (!st.handle && !lt_ok(hipblasLtCreate(&st.handle))) return hipErrorNotSupported;
-    const hipDataType itype = f32 ? HIP_R_32F : HIP_R_16BF;
-    const hipDataType ydt = p.y_bf16 ? HIP_R_16BF : HIP_R_32F;
-    const bool beta_on = p.out_mode != OUT_STORE;
-    // G2's reduction: fp32 over the N_T real columns of A (row stride ntq); bf16 over all P ntq
-    // columns against the zero-padded copies of W_out
-    const int64_t k2 = f32 ? NT : P * ntq;
-    GemmEntry* g1 = get_gemm(st, NT, B, H, true, itype, HIP_R_32F, H, ntq);
-    GemmEntry* g2 = get_gemm(st, H, B, k2, false, itype, ydt, f32 ? ntq : k2, H);
-    if (!g1 || !g2) return hipErrorNotSupported;  // no hipBLASLt algorithm for a product
-    const float one = 1.0f, zero = 0.0f;
-    // G1: L^T (column-major [N_T, B], leading dimension ntq) = W_in (row-major [N_T, H]) x^T
-    auto run_g1 = [&](const hipblasLtMatmulAlgo_t& algo) {
-        return lt_ok(hipblasLtMatmul(st.handle, g1->desc, &one, p.w_in, g1->a, p.x, g1->b, &zero, L, g1->c, L,
-                                     g1->c, &algo, lt_ws, LT_WORKSPACE, stream));
-    };
-    if (!run_g1(g1->algo)) return hipErrorLaunchFailure;
-    if (!f32) {
-        const int64_t n = NT * H / 8, np = ntq * H / 8;
-        const int grid = int(std::min<int64_t>((np + 255) / 256, 2048));
-        hipLaunchKernelGGL(repeat_kernel, dim3(grid), dim3(256), 0, stream, reinterpret_cast<const uint4*>(p.w_out),
-                           reinterpret_cast<uint4*>(Wrep), n, np, P);
+    {
+        const dim3 grid(unsigned((ntq + 63) / 64), unsigned((H + 63) / 64));
+        if (f32)
+            hipLaunchKernelGGL(transpose_repeat_kernel<false>, grid, dim3(256), 0, stream, p.w_out, WT, NT, ntq, H, 1);
+        else
+            hipLaunchKernelGGL(transpose_repeat_kernel<true>, grid, dim3(256), 0, stream, p.w_out, WT, NT, ntq, H, P);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -319,13 +253,18 @@ hipError_t run_masked(const Params& p, void* workspace, hipStream_t stream) {
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // G2: y^T (column-major [H, B]) = Wrep^T (column-major [H, k2]) A^T, plus C (y or x)
-    const void* C = p.out_mode == OUT_RESIDUAL ? p.x : p.y;
-    const void* W2 = f32 ? p.w_out : static_cast<const void*>(Wrep);
-    if (!lt_ok(hipblasLtMatmul(st.handle, g2->desc, &one, W2, g2->a, A, g2->b, beta_on ? &one : &zero, C, g2->c, p.y,
-                               g2->c, &g2->algo, lt_ws, LT_WORKSPACE, stream)))
-        return hipErrorLaunchFailure;
-    return hipSuccess;
+    // G2: y = A WT^T plus the layer's source (x for the residual, y for accumulation)
+    const int64_t k2 = int64_t(P) * ntq;
+    int out = GEMM_OUT_SRC_NONE;
+    const void* src = nullptr;
+    if (p.out_mode == OUT_RESIDUAL) {
+        src = p.x;
+        out = p.x_bf16 ? GEMM_OUT_SRC_BF16 : GEMM_OUT_SRC_F32;
+    } else if (p.out_mode == OUT_ACCUMULATE) {
+        src = p.y;
+        out = p.y_bf16 ? GEMM_OUT_SRC_BF16 : GEMM_OUT_SRC_F32;
+    }
+    return gemm_nt(!f32, out, p.y_bf16, A, WT, p.y, src, B, H, k2, k2, k2, H, cu_count, stream);
 }
 
 }  // namespace fff

@@ -548,6 +548,14 @@ def test_masked_f32_shapes(fff_lib, k, d, B):
     check_layer(fff_lib, f"masked f32 {k}x{d} B={B}", L, d, k, "f32", mode="masked")
 
 
+@pytest.mark.parametrize("dt,H", [("bf16", 200), ("bf16", 8), ("f32", 104), ("f32", 8)])
+def test_masked_ragged_hidden(fff_lib, dt, H):
+    """A hidden size that is not a whole number of the products' K steps (64 bf16 or 32 fp32
+    elements) takes the register-staged product kernel, which masks the K tail."""
+    L = layer(460 + H, 300, H, 2, 16, dt, dt)
+    check_layer(fff_lib, f"masked {dt} H={H}", L, 2, 16, dt, mode="masked")
+
+
 @pytest.mark.parametrize("out", ["residual", "accumulate"])
 def test_masked_f32_output_modes(fff_lib, out):
     L = layer(450, 300, 768, 2, 16, "f32", "f32")
