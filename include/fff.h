@@ -219,7 +219,8 @@ int fff_forward_static(const fff_args* a);
  * tree), plus for TILED the leaf buckets (int32 counts; token slots, a few
  * times the mean tokens per leaf, each with its D+1 fp32 activations; a spill
  * list), and at depth <= 7 MASKED's logits of every node (fp32), their bf16
- * parts and W_out transposed and repeated three times.  The result
+ * parts, W_out transposed and repeated three times and 32 MiB for the
+ * partial sums of a product split along K (few tokens).  The result
  * covers every mode; the split level (-1..depth) does not change it.
  * Returns 0 for invalid shapes. */
 size_t fff_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden,

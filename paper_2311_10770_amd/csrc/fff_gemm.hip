@@ -22,6 +22,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 namespace fff {
@@ -40,12 +41,15 @@ __device__ __forceinline__ void gemm_store(void* C, const void* src, int64_t ldc
     else static_cast<uint16_t*>(C)[e] = f32_to_bf16(v);
 }
 
+// Workgroup (blockIdx.x, blockIdx.y): tile xcd_tile(blockIdx.x) of C over K elements
+// [blockIdx.y kchunk, +kchunk) (kchunk a whole number of steps; one chunk unless K is split, when C
+// is the partial sums [gridDim.y][M][ldc] and OUT is GOUT_F32).
 template <bool BF, int TM, int TN, int WGM, int WGN, int S, int OUT, bool DBF>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_dma_kernel(const void* __restrict__ A,
                                                                      const void* __restrict__ B, void* C,
                                                                      const void* src, int64_t M, int64_t N,
                                                                      int64_t K, int64_t lda, int64_t ldb,
-                                                                     int64_t ldc) {
+                                                                     int64_t ldc, int64_t kchunk) {
     using G = DmaCfg<TM, TN, WGM, WGN, S>;
     extern __shared__ __align__(16) unsigned char gsm[];  // [S stages][A rows, B rows][128 bytes]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -54,8 +58,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_dma_kernel(const void*
     const int64_t tiles_n = (N + G::BN - 1) / G::BN;
     const int64_t t = xcd_tile(blockIdx.x, tiles_n * ((M + G::BM - 1) / G::BM));
     const int64_t m0 = (t / tiles_n) * G::BM, n0 = (t % tiles_n) * G::BN;
+    const int64_t kb = int64_t(blockIdx.y) * kchunk, kl = K - kb < kchunk ? K - kb : kchunk;
+    const int esz = BF ? 2 : 4;
+    if (gridDim.y > 1) C = static_cast<float*>(C) + int64_t(blockIdx.y) * M * ldc;
     tile_v4f acc[TM][TN];
-    dma_product<BF, TM, TN, WGM, WGN, S>(A, B, M, N, K, lda, ldb, m0, n0, gsm, acc);
+    dma_product<BF, TM, TN, WGM, WGN, S>(static_cast<const char*>(A) + kb * esz, static_cast<const char*>(B) + kb * esz,
+                                         M, N, kl, lda, ldb, m0, n0, gsm, acc);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -69,26 +77,69 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_dma_kernel(const void*
         }
 }
 
+// C = sum over the splits of the partial sums, in split order, through the product's store.
+// ldc is a multiple of 4, so each thread reads four columns of every split as one 16-byte load.
+template <int OUT, bool DBF>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, void* C,
+                                                            const void* src, int64_t M, int64_t N, int64_t ldc) {
+    const int64_t nq = (N + 3) / 4;
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < M * nq; i += int64_t(gridDim.x) * 256) {
+        const int64_t m = i / nq, n = (i - m * nq) * 4;
+        float4 v = *reinterpret_cast<const float4*>(part + m * ldc + n);
+        for (int sp = 1; sp < splits; ++sp) {
+            const float4 w = *reinterpret_cast<const float4*>(part + (int64_t(sp) * M + m) * ldc + n);
+            v.x += w.x;
+            v.y += w.y;
+            v.z += w.z;
+            v.w += w.w;
+        }
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (n + k < N) gemm_store<OUT, DBF>(C, src, ldc, m, n + k, vv[k]);
+    }
+}
+
 template <bool BF, int TM, int TN, int WGM, int WGN, int S, int OUT, bool DBF>
 void launch_dma(const void* A, const void* B, void* C, const void* src, int64_t M, int64_t N, int64_t K,
-                int64_t lda, int64_t ldb, int64_t ldc, hipStream_t stream) {
+                int64_t lda, int64_t ldb, int64_t ldc, hipStream_t stream, int splits = 1, int64_t kchunk = 0) {
     using G = DmaCfg<TM, TN, WGM, WGN, S>;
-    const dim3 grid(unsigned(((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM)));
+    const dim3 grid(unsigned(((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM)), unsigned(splits));
     hipLaunchKernelGGL((gemm_nt_dma_kernel<BF, TM, TN, WGM, WGN, S, OUT, DBF>), grid, dim3(G::THREADS), G::LDS, stream,
-                       A, B, C, src, M, N, K, lda, ldb, ldc);
+                       A, B, C, src, M, N, K, lda, ldb, ldc, splits > 1 ? kchunk : K);
 }
 
 // Tile choice, from the shapes and the CU count only: 256 x 256 tiles (128 x 128 per wave, bf16)
 // or 256 x 192 (128 x 96 per wave), one workgroup per CU, whichever leaves fewer tile-rounds of
 // idle CUs (the narrower tile reads ~7% more LDS per MFMA; its fp32 form is the only wide one
-// that needs no spills), or 128 x 128 tiles with two workgroups per CU for small products.
+// that needs no spills), or 128 x 128 tiles with two workgroups per CU for small products.  A
+// small product with too few tiles for the CUs and a long K is split along K into chunks of
+// whole steps (at least four each), up to two workgroups per CU and the partial sums' buffer,
+// and reduced in split order: the split depends on the shapes, the CU count and split_bytes only.
 template <bool BF, int OUT, bool DBF>
 hipError_t launch_gemm(const void* A, const void* B, void* C, const void* src, int64_t M, int64_t N, int64_t K,
-                       int64_t lda, int64_t ldb, int64_t ldc, int cu_count, hipStream_t stream) {
+                       int64_t lda, int64_t ldb, int64_t ldc, int cu_count, void* split_ws, size_t split_bytes,
+                       hipStream_t stream) {
     auto cdiv = [](int64_t a, int64_t b) { return (a + b - 1) / b; };
     const int64_t slots = cu_count > 0 ? cu_count : 256;
     const int64_t t88 = cdiv(M, 256) * cdiv(N, 256), t86 = cdiv(M, 256) * cdiv(N, 192);
     if (t88 < slots / 4) {
+        const int64_t t44 = cdiv(M, 128) * cdiv(N, 128), bk = BF ? 64 : 32, steps = cdiv(K, bk);
+        int64_t splits = 1;
+        if (split_ws && ldc % 4 == 0 && t44 < slots) {
+            splits = std::min<int64_t>({cdiv(2 * slots, t44), steps / 4, int64_t(split_bytes / (size_t(M) * ldc * 4))});
+        }
+        if (splits >= 2) {
+            const int64_t kchunk = cdiv(steps, splits) * bk;
+            splits = cdiv(K, kchunk);
+            launch_dma<BF, 4, 4, 2, 2, 2, GOUT_F32, false>(A, B, split_ws, nullptr, M, N, K, lda, ldb, ldc, stream,
+                                                           int(splits), kchunk);
+            const int64_t work = M * cdiv(N, 4);
+            const unsigned blocks = unsigned(std::min<int64_t>(cdiv(work, 256), 4 * slots));
+            hipLaunchKernelGGL((splitk_reduce_kernel<OUT, DBF>), dim3(blocks), dim3(256), 0, stream,
+                               static_cast<const float*>(split_ws), int(splits), C, src, M, N, ldc);
+            return hipGetLastError();
+        }
         launch_dma<BF, 4, 4, 2, 2, 2, OUT, DBF>(A, B, C, src, M, N, K, lda, ldb, ldc, stream);
         return hipGetLastError();
     }
@@ -106,26 +157,26 @@ hipError_t launch_gemm(const void* A, const void* B, void* C, const void* src, i
 
 hipError_t gemm_nt(bool bf16, int out, bool dst_bf16, const void* A, const void* B, void* C, const void* src,
                    int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int cu_count,
-                   hipStream_t stream) {
+                   void* split_ws, size_t split_bytes, hipStream_t stream) {
     if (M == 0 || N == 0) return hipSuccess;
     if (bf16) {
         switch (out) {
-            case GEMM_OUT_F32: return launch_gemm<true, GOUT_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
+            case GEMM_OUT_F32: return launch_gemm<true, GOUT_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
             case GEMM_OUT_SRC_NONE:
-                return dst_bf16 ? launch_gemm<true, GOUT_SRC_NONE, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream)
-                                : launch_gemm<true, GOUT_SRC_NONE, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
+                return dst_bf16 ? launch_gemm<true, GOUT_SRC_NONE, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream)
+                                : launch_gemm<true, GOUT_SRC_NONE, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
             case GEMM_OUT_SRC_F32:
-                return dst_bf16 ? launch_gemm<true, GOUT_SRC_F32, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream)
-                                : launch_gemm<true, GOUT_SRC_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
+                return dst_bf16 ? launch_gemm<true, GOUT_SRC_F32, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream)
+                                : launch_gemm<true, GOUT_SRC_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
             default:
-                return dst_bf16 ? launch_gemm<true, GOUT_SRC_BF16, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream)
-                                : launch_gemm<true, GOUT_SRC_BF16, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
+                return dst_bf16 ? launch_gemm<true, GOUT_SRC_BF16, true>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream)
+                                : launch_gemm<true, GOUT_SRC_BF16, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
         }
     }
     switch (out) {
-        case GEMM_OUT_F32: return launch_gemm<false, GOUT_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
-        case GEMM_OUT_SRC_NONE: return launch_gemm<false, GOUT_SRC_NONE, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
-        default: return launch_gemm<false, GOUT_SRC_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, stream);
+        case GEMM_OUT_F32: return launch_gemm<false, GOUT_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
+        case GEMM_OUT_SRC_NONE: return launch_gemm<false, GOUT_SRC_NONE, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
+        default: return launch_gemm<false, GOUT_SRC_F32, false>(A, B, C, src, M, N, K, lda, ldb, ldc, cu_count, split_ws, split_bytes, stream);
     }
 }
 

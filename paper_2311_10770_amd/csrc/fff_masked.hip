@@ -16,7 +16,8 @@
 //      exact and y is rounded once; accumulation and the residual are added in
 //      the product's store.
 // With fp32 x, W and y both products are fp32 (fp32 MFMA) and A holds the
-// activations whole.  The workspace holds L, A and the transposed W_out.
+// activations whole.  The workspace holds L, A, the transposed W_out and the partial sums of a
+// product split along K (few tokens, long K).
 #include "fff_common.hpp"
 #include "fff_device.hpp"
 #include "fff_internal.hpp"
@@ -207,7 +208,7 @@ size_t masked_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, 
     const size_t ntq = size_t(padded_cols(((int64_t(1) << (depth + 1)) - 1) * n_trees));
     const int P = 3;  // the larger part count (fp32 y); three bf16 parts also cover one fp32 row
     return align256(size_t(n_tokens) * ntq * sizeof(float)) + align256(size_t(n_tokens) * P * ntq * sizeof(uint16_t)) +
-           align256(size_t(P) * ntq * size_t(hidden) * sizeof(uint16_t));
+           align256(size_t(P) * ntq * size_t(hidden) * sizeof(uint16_t)) + GEMM_SPLIT_BYTES;
 }
 
 hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_t stream) {
@@ -220,9 +221,12 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
     void* A = ws;                             // bf16 [B, P, ntq] or fp32 [B, ntq]
     ws += align256(size_t(B) * 3 * ntq * sizeof(uint16_t));
     void* WT = ws;                            // bf16 [H, P ntq] or fp32 [H, ntq]: W_out transposed
+    ws += align256(size_t(3) * ntq * size_t(H) * sizeof(uint16_t));
+    void* SP = ws;                            // partial sums of a product split along K
 
     // G1: L = x W_in^T (logits of every node; the padding columns are not written)
-    hipError_t e = gemm_nt(!f32, GEMM_OUT_F32, false, p.x, p.w_in, L, nullptr, B, NT, H, H, H, ntq, cu_count, stream);
+    hipError_t e = gemm_nt(!f32, GEMM_OUT_F32, false, p.x, p.w_in, L, nullptr, B, NT, H, H, H, ntq, cu_count, SP,
+                           GEMM_SPLIT_BYTES, stream);
     if (e != hipSuccess) return e;
     {
         const dim3 grid(unsigned((ntq + 63) / 64), unsigned((H + 63) / 64));
@@ -264,7 +268,7 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
         src = p.y;
         out = p.y_bf16 ? GEMM_OUT_SRC_BF16 : GEMM_OUT_SRC_F32;
     }
-    return gemm_nt(!f32, out, p.y_bf16, A, WT, p.y, src, B, H, k2, k2, k2, H, cu_count, stream);
+    return gemm_nt(!f32, out, p.y_bf16, A, WT, p.y, src, B, H, k2, k2, k2, H, cu_count, SP, GEMM_SPLIT_BYTES, stream);
 }
 
 }  // namespace fff
