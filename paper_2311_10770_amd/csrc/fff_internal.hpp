@@ -184,14 +184,16 @@ size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, i
 int default_split_level(int32_t depth, int32_t n_trees);
 
 // Masked mode (two dense products around the walk, fff_masked.hip): the deepest tree it takes,
-// and where AUTO picks it: depth at most MASKED_AUTO_DEPTH (bf16 x and W) or
-// MASKED_AUTO_DEPTH_F32 (fp32 x, W and y), with at least MASKED_AUTO_TREES trees, or half as
-// many and MASKED_AUTO_TOKENS tokens (its two GEMMs and the selection cost about 35 us at any
-// size, which fewer trees do not win back).
+// and where AUTO picks it: bf16 x and W at depth at most MASKED_AUTO_DEPTH with at least
+// MASKED_AUTO_TREES trees, or three quarters as many and MASKED_AUTO_TOKENS tokens; fp32 x, W and
+// y at depth at most MASKED_AUTO_DEPTH_F32 with at least MASKED_AUTO_TREES_F32 trees (its
+// products and selection cost 30-55 us even at a few hundred tokens, which fewer trees do not
+// win back; measured against every mode at 4..64 trees, 1024 and 16384 tokens).
 constexpr int MASKED_MAX_DEPTH = 7;
 constexpr int MASKED_AUTO_DEPTH = 5;
 constexpr int MASKED_AUTO_DEPTH_F32 = 4;
 constexpr int MASKED_AUTO_TREES = 16;
+constexpr int MASKED_AUTO_TREES_F32 = 32;
 constexpr int64_t MASKED_AUTO_TOKENS = 16384;
 // Whether a validated request can run masked (types, depth, no LayerNorm, residual types).
 bool masked_shape(const Params& p);

@@ -1173,21 +1173,27 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         // * other single trees grouped by subtree at depth >= 11 from 48M elements, or from 16384
         //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16, and
         //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
+        // * eight trees at small batches grouped, its walk tree-affine (one tree per XCD: eight
+        //   times the fused kernel's workgroups, each with one tree's top levels in LDS): up to
+        //   2048 tokens in bf16 (4096 at depth >= 6; depth 5, 1024 tokens: 22 against 31 us),
+        //   1024 with fp32 weights;
         // * else the fused descent kernel.
         const bool big = p.n_trees == 1 && p.n_tokens * int64_t(p.hidden) >= (int64_t(48) << 20);
         const int64_t tiled_ws = int64_t(tiled_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
         const int64_t grouped_ws = int64_t(grouped_workspace_bytes(p.n_tokens, p.depth, p.n_trees, 0));
         const int64_t masked_ws = int64_t(masked_workspace_bytes(p.n_tokens, p.depth, p.n_trees, p.hidden));
         // Shallow layers: a token uses (D+1)/(2^(D+1)-1) of the nodes, at least 9.5 % at depth
-        // <= 5, where bf16 MFMA products beat the walk; fp32 products (about 125 TFLOP/s against
-        // the walk's 16) win down to 16 % (depth <= 4).
+        // <= 5, where bf16 MFMA products beat the walk of 16 trees or more; fp32 products (about
+        // 125 TFLOP/s against the walk's 16) win down to 16 % (depth <= 4) from 32 trees.
         const int64_t elems = p.n_tokens * int64_t(p.hidden);
         const bool one = p.n_trees == 1;
         if (subtree_auto(p))
             mode = MODE_SUBTREE;
-        else if (masked_ok && masked_shape(p) && p.depth <= (p.w_bf16 ? MASKED_AUTO_DEPTH : MASKED_AUTO_DEPTH_F32) &&
-                 (p.n_trees >= MASKED_AUTO_TREES ||
-                  (p.n_trees >= MASKED_AUTO_TREES / 2 && p.n_tokens >= MASKED_AUTO_TOKENS)) &&
+        else if (masked_ok && masked_shape(p) &&
+                 (p.w_bf16 ? p.depth <= MASKED_AUTO_DEPTH &&
+                                 (p.n_trees >= MASKED_AUTO_TREES ||
+                                  (p.n_trees >= MASKED_AUTO_TREES * 3 / 4 && p.n_tokens >= MASKED_AUTO_TOKENS))
+                           : p.depth <= MASKED_AUTO_DEPTH_F32 && p.n_trees >= MASKED_AUTO_TREES_F32) &&
                  int64_t(workspace_bytes) >= masked_ws)
             mode = MODE_MASKED;
         else if (!v) mode = MODE_GENERIC;
@@ -1199,6 +1205,9 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         else if (one && int64_t(workspace_bytes) >= grouped_ws &&
                  ((p.depth >= 11 && (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20))))) ||
                   (!p.w_bf16 && p.depth >= 5 && p.n_tokens >= 65536)))
+            mode = MODE_GROUPED;
+        else if (p.n_trees == XCDS && int64_t(workspace_bytes) >= grouped_ws &&
+                 (p.w_bf16 ? p.n_tokens <= 2048 || (p.depth >= 6 && p.n_tokens <= 4096) : p.n_tokens <= 1024))
             mode = MODE_GROUPED;
         else mode = MODE_DESCENT;
     }

@@ -580,7 +580,8 @@ def test_masked_output_modes(fff_lib, out):
 
 def test_masked_mode_limits_and_auto(fff_lib):
     """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it at depth <= 5
-    (bf16) or <= 4 (fp32) for 16 trees or more, or 8 and 16384 tokens (planning only)."""
+    for 16 bf16 trees or more, or 12 and 16384 tokens, and at depth <= 4 for 32 fp32 trees or more
+    (planning only)."""
     L = layer(430, 64, 768, 3, 8, "f32", "bf16")
     x, wi, wo = (fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out"))
     with pytest.raises(fff_lib.FffError):
@@ -596,18 +597,36 @@ def test_masked_mode_limits_and_auto(fff_lib):
         fff_lib.forward(xb[:64], w8, w8, 8, 1, mode="masked")  # depth 8
     w16 = torch.zeros((16, 15, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb[:512], w16, w16, 3, 16).startswith("masked<")  # 16 trees
+    w12 = torch.zeros((12, 15, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xb, w12, w12, 3, 12).startswith("masked<")  # 12 trees, 16384 tokens
+    assert not fff_lib.describe(xb[:8192], w12, w12, 3, 12).startswith("masked<")  # 12 trees, 8192 tokens
     w8t = torch.zeros((8, 15, 768), dtype=torch.bfloat16, device=DEV)
-    assert fff_lib.describe(xb, w8t, w8t, 3, 8).startswith("masked<")  # 8 trees, 16384 tokens
-    assert not fff_lib.describe(xb[:8192], w8t, w8t, 3, 8).startswith("masked<")  # 8 trees, 8192 tokens
+    assert not fff_lib.describe(xb, w8t, w8t, 3, 8).startswith("masked<")  # 8 trees: the walk
     w1 = torch.zeros((1, 15, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb, w1, w1, 3, 1).startswith("descent<")  # one tree: the walk
     w6 = torch.zeros((16, 127, 768), dtype=torch.bfloat16, device=DEV)
     assert not fff_lib.describe(xb[:4096], w6, w6, 6, 16).startswith("masked<")  # depth 6: the walk
     xf = torch.zeros((4096, 768), dtype=torch.float32, device=DEV)
-    w4 = torch.zeros((16, 31, 768), dtype=torch.float32, device=DEV)
-    assert fff_lib.describe(xf, w4, w4, 4, 16).startswith("masked<fp32")  # fp32, depth 4
-    w5 = torch.zeros((16, 63, 768), dtype=torch.float32, device=DEV)
-    assert not fff_lib.describe(xf, w5, w5, 5, 16).startswith("masked<")  # fp32, depth 5: the walk
+    w4 = torch.zeros((32, 31, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf, w4, w4, 4, 32).startswith("masked<fp32")  # fp32, depth 4, 32 trees
+    assert not fff_lib.describe(xf, w4[:16], w4[:16], 4, 16).startswith("masked<")  # 16 fp32 trees: the walk
+    w5 = torch.zeros((32, 63, 768), dtype=torch.float32, device=DEV)
+    assert not fff_lib.describe(xf, w5, w5, 5, 32).startswith("masked<")  # fp32, depth 5: the walk
+
+
+def test_auto_eight_trees_small_batches(fff_lib):
+    """Eight trees at small batches plan GROUPED (its walk one tree per XCD), larger batches the
+    fused DESCENT kernel (planning only)."""
+    for wd, small, large in (("bf16", 2048, 4096), ("f32", 1024, 2048)):
+        dt = torch.bfloat16 if wd == "bf16" else torch.float32
+        w = torch.zeros((8, 31, 768), dtype=dt, device=DEV)
+        for B, want in ((small, "grouped<"), (large, "descent<")):
+            x = torch.zeros((B, 768), dtype=dt, device=DEV)
+            assert fff_lib.describe(x, w, w, 4, 8).startswith(want), (wd, B)
+    w7 = torch.zeros((8, 255, 768), dtype=torch.bfloat16, device=DEV)
+    x = torch.zeros((4096, 768), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(x, w7, w7, 7, 8).startswith("grouped<")  # depth 7: up to 4096 tokens
+    assert fff_lib.describe(x[:16], w7[:4], w7[:4], 7, 4).startswith(("descent<", "subtree<"))  # four trees
 
 
 # ----------------------------------------------------- SUBTREE (a workgroup per token)
