@@ -567,6 +567,21 @@ def test_masked_f32_output_modes(fff_lib, out):
                          base_dev=base)
 
 
+@pytest.mark.parametrize("dt,out", [("f32", "residual"), ("f32", "accumulate"), ("bf16", "residual"),
+                                    ("bf16", "accumulate"), ("bf16", "store")])
+def test_masked_split_output_modes(fff_lib, dt, out):
+    """At 300 tokens the output product (K = N_T' fp32 or 2 N_T' bf16 columns) is split along K;
+    the reduction applies the layer's output form (residual, accumulate, plain store)."""
+    k, d, B = 256, 3, 300
+    L = layer(470 + len(out), B, 768, d, k, dt, dt)
+    y0 = synth.make_x(471, B, 768, dt) if out == "accumulate" else None
+    got = run_fff(fff_lib, L, d, k, dt, mode="masked", out=out, y_init=y0)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], d, k)
+    base = None if out == "store" else (L["x"] if out == "residual" else y0)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], d, k, ref, got["y"], got["nodes"],
+                         tol=1e-5 if dt == "f32" else 2e-2, base_dev=base)
+
+
 @pytest.mark.parametrize("out", ["residual", "accumulate"])
 def test_masked_output_modes(fff_lib, out):
     L = layer(420, 1000, 768, 3, 32, "bf16", "bf16")
@@ -705,10 +720,11 @@ from paper_2311_10770_amd import synth
 fff.load_library()
 dev = torch.device("cuda:0")
 out = []
-for xd, yd, k, d in (("bf16", "bf16", 512, 2), ("bf16", "f32", 64, 5), ("f32", "f32", 128, 4)):
-    L = synth.make_layer(77, 4096, 768, d, k, xd, xd)
+for xd, yd, k, d, B in (("bf16", "bf16", 512, 2, 4096), ("bf16", "f32", 64, 5, 4096), ("f32", "f32", 128, 4, 4096),
+                        ("bf16", "bf16", 3072, 0, 256), ("f32", "f32", 256, 3, 300)):
+    L = synth.make_layer(77, B, 768, d, k, xd, xd)
     x, wi, wo = (fff.from_numpy(L[n], dev) for n in ("x", "w_in", "w_out"))
-    y = torch.empty((4096, 768), dtype=torch.bfloat16 if yd == "bf16" else torch.float32, device=dev)
+    y = torch.empty((B, 768), dtype=torch.bfloat16 if yd == "bf16" else torch.float32, device=dev)
     fff.forward(x, wi, wo, d, k, y, mode="masked")
     torch.cuda.synchronize()
     out.append(hashlib.sha256(y.view(torch.uint8).cpu().numpy().tobytes()).hexdigest())
@@ -717,8 +733,9 @@ print(" ".join(out))
 
 
 def test_masked_bits_do_not_depend_on_the_process():
-    """Masked mode's products run a fixed algorithm per shape (no timing-based choice), so two fresh
-    processes produce the same output bits."""
+    """Masked mode's products run a fixed algorithm per shape (no timing-based choice; a K split and
+    its reduction order fixed by the shapes and the CU count: the 256- and 300-token cases split the
+    output product), so two fresh processes produce the same output bits."""
     import subprocess
     import sys
 
