@@ -83,6 +83,32 @@ __device__ __forceinline__ void record(const Params& p, int64_t b, int t, int l,
     if (p.logits_out) p.logits_out[rec] = logit;
 }
 
+// Depth 0: every node is its tree's root and is visited, so the selection is elementwise: each
+// thread takes eight columns of one token's row (the padding columns, past N_T, give zeros),
+// with no LDS and no barrier.
+template <bool F32>
+__global__ __launch_bounds__(SELECT_BLOCK) void select_depth0_kernel(Params p, const float* __restrict__ L,
+                                                                     void* __restrict__ Aout, int parts, int ntq) {
+    const int64_t nv = ntq / 8, nt = int64_t(p.n_trees);
+    const bool rec = p.nodes_out || p.logits_out;
+    for (int64_t i = int64_t(blockIdx.x) * SELECT_BLOCK + threadIdx.x; i < p.n_tokens * nv;
+         i += int64_t(gridDim.x) * SELECT_BLOCK) {
+        const int64_t b = i / nv;
+        const int v = int(i - b * nv);
+        const float4* lrow = reinterpret_cast<const float4*>(L + b * ntq) + 2 * v;
+        const float4 l0 = lrow[0], l1 = lrow[1];
+        const float lg[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+        float val[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int t = 8 * v + k;
+            val[k] = t < nt ? activation(lg[k], p.act) : 0.0f;
+            if (rec && t < nt) record(p, b, t, 0, 0, lg[k]);
+        }
+        emit8<F32>(Aout, b, v, ntq, parts, val);
+    }
+}
+
 // One workgroup per token, its row of logits (ntq <= SELECT_LDS_COLS) staged in
 // LDS with 16-byte loads: a thread per tree walks its tree there, replacing each
 // visited node's logit by its activation and flagging it; then the row of A is
@@ -238,7 +264,14 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
         if (e != hipSuccess) return e;
     }
     const int nq = int(ntq);
-    if (ntq <= SELECT_LDS_COLS) {
+    if (p.depth == 0) {
+        const int64_t work = B * (ntq / 8);
+        const unsigned blocks = unsigned(std::min<int64_t>((work + SELECT_BLOCK - 1) / SELECT_BLOCK, int64_t(cu_count > 0 ? cu_count : 256) * 16));
+        if (f32)
+            hipLaunchKernelGGL(select_depth0_kernel<true>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, 1, nq);
+        else
+            hipLaunchKernelGGL(select_depth0_kernel<false>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, P, nq);
+    } else if (ntq <= SELECT_LDS_COLS) {
         const size_t lds = size_t(ntq) * (sizeof(float) + 1);
         if (f32)
             hipLaunchKernelGGL(select_staged_kernel<true>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
