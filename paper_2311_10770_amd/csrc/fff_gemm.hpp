@@ -42,8 +42,8 @@ __device__ __forceinline__ int swz(int r16) {
 
 // The compiler is not told that this load writes LDS (it would otherwise wait for every
 // outstanding load before each LDS read): completion is awaited by wait_vmem and a barrier.
-// m0 is written nowhere else in these kernels, so its clobber (which the compiler warns about, m0
-// being reserved) is safe.
+// m0 is written nowhere else in these kernels (their assembly writes it only in these sequences),
+// so its clobber (which the compiler warns about, m0 being reserved) is safe.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
