@@ -215,27 +215,33 @@ def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out
 _WORKSPACES: dict = {}
 
 
-def workspace_for(n_tokens: int, depth: int, n_trees: int, hidden: int, device) -> torch.Tensor:
-    """A cached device workspace large enough for grouped mode (reused across calls on one device;
-    calls that overlap on different streams must pass their own)."""
+def workspace_for(n_tokens: int, depth: int, n_trees: int, hidden: int, device, stream=None) -> torch.Tensor:
+    """A cached device workspace large enough for every mode, one per (device, stream): calls on one
+    stream run in order and share it; calls on different streams never share one.  A larger
+    request replaces the stream's buffer (torch frees the old one in that stream's order)."""
     need = workspace_bytes(n_tokens, depth, n_trees, hidden, 0)
     dev = torch.device(device)
-    ws = _WORKSPACES.get(dev)
+    if dev.index is None:
+        dev = torch.device(dev.type, torch.cuda.current_device())
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    key = (dev, int(s.cuda_stream))
+    ws = _WORKSPACES.get(key)
     if ws is None or ws.numel() < need:
-        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
-        _WORKSPACES[dev] = ws
+        with torch.cuda.stream(s):
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        _WORKSPACES[key] = ws
     return ws
 
 
 def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=None, **kw):
     """FFF forward through ``fff_forward_ex``; returns y (allocated if not given).
 
-    In auto and grouped mode a cached per-device workspace is passed unless ``workspace`` is
-    given (calls that may overlap on different streams must pass their own)."""
+    In the modes that need scratch a cached workspace of the call's device and stream is passed
+    unless ``workspace`` is given."""
     if y is None:
         y = torch.empty(x.shape, dtype=y_dtype or x.dtype, device=x.device)
     if kw.get("mode", "auto") in ("grouped", "auto", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
-        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device, kw.get("stream"))
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     lib = load_library()
     with torch.cuda.device(x.device):
@@ -290,7 +296,7 @@ def forward_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw):
     if y is None:
         y = torch.empty_like(x)
     if kw.get("mode", "auto") in ("auto", "grouped", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
-        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device, kw.get("stream"))
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     with torch.cuda.device(x.device):
         _check(load_library().fff_forward_stack(ctypes.byref(a), arr, len(layers)))
@@ -301,7 +307,7 @@ def describe_stack(x, layers, depth: int, n_trees: int = 1, y=None, **kw) -> str
     if y is None:
         y = torch.empty_like(x)
     if kw.get("mode", "auto") in ("auto", "grouped", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
-        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device, kw.get("stream"))
     a, arr = _stack_args(x, layers, depth, n_trees, y, kw)
     buf = ctypes.create_string_buffer(512)
     with torch.cuda.device(x.device):
@@ -353,10 +359,13 @@ def backward(x, w_in, w_out, depth: int, n_trees: int, dy, leaves, logits, *, dx
         _dev_tensor(dx, "dx", device)
     if (dw_in is not None or dw_out is not None) and workspace is None:
         need = backward_workspace_bytes(B, depth, n_trees, H)
-        ws = _BWD_WORKSPACES.get(device)
+        s = stream if stream is not None else torch.cuda.current_stream(device)
+        key = (device, int(s.cuda_stream))  # one per (device, stream), as for the forward
+        ws = _BWD_WORKSPACES.get(key)
         if ws is None or ws.numel() < need:
-            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
-            _BWD_WORKSPACES[device] = ws
+            with torch.cuda.stream(s):
+                ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+            _BWD_WORKSPACES[key] = ws
         workspace = ws
     a = FffBackwardArgs()
     a.x = x.data_ptr() if x is not None else None
@@ -398,7 +407,7 @@ def describe(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, **kw) -> str:
         y = torch.empty(x.shape, dtype=kw.pop("y_dtype", None) or x.dtype, device=x.device)
     kw.pop("y_dtype", None)
     if kw.get("mode", "auto") in ("grouped", "auto", "tiled", "masked", 0, 2, 4, 5) and kw.get("workspace") is None:
-        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device)
+        kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device, kw.get("stream"))
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     buf = ctypes.create_string_buffer(512)
     with torch.cuda.device(x.device):

@@ -629,6 +629,31 @@ def test_masked_mode_limits_and_auto(fff_lib):
     assert not fff_lib.describe(xf, w5, w5, 5, 32).startswith("masked<")  # fp32, depth 5: the walk
 
 
+def test_binding_workspace_per_stream(fff_lib):
+    """The binding's cached workspace is one per (device, stream): two tiled forwards enqueued on two
+    streams at once, each on its own inputs, both match the oracle, on different buffers."""
+    d, B = 9, 8192
+    Ls = [layer(480 + i, B, 768, d, 1, "bf16", "bf16") for i in range(2)]
+    dev_in = [[fff_lib.from_numpy(L[k], DEV) for k in ("x", "w_in", "w_out")] for L in Ls]
+    ys = [torch.empty((B, 768), dtype=torch.bfloat16, device=DEV) for _ in Ls]
+    recs = [torch.empty((B, 1, d + 1), dtype=torch.int32, device=DEV) for _ in Ls]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    main = torch.cuda.current_stream()
+    for s in streams:
+        s.wait_stream(main)
+    for i, s in enumerate(streams):
+        with torch.cuda.stream(s):
+            x, wi, wo = dev_in[i]
+            fff_lib.forward(x, wi, wo, d, 1, ys[i], mode="tiled", nodes_out=recs[i])
+    torch.cuda.synchronize()
+    w = [fff_lib.fff.workspace_for(B, d, 1, 768, DEV, s).data_ptr() for s in streams]
+    assert w[0] != w[1]
+    for i, L in enumerate(Ls):
+        ref = oracle.forward(L["x"], L["w_in"], L["w_out"], d, 1)
+        parity.assert_parity(L["x"], L["w_in"], L["w_out"], d, 1, ref, fff_lib.to_numpy(ys[i]),
+                             recs[i].cpu().numpy(), tol=2e-2)
+
+
 def test_auto_eight_trees_small_batches(fff_lib):
     """Eight trees at small batches plan GROUPED (its walk one tree per XCD), larger batches the
     fused DESCENT kernel (planning only)."""
