@@ -629,6 +629,17 @@ def test_masked_mode_limits_and_auto(fff_lib):
     assert not fff_lib.describe(xf, w5, w5, 5, 32).startswith("masked<")  # fp32, depth 5: the walk
 
 
+@pytest.mark.parametrize("dt,B,d", [("bf16", 1024, 5), ("bf16", 4096, 7), ("f32", 1024, 4)])
+def test_auto_eight_trees_grouped_parity(fff_lib, dt, B, d):
+    """What AUTO plans for eight trees at small batches (GROUPED, its walk one tree per XCD) against
+    the oracle."""
+    L = layer(490 + d, B, 768, d, 8, dt, dt)
+    x = fff_lib.from_numpy(L["x"], DEV)
+    wi = fff_lib.from_numpy(L["w_in"], DEV)
+    assert fff_lib.describe(x, wi, wi, d, 8).startswith("grouped<")
+    check_layer(fff_lib, f"auto 8 trees {dt} B={B} d={d}", L, d, 8, dt)
+
+
 def test_binding_workspace_per_stream(fff_lib):
     """The binding's cached workspace is one per (device, stream): two tiled forwards enqueued on two
     streams at once, each on its own inputs, both match the oracle, on different buffers."""
