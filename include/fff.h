@@ -73,11 +73,15 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * and activations in the workspace, then the output rows are accumulated with
  * tokens grouped by their tree-0 node at a split level, each group's subtree
  * handled by the workgroups of one XCD so that its rows stay in that XCD's L2.
+ * With 2, 4 or 8 trees (GROUPED and TILED) each walk workgroup walks the tree
+ * of its XCD, with that tree's top levels in LDS.
  * GENERIC: any hidden size, one wave per token.
- * TILED: one tree, depth 5..15, hidden a multiple of 128: the walk drops each
- * token into a bucket of its leaf, and the output rows of up to 16 tokens that
- * share a leaf (hence all D+1 nodes) are accumulated as one dense product on
- * MFMA: fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
+ * TILED: 1..16 trees, depth 5..15, hidden a multiple of 128: the walk drops
+ * each token into a bucket of its leaf in every tree, and the output rows of up
+ * to 16 tokens that share a leaf (hence all D+1 nodes) are accumulated as one
+ * dense product on MFMA, one launch per tree in tree order, each adding its
+ * tree to the running sum (fp32 y in place; for a bf16 y an fp32 row of the
+ * workspace, rounded once by the last tree): fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
  * activations split into bf16 parts (three parts: fp32 working accuracy; two,
  * relative error about 2^-17, when y is bf16 and either stored or the residual
  * of bf16 x).  When more tokens reach a leaf than its bucket holds, all of
