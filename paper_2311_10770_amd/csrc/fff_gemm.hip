@@ -44,7 +44,7 @@ __device__ __forceinline__ void gemm_store(void* C, const void* src, int64_t ldc
 // Workgroup (blockIdx.x, blockIdx.y): tile xcd_tile(blockIdx.x) of C over K elements
 // [blockIdx.y kchunk, +kchunk) (kchunk a whole number of steps; one chunk unless K is split, when C
 // is the partial sums [gridDim.y][M][ldc] and OUT is GOUT_F32).
-template <bool BF, int TM, int TN, int WGM, int WGN, int S, int OUT, bool DBF>
+template <bool BF, int TM, int TN, int WGM, int WGN, int S, bool M32, int OUT, bool DBF>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_dma_kernel(const void* __restrict__ A,
                                                                      const void* __restrict__ B, void* C,
                                                                      const void* src, int64_t M, int64_t N,
@@ -61,20 +61,37 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_dma_kernel(const void*
     const int64_t kb = int64_t(blockIdx.y) * kchunk, kl = K - kb < kchunk ? K - kb : kchunk;
     const int esz = BF ? 2 : 4;
     if (gridDim.y > 1) C = static_cast<float*>(C) + int64_t(blockIdx.y) * M * ldc;
-    tile_v4f acc[TM][TN];
-    dma_product<BF, TM, TN, WGM, WGN, S>(static_cast<const char*>(A) + kb * esz, static_cast<const char*>(B) + kb * esz,
-                                         M, N, kl, lda, ldb, m0, n0, gsm, acc);
+    WaveAcc<TM, TN, M32> acc;
+    dma_product<BF, TM, TN, WGM, WGN, S, M32>(static_cast<const char*>(A) + kb * esz,
+                                              static_cast<const char*>(B) + kb * esz, M, N, kl, lda, ldb, m0, n0, gsm,
+                                              acc);
+    if constexpr (M32) {
+        // 32 x 32 result: lane l, register r holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+        const int r32 = lane & 31, hv = lane >> 5;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM / 2; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t n = n0 + wn * 16 * TN + j * 16 + r16;
+            for (int j = 0; j < TN / 2; ++j) {
+                const int64_t n = n0 + wn * 16 * TN + j * 32 + r32;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t m = m0 + wm * 16 * TM + i * 16 + 4 * q + r;
-                if (m < M && n < N) gemm_store<OUT, DBF>(C, src, ldc, m, n, acc[i][j][r]);
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t m = m0 + wm * 16 * TM + i * 32 + 8 * (r / 4) + 4 * hv + (r % 4);
+                    if (m < M && n < N) gemm_store<OUT, DBF>(C, src, ldc, m, n, acc.t[i][j][r]);
+                }
             }
-        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t n = n0 + wn * 16 * TN + j * 16 + r16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int64_t m = m0 + wm * 16 * TM + i * 16 + 4 * q + r;
+                    if (m < M && n < N) gemm_store<OUT, DBF>(C, src, ldc, m, n, acc.t[i][j][r]);
+                }
+            }
+    }
 }
 
 // C = sum over the splits of the partial sums, in split order, through the product's store.
@@ -105,7 +122,8 @@ void launch_dma(const void* A, const void* B, void* C, const void* src, int64_t 
                 int64_t lda, int64_t ldb, int64_t ldc, hipStream_t stream, int splits = 1, int64_t kchunk = 0) {
     using G = DmaCfg<TM, TN, WGM, WGN, S>;
     const dim3 grid(unsigned(((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM)), unsigned(splits));
-    hipLaunchKernelGGL((gemm_nt_dma_kernel<BF, TM, TN, WGM, WGN, S, OUT, DBF>), grid, dim3(G::THREADS), G::LDS, stream,
+    // bf16 on 32 x 32 x 16 MFMA tiles (twice the 16 x 16 x 32 rate per flop); fp32 on 16 x 16 x 4
+    hipLaunchKernelGGL((gemm_nt_dma_kernel<BF, TM, TN, WGM, WGN, S, BF, OUT, DBF>), grid, dim3(G::THREADS), G::LDS, stream,
                        A, B, C, src, M, N, K, lda, ldb, ldc, splits > 1 ? kchunk : K);
 }
 
