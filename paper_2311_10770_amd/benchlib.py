@@ -4,7 +4,7 @@ from __future__ import annotations
 
 import ctypes
 import time
-from ctypes import c_char_p, c_int, c_int32, c_int64, c_void_p
+from ctypes import c_double, c_char_p, c_int, c_int32, c_int64, c_void_p
 from pathlib import Path
 
 import torch
@@ -34,6 +34,8 @@ def load():
         lib.fffb_mb_read.restype = c_int
         lib.fffb_mb_gather.argtypes = [c_void_p, c_int64, c_int, c_int, c_int, c_int, c_void_p, c_void_p]
         lib.fffb_mb_gather.restype = c_int
+        lib.fffb_mb_mfma.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p]
+        lib.fffb_mb_mfma.restype = c_double
         _lib = lib
     return _lib
 

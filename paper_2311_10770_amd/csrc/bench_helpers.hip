@@ -150,6 +150,46 @@ __global__ void mb_gather_kernel(const uint4* __restrict__ table, int64_t rows, 
     if (acc == 0x7fffffffu) out[0] = acc;
 }
 
+// mb_mfma: the matrix cores' issue rate.  Every wave runs `iters` rounds of NACC independent MFMAs
+// on register operands (no memory traffic); launched with 1, 2 or 4 waves per SIMD.
+typedef __bf16 mb_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float mb_v4f __attribute__((ext_vector_type(4)));
+typedef float mb_v16f __attribute__((ext_vector_type(16)));
+
+template <int SHAPE, int NACC>
+__global__ __launch_bounds__(256) void mb_mfma_kernel(int iters, float seed, float* out) {
+    mb_bf16x8 a, b;
+    for (int i = 0; i < 8; ++i) {
+        a[i] = (__bf16)(seed * float(threadIdx.x + i));
+        b[i] = (__bf16)(seed - float(i));
+    }
+    const float af = seed * float(threadIdx.x), bf = seed - 1.0f;
+    float s = 0.0f;
+    if constexpr (SHAPE == 0 || SHAPE == 2) {
+        mb_v4f acc[NACC];
+        for (int j = 0; j < NACC; ++j) acc[j] = mb_v4f{0.f, 0.f, 0.f, 0.f};
+        for (int it = 0; it < iters; ++it)
+#pragma unroll
+            for (int j = 0; j < NACC; ++j) {
+                if constexpr (SHAPE == 0) acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+                else acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af, bf, acc[j], 0, 0, 0);
+            }
+        for (int j = 0; j < NACC; ++j) s += acc[j][0];
+    } else {
+        mb_v16f acc[NACC];
+        for (int j = 0; j < NACC; ++j)
+            for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+        for (int it = 0; it < iters; ++it)
+#pragma unroll
+            for (int j = 0; j < NACC; ++j) {
+                if constexpr (SHAPE == 1) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+                else acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af, bf, acc[j], 0, 0, 0);
+            }
+        for (int j = 0; j < NACC; ++j) s += acc[j][0];
+    }
+    out[int64_t(blockIdx.x) * blockDim.x + threadIdx.x] = s;
+}
+
 }  // namespace
 
 FFFB_EXPORT int fffb_mb_read(const void* buf, int64_t footprint_bytes, int64_t total_bytes, void* out, int grid,
@@ -236,4 +276,25 @@ FFFB_EXPORT int fffb_copy(const void* src, void* dst, int64_t bytes, void* strea
     hipLaunchKernelGGL(copy_kernel, dim3(unsigned(grid)), dim3(block), 0, reinterpret_cast<hipStream_t>(stream),
                        reinterpret_cast<const uint4*>(src), reinterpret_cast<uint4*>(dst), n);
     return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+// shape: 0 = 16x16x32 bf16, 1 = 32x32x16 bf16, 2 = 16x16x4 fp32, 3 = 32x32x2 fp32 (16 or 8 independent
+// accumulators per wave); blocks of four waves, waves_per_simd blocks per CU; out: blocks x 256 floats.
+// Returns the flops one launch performs, or a negative value.
+FFFB_EXPORT double fffb_mb_mfma(int shape, int cus, int waves_per_simd, int iters, void* out, void* stream) {
+    if (cus < 1 || waves_per_simd < 1 || iters < 1 || shape < 0 || shape > 3) return -1.0;
+    const int blocks = cus * waves_per_simd;
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    float* o = reinterpret_cast<float*>(out);
+    const double waves = double(blocks) * 4, per_mfma[4] = {16.0 * 16 * 32 * 2, 32.0 * 32 * 16 * 2, 16.0 * 16 * 4 * 2,
+                                                              32.0 * 32 * 2 * 2};
+    const int nacc = shape == 0 || shape == 2 ? 16 : 8;
+    switch (shape) {
+        case 0: hipLaunchKernelGGL((mb_mfma_kernel<0, 16>), dim3(blocks), dim3(256), 0, st, iters, 0.5f, o); break;
+        case 1: hipLaunchKernelGGL((mb_mfma_kernel<1, 8>), dim3(blocks), dim3(256), 0, st, iters, 0.5f, o); break;
+        case 2: hipLaunchKernelGGL((mb_mfma_kernel<2, 16>), dim3(blocks), dim3(256), 0, st, iters, 0.5f, o); break;
+        default: hipLaunchKernelGGL((mb_mfma_kernel<3, 8>), dim3(blocks), dim3(256), 0, st, iters, 0.5f, o); break;
+    }
+    if (hipGetLastError() != hipSuccess) return -2.0;
+    return waves * iters * nacc * per_mfma[shape];
 }

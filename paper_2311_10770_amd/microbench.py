@@ -6,7 +6,9 @@
   only HBM;
 * 1.5 KB row gathers by 16-lane groups (one bf16 row at hidden 768) from
   tables of those sizes, with independent row ids or a dependent chain (each
-  row id computed from the previous row, like a tree walk).
+  row id computed from the previous row, like a tree walk);
+* the matrix cores' issue rate for the 16x16 and 32x32 MFMA shapes in bf16 and
+  fp32 at 1, 2 and 4 waves per SIMD (register operands, no memory traffic).
 Prints one JSON object.
 """
 from __future__ import annotations
@@ -59,6 +61,18 @@ def main():
                                       "GBps": by / t / 1e9, "us": t * 1e6})
                 print(f"gather table {fp / 2**20:7.0f} MiB dep={dep} groups {groups:6d}: {by / t / 1e9:8.0f} GB/s "
                       f"({t * 1e6:.1f} us)", file=sys.stderr, flush=True)
+    res["mfma"] = []
+    names = {0: "16x16x32 bf16", 1: "32x32x16 bf16", 2: "16x16x4 fp32", 3: "32x32x2 fp32"}
+    mout = torch.empty(cus * 4 * 256, dtype=torch.float32, device=dev)
+    for shape in (0, 1, 2, 3):
+        for wps in (1, 2, 4):
+            flops = lib.fffb_mb_mfma(shape, cus, wps, 1000, mout.data_ptr(), st)
+            if flops < 0:
+                raise RuntimeError("fffb_mb_mfma failed")
+            t = _time(lambda: lib.fffb_mb_mfma(shape, cus, wps, 1000, mout.data_ptr(), st))
+            res["mfma"].append({"shape": names[shape], "waves_per_simd": wps, "TFLOPs": flops / t / 1e12})
+            print(f"mfma {names[shape]:14s} waves/SIMD {wps}: {flops / t / 1e12:7.1f} TFLOP/s", file=sys.stderr,
+                  flush=True)
     print(json.dumps(res))
 
 
