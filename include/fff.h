@@ -86,8 +86,11 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * relative error about 2^-17, when y is bf16 and either stored or the residual
  * of bf16 x).  When more tokens reach a leaf than its bucket holds, all of
  * that leaf's tokens take the per-token emit instead, so the output bits do
- * not depend on the order in which the walk filled the bucket's slots.  Needs
- * the workspace of fff_workspace_bytes.
+ * not depend on the order in which the walk filled the bucket's slots.  A call
+ * with more than (2^31 - 1) / (4 hidden) tokens (699050 at hidden 768) runs as
+ * consecutive chunks of that many tokens, each a complete tiled forward (the
+ * output stores use 32-bit offsets).  Needs the workspace of
+ * fff_workspace_bytes.
  * MASKED: bf16 x and W, or fp32 x, W and y; depth <= 7, no LayerNorm (a
  * residual needs y of x's type): the layer as two dense products around the
  * walk, for shallow trees
@@ -223,7 +226,7 @@ int fff_forward_static(const fff_args* a);
  * tokens: one fp32 activation per visited node and one int32 leaf per (token,
  * tree), plus for TILED the leaf buckets (int32 counts; token slots, a few
  * times the mean tokens per leaf, each with its D+1 fp32 activations; a spill
- * list), and at depth <= 7 MASKED's logits of every node (fp32), their bf16
+ * list; for one chunk of tokens at most), and at depth <= 7 MASKED's logits of every node (fp32), their bf16
  * parts, W_out transposed and repeated three times and 32 MiB for the
  * partial sums of a product split along K (few tokens).  The result
  * covers every mode; the split level (-1..depth) does not change it.

@@ -38,7 +38,6 @@ struct Params {
     int32_t* bk_spill;    // [T, B] tokens that found their bucket full
     int32_t* bk_nspill;   // [T] how many
     float* bk_act;        // [T, 2^D, bk_cap, TILE_REC] activations of the bucketed tokens, by slot
-    void* bk_junk;        // target of the stores of empty tile rows
     int32_t bk_cap;
     int32_t tile_tree;    // the tree a tile launch accumulates
     const void* tile_src; // [B, H] row the tile launch adds its result to (or null)

@@ -405,23 +405,6 @@ constexpr int TILE_MAX_STEPS = 4;  // fp32 weights: depth <= 15, at most 16 leve
 // (larger workgroups would cap the registers of the spill path below 128).
 constexpr int tile_waves(int h) { return h / 128 < 8 ? h / 128 : 8; }
 
-template <bool WBF>
-__device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out) {
-    if constexpr (WBF) {
-        const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(w) + at);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            out[2 * j] = bf16_lo(word(v, j));
-            out[2 * j + 1] = bf16_hi(word(v, j));
-        }
-    } else {
-        const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(w) + at);
-        const float4 b = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(w) + at + 4);
-        out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
-        out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
-    }
-}
-
 // Output forms of the tile kernel, fixed at compile time: the tile's result is
 // added to a source row (none; fp32; bf16) and written to a destination row
 // (fp32 or bf16).  One tree: the source is x (residual), y (accumulate) or
@@ -433,30 +416,53 @@ __device__ __forceinline__ void tile_load8(const void* w, int64_t at, float* out
 // for the prefetched operands without draining the stores.
 enum { TSRC_NONE = 0, TSRC_F32 = 1, TSRC_BF16 = 2 };
 
-// Bytes of the junk area that stores of empty tile rows are sent to: one
-// 32-byte slot per lane of 128 wave slots.
-constexpr size_t TILE_JUNK_BYTES = 128 * 64 * 32;
+// The tile kernel's stores and source loads go through buffer resources over the
+// [B, H] row blocks with 32-bit byte offsets; a forward whose fp32 rows would
+// reach 2^31 bytes runs in chunks of this many tokens (the offset TILE_NO_ROW of
+// empty rows then lies past every block).
+static int64_t tile_chunk_tokens(int64_t hidden) { return ((int64_t(1) << 31) - 1) / (4 * hidden); }
 
-// Eight consecutive output columns of one token: add the source and store.
-// src / dst point at the eight elements (or at junk).
+// Eight consecutive output columns of one token: add the source and store,
+// through buffer resources over the source and destination rows.  An offset
+// past the resource's size (TILE_NO_ROW) makes the hardware drop the store and
+// read zeros, without a memory access.
+typedef uint32_t tile_u4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t TILE_NO_ROW = 0x80000000u;
+
 template <int SRC, bool DBF>
-__device__ __forceinline__ void tile_store8(const void* src, void* dst, const float* v8) {
+__device__ __forceinline__ void tile_store8_buf(__amdgpu_buffer_rsrc_t rs, uint32_t os, __amdgpu_buffer_rsrc_t rd,
+                                                uint32_t od, const float* v8) {
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = v8[i];
-    if constexpr (SRC != TSRC_NONE) {
-        float b[8];
-        tile_load8<SRC == TSRC_BF16>(src, 0, b);
+    if constexpr (SRC == TSRC_F32) {
+        const tile_u4 a = __builtin_amdgcn_raw_buffer_load_b128(rs, int(os), 0, 0);
+        const tile_u4 b = __builtin_amdgcn_raw_buffer_load_b128(rs, int(os + 16), 0, 0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += b[i];
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t ai = a[i], bi = b[i];  // scalar copies: this compiler bit-casts a vector element as element 0
+            v[i] += __builtin_bit_cast(float, ai);
+            v[4 + i] += __builtin_bit_cast(float, bi);
+        }
+    } else if constexpr (SRC == TSRC_BF16) {
+        const tile_u4 a = __builtin_amdgcn_raw_buffer_load_b128(rs, int(os), 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] += bf16_lo(a[i]);
+            v[2 * i + 1] += bf16_hi(a[i]);
+        }
     }
     if constexpr (DBF) {
-        *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                                    pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+        const tile_u4 d = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                           pack_bf16x2(v[6], v[7])};
+        __builtin_amdgcn_raw_buffer_store_b128(d, rd, int(od), 0, 0);
     } else {
-        float4* d = reinterpret_cast<float4*>(dst);
-        d[0] = make_float4(v[0], v[1], v[2], v[3]);
-        d[1] = make_float4(v[4], v[5], v[6], v[7]);
+        const tile_u4 d0 = {__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
+                            __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])};
+        const tile_u4 d1 = {__builtin_bit_cast(uint32_t, v[4]), __builtin_bit_cast(uint32_t, v[5]),
+                            __builtin_bit_cast(uint32_t, v[6]), __builtin_bit_cast(uint32_t, v[7])};
+        __builtin_amdgcn_raw_buffer_store_b128(d0, rd, int(od), 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(d1, rd, int(od + 16), 0, 0);
     }
 }
 
@@ -568,24 +574,29 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     const int n = lane & 15, kq = lane >> 4;
     constexpr int SSZ = SRC == TSRC_BF16 ? 2 : 4;
     constexpr int DSZ = DBF ? 2 : 4;
-    char* const junk = reinterpret_cast<char*>(p.bk_junk) + ((int64_t(blockIdx.x) * WAVES + wave) % 128 * 64 + lane) * 32;
+    // Stores and source loads through buffer resources over the row blocks (the
+    // host keeps B H 4 below 2^31): rows of empty slots are dropped by the hardware.
+    const int row_elems = int(p.n_tokens * H);
+    const __amdgpu_buffer_rsrc_t rdst = __builtin_amdgcn_make_buffer_rsrc(p.tile_dst, 0, row_elems * DSZ, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(SRC != TSRC_NONE ? p.tile_src : p.tile_dst), 0, row_elems * SSZ, 0x00020000);
     // Every load below is in bounds and unconditional (slots and levels are
     // clamped; values past the count or past D are replaced by 0 where used), so
     // each path through a tile issues the same memory operations.
 
     // stores of one tile's outputs: lane (n, kq) holds tokens 4 kq + r of the
-    // tile, whose ids come from the lanes that loaded them; empty rows go to junk
+    // tile, whose ids come from the lanes that loaded them
     auto store_tile = [&](int32_t tok_a, const tile_v4f* acc, int64_t col) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int32_t tok = __shfl(tok_a, 4 * kq + r, 64);
             const int64_t e = int64_t(tok) * H + col;
-            void* yd = tok >= 0 ? static_cast<char*>(p.tile_dst) + e * DSZ : junk;
-            const void* xs = tok >= 0 && SRC != TSRC_NONE ? static_cast<const char*>(p.tile_src) + e * SSZ : junk;
             float v8[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
-            tile_store8<SRC, DBF>(xs, yd, v8);
+            const uint32_t od = tok >= 0 ? uint32_t(e * DSZ) : TILE_NO_ROW;
+            const uint32_t os = tok >= 0 ? uint32_t(e * SSZ) : TILE_NO_ROW;
+            tile_store8_buf<SRC, DBF>(rsrc, os, rdst, od, v8);
         }
     };
 
@@ -1094,16 +1105,17 @@ static int32_t tile_cap(int64_t n_tokens, int32_t depth) {
 
 // Tiled workspace, in order: token records and leaves (as grouped; the records
 // are used by spilled tokens only), bucket counts + spill counts, bucket token
-// ids, spill lists, bucket activation records, the junk area for empty tile
-// rows, and with several trees an fp32 [B, H] running sum (used when y is bf16).
+// ids, spill lists, bucket activation records, and with several trees an fp32
+// [B, H] running sum (used when y is bf16); B is at most one chunk of tokens.
 size_t tiled_workspace_bytes(int64_t n_tokens, int32_t depth, int32_t n_trees, int32_t hidden) {
     if (!tiled_shape(depth, n_trees, hidden)) return 0;
+    n_tokens = std::min(n_tokens, tile_chunk_tokens(hidden));
     const size_t T = size_t(n_trees);
     const size_t leaves = size_t(1) << depth;
     const size_t cap = size_t(tile_cap(n_tokens, depth));
     return grouped_workspace_bytes(n_tokens, depth, n_trees, 0) + align256(T * (leaves + 1) * sizeof(int32_t)) +
            align256(T * leaves * cap * sizeof(int32_t)) + align256(T * size_t(n_tokens) * sizeof(int32_t)) +
-           align256(T * leaves * cap * size_t(TILE_REC) * sizeof(float)) + TILE_JUNK_BYTES +
+           align256(T * leaves * cap * size_t(TILE_REC) * sizeof(float)) +
            (T > 1 ? align256(size_t(n_tokens) * size_t(hidden) * sizeof(float)) : 0);
 }
 
@@ -1336,6 +1348,59 @@ hipError_t run_stack(const StackParams& sp, const Plan& plan, hipStream_t stream
     return hipLaunchKernel(L.kernel, dim3(L.grid), dim3(L.block), args, L.lds_bytes, stream);
 }
 
+// One tiled forward (fill, walk, one tile launch per tree) over the tokens of p.
+static hipError_t run_tiled(const Params& p, const Plan& plan, void* workspace, hipStream_t stream) {
+    const size_t T = size_t(p.n_trees);
+    const size_t recs = size_t(p.n_tokens) * T;
+    const int64_t leaves = int64_t(1) << p.depth;
+    char* ws = static_cast<char*>(workspace);
+    Params q = p;
+    q.lds_levels = plan.lds_levels;
+    q.walk_affine = plan.walk_affine;
+    q.ws_act = reinterpret_cast<float*>(ws);
+    ws += align256(recs * size_t(p.depth + 1) * sizeof(float));
+    q.ws_leaf = reinterpret_cast<int32_t*>(ws);
+    ws += align256(recs * sizeof(int32_t));
+    q.bk_count = reinterpret_cast<int32_t*>(ws);
+    q.bk_nspill = q.bk_count + T * leaves;
+    ws += align256(T * (size_t(leaves) + 1) * sizeof(int32_t));
+    q.bk_cap = tile_cap(p.n_tokens, p.depth);
+    q.bk_tok = reinterpret_cast<int32_t*>(ws);
+    ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * sizeof(int32_t));
+    q.bk_spill = reinterpret_cast<int32_t*>(ws);
+    ws += align256(T * size_t(p.n_tokens) * sizeof(int32_t));
+    q.bk_act = reinterpret_cast<float*>(ws);
+    ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * size_t(TILE_REC) * sizeof(float));
+    void* sum = p.y_bf16 && T > 1 ? static_cast<void*>(ws) : p.y;  // fp32 running sum over trees
+    q.split_level = plan.split_level;
+    int32_t* fa = q.bk_count;
+    int64_t fn = int64_t(T) * (leaves + 1);
+    void* fargs[] = {&fa, &fn};
+    const Launch& F = plan.launch[0];
+    hipError_t e = hipLaunchKernel(F.kernel, dim3(F.grid), dim3(F.block), fargs, 0, stream);
+    if (e != hipSuccess) return e;
+    void* wargs[] = {&q};
+    const Launch& W = plan.launch[1];
+    e = hipLaunchKernel(W.kernel, dim3(W.grid), dim3(W.block), wargs, W.lds_bytes, stream);
+    if (e != hipSuccess) return e;
+    const Variant* v = find_variant(p);
+    const Launch& E = plan.launch[2];
+    int leaf_blocks = int(leaves);
+    const void* src0 = out_src_kind(p) == TSRC_NONE ? nullptr : p.out_mode == OUT_RESIDUAL ? p.x : p.y;
+    // trees in order: tree t adds its contribution to the running sum of trees 0..t-1 (a fixed
+    // order of the sum over trees, so the output bits do not depend on scheduling)
+    for (int t = 0; t < int(T); ++t) {
+        Params qt = q;
+        qt.tile_tree = t;
+        qt.tile_src = t > 0 ? sum : src0;
+        qt.tile_dst = t == int(T) - 1 ? p.y : sum;
+        void* targs[] = {&qt, &leaf_blocks};
+        e = hipLaunchKernel(tile_kernel_for(*v, p, t), dim3(E.grid), dim3(E.block), targs, 0, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_t workspace_bytes,
                        hipStream_t stream) {
     if (plan.kind == KIND_MASKED) return run_masked(p, workspace, plan.cu_count, stream);
@@ -1352,52 +1417,19 @@ hipError_t run_forward(const Params& p, const Plan& plan, void* workspace, size_
         (void)workspace_bytes;
     }
     if (plan.kind == KIND_TILED) {
-        const size_t T = size_t(p.n_trees);
-        const size_t recs = size_t(p.n_tokens) * T;
-        const int64_t leaves = int64_t(1) << p.depth;
-        char* ws = static_cast<char*>(workspace);
-        q.ws_act = reinterpret_cast<float*>(ws);
-        ws += align256(recs * size_t(p.depth + 1) * sizeof(float));
-        q.ws_leaf = reinterpret_cast<int32_t*>(ws);
-        ws += align256(recs * sizeof(int32_t));
-        q.bk_count = reinterpret_cast<int32_t*>(ws);
-        q.bk_nspill = q.bk_count + T * leaves;
-        ws += align256(T * (size_t(leaves) + 1) * sizeof(int32_t));
-        q.bk_cap = tile_cap(p.n_tokens, p.depth);
-        q.bk_tok = reinterpret_cast<int32_t*>(ws);
-        ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * sizeof(int32_t));
-        q.bk_spill = reinterpret_cast<int32_t*>(ws);
-        ws += align256(T * size_t(p.n_tokens) * sizeof(int32_t));
-        q.bk_act = reinterpret_cast<float*>(ws);
-        ws += align256(T * size_t(leaves) * size_t(q.bk_cap) * size_t(TILE_REC) * sizeof(float));
-        q.bk_junk = ws;
-        ws += TILE_JUNK_BYTES;
-        void* sum = p.y_bf16 && T > 1 ? static_cast<void*>(ws) : p.y;  // fp32 running sum over trees
-        q.split_level = plan.split_level;
-        (void)workspace_bytes;
-        int32_t* fa = q.bk_count;
-        int64_t fn = int64_t(T) * (leaves + 1);
-        void* fargs[] = {&fa, &fn};
-        const Launch& F = plan.launch[0];
-        hipError_t e = hipLaunchKernel(F.kernel, dim3(F.grid), dim3(F.block), fargs, 0, stream);
-        if (e != hipSuccess) return e;
-        void* wargs[] = {&q};
-        const Launch& W = plan.launch[1];
-        e = hipLaunchKernel(W.kernel, dim3(W.grid), dim3(W.block), wargs, W.lds_bytes, stream);
-        if (e != hipSuccess) return e;
-        const Variant* v = find_variant(p);
-        const Launch& E = plan.launch[2];
-        int leaf_blocks = int(leaves);
-        const void* src0 = out_src_kind(p) == TSRC_NONE ? nullptr : p.out_mode == OUT_RESIDUAL ? p.x : p.y;
-        // trees in order: tree t adds its contribution to the running sum of trees 0..t-1 (a fixed
-        // order of the sum over trees, so the output bits do not depend on scheduling)
-        for (int t = 0; t < int(T); ++t) {
-            Params qt = q;
-            qt.tile_tree = t;
-            qt.tile_src = t > 0 ? sum : src0;
-            qt.tile_dst = t == int(T) - 1 ? p.y : sum;
-            void* targs[] = {&qt, &leaf_blocks};
-            e = hipLaunchKernel(tile_kernel_for(*v, p, t), dim3(E.grid), dim3(E.block), targs, 0, stream);
+        // The tile kernel addresses [B, H] row blocks with 32-bit offsets, so a call whose fp32
+        // rows would not fit them runs as consecutive token chunks, each a complete tiled forward
+        // in the same workspace (sized for one chunk).
+        const int64_t chunk = tile_chunk_tokens(p.hidden);
+        const int64_t H = p.hidden, R = int64_t(p.n_trees) * (p.depth + 1);
+        for (int64_t c0 = 0; c0 < p.n_tokens; c0 += chunk) {
+            Params c = p;
+            c.n_tokens = std::min(chunk, p.n_tokens - c0);
+            c.x = static_cast<const char*>(p.x) + c0 * H * (p.x_bf16 ? 2 : 4);
+            c.y = static_cast<char*>(p.y) + c0 * H * (p.y_bf16 ? 2 : 4);
+            if (p.nodes_out) c.nodes_out = p.nodes_out + c0 * R;
+            if (p.logits_out) c.logits_out = p.logits_out + c0 * R;
+            const hipError_t e = run_tiled(c, plan, workspace, stream);
             if (e != hipSuccess) return e;
         }
         return hipSuccess;

@@ -447,6 +447,37 @@ def test_tiled_headline_full_size(fff_lib):
     check_layer(fff_lib, "tiled headline", L, w.depth, w.n_trees, w.y_dtype, mode="tiled")
 
 
+@pytest.mark.parametrize("case", ["bf16_2trees_store", "f32_residual"])
+def test_tiled_token_chunks(fff_lib, case):
+    """A tiled call whose fp32 rows pass 2^31 bytes runs as consecutive token chunks of
+    (2^31 - 1) / (4 H) tokens: 700000 tokens at H = 768 are 699050 + 4950.  Every output row is
+    written (no NaN left, every node recorded); tokens at the start, on both sides of the seam
+    and at the end match the oracle (two trees with a bf16 y: the fp32 running sum of each
+    chunk; fp32 residual: the source rows of each chunk)."""
+    B, H, D = 700000, 768, 11
+    chunk = ((1 << 31) - 1) // (4 * H)
+    T, dt, out = (2, "bf16", "store") if case == "bf16_2trees_store" else (1, "f32", "residual")
+    x = synth.make_x(240, B, H, dt)
+    wi, wo = synth.make_weights(240, H, D, T, dt)
+    flush_print(f"[gpu] tiled token chunks {case}: B={B} chunk={chunk}")
+    xd, wid, wod = (fff_lib.from_numpy(a, DEV) for a in (x, wi, wo))
+    y = torch.full((B, H), float("nan"), dtype=TORCH_DT[dt], device=DEV)
+    nodes = torch.full((B, T, D + 1), -7, dtype=torch.int32, device=DEV)
+    assert fff_lib.describe(xd, wid, wod, D, T, mode="tiled", out=out).startswith("tiled<")
+    fff_lib.forward(xd, wid, wod, D, T, y, nodes_out=nodes, mode="tiled", out=out)
+    torch.cuda.synchronize()
+    assert not bool(torch.isnan(y).any()) and bool((nodes >= 0).all())
+    idx = np.r_[0:256, chunk - 256:chunk + 256, B - 256:B]
+    it = torch.from_numpy(idx).to(DEV)
+    got_y = fff_lib.to_numpy(y.index_select(0, it))
+    got_nodes = nodes.index_select(0, it).cpu().numpy()
+    del y, nodes, xd
+    xs = x[idx]
+    ref = oracle.forward(xs, wi, wo, D, T)
+    parity.assert_parity(xs, wi, wo, D, T, ref, got_y, got_nodes, tol=tol_for(dt, dt),
+                         base_dev=xs if out == "residual" else None)
+
+
 @pytest.mark.parametrize("yd", ["f32", "bf16"])
 def test_tiled_with_layernorm(fff_lib, yd):
     """The leaf-tiled path behind the LayerNorm prologue, with the residual: y = x + FFF(LN(x)),
