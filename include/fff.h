@@ -113,12 +113,15 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * them in LDS, then loads the path's W_out rows together.  Reads up to 63/6
  * times the W_in rows of a walk.
  * AUTO (from measurements on MI355X): SUBTREE for at most 4 trees of depth
- * >= 5 and 256 token-tree pairs (32 at hidden 4096); MASKED at depth <= 5
+ * >= 5 and 256 token-tree pairs (32 at hidden 4096, 128 with fp32 W at depth
+ * 11 or more); MASKED at depth <= 5
  * for 16 bf16 trees or more (12 from 16384 tokens), or at depth <= 4 for 32
  * fp32 trees or more, when the workspace covers it; for single-tree layers whose
  * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
  * leaf and 48M input elements (tokens x hidden), or 16 tokens per leaf and
- * 16M elements (bf16 W at depth 9: from 96M elements); else GROUPED at depth
+ * 16M elements (bf16 W at depth 9: from 96M elements), and at depth 11 or
+ * more with 8 tokens per leaf (fp32 W) or 4 per leaf at hidden 2048 or more
+ * (bf16 W); else GROUPED at depth
  * 11 or more from 48M elements, or from 16384 tokens with fp32 W or 24M
  * elements, and with fp32 W at depth 5 or more from 65536 tokens; GROUPED
  * for 8 trees up to 2048 tokens with bf16 W (4096 at depth 6 or more) or

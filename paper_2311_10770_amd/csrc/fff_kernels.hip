@@ -1180,8 +1180,12 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         //   12.3 us);
         // * shallow layers with many trees as dense products (masked; see its constants);
         // * single trees of depth 9..15 leaf-tiled on MFMA with at least 8 tokens per leaf from
-        //   48M input elements, or 16 per leaf from 16M (depth 11 at 32768 tokens: 52 against
+        //   48M input elements, or 16 per leaf from 16M (depth 11 at 32768 tokens: 51 against
         //   60 us in bf16); at depth 9 in bf16 only from 96M (the fused kernel stays ahead below);
+        //   with fp32 weights at depth >= 11 from 8 per leaf (16384 tokens: 64 against 67 us per
+        //   call, 61 against 67 back to back); in bf16 at depth >= 11 from 4 per leaf when the
+        //   rows are long (hidden 4096, 8192 tokens: 107 against 113 us; at hidden 768 the
+        //   grouped emit is ahead at 4 per leaf, depth 13: 80 against 86 us);
         // * other single trees grouped by subtree at depth >= 11 from 48M elements, or from 16384
         //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16, and
         //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
@@ -1212,7 +1216,9 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         else if (tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws && p.depth >= 9 &&
                  (!p.w_bf16 || p.depth >= 10 || elems >= (int64_t(96) << 20)) &&
                  ((big && p.n_tokens >= (int64_t(8) << p.depth)) ||
-                  (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth))))
+                  (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth)) ||
+                  (one && !p.w_bf16 && p.depth >= 11 && p.n_tokens >= (int64_t(8) << p.depth)) ||
+                  (one && p.w_bf16 && p.depth >= 11 && p.hidden >= 2048 && p.n_tokens >= (int64_t(4) << p.depth))))
             mode = MODE_TILED;
         else if (one && int64_t(workspace_bytes) >= grouped_ws &&
                  ((p.depth >= 11 && (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20))))) ||

@@ -229,7 +229,10 @@ const char* subtree_name(const Params& p) {
 
 bool subtree_auto(const Params& p) {
     if (!subtree_shape(p) || p.depth < SUBTREE_AUTO_DEPTH || p.n_trees > SUBTREE_AUTO_TREES) return false;
-    return p.n_tokens * p.n_trees <= (p.hidden <= 1024 ? SUBTREE_AUTO_PAIRS : SUBTREE_AUTO_PAIRS_WIDE);
+    const int64_t pairs = p.hidden > 1024                           ? SUBTREE_AUTO_PAIRS_WIDE
+                          : !p.w_bf16 && p.depth >= SUBTREE_DEEP_F32 ? SUBTREE_AUTO_PAIRS_DEEP_F32
+                                                                     : SUBTREE_AUTO_PAIRS;
+    return p.n_tokens * p.n_trees <= pairs;
 }
 
 int subtree_block(const Params& p) {

@@ -357,7 +357,13 @@ def test_describe_names_the_kernel(fff_lib):
     assert d.startswith("descent<"), d
     xf = torch.zeros((16384, 768), dtype=torch.float32, device=DEV)
     wf = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.float32, device=DEV)
-    assert fff_lib.describe(xf, wf, wf, 11, 1).startswith("grouped<")  # fp32, 16384 tokens
+    assert fff_lib.describe(xf, wf, wf, 11, 1).startswith("tiled<")  # fp32, 16384 tokens: 8 per leaf
+    assert fff_lib.describe(xf[:8192], wf, wf, 11, 1).startswith("descent<")  # 4 per leaf
+    xw = torch.zeros((8192, 4096), dtype=torch.bfloat16, device=DEV)
+    ww = torch.zeros((1, (1 << 12) - 1, 4096), dtype=torch.bfloat16, device=DEV)
+    assert fff_lib.describe(xw, ww, ww, 11, 1).startswith("tiled<")  # 4 per leaf, hidden 4096
+    assert fff_lib.describe(xw[:4096], ww, ww, 11, 1).startswith("descent<")  # 2 per leaf
+    del xw, ww
     w9 = torch.zeros((1, (1 << 10) - 1, 768), dtype=torch.bfloat16, device=DEV)
     xb9 = torch.zeros((32768, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb9, w9, w9, 9, 1).startswith("descent<")  # bf16 depth 9, 32768 tokens
@@ -755,7 +761,7 @@ def test_subtree_output_modes(fff_lib, out, xd, wd):
 
 def test_subtree_auto_and_limits(fff_lib):
     """AUTO takes SUBTREE for at most 4 trees of depth >= 5 and 256 token-tree pairs (32 at hidden
-    4096); no LayerNorm, no other widths."""
+    4096, 128 with fp32 weights from depth 11); no LayerNorm, no other widths."""
     xb = torch.zeros((300, 768), dtype=torch.bfloat16, device=DEV)
     w11 = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xb[:256], w11, w11, 11, 1).startswith("subtree<")
@@ -772,6 +778,13 @@ def test_subtree_auto_and_limits(fff_lib):
     w12 = torch.zeros((1, (1 << 13) - 1, 4096), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(x4[:32], w12, w12, 12, 1).startswith("subtree<")
     assert not fff_lib.describe(x4[:33], w12, w12, 12, 1).startswith("subtree<")
+    # fp32 weights from depth 11: 128 pairs
+    xf = torch.zeros((300, 768), dtype=torch.float32, device=DEV)
+    wf11 = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf[:128], wf11, wf11, 11, 1).startswith("subtree<")
+    assert fff_lib.describe(xf[:129], wf11, wf11, 11, 1).startswith("descent<")
+    wf9 = torch.zeros((1, (1 << 10) - 1, 768), dtype=torch.float32, device=DEV)
+    assert fff_lib.describe(xf[:256], wf9, wf9, 9, 1).startswith("subtree<")
     x5 = torch.zeros((4, 640), dtype=torch.bfloat16, device=DEV)
     w5w = torch.zeros((1, 63, 640), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(fff_lib.FffError):
