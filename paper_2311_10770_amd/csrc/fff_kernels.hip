@@ -981,6 +981,7 @@ struct Variant {
     int hidden;
     bool xbf, wbf;
     int lanes;
+    int walk_lanes;  // the walk kernel's lanes per token (its own registers: x and one row, no output)
     int emit_lanes;  // the emit has no cross-lane reduction: wider groups hold fewer registers per lane
     const void* descent;
     const void* walk;
@@ -999,33 +1000,35 @@ struct Variant {
     {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false>),                                       \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true>),                                        \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true>)}
-#define FFF_VARIANT(H, XB, WB, L, NV, EL, ENV)                                                                \
+#define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, EL, ENV)                                                      \
     Variant {                                                                                                 \
-        H, XB, WB, L, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                                 \
-            FFF_K(walk_kernel<L, NV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),      \
+        H, XB, WB, L, WL, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                             \
+            FFF_K(walk_kernel<WL, WNV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),  \
             {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE), FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32),                \
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16)},                                                       \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
-            FFF_K(walk_kernel<L, NV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
+            FFF_K(walk_kernel<WL, WNV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
     }
 
 static const Variant kVariants[] = {
-    // H = 768 (BERT-base width); the emit takes 32 (bf16 W) or 64 (fp32 W) lanes per token
-    FFF_VARIANT(768, true, true, 16, 6, 32, 3),
-    FFF_VARIANT(768, false, true, 16, 6, 32, 3),
-    FFF_VARIANT(768, false, false, 32, 6, 64, 3),
-    FFF_VARIANT(768, true, false, 32, 6, 64, 3),
+    // H = 768 (BERT-base width); the emit takes 32 (bf16 W) or 64 (fp32 W) lanes per token, the
+    // walk 16 (with fp32 W: 124 VGPRs and four waves per SIMD, 64 tokens in flight per CU against
+    // 48 with 32 lanes; the fused kernel keeps 32, its output accumulators need the registers)
+    FFF_VARIANT(768, true, true, 16, 6, 16, 6, 32, 3),
+    FFF_VARIANT(768, false, true, 16, 6, 16, 6, 32, 3),
+    FFF_VARIANT(768, false, false, 32, 6, 16, 12, 64, 3),
+    FFF_VARIANT(768, true, false, 32, 6, 16, 12, 64, 3),
     // H = 1024
-    FFF_VARIANT(1024, true, true, 16, 8, 32, 4),
-    FFF_VARIANT(1024, false, true, 16, 8, 32, 4),
-    FFF_VARIANT(1024, false, false, 32, 8, 64, 4),
-    FFF_VARIANT(1024, true, false, 32, 8, 64, 4),
+    FFF_VARIANT(1024, true, true, 16, 8, 16, 8, 32, 4),
+    FFF_VARIANT(1024, false, true, 16, 8, 16, 8, 32, 4),
+    FFF_VARIANT(1024, false, false, 32, 8, 32, 8, 64, 4),
+    FFF_VARIANT(1024, true, false, 32, 8, 32, 8, 64, 4),
     // H = 4096 (LLM width)
-    FFF_VARIANT(4096, true, true, 64, 8, 64, 8),
-    FFF_VARIANT(4096, false, true, 64, 8, 64, 8),
-    FFF_VARIANT(4096, false, false, 64, 16, 64, 16),
-    FFF_VARIANT(4096, true, false, 64, 16, 64, 16),
+    FFF_VARIANT(4096, true, true, 64, 8, 64, 8, 64, 8),
+    FFF_VARIANT(4096, false, true, 64, 8, 64, 8, 64, 8),
+    FFF_VARIANT(4096, false, false, 64, 16, 64, 16, 64, 16),
+    FFF_VARIANT(4096, true, false, 64, 16, 64, 16, 64, 16),
 };
 
 static const void* generic_kernel_for(bool xbf, bool wbf) {
@@ -1160,7 +1163,7 @@ static bool plan_walk(const Params& p, const Variant& v, int lds_levels_req, con
     W.kernel = p.norm ? v.walk_norm : v.walk;
     W.block = WALK_BLOCK;
     W.lds_bytes = rows_lds_bytes(one, kw, 1);
-    const int64_t groups = token_groups(p, v.lanes) * (affine ? p.n_trees : 1);
+    const int64_t groups = token_groups(p, v.walk_lanes) * (affine ? p.n_trees : 1);
     int64_t want = (groups + WALK_BLOCK / 64 - 1) / (WALK_BLOCK / 64);
     if (affine) want = (want + XCDS - 1) / XCDS * XCDS;
     W.grid = resident_grid(dev, W.kernel, W.lds_bytes, want, WALK_BLOCK);
@@ -1252,7 +1255,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
     if (mode == MODE_TILED) {
         if (!tiled_shape(p.depth, p.n_trees, p.hidden)) return ST_UNSUPPORTED;
         plan->kind = KIND_TILED;
-        plan->lanes = v->lanes;
+        plan->lanes = v->walk_lanes;
         plan->emit_lanes = v->emit_lanes;
         plan->split_level = std::min<int>(p.depth - 2, 5);  // subtrees of at least four leaves
         plan->name = v->name;
@@ -1296,7 +1299,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         const int ke = pick_levels(p, lds_levels_req, 1, EMIT_LDS_BUDGET, dev.lds_per_block, &ok_e);
         if (!ok_e) return ST_UNSUPPORTED;
         plan->kind = KIND_GROUPED;
-        plan->lanes = v->lanes;
+        plan->lanes = v->walk_lanes;
         plan->split_level = split;
         plan->name = v->name;
         Launch& W = plan->launch[plan->n_launch++];
