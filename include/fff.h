@@ -123,9 +123,15 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * more with 8 tokens per leaf (fp32 W) or 4 per leaf at hidden 2048 or more
  * (bf16 W); else GROUPED at depth
  * 11 or more from 48M elements, or from 16384 tokens with fp32 W or 24M
- * elements, and with fp32 W at depth 5 or more from 65536 tokens; GROUPED
- * for 8 trees up to 2048 tokens with bf16 W (4096 at depth 6 or more) or
- * 1024 with fp32 W (the workspace covering it); otherwise DESCENT when a
+ * elements, and with fp32 W at depth 5 or more from 65536 tokens; for 2, 4
+ * or 8 trees of depth 7 or more (the walk tree-affine), with fp32 W TILED at
+ * depth 11 or more from 8 tokens per leaf or, with 4 or 8 trees, at depth 9
+ * or more from 65536 tokens, else GROUPED from 65536 tokens (16384 with 8
+ * trees), and with bf16 W GROUPED for 8 trees, for 4 from 4096 tokens at
+ * depth 8 or more (65536 at depth 7) and for 2 from 65536 tokens at depth 8
+ * or more; GROUPED for 8 trees up to 2048 tokens with bf16 W (4096 at depth
+ * 6 or more) or 1024 with fp32 W (the workspace covering it); otherwise
+ * DESCENT when a
  * kernel is compiled for the hidden size and types, else GENERIC. */
 typedef enum {
     FFF_MODE_AUTO = 0,

@@ -1192,6 +1192,15 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         // * other single trees grouped by subtree at depth >= 11 from 48M elements, or from 16384
         //   tokens with fp32 weights (depth 11: 66 against 70 us) or 24M elements in bf16, and
         //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
+        // * 2, 4 or 8 trees of depth >= 7 (the walk tree-affine: the workgroups of an XCD walk
+        //   one tree, its top levels in LDS and its deep rows in that XCD's L2): with fp32 weights
+        //   leaf-tiled at depth >= 11 from 8 tokens per leaf and, with 4 or 8 trees, at depth >= 9
+        //   from 65536 tokens (eight trees of depth 11, 65536 tokens: 1561 against 2579 us fused;
+        //   four of depth 9: 590 against 664; at 16384 tokens 155.5 against 160.1 back to back, but
+        //   as the residual of a 12-layer stack 171 against 169 per layer), else grouped from
+        //   65536 tokens (16384 with 8 trees); with bf16 weights grouped for 8 trees, for 4 from
+        //   4096 tokens at depth >= 8 (65536 at depth 7), for 2 from 65536 tokens at depth >= 8
+        //   (four trees of depth 9, 65536 tokens: 272 against 306 us);
         // * eight trees at small batches grouped, its walk tree-affine (one tree per XCD: eight
         //   times the fused kernel's workgroups, each with one tree's top levels in LDS): up to
         //   2048 tokens in bf16 (4096 at depth >= 6; depth 5, 1024 tokens: 22 against 31 us),
@@ -1206,6 +1215,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         // 125 TFLOP/s against the walk's 16) win down to 16 % (depth <= 4) from 32 trees.
         const int64_t elems = p.n_tokens * int64_t(p.hidden);
         const bool one = p.n_trees == 1;
+        const bool affine = p.n_trees > 1 && XCDS % p.n_trees == 0;  // 2, 4 or 8 trees: tree-affine walk
         if (subtree_auto(p))
             mode = MODE_SUBTREE;
         else if (masked_ok && masked_shape(p) &&
@@ -1226,6 +1236,15 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         else if (one && int64_t(workspace_bytes) >= grouped_ws &&
                  ((p.depth >= 11 && (big || (p.n_tokens >= 16384 && (!p.w_bf16 || elems >= (int64_t(24) << 20))))) ||
                   (!p.w_bf16 && p.depth >= 5 && p.n_tokens >= 65536)))
+            mode = MODE_GROUPED;
+        else if (affine && !p.w_bf16 && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws &&
+                 ((p.depth >= 11 && p.n_tokens >= (int64_t(8) << p.depth)) ||
+                  (p.n_trees >= 4 && p.depth >= 9 && p.n_tokens >= 65536)))
+            mode = MODE_TILED;
+        else if (affine && int64_t(workspace_bytes) >= grouped_ws && p.depth >= 7 &&
+                 (p.w_bf16 ? p.n_trees == XCDS || (p.n_trees == 4 && p.n_tokens >= (p.depth >= 8 ? 4096 : 65536)) ||
+                                 (p.depth >= 8 && p.n_tokens >= 65536)
+                           : p.n_tokens >= 65536 || (p.n_trees == XCDS && p.n_tokens >= 16384)))
             mode = MODE_GROUPED;
         else if (p.n_trees == XCDS && int64_t(workspace_bytes) >= grouped_ws &&
                  (p.w_bf16 ? p.n_tokens <= 2048 || (p.depth >= 6 && p.n_tokens <= 4096) : p.n_tokens <= 1024))

@@ -253,12 +253,14 @@ def test_twelve_layer_4x9_stack_full_size(fff_lib):
     x = dev(fff_lib, xs)
     kw = dict(norm="layernorm", norm_eps=EPS)
     flush_print(f"[gpu] 12x 4x9: {fff_lib.describe_stack(x, dl, D, T, mode='descent', **kw)}")
+    # AUTO: per-layer launches of the fused kernel
     assert fff_lib.describe_stack(x, dl, D, T, **kw).startswith("per-layer descent")
     ys = fff_lib.forward_stack(x, dl, D, T, mode="descent", **kw)
     yc, outs, nodes = chained(fff_lib, x, dl, D, T, True, "descent", records=True)
+    ya, _, _ = chained(fff_lib, x, dl, D, T, True, "auto")
     torch.cuda.synchronize()
     assert torch.equal(ys, yc)
-    assert torch.equal(fff_lib.forward_stack(x, dl, D, T, **kw), yc)  # AUTO: per-layer launches
+    assert torch.equal(fff_lib.forward_stack(x, dl, D, T, **kw), ya)
     rows = np.random.default_rng(0).choice(B, 1024, replace=False)
     x_last = fff_lib.to_numpy(outs[-2])[rows]
     lay = layers[-1]

@@ -702,6 +702,42 @@ def test_binding_workspace_per_stream(fff_lib):
                              recs[i].cpu().numpy(), tol=2e-2)
 
 
+def test_auto_multi_tree_deep_plans(fff_lib):
+    """2, 4 or 8 trees of depth >= 7 plan the tree-affine walk: leaf-tiled with fp32 weights at
+    depth >= 11 from 8 tokens per leaf or, with 4 or 8 trees, at depth >= 9 from 65536 tokens;
+    otherwise GROUPED at large batches; the fused kernel below (planning only)."""
+    def plan(T, d, B, dt):
+        t = torch.bfloat16 if dt == "bf16" else torch.float32
+        x = torch.zeros((B, 768), dtype=t, device=DEV)
+        w = torch.zeros((T, (1 << (d + 1)) - 1, 768), dtype=t, device=DEV)
+        return fff_lib.describe(x, w, w, d, T).split("<")[0]
+    assert plan(4, 9, 16384, "f32") == "descent"    # UltraFastBERT-4x9 at 16384 tokens
+    assert plan(4, 9, 65536, "f32") == "tiled"
+    assert plan(4, 8, 16384, "f32") == "descent"    # depth 8
+    assert plan(8, 11, 65536, "f32") == "tiled"
+    assert plan(2, 11, 16384, "f32") == "tiled"     # 8 per leaf at depth 11
+    assert plan(2, 9, 65536, "f32") == "grouped"    # two trees: not tiled at depth 9
+    assert plan(8, 8, 16384, "f32") == "grouped"
+    assert plan(4, 7, 16384, "f32") == "descent"
+    assert plan(4, 9, 4096, "bf16") == "grouped"
+    assert plan(4, 7, 16384, "bf16") == "descent"   # depth 7: from 65536 tokens
+    assert plan(2, 9, 16384, "bf16") == "descent"
+    assert plan(2, 9, 65536, "bf16") == "grouped"
+    assert plan(8, 7, 65536, "bf16") == "grouped"
+    assert plan(4, 6, 65536, "bf16") == "descent"   # depth 6
+
+
+@pytest.mark.parametrize("T,d,B,dt,want", [(4, 9, 4096, "bf16", "grouped<"), (8, 8, 16384, "f32", "grouped<"),
+                                           (2, 11, 16384, "f32", "tiled<")])
+def test_auto_multi_tree_deep_parity(fff_lib, T, d, B, dt, want):
+    """The plans AUTO takes for deep multi-tree layers against the oracle."""
+    L = layer(520 + T + d, B, 768, d, T, dt, dt)
+    x = fff_lib.from_numpy(L["x"], DEV)
+    wi = fff_lib.from_numpy(L["w_in"], DEV)
+    assert fff_lib.describe(x, wi, wi, d, T).startswith(want)
+    check_layer(fff_lib, f"auto {T} trees {dt} B={B} d={d}", L, d, T, dt)
+
+
 def test_auto_eight_trees_small_batches(fff_lib):
     """Eight trees at small batches plan GROUPED (its walk one tree per XCD), larger batches the
     fused DESCENT kernel (planning only)."""
