@@ -400,6 +400,9 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
 // are handled by extra workgroups with the per-token emit.
 
 constexpr int TILE_MAX_STEPS = 4;  // fp32 weights: depth <= 15, at most 16 levels, four steps of four
+// fp32 weights up to depth 11 take three steps: the B operands of the fourth step would hold eight
+// more VGPRs per lane (94 against 106: five waves per SIMD instead of four)
+constexpr int TILE_STEPS_SHALLOW = 3;
 
 // Waves per tiled workgroup for hidden size h: one per 128-column group, at most 8
 // (larger workgroups would cap the registers of the spill path below 128).
@@ -500,8 +503,9 @@ __device__ __forceinline__ void store_token_sd(const void* src, void* dst, float
 // the subtree at the split level), then spill workgroups.  ELANES/ENV: the
 // per-token emit layout for tokens of overflowing leaves; SRC/DBF: the output
 // form (p.tile_src, p.tile_dst); P2: two bf16 parts of each activation (the
-// layer's output is bf16) instead of three.
-template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2>
+// layer's output is bf16) instead of three.  FSTEPS: MFMA steps of four levels
+// with fp32 weights (at least (D + 4) / 4; unused with bf16 weights).
+template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2, int FSTEPS>
 __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
     constexpr int H = 16 * CB;
     static_assert(H % 128 == 0, "128-column groups");
@@ -691,12 +695,12 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
     } else {
         const int steps = (D + 4) / 4;
         // level of step s for this lane, clamped to D
-        int lvl_c[TILE_MAX_STEPS];
+        int lvl_c[FSTEPS];
 #pragma unroll
-        for (int s = 0; s < TILE_MAX_STEPS; ++s) lvl_c[s] = 4 * s + kq <= D ? 4 * s + kq : D;
+        for (int s = 0; s < FSTEPS; ++s) lvl_c[s] = 4 * s + kq <= D ? 4 * s + kq : D;
         struct Raw {
             int32_t tok;
-            float a[TILE_MAX_STEPS];
+            float a[FSTEPS];
         };
         // token id of slot t0 + n and its activations at levels 4s + kq
         auto load_tile = [&](int t0, Raw& r) {
@@ -704,15 +708,15 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             r.tok = bucket[slot];
             const float* rec = act + int64_t(slot) * TILE_REC;
 #pragma unroll
-            for (int s = 0; s < TILE_MAX_STEPS; ++s) r.a[s] = rec[lvl_c[s]];
+            for (int s = 0; s < FSTEPS; ++s) r.a[s] = rec[lvl_c[s]];
         };
         for (int g = wave; g < GROUPS; g += WAVES) {
             const int64_t col = int64_t(g) * 128 + 8 * n;
             // B operand: this lane's eight weights of the row at level 4s + kq, kept
             // as loaded for all of the leaf's tiles
-            float4 w[TILE_MAX_STEPS][2];
+            float4 w[FSTEPS][2];
 #pragma unroll
-            for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+            for (int s = 0; s < FSTEPS; ++s) {
                 const int64_t at = (int64_t(leaf1 >> (D - lvl_c[s])) - 1) * H + col;
                 w[s][0] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at);
                 w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + 4);
@@ -724,7 +728,7 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 #pragma unroll
                 for (int j = 0; j < 8; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int s = 0; s < TILE_MAX_STEPS; ++s) {
+                for (int s = 0; s < FSTEPS; ++s) {
                     if (s < steps) {
                         const float a = in && 4 * s + kq <= D ? cur.a[s] : 0.0f;
 #pragma unroll
@@ -987,6 +991,7 @@ struct Variant {
     const void* walk;
     const void* emit;
     const void* tile[3][3];  // [source TSRC_*][form: fp32 dst 3 parts, fp32 dst 2 parts, bf16 dst 2 parts]
+    const void* tile_deep[3][3];  // the same for fp32 weights deeper than TILE_STEPS_SHALLOW steps
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -996,16 +1001,22 @@ struct Variant {
 };
 
 #define FFF_K(...) reinterpret_cast<const void*>(&__VA_ARGS__)
-#define FFF_TILES(H, XB, WB, EL, ENV, SRC)                                                                    \
-    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false>),                                       \
-     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true>),                                        \
-     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true>)}
+#define FFF_TILES(H, XB, WB, EL, ENV, SRC, FS)                                                                \
+    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, FS>),                                   \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, FS>),                                    \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, FS>)}
+// bf16 weights take one instantiation for both arrays
+#define FFF_TILE_STEPS(WB) ((WB) ? TILE_MAX_STEPS : TILE_STEPS_SHALLOW)
 #define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, EL, ENV)                                                      \
     Variant {                                                                                                 \
         H, XB, WB, L, WL, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                             \
             FFF_K(walk_kernel<WL, WNV, XB, WB, WALK_BLOCK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),  \
-            {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE), FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32),                \
-             FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16)},                                                       \
+            {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE, FFF_TILE_STEPS(WB)),                                    \
+             FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32, FFF_TILE_STEPS(WB)),                                     \
+             FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16, FFF_TILE_STEPS(WB))},                                   \
+            {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE, TILE_MAX_STEPS),                                        \
+             FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32, TILE_MAX_STEPS),                                         \
+             FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16, TILE_MAX_STEPS)},                                       \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<WL, WNV, false, WB, WALK_BLOCK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -1145,7 +1156,8 @@ static int tile_src_kind(const Params& p, int t) { return t > 0 ? int(TSRC_F32) 
 static const void* tile_kernel_for(const Variant& v, const Params& p, int t) {
     const bool last = t == p.n_trees - 1;
     const int form = last && p.y_bf16 ? 2 : p.y_bf16 ? 1 : 0;
-    return v.tile[tile_src_kind(p, t)][form];
+    return (p.depth + 4) / 4 <= TILE_STEPS_SHALLOW ? v.tile[tile_src_kind(p, t)][form]
+                                                   : v.tile_deep[tile_src_kind(p, t)][form];
 }
 
 // The walk launch of the grouped and tiled plans: with 2, 4 or 8 trees one tree per workgroup
