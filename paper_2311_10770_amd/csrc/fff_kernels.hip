@@ -375,10 +375,13 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
 //     Y[16 tokens, H] = A[16 tokens, D+1 levels] x W_out[path rows, H],
 // with A the tokens' activations.  One workgroup takes one leaf; its wave w
 // takes the 128-column groups g = w, w + waves, ...  Every 16x16 MFMA used here
-// returns D[4(l/16)+r][l%16] to lane l, register r; in group g, MFMA column n of
-// block j is output column 128 g + 8 n + j, so a lane holds eight consecutive
-// output columns of four tokens and sixteen lanes write 256 contiguous bytes
-// of a token's row.
+// returns D[4(l/16)+r][l%16] to lane l, register r.  In group g, MFMA column n
+// of block j is output column 128 g + 8 n + j when y is bf16, so a lane holds
+// eight consecutive output columns of four tokens and sixteen lanes write 256
+// contiguous bytes of a token's row; when y is fp32 it is output column
+// 128 g + 64 (j/4) + 4 n + j%4, and the two halves (blocks 0..3, then 4..7) are
+// computed and stored in turn, sixteen lanes writing 256 contiguous bytes per
+// half, so four accumulators are live at a time instead of eight.
 //
 // bf16 weights: v_mfma_f32_16x16x32_bf16 takes 32 (level, part) products per
 // lane group.  Lane group q = l/16 covers levels 8(q%2) .. 8(q%2)+7; each
@@ -387,13 +390,13 @@ __global__ __launch_bounds__(BLOCK) void emit_kernel(Params p) {
 // group q supplies part q/2 in the first MFMA and part q/2 + 2 (lo, or zero)
 // in the second.  Two parts (hi + mid, relative error about 2^-17) are used
 // when y is stored in bf16, whose own rounding is 2^-9.  The B operand of
-// lane (n, q) for block j is the column 128 g + 8n + j of its eight path rows:
-// eight 16-byte row loads, transposed in registers once per leaf.  Products
-// of bf16 values are exact; the MFMA accumulates in fp32.
+// lane (n, q) for block j is that block's column of its eight path rows: eight
+// 16-byte row loads (sixteen of 8 bytes for an fp32 y), transposed in registers
+// once per leaf.  Products of bf16 values are exact; the MFMA accumulates in fp32.
 //
 // fp32 weights: v_mfma_f32_16x16x4_f32, four levels per step: lane l supplies
-// A[l%16][l/16] (token l%16, level 4s + l/16) and the eight weights of its
-// level's row for blocks j = 0..7 from one 32-byte load.
+// A[l%16][l/16] (token l%16, level 4s + l/16) and the weights of its level's
+// row for blocks j = 0..7 from two 16-byte loads, one per half.
 //
 // Activation records of bucketed tokens are TILE_REC floats apart (depth at
 // most 15).  Tokens whose bucket was full (more than bk_cap reached one leaf)
@@ -430,6 +433,7 @@ static int64_t tile_chunk_tokens(int64_t hidden) { return ((int64_t(1) << 31) - 
 // past the resource's size (TILE_NO_ROW) makes the hardware drop the store and
 // read zeros, without a memory access.
 typedef uint32_t tile_u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t tile_u2 __attribute__((ext_vector_type(2)));
 constexpr uint32_t TILE_NO_ROW = 0x80000000u;
 
 template <int SRC, bool DBF>
@@ -466,6 +470,35 @@ __device__ __forceinline__ void tile_store8_buf(__amdgpu_buffer_rsrc_t rs, uint3
                             __builtin_bit_cast(uint32_t, v[6]), __builtin_bit_cast(uint32_t, v[7])};
         __builtin_amdgcn_raw_buffer_store_b128(d0, rd, int(od), 0, 0);
         __builtin_amdgcn_raw_buffer_store_b128(d1, rd, int(od + 16), 0, 0);
+    }
+}
+
+// The same for four consecutive columns.
+template <int SRC, bool DBF>
+__device__ __forceinline__ void tile_store4_buf(__amdgpu_buffer_rsrc_t rs, uint32_t os, __amdgpu_buffer_rsrc_t rd,
+                                                uint32_t od, const float* v4) {
+    float v[4] = {v4[0], v4[1], v4[2], v4[3]};
+    if constexpr (SRC == TSRC_F32) {
+        const tile_u4 a = __builtin_amdgcn_raw_buffer_load_b128(rs, int(os), 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t ai = a[i];  // a scalar copy: this compiler bit-casts a vector element as element 0
+            v[i] += __builtin_bit_cast(float, ai);
+        }
+    } else if constexpr (SRC == TSRC_BF16) {
+        const tile_u2 a = __builtin_amdgcn_raw_buffer_load_b64(rs, int(os), 0, 0);
+        v[0] += bf16_lo(a[0]);
+        v[1] += bf16_hi(a[0]);
+        v[2] += bf16_lo(a[1]);
+        v[3] += bf16_hi(a[1]);
+    }
+    if constexpr (DBF) {
+        const tile_u2 d = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        __builtin_amdgcn_raw_buffer_store_b64(d, rd, int(od), 0, 0);
+    } else {
+        const tile_u4 d = {__builtin_bit_cast(uint32_t, v[0]), __builtin_bit_cast(uint32_t, v[1]),
+                           __builtin_bit_cast(uint32_t, v[2]), __builtin_bit_cast(uint32_t, v[3])};
+        __builtin_amdgcn_raw_buffer_store_b128(d, rd, int(od), 0, 0);
     }
 }
 
@@ -590,17 +623,27 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 
     // stores of one tile's outputs: lane (n, kq) holds tokens 4 kq + r of the
     // tile, whose ids come from the lanes that loaded them
+    // Column layout in a 128-column group g.  With an fp32 destination (HALVES) MFMA column n of
+    // block j is output column 128 g + 64 (j/4) + 4n + j%4, and the two halves (blocks 0..3, then
+    // 4..7) are computed and stored in turn, so only four accumulators are live (fp32 weights: 74
+    // VGPRs, six waves per SIMD); with a bf16 destination column 128 g + 8n + j, all eight blocks
+    // at once, one 16-byte store per row (measured faster there).
+    constexpr bool HALVES = !DBF;
+    constexpr int NB = HALVES ? 4 : 8;  // blocks per store
     auto store_tile = [&](int32_t tok_a, const tile_v4f* acc, int64_t col) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int32_t tok = __shfl(tok_a, 4 * kq + r, 64);
             const int64_t e = int64_t(tok) * H + col;
-            float v8[8];
+            float v[NB];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) v8[j] = acc[j][r];
+            for (int j = 0; j < NB; ++j) v[j] = acc[j][r];
             const uint32_t od = tok >= 0 ? uint32_t(e * DSZ) : TILE_NO_ROW;
             const uint32_t os = tok >= 0 ? uint32_t(e * SSZ) : TILE_NO_ROW;
-            tile_store8_buf<SRC, DBF>(rsrc, os, rdst, od, v8);
+            if constexpr (HALVES)
+                tile_store4_buf<SRC, DBF>(rsrc, os, rdst, od, v);
+            else
+                tile_store8_buf<SRC, DBF>(rsrc, os, rdst, od, v);
         }
     };
 
@@ -619,11 +662,34 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             r.a1 = rec[1];
         };
         for (int g = wave; g < GROUPS; g += WAVES) {
-            const int64_t col = int64_t(g) * 128 + 8 * n;
-            // B operands: bj[j] holds column 128 g + 8n + j of the rows of levels 8h .. 8h+7
-            // (levels past D repeat the leaf row: their activations are 0)
+            const int64_t col = int64_t(g) * 128 + (HALVES ? 4 : 8) * n;
+            // B operands: bj[j] holds the column of block j (see the layout above) of the rows of
+            // levels 8h .. 8h+7 (levels past D repeat the leaf row: their activations are 0)
             uint4 bj[8];
-            {
+            if constexpr (HALVES) {
+                uint2 row[2][8];
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const int lvl = 8 * h + i <= D ? 8 * h + i : D;
+                        row[c][i] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(w_out) +
+                                                                    (int64_t(leaf1 >> (D - lvl)) - 1) * H + col + 64 * c);
+                    }
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        uint32_t w4[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t lo = j / 2 ? row[c][2 * q].y : row[c][2 * q].x;
+                            const uint32_t hi = j / 2 ? row[c][2 * q + 1].y : row[c][2 * q + 1].x;
+                            w4[q] = (j & 1) ? (lo >> 16) | (hi & 0xffff0000u) : (lo & 0xffffu) | (hi << 16);
+                        }
+                        bj[4 * c + j] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+                    }
+            } else {
                 uint4 row[8];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
@@ -664,20 +730,24 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
                     }
                 }
                 const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, make_uint4(p0[0], p0[1], p0[2], p0[3]));
-                tile_v4f acc[8];
+                // the halves in turn (HALVES) or all eight blocks at once
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8_t, bj[j]),
-                                                                     tile_v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                }
-                if constexpr (PARTS == 3) {
-                    const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, make_uint4(p1[0], p1[1], p1[2], p1[3]));
+                for (int c = 0; c < 8 / NB; ++c) {
+                    tile_v4f acc[NB];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8_t, bj[j]),
-                                                                         acc[j], 0, 0, 0);
+                    for (int j = 0; j < NB; ++j) {
+                        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            a0, __builtin_bit_cast(bf16x8_t, bj[NB * c + j]), tile_v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    }
+                    if constexpr (PARTS == 3) {
+                        const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, make_uint4(p1[0], p1[1], p1[2], p1[3]));
+#pragma unroll
+                        for (int j = 0; j < NB; ++j)
+                            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                a1, __builtin_bit_cast(bf16x8_t, bj[NB * c + j]), acc[j], 0, 0, 0);
+                    }
+                    store_tile(tok_a, acc, col + 64 * c);
                 }
-                store_tile(tok_a, acc, col);
             };
             // two operand sets in turn: the next tile's loads are in flight while
             // this one runs, and no register copy makes the wait early
@@ -711,32 +781,37 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             for (int s = 0; s < FSTEPS; ++s) r.a[s] = rec[lvl_c[s]];
         };
         for (int g = wave; g < GROUPS; g += WAVES) {
-            const int64_t col = int64_t(g) * 128 + 8 * n;
-            // B operand: this lane's eight weights of the row at level 4s + kq, kept
-            // as loaded for all of the leaf's tiles
+            const int64_t col = int64_t(g) * 128 + (HALVES ? 4 : 8) * n;
+            // B operand: this lane's weights of the row at level 4s + kq for its eight blocks (see
+            // the layout above), kept as loaded for all of the leaf's tiles
             float4 w[FSTEPS][2];
 #pragma unroll
             for (int s = 0; s < FSTEPS; ++s) {
                 const int64_t at = (int64_t(leaf1 >> (D - lvl_c[s])) - 1) * H + col;
                 w[s][0] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at);
-                w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + 4);
+                w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + (HALVES ? 64 : 4));
             }
             auto tile = [&](int t0, const Raw& cur) {
                 const bool in = t0 + n < cnt;
                 const int32_t tok_a = in ? cur.tok : -1;
-                tile_v4f acc[8];
+                // the halves in turn (HALVES) or all eight blocks at once
 #pragma unroll
-                for (int j = 0; j < 8; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
+                for (int c = 0; c < 8 / NB; ++c) {
+                    tile_v4f acc[NB];
 #pragma unroll
-                for (int s = 0; s < FSTEPS; ++s) {
-                    if (s < steps) {
-                        const float a = in && 4 * s + kq <= D ? cur.a[s] : 0.0f;
+                    for (int j = 0; j < NB; ++j) acc[j] = tile_v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                        for (int j = 0; j < 8; ++j)
-                            acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, fword(w[s][j / 4], j % 4), acc[j], 0, 0, 0);
+                    for (int s = 0; s < FSTEPS; ++s) {
+                        if (s < steps) {
+                            const float a = in && 4 * s + kq <= D ? cur.a[s] : 0.0f;
+#pragma unroll
+                            for (int j = 0; j < NB; ++j)
+                                acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    a, fword(w[s][(NB * c + j) / 4], (NB * c + j) % 4), acc[j], 0, 0, 0);
+                        }
                     }
+                    store_tile(tok_a, acc, col + 64 * c);
                 }
-                store_tile(tok_a, acc, col);
             };
             Raw r0, r1;
             load_tile(0, r0);
