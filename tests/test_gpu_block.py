@@ -253,8 +253,8 @@ def test_twelve_layer_4x9_stack_full_size(fff_lib):
     x = dev(fff_lib, xs)
     kw = dict(norm="layernorm", norm_eps=EPS)
     flush_print(f"[gpu] 12x 4x9: {fff_lib.describe_stack(x, dl, D, T, mode='descent', **kw)}")
-    # AUTO: per-layer launches of the fused kernel
-    assert fff_lib.describe_stack(x, dl, D, T, **kw).startswith("per-layer descent")
+    # AUTO: per-layer launches, leaf-tiled (four fp32 trees of depth 9, 32 tokens per leaf)
+    assert fff_lib.describe_stack(x, dl, D, T, **kw).startswith("per-layer tiled")
     ys = fff_lib.forward_stack(x, dl, D, T, mode="descent", **kw)
     yc, outs, nodes = chained(fff_lib, x, dl, D, T, True, "descent", records=True)
     ya, _, _ = chained(fff_lib, x, dl, D, T, True, "auto")

@@ -704,15 +704,15 @@ def test_binding_workspace_per_stream(fff_lib):
 
 def test_auto_multi_tree_deep_plans(fff_lib):
     """2, 4 or 8 trees of depth >= 7 plan the tree-affine walk: leaf-tiled with fp32 weights at
-    depth >= 11 from 8 tokens per leaf or, with 4 or 8 trees, at depth >= 9 from 65536 tokens;
+    depth >= 11 from 8 tokens per leaf or, with 4 or 8 trees, at depth >= 9 from 32 per leaf;
     otherwise GROUPED at large batches; the fused kernel below (planning only)."""
     def plan(T, d, B, dt):
         t = torch.bfloat16 if dt == "bf16" else torch.float32
         x = torch.zeros((B, 768), dtype=t, device=DEV)
         w = torch.zeros((T, (1 << (d + 1)) - 1, 768), dtype=t, device=DEV)
         return fff_lib.describe(x, w, w, d, T).split("<")[0]
-    assert plan(4, 9, 16384, "f32") == "descent"    # UltraFastBERT-4x9 at 16384 tokens
-    assert plan(4, 9, 65536, "f32") == "tiled"
+    assert plan(4, 9, 16384, "f32") == "tiled"      # UltraFastBERT-4x9: 32 per leaf
+    assert plan(4, 9, 8192, "f32") == "descent"     # 16 per leaf
     assert plan(4, 8, 16384, "f32") == "descent"    # depth 8
     assert plan(8, 11, 65536, "f32") == "tiled"
     assert plan(2, 11, 16384, "f32") == "tiled"     # 8 per leaf at depth 11
