@@ -125,6 +125,34 @@ def _check(rc: int):
         raise FffError(rc, msg)
 
 
+def _raw_stream(device: torch.device, stream=None) -> int:
+    """The HIP stream handle a call is enqueued on: ``stream``'s, else the device's current one."""
+    if stream is not None:
+        return stream.cuda_stream
+    getter = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if getter is not None:
+        return getter(device.index if device.index is not None else torch.cuda.current_device())
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+class _on_device:
+    """``torch.cuda.device(device)`` when it is not already the current device (the library enqueues
+    on the current device's stream and queries the current device's properties)."""
+
+    def __init__(self, device: torch.device):
+        self.ctx = None if device.index is None or device.index == torch.cuda.current_device() else \
+            torch.cuda.device(device)
+
+    def __enter__(self):
+        if self.ctx is not None:
+            self.ctx.__enter__()
+
+    def __exit__(self, *exc):
+        if self.ctx is not None:
+            return self.ctx.__exit__(*exc)
+        return False
+
+
 def _dt(t: torch.Tensor, what: str) -> int:
     try:
         return _TORCH_DT[t.dtype]
@@ -207,26 +235,29 @@ def make_args(x, w_in, w_out, depth, n_trees, y, *, act="gelu", mode="auto", out
     if workspace is not None:
         _dev_tensor(workspace, "workspace", device)
         a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
-    s = stream if stream is not None else torch.cuda.current_stream(device)
-    a.hip_stream = s.cuda_stream
+    a.hip_stream = _raw_stream(device, stream)
     return a
 
 
 _WORKSPACES: dict = {}
+_NEED: dict = {}  # workspace bytes per (n_tokens, depth, n_trees, hidden)
 
 
 def workspace_for(n_tokens: int, depth: int, n_trees: int, hidden: int, device, stream=None) -> torch.Tensor:
     """A cached device workspace large enough for every mode, one per (device, stream): calls on one
     stream run in order and share it; calls on different streams never share one.  A larger
     request replaces the stream's buffer (torch frees the old one in that stream's order)."""
-    need = workspace_bytes(n_tokens, depth, n_trees, hidden, 0)
-    dev = torch.device(device)
+    shape = (n_tokens, depth, n_trees, hidden)
+    need = _NEED.get(shape)
+    if need is None:
+        need = _NEED[shape] = workspace_bytes(n_tokens, depth, n_trees, hidden, 0)
+    dev = device if isinstance(device, torch.device) else torch.device(device)
     if dev.index is None:
         dev = torch.device(dev.type, torch.cuda.current_device())
-    s = stream if stream is not None else torch.cuda.current_stream(dev)
-    key = (dev, int(s.cuda_stream))
+    key = (dev, int(_raw_stream(dev, stream)))
     ws = _WORKSPACES.get(key)
     if ws is None or ws.numel() < need:
+        s = stream if stream is not None else torch.cuda.current_stream(dev)
         with torch.cuda.stream(s):
             ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
         _WORKSPACES[key] = ws
@@ -244,7 +275,7 @@ def forward(x, w_in, w_out, depth: int, n_trees: int = 1, y=None, *, y_dtype=Non
         kw["workspace"] = workspace_for(x.shape[0], depth, n_trees, x.shape[1], x.device, kw.get("stream"))
     a = make_args(x, w_in, w_out, depth, n_trees, y, **kw)
     lib = load_library()
-    with torch.cuda.device(x.device):
+    with _on_device(x.device):
         _check(lib.fff_forward_ex(ctypes.byref(a)))
     return y
 
