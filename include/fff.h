@@ -125,8 +125,8 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * 11 or more from 48M elements, or from 16384 tokens with fp32 W or 24M
  * elements, and with fp32 W at depth 5 or more from 65536 tokens; for 2, 4
  * or 8 trees of depth 7 or more (the walk tree-affine), with fp32 W TILED at
- * depth 11 or more from 8 tokens per leaf or, with 4 or 8 trees, at depth 9
- * or more from 32 tokens per leaf, else GROUPED from 65536 tokens (16384 with 8
+ * depth 11 or more from 8 tokens per leaf or at depth 9 or more from 32
+ * tokens per leaf, else GROUPED from 65536 tokens (16384 with 8
  * trees), and with bf16 W GROUPED for 8 trees, for 4 from 4096 tokens at
  * depth 8 or more (65536 at depth 7) and for 2 from 65536 tokens at depth 8
  * or more; GROUPED for 8 trees up to 2048 tokens with bf16 W (4096 at depth

@@ -1286,9 +1286,9 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
         // * 2, 4 or 8 trees of depth >= 7 (the walk tree-affine: the workgroups of an XCD walk
         //   one tree, its top levels in LDS and its deep rows in that XCD's L2): with fp32 weights
-        //   leaf-tiled at depth >= 11 from 8 tokens per leaf and, with 4 or 8 trees, at depth >= 9
-        //   from 32 per leaf (eight trees of depth 11, 65536 tokens: 1561 against 2579 us fused;
-        //   four of depth 9: 590 against 664 at 65536 tokens, 153 against 160 at 16384), else grouped from
+        //   leaf-tiled at depth >= 11 from 8 tokens per leaf and at depth >= 9 from 32 per leaf
+        //   (eight trees of depth 11, 65536 tokens: 1481 against 2556 us fused; four of depth 9:
+        //   554 against 665 at 65536 tokens, 149 against 160 at 16384), else grouped from
         //   65536 tokens (16384 with 8 trees); with bf16 weights grouped for 8 trees, for 4 from
         //   4096 tokens at depth >= 8 (65536 at depth 7), for 2 from 65536 tokens at depth >= 8
         //   (four trees of depth 9, 65536 tokens: 272 against 306 us);
@@ -1330,7 +1330,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
             mode = MODE_GROUPED;
         else if (affine && !p.w_bf16 && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws &&
                  ((p.depth >= 11 && p.n_tokens >= (int64_t(8) << p.depth)) ||
-                  (p.n_trees >= 4 && p.depth >= 9 && p.n_tokens >= (int64_t(32) << p.depth))))
+                  (p.depth >= 9 && p.n_tokens >= (int64_t(32) << p.depth))))
             mode = MODE_TILED;
         else if (affine && int64_t(workspace_bytes) >= grouped_ws && p.depth >= 7 &&
                  (p.w_bf16 ? p.n_trees == XCDS || (p.n_trees == 4 && p.n_tokens >= (p.depth >= 8 ? 4096 : 65536)) ||

@@ -704,7 +704,7 @@ def test_binding_workspace_per_stream(fff_lib):
 
 def test_auto_multi_tree_deep_plans(fff_lib):
     """2, 4 or 8 trees of depth >= 7 plan the tree-affine walk: leaf-tiled with fp32 weights at
-    depth >= 11 from 8 tokens per leaf or, with 4 or 8 trees, at depth >= 9 from 32 per leaf;
+    depth >= 11 from 8 tokens per leaf or at depth >= 9 from 32 per leaf;
     otherwise GROUPED at large batches; the fused kernel below (planning only)."""
     def plan(T, d, B, dt):
         t = torch.bfloat16 if dt == "bf16" else torch.float32
@@ -716,7 +716,8 @@ def test_auto_multi_tree_deep_plans(fff_lib):
     assert plan(4, 8, 16384, "f32") == "descent"    # depth 8
     assert plan(8, 11, 65536, "f32") == "tiled"
     assert plan(2, 11, 16384, "f32") == "tiled"     # 8 per leaf at depth 11
-    assert plan(2, 9, 65536, "f32") == "grouped"    # two trees: not tiled at depth 9
+    assert plan(2, 9, 65536, "f32") == "tiled"      # 128 per leaf
+    assert plan(2, 8, 65536, "f32") == "grouped"    # depth 8
     assert plan(8, 8, 16384, "f32") == "grouped"
     assert plan(4, 7, 16384, "f32") == "descent"
     assert plan(4, 9, 4096, "bf16") == "grouped"
