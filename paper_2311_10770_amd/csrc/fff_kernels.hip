@@ -1053,8 +1053,8 @@ constexpr int BLOCK = 256;
 constexpr size_t DESCENT_LDS_BUDGET = 32 * 1024;  // per 256-thread block: keeps 4-5 blocks per CU
 constexpr int WALK_BLOCK = 512;                     // walk workgroups: twice the rows in LDS per wave
 constexpr size_t WALK_LDS_BUDGET = 48 * 1024;     // per 512-thread walk block: three blocks per CU
-// Walks of four waves per SIMD (fp32 weights, 16 lanes per token) fit one 1024-thread block per CU,
-// which then holds twice the rows in LDS (one more level of fp32 rows)
+// Walks of four waves per SIMD (fp32 x or fp32 weights, 16 lanes per token) fit one 1024-thread
+// block per CU, which then holds twice the rows in LDS (one more level)
 constexpr int WALK_BLOCK_WIDE = 1024;
 constexpr size_t EMIT_LDS_BUDGET = 32 * 1024;
 constexpr int GENERIC_MAX_PAIRS = 2048;
@@ -1106,7 +1106,7 @@ static const Variant kVariants[] = {
     // walk 16 (with fp32 W: 124 VGPRs and four waves per SIMD, 64 tokens in flight per CU against
     // 48 with 32 lanes; the fused kernel keeps 32, its output accumulators need the registers)
     FFF_VARIANT(768, true, true, 16, 6, 16, 6, WALK_BLOCK, 32, 3),
-    FFF_VARIANT(768, false, true, 16, 6, 16, 6, WALK_BLOCK, 32, 3),
+    FFF_VARIANT(768, false, true, 16, 6, 16, 6, WALK_BLOCK_WIDE, 32, 3),
     FFF_VARIANT(768, false, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, 64, 3),
     FFF_VARIANT(768, true, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, 64, 3),
     // H = 1024
