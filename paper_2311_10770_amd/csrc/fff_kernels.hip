@@ -1065,6 +1065,7 @@ struct Variant {
     int lanes;
     int walk_lanes;  // the walk kernel's lanes per token (its own registers: x and one row, no output)
     int walk_block;  // its workgroup size (WALK_BLOCK, or WALK_BLOCK_WIDE for walks of four waves per SIMD)
+    int walk_norm_block;  // the same for the LayerNorm walk (x widened to fp32)
     int emit_lanes;  // the emit has no cross-lane reduction: wider groups hold fewer registers per lane
     const void* descent;
     const void* walk;
@@ -1086,9 +1087,9 @@ struct Variant {
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, FS>)}
 // bf16 weights take one instantiation for both arrays
 #define FFF_TILE_STEPS(WB) ((WB) ? TILE_MAX_STEPS : TILE_STEPS_SHALLOW)
-#define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, WBLK, EL, ENV)                                                \
+#define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, WBLK, WNBLK, EL, ENV)                                         \
     Variant {                                                                                                 \
-        H, XB, WB, L, WL, WBLK, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                       \
+        H, XB, WB, L, WL, WBLK, WNBLK, EL, FFF_K(descent_kernel<L, NV, XB, WB, BLOCK, false>),                \
             FFF_K(walk_kernel<WL, WNV, XB, WB, WBLK, false>), FFF_K(emit_kernel<EL, ENV, XB, WB, BLOCK>),        \
             {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE, FFF_TILE_STEPS(WB)),                                    \
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32, FFF_TILE_STEPS(WB)),                                     \
@@ -1097,7 +1098,7 @@ struct Variant {
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32, TILE_MAX_STEPS),                                         \
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16, TILE_MAX_STEPS)},                                       \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
-            FFF_K(walk_kernel<WL, WNV, false, WB, WBLK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
+            FFF_K(walk_kernel<WL, WNV, false, WB, WNBLK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
     }
 
@@ -1105,20 +1106,20 @@ static const Variant kVariants[] = {
     // H = 768 (BERT-base width); the emit takes 32 (bf16 W) or 64 (fp32 W) lanes per token, the
     // walk 16 (with fp32 W: 124 VGPRs and four waves per SIMD, 64 tokens in flight per CU against
     // 48 with 32 lanes; the fused kernel keeps 32, its output accumulators need the registers)
-    FFF_VARIANT(768, true, true, 16, 6, 16, 6, WALK_BLOCK, 32, 3),
-    FFF_VARIANT(768, false, true, 16, 6, 16, 6, WALK_BLOCK_WIDE, 32, 3),
-    FFF_VARIANT(768, false, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, 64, 3),
-    FFF_VARIANT(768, true, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, 64, 3),
+    FFF_VARIANT(768, true, true, 16, 6, 16, 6, WALK_BLOCK, WALK_BLOCK_WIDE, 32, 3),
+    FFF_VARIANT(768, false, true, 16, 6, 16, 6, WALK_BLOCK_WIDE, WALK_BLOCK_WIDE, 32, 3),
+    FFF_VARIANT(768, false, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, WALK_BLOCK_WIDE, 64, 3),
+    FFF_VARIANT(768, true, false, 32, 6, 16, 12, WALK_BLOCK_WIDE, WALK_BLOCK_WIDE, 64, 3),
     // H = 1024
-    FFF_VARIANT(1024, true, true, 16, 8, 16, 8, WALK_BLOCK, 32, 4),
-    FFF_VARIANT(1024, false, true, 16, 8, 16, 8, WALK_BLOCK, 32, 4),
-    FFF_VARIANT(1024, false, false, 32, 8, 32, 8, WALK_BLOCK, 64, 4),
-    FFF_VARIANT(1024, true, false, 32, 8, 32, 8, WALK_BLOCK, 64, 4),
+    FFF_VARIANT(1024, true, true, 16, 8, 16, 8, WALK_BLOCK, WALK_BLOCK, 32, 4),
+    FFF_VARIANT(1024, false, true, 16, 8, 16, 8, WALK_BLOCK, WALK_BLOCK, 32, 4),
+    FFF_VARIANT(1024, false, false, 32, 8, 32, 8, WALK_BLOCK, WALK_BLOCK, 64, 4),
+    FFF_VARIANT(1024, true, false, 32, 8, 32, 8, WALK_BLOCK, WALK_BLOCK, 64, 4),
     // H = 4096 (LLM width)
-    FFF_VARIANT(4096, true, true, 64, 8, 64, 8, WALK_BLOCK, 64, 8),
-    FFF_VARIANT(4096, false, true, 64, 8, 64, 8, WALK_BLOCK, 64, 8),
-    FFF_VARIANT(4096, false, false, 64, 16, 64, 16, WALK_BLOCK, 64, 16),
-    FFF_VARIANT(4096, true, false, 64, 16, 64, 16, WALK_BLOCK, 64, 16),
+    FFF_VARIANT(4096, true, true, 64, 8, 64, 8, WALK_BLOCK, WALK_BLOCK, 64, 8),
+    FFF_VARIANT(4096, false, true, 64, 8, 64, 8, WALK_BLOCK, WALK_BLOCK, 64, 8),
+    FFF_VARIANT(4096, false, false, 64, 16, 64, 16, WALK_BLOCK, WALK_BLOCK, 64, 16),
+    FFF_VARIANT(4096, true, false, 64, 16, 64, 16, WALK_BLOCK, WALK_BLOCK, 64, 16),
 };
 
 static const void* generic_kernel_for(bool xbf, bool wbf) {
@@ -1247,7 +1248,7 @@ static bool plan_walk(const Params& p, const Variant& v, int lds_levels_req, con
     Params one = p;
     if (affine) one.n_trees = 1;
     bool ok;
-    const int blk = v.walk_block;
+    const int blk = p.norm ? v.walk_norm_block : v.walk_block;
     const int kw = pick_levels(one, lds_levels_req, 1, WALK_LDS_BUDGET * (blk / WALK_BLOCK), dev.lds_per_block, &ok);
     if (!ok) return false;
     plan->lds_levels = kw;
