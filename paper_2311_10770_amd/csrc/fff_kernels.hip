@@ -1053,9 +1053,17 @@ constexpr int BLOCK = 256;
 constexpr size_t DESCENT_LDS_BUDGET = 32 * 1024;  // per 256-thread block: keeps 4-5 blocks per CU
 constexpr int WALK_BLOCK = 512;                     // walk workgroups: twice the rows in LDS per wave
 constexpr size_t WALK_LDS_BUDGET = 48 * 1024;     // per 512-thread walk block: three blocks per CU
-// Walks of four waves per SIMD (fp32 x or fp32 weights, 16 lanes per token) fit one 1024-thread
-// block per CU, which then holds twice the rows in LDS (one more level)
+// Walk workgroups larger than WALK_BLOCK, where measured faster: at four waves per SIMD (16-lane
+// walks of fp32 x or fp32 weights at hidden 768, LayerNorm walks of bf16 weights) one 1024-thread
+// block per CU; at five (fp32 weights at hidden 1024) two of 640 threads.  Fewer, larger blocks at
+// the same waves per CU hold one more level of rows in LDS.  (Two 640-thread blocks for the bf16
+// walks of hidden 1024 and 4096 were slower: grouped at hidden 1024, depth 11, 32768 tokens
+// 80.9 -> 87.8 us.)
 constexpr int WALK_BLOCK_WIDE = 1024;
+constexpr int WALK_BLOCK_5 = 640;
+static size_t walk_lds_budget(int block) {
+    return block == WALK_BLOCK ? WALK_LDS_BUDGET : block == WALK_BLOCK_5 ? size_t(78) << 10 : size_t(96) << 10;
+}
 constexpr size_t EMIT_LDS_BUDGET = 32 * 1024;
 constexpr int GENERIC_MAX_PAIRS = 2048;
 
@@ -1113,8 +1121,8 @@ static const Variant kVariants[] = {
     // H = 1024
     FFF_VARIANT(1024, true, true, 16, 8, 16, 8, WALK_BLOCK, WALK_BLOCK, 32, 4),
     FFF_VARIANT(1024, false, true, 16, 8, 16, 8, WALK_BLOCK, WALK_BLOCK, 32, 4),
-    FFF_VARIANT(1024, false, false, 32, 8, 32, 8, WALK_BLOCK, WALK_BLOCK, 64, 4),
-    FFF_VARIANT(1024, true, false, 32, 8, 32, 8, WALK_BLOCK, WALK_BLOCK, 64, 4),
+    FFF_VARIANT(1024, false, false, 32, 8, 32, 8, WALK_BLOCK_5, WALK_BLOCK_5, 64, 4),
+    FFF_VARIANT(1024, true, false, 32, 8, 32, 8, WALK_BLOCK_5, WALK_BLOCK_5, 64, 4),
     // H = 4096 (LLM width)
     FFF_VARIANT(4096, true, true, 64, 8, 64, 8, WALK_BLOCK, WALK_BLOCK, 64, 8),
     FFF_VARIANT(4096, false, true, 64, 8, 64, 8, WALK_BLOCK, WALK_BLOCK, 64, 8),
@@ -1249,7 +1257,7 @@ static bool plan_walk(const Params& p, const Variant& v, int lds_levels_req, con
     if (affine) one.n_trees = 1;
     bool ok;
     const int blk = p.norm ? v.walk_norm_block : v.walk_block;
-    const int kw = pick_levels(one, lds_levels_req, 1, WALK_LDS_BUDGET * (blk / WALK_BLOCK), dev.lds_per_block, &ok);
+    const int kw = pick_levels(one, lds_levels_req, 1, walk_lds_budget(blk), dev.lds_per_block, &ok);
     if (!ok) return false;
     plan->lds_levels = kw;
     plan->walk_affine = affine;
