@@ -126,7 +126,7 @@ def test_grouped_split_levels_and_ragged(fff_lib, split, B):
 
 
 @pytest.mark.parametrize("xd,wd,yd", DTYPE_COMBOS)
-@pytest.mark.parametrize("H", [768, 4096])
+@pytest.mark.parametrize("H", [768, 1024, 4096])
 def test_grouped_dtype_combinations(fff_lib, xd, wd, yd, H):
     depth = 6 if H == 4096 else 9
     L = layer(170 + H, 900, H, depth, 2, xd, wd)
