@@ -207,15 +207,26 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
 // K a multiple of 8 for bf16 or 4 for fp32), bf16 (bf16 = true) or fp32 inputs, fp32 accumulation.
 // out: GEMM_OUT_F32 stores C as fp32; GEMM_OUT_SRC_* add a source matrix (none, fp32, bf16; leading
 // dimension ldc like C, may be C itself) and store as bf16 (dst_bf16) or fp32.  fp32 inputs take
-// fp32 sources and destinations only.  cu_count: compute units of the device (tile choice).
+// fp32 sources and destinations only.  GEMM_OUT_ACT_* store the activation a = act(C) over whole
+// rows of ldc >= N columns (zeros past N, ldc a multiple of 4): GEMM_OUT_ACT_F32 (fp32 inputs)
+// as fp32, GEMM_OUT_ACT_P2 (bf16 inputs) as hi = bf16(a) at element 2 m ldc + n and
+// bf16(a - hi) at ldc past it.  Any other combination returns hipErrorInvalidValue.  cu_count:
+// compute units of the device (tile choice).
 // split_ws / split_bytes: device scratch for the partial sums of a product split along K (a small
 // product with a long K; none when null), fully overwritten before it is read.  The kernels, tile
 // shape and split depend on the shapes, cu_count and split_bytes only, so the result bits do too.
-enum { GEMM_OUT_F32 = 0, GEMM_OUT_SRC_NONE = 1, GEMM_OUT_SRC_F32 = 2, GEMM_OUT_SRC_BF16 = 3 };
+enum {
+    GEMM_OUT_F32 = 0,
+    GEMM_OUT_SRC_NONE = 1,
+    GEMM_OUT_SRC_F32 = 2,
+    GEMM_OUT_SRC_BF16 = 3,
+    GEMM_OUT_ACT_F32 = 4,
+    GEMM_OUT_ACT_P2 = 5
+};
 constexpr size_t GEMM_SPLIT_BYTES = size_t(32) << 20;  // masked mode's partial-sum scratch
 hipError_t gemm_nt(bool bf16, int out, bool dst_bf16, const void* A, const void* B, void* C, const void* src,
                    int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc, int cu_count,
-                   void* split_ws, size_t split_bytes, hipStream_t stream);
+                   void* split_ws, size_t split_bytes, int act, hipStream_t stream);
 
 // Subtree mode (fff_subtree.hip): a workgroup per token evaluates whole subtrees of logits per
 // step.  AUTO takes it for at most SUBTREE_AUTO_TREES trees of depth at least SUBTREE_AUTO_DEPTH

@@ -217,6 +217,37 @@ __global__ __launch_bounds__(256) void transpose_repeat_kernel(const void* __res
     }
 }
 
+// The selection: A from the logits L (depth 0 elementwise; else staged in LDS or by paths).
+void launch_select(const Params& p, const float* L, void* A, bool f32, int P, int64_t ntq, int cu_count,
+                   hipStream_t stream) {
+    const int64_t B = p.n_tokens;
+    const int nq = int(ntq);
+    if (p.depth == 0) {
+        const int64_t work = B * (ntq / 8);
+        const unsigned blocks = unsigned(std::min<int64_t>((work + SELECT_BLOCK - 1) / SELECT_BLOCK, int64_t(cu_count > 0 ? cu_count : 256) * 16));
+        if (f32)
+            hipLaunchKernelGGL(select_depth0_kernel<true>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, 1, nq);
+        else
+            hipLaunchKernelGGL(select_depth0_kernel<false>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, P, nq);
+    } else if (ntq <= SELECT_LDS_COLS) {
+        const size_t lds = size_t(ntq) * (sizeof(float) + 1);
+        if (f32)
+            hipLaunchKernelGGL(select_staged_kernel<true>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
+                               1, nq);
+        else
+            hipLaunchKernelGGL(select_staged_kernel<false>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L,
+                               A, P, nq);
+    } else {
+        const size_t lds = size_t(p.n_trees) * (p.depth + 1) * 8;
+        if (f32)
+            hipLaunchKernelGGL(select_paths_kernel<true>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
+                               1, nq);
+        else
+            hipLaunchKernelGGL(select_paths_kernel<false>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
+                               P, nq);
+    }
+}
+
 }  // namespace
 
 bool masked_shape(const Params& p) {
@@ -250,9 +281,22 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
     ws += align256(size_t(3) * ntq * size_t(H) * sizeof(uint16_t));
     void* SP = ws;                            // partial sums of a product split along K
 
-    // G1: L = x W_in^T (logits of every node; the padding columns are not written)
-    hipError_t e = gemm_nt(!f32, GEMM_OUT_F32, false, p.x, p.w_in, L, nullptr, B, NT, H, H, H, ntq, cu_count, SP,
-                           GEMM_SPLIT_BYTES, stream);
+    // Depth 0 with no records: every node is visited, so A is the activation of every logit, and
+    // the first product writes it itself (the same activation and part split as the selection),
+    // whole or as two parts.  Three parts (fp32 y from bf16 operands) keep the selection pass:
+    // the third part's stores made the fused product slower than the two kernels (3072x0 at
+    // 16384 tokens: 537 against 530 us per forward, while two parts take 404 against 432 us).
+    const bool fused = p.depth == 0 && !p.nodes_out && !p.logits_out && P <= 2;
+    // G1: L = x W_in^T (logits of every node; the padding columns are not written), or A itself
+    hipError_t e;
+    if (fused) {
+        const int out = f32 ? GEMM_OUT_ACT_F32 : GEMM_OUT_ACT_P2;
+        e = gemm_nt(!f32, out, false, p.x, p.w_in, A, nullptr, B, NT, H, H, H, ntq, cu_count, SP, GEMM_SPLIT_BYTES,
+                    p.act, stream);
+    } else {
+        e = gemm_nt(!f32, GEMM_OUT_F32, false, p.x, p.w_in, L, nullptr, B, NT, H, H, H, ntq, cu_count, SP,
+                    GEMM_SPLIT_BYTES, 0, stream);
+    }
     if (e != hipSuccess) return e;
     {
         const dim3 grid(unsigned((ntq + 63) / 64), unsigned((H + 63) / 64));
@@ -263,33 +307,11 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int nq = int(ntq);
-    if (p.depth == 0) {
-        const int64_t work = B * (ntq / 8);
-        const unsigned blocks = unsigned(std::min<int64_t>((work + SELECT_BLOCK - 1) / SELECT_BLOCK, int64_t(cu_count > 0 ? cu_count : 256) * 16));
-        if (f32)
-            hipLaunchKernelGGL(select_depth0_kernel<true>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, 1, nq);
-        else
-            hipLaunchKernelGGL(select_depth0_kernel<false>, dim3(blocks), dim3(SELECT_BLOCK), 0, stream, p, L, A, P, nq);
-    } else if (ntq <= SELECT_LDS_COLS) {
-        const size_t lds = size_t(ntq) * (sizeof(float) + 1);
-        if (f32)
-            hipLaunchKernelGGL(select_staged_kernel<true>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
-                               1, nq);
-        else
-            hipLaunchKernelGGL(select_staged_kernel<false>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L,
-                               A, P, nq);
-    } else {
-        const size_t lds = size_t(p.n_trees) * (p.depth + 1) * 8;
-        if (f32)
-            hipLaunchKernelGGL(select_paths_kernel<true>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
-                               1, nq);
-        else
-            hipLaunchKernelGGL(select_paths_kernel<false>, dim3(unsigned(B)), dim3(SELECT_BLOCK), lds, stream, p, L, A,
-                               P, nq);
+    if (!fused) {
+        launch_select(p, L, A, f32, P, ntq, cu_count, stream);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
     // G2: y = A WT^T plus the layer's source (x for the residual, y for accumulation)
     const int64_t k2 = int64_t(P) * ntq;
     int out = GEMM_OUT_SRC_NONE;
@@ -301,7 +323,8 @@ hipError_t run_masked(const Params& p, void* workspace, int cu_count, hipStream_
         src = p.y;
         out = p.y_bf16 ? GEMM_OUT_SRC_BF16 : GEMM_OUT_SRC_F32;
     }
-    return gemm_nt(!f32, out, p.y_bf16, A, WT, p.y, src, B, H, k2, k2, k2, H, cu_count, SP, GEMM_SPLIT_BYTES, stream);
+    return gemm_nt(!f32, out, p.y_bf16, A, WT, p.y, src, B, H, k2, k2, k2, H, cu_count, SP, GEMM_SPLIT_BYTES, 0,
+                   stream);
 }
 
 }  // namespace fff

@@ -630,6 +630,33 @@ def test_masked_output_modes(fff_lib, out):
                          base_dev=base)
 
 
+@pytest.mark.parametrize("k,B,dt,yd,out,act", [(3072, 131, "bf16", "bf16", "store", "gelu"),
+                                                (3072, 131, "bf16", "f32", "accumulate", "gelu_tanh"),
+                                                (3072, 67, "f32", "f32", "accumulate", "gelu"),
+                                                (100, 1000, "bf16", "bf16", "residual", "identity"),
+                                                (100, 1000, "f32", "f32", "store", "gelu"),
+                                                (3072, 37, "bf16", "bf16", "accumulate", "gelu"),
+                                                (3072, 64, "f32", "f32", "residual", "gelu_tanh"),
+                                                (3, 5, "bf16", "bf16", "store", "gelu")])
+def test_masked_depth0_without_records(fff_lib, k, B, dt, yd, out, act):
+    """Depth 0 with no records: the logit product stores the activations (two bf16 parts, or
+    whole for fp32) over the padded rows itself, with no selection pass (bf16 operands with an
+    fp32 output, three parts, keep the selection).  Against the oracle (at depth 0 every path is
+    the root, so the paths are the oracle's), and bit for bit against the same call with records,
+    which selects from stored logits.  k = 100 pads the rows from 100 to 128 columns and k = 3
+    from 3 to 64; 37 and 64 tokens split the logit product along K."""
+    L = layer(480 + k + B, B, 768, 0, k, dt, dt)
+    y0 = synth.make_x(481, B, 768, yd) if out == "accumulate" else None
+    flush_print(f"[gpu] masked depth 0 without records: k={k} B={B} {dt} y={yd} {out} {act}")
+    got = run_fff(fff_lib, L, 0, k, yd, record=False, y_init=y0, mode="masked", out=out, act=act)
+    rec = run_fff(fff_lib, L, 0, k, yd, y_init=y0, mode="masked", out=out, act=act)
+    ref = oracle.forward(L["x"], L["w_in"], L["w_out"], 0, k, act=act)
+    base = None if out == "store" else (L["x"] if out == "residual" else y0)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 0, k, ref, got["y"], ref["nodes"], tol=tol_for(dt, yd),
+                         act=act, base_dev=base)
+    assert np.array_equal(got["y"].view(np.uint8), rec["y"].view(np.uint8))
+
+
 def test_masked_mode_limits_and_auto(fff_lib):
     """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it at depth <= 5
     for 16 bf16 trees or more, or 12 and 16384 tokens, and at depth <= 4 for 32 fp32 trees or more
