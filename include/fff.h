@@ -101,7 +101,9 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * parts (two when y is bf16, three otherwise) and zeros elsewhere, then the
  * output as a second GEMM against W_out transposed and repeated once per
  * part.  With fp32 x, W and y both GEMMs are fp32 (fp32 MFMA) and the
- * activations go in whole.  The products' kernel and tile shapes depend on
+ * activations go in whole.  At depth 0 with no records, where every node is
+ * visited, the first product stores the activations itself (fp32, or two
+ * bf16 parts when y is bf16), with the same bits.  The products' kernel and tile shapes depend on
  * the shapes and the device's CU count only, so the result bits do too.
  * Needs the workspace of fff_workspace_bytes (logits, parts, the transposed
  * W_out).
