@@ -32,6 +32,8 @@ def load():
         lib.fffb_copy.restype = c_int
         lib.fffb_mb_read.argtypes = [c_void_p, c_int64, c_int64, c_void_p, c_int, c_void_p]
         lib.fffb_mb_read.restype = c_int
+        lib.fffb_mb_write.argtypes = [c_void_p, c_int64, c_int64, c_int, c_void_p]
+        lib.fffb_mb_write.restype = c_int
         lib.fffb_mb_gather.argtypes = [c_void_p, c_int64, c_int, c_int, c_int, c_int, c_void_p, c_void_p]
         lib.fffb_mb_gather.restype = c_int
         lib.fffb_mb_mfma.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p]

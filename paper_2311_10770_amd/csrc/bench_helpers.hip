@@ -120,6 +120,13 @@ __global__ void mb_read_kernel(const uint4* __restrict__ buf, int64_t mask, int6
     if (acc == 0x9e3779b9u) out[0] = acc;  // keeps the loads alive; practically never stores
 }
 
+// mb_write: every thread streams 16-byte vector stores over a footprint of (mask + 1) vectors,
+// `total` vectors in all (wrapping), like mb_read.
+__global__ void mb_write_kernel(uint4* __restrict__ buf, int64_t mask, int64_t total, uint32_t seed) {
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x)
+        buf[i & mask] = make_uint4(seed, seed ^ uint32_t(i), seed, seed);
+}
+
 // mb_gather: groups of 16 lanes gather whole rows (`row_vecs` 16-byte vectors)
 // from a table of `rows` rows; `steps` rows per group.  dependent = 0: row ids
 // come from a hash (independent loads); dependent = 1: each row id is derived
@@ -198,6 +205,14 @@ FFFB_EXPORT int fffb_mb_read(const void* buf, int64_t footprint_bytes, int64_t t
     if (nvec < 1 || (nvec & (nvec - 1)) || total_bytes < 16 || grid < 1) return -1;
     hipLaunchKernelGGL(mb_read_kernel, dim3(grid), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
                        reinterpret_cast<const uint4*>(buf), nvec - 1, total_bytes / 16, reinterpret_cast<uint32_t*>(out));
+    return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+FFFB_EXPORT int fffb_mb_write(void* buf, int64_t footprint_bytes, int64_t total_bytes, int grid, void* stream) {
+    const int64_t nvec = footprint_bytes / 16;
+    if (nvec < 1 || (nvec & (nvec - 1)) || total_bytes < 16 || grid < 1) return -1;
+    hipLaunchKernelGGL(mb_write_kernel, dim3(grid), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<uint4*>(buf), nvec - 1, total_bytes / 16, 0x5bd1e995u);
     return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 

@@ -3,7 +3,8 @@
     python -m paper_2311_10770_amd.microbench
 
 * stream read bandwidth with footprints that fit one XCD's L2, the MALL, or
-  only HBM;
+  only HBM; stream write bandwidth likewise, and a copy of the output size of
+  the headline layer (100.7 MB) and of 1 GiB;
 * 1.5 KB row gathers by 16-lane groups (one bf16 row at hidden 768) from
   tables of those sizes, with independent row ids or a dependent chain (each
   row id computed from the previous row, like a tree walk);
@@ -61,6 +62,23 @@ def main():
                                       "GBps": by / t / 1e9, "us": t * 1e6})
                 print(f"gather table {fp / 2**20:7.0f} MiB dep={dep} groups {groups:6d}: {by / t / 1e9:8.0f} GB/s "
                       f"({t * 1e6:.1f} us)", file=sys.stderr, flush=True)
+    res["write"] = []
+    for fp in (16 << 20, 128 << 20, 1 << 30, 2 << 30):
+        total = max(4 << 30, 4 * fp)
+        for grid in (cus * 8, cus * 32):
+            if lib.fffb_mb_write(big.data_ptr(), fp, total, grid, st) != 0:
+                raise RuntimeError("fffb_mb_write failed")
+            t = _time(lambda: lib.fffb_mb_write(big.data_ptr(), fp, total, grid, st))
+            res["write"].append({"footprint_mb": fp / 2**20, "grid": grid, "GBps": total / t / 1e9})
+            print(f"write footprint {fp / 2**20:7.0f} MiB grid {grid:5d}: {total / t / 1e9:8.0f} GB/s", file=sys.stderr,
+                  flush=True)
+    res["copy"] = []
+    for nbytes in (65536 * 768 * 2, 1 << 30):  # the headline's y (bf16) and 1 GiB
+        src, dst = big[:nbytes], big[1 << 30:(1 << 30) + nbytes]
+        t = _time(lambda: benchlib.copy(src, dst))
+        res["copy"].append({"bytes": nbytes, "GBps_read_plus_write": 2 * nbytes / t / 1e9, "us": t * 1e6})
+        print(f"copy {nbytes / 1e6:8.1f} MB: {2 * nbytes / t / 1e9:8.0f} GB/s read + write ({t * 1e6:.1f} us)",
+              file=sys.stderr, flush=True)
     res["mfma"] = []
     names = {0: "16x16x32 bf16", 1: "32x32x16 bf16", 2: "16x16x4 fp32", 3: "32x32x2 fp32"}
     mout = torch.empty(cus * 4 * 256, dtype=torch.float32, device=dev)
