@@ -657,6 +657,26 @@ def test_masked_depth0_without_records(fff_lib, k, B, dt, yd, out, act):
     assert np.array_equal(got["y"].view(np.uint8), rec["y"].view(np.uint8))
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_masked_depth0_full_size_sampled(fff_lib, dt):
+    """3072 trees of depth 0 at 16384 tokens, as the KxD sweep times it: AUTO (masked, the logit
+    product storing the activations), no records; 384 sampled tokens against the oracle."""
+    B, k = 16384, 3072
+    L = layer(490, B, 768, 0, k, dt, dt)
+    x = fff_lib.from_numpy(L["x"], DEV)
+    wi = fff_lib.from_numpy(L["w_in"], DEV)
+    wo = fff_lib.from_numpy(L["w_out"], DEV)
+    y = torch.full((B, 768), float("nan"), dtype=TORCH_DT[dt], device=DEV)
+    assert fff_lib.describe(x, wi, wo, 0, k, y).startswith("masked<")
+    flush_print(f"[gpu] masked depth 0 full size: k={k} B={B} {dt}")
+    fff_lib.forward(x, wi, wo, 0, k, y)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(491).choice(B, 384, replace=False))
+    ref = oracle.forward(L["x"][rows], L["w_in"], L["w_out"], 0, k)
+    parity.assert_parity(L["x"], L["w_in"], L["w_out"], 0, k, ref, fff_lib.to_numpy(y), rows=rows,
+                         tol=tol_for(dt, dt))
+
+
 def test_masked_mode_limits_and_auto(fff_lib):
     """Masked needs bf16 x and W, or fp32 x, W and y, and depth <= 7; AUTO takes it at depth <= 5
     for 16 bf16 trees or more, or 12 and 16384 tokens, and at depth <= 4 for 32 fp32 trees or more
