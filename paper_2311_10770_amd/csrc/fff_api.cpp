@@ -532,6 +532,8 @@ void format_plan(const fff::Plan& plan, const char* prefix, char* buf, size_t le
     if ((plan.kind == fff::KIND_GROUPED || plan.kind == fff::KIND_TILED) && n > 0 && size_t(n) < len)
         n += std::snprintf(buf + n, len - n, " emit_lds_levels=%d split_level=%d emit_lanes=%d walk_tree_per_xcd=%d",
                            plan.emit_lds_levels, plan.split_level, plan.emit_lanes, plan.walk_affine);
+    if (plan.kind == fff::KIND_TILED && n > 0 && size_t(n) < len)
+        n += std::snprintf(buf + n, len - n, " leaf_pairs=%d", plan.tile_pair);
     for (int i = 0; i < plan.n_launch && n > 0 && size_t(n) < len; ++i)
         n += std::snprintf(buf + n, len - n, " | launch%d grid=%d block=%d lds_bytes=%zu", i, plan.launch[i].grid,
                            plan.launch[i].block, plan.launch[i].lds_bytes);

@@ -141,6 +141,7 @@ struct Plan {
     int emit_lds_levels = 0;       // grouped emit
     int split_level = 0;           // grouped mode
     int walk_affine = 0;           // grouped / tiled: one tree per walk workgroup, by XCD
+    int tile_pair = 0;             // tiled: a tile workgroup per pair of sibling leaves
     int cu_count = 0;              // masked: compute units, for the products' tile choice
     const char* name = "";
 };

@@ -537,9 +537,14 @@ __device__ __forceinline__ void store_token_sd(const void* src, void* dst, float
 // per-token emit layout for tokens of overflowing leaves; SRC/DBF: the output
 // form (p.tile_src, p.tile_dst); P2: two bf16 parts of each activation (the
 // layer's output is bf16) instead of three.  FSTEPS: MFMA steps of four levels
-// with fp32 weights (at least (D + 4) / 4; unused with bf16 weights).
-template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2, int FSTEPS>
+// with fp32 weights (at least (D + 4) / 4; unused with bf16 weights).  PAIR (fp32
+// weights): a workgroup per pair of sibling leaves, whose tokens share one list of
+// tiles: the rows of levels 0 .. D-1 are common, and two virtual levels D and D+1
+// hold the left and the right leaf's row, each token's leaf activation going to its
+// own leaf's level and a zero to the other (at least (D + 5) / 4 steps).
+template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2, int FSTEPS, bool PAIR = false>
 __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
+    static_assert(!PAIR || !WBF, "leaf pairs: fp32 weights");
     constexpr int H = 16 * CB;
     static_assert(H % 128 == 0, "128-column groups");
     constexpr int GROUPS = H / 128;
@@ -585,28 +590,37 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
         return;
     }
 
-    // this workgroup's leaf: XCD x (blockIdx % 8) takes the subtrees at the split level that are x mod 8
-    int64_t leaf = blockIdx.x;
+    // this workgroup's leaf (or pair of sibling leaves): XCD x (blockIdx % 8) takes the subtrees at
+    // the split level that are x mod 8
+    constexpr int LPW = PAIR ? 2 : 1;  // leaves per workgroup
+    int64_t unit = blockIdx.x;
     if (p.split_level > 0) {
-        const int64_t per = int64_t(1) << (D - p.split_level);  // leaves per subtree
+        const int64_t per = (int64_t(1) << (D - p.split_level)) / LPW;  // workgroups per subtree
         const int64_t x = blockIdx.x % XCDS, lb = blockIdx.x / XCDS;
-        leaf = (x + XCDS * (lb / per)) * per + lb % per;
+        unit = (x + XCDS * (lb / per)) * per + lb % per;
     }
+    const int64_t leaf = unit * LPW;  // the (left) leaf
     const int64_t bin = int64_t(tree) * L + leaf;
     const int32_t cnt_all = p.bk_count[bin];
-    if (cnt_all == 0) return;  // workgroup-uniform
+    const int32_t cnt_r = PAIR ? p.bk_count[bin + 1] : 0;  // the right sibling's
+    if (cnt_all == 0 && cnt_r == 0) return;  // workgroup-uniform
     const int cap = p.bk_cap;
     const int32_t* bucket = p.bk_tok + bin * cap;
     const float* act = p.bk_act + bin * int64_t(cap) * TILE_REC;
-    if (cnt_all > cap) {
+    if (cnt_all > cap || cnt_r > cap) {
         // An overflowing leaf: which of its tokens found a slot depends on the order of the walk's
         // atomics, so all of them take the per-token emit (these from their slots, the rest in the
-        // spill workgroups) and every token's output is the same bits on every run.
-        emit_per_token(int64_t(cap), wave, WAVES, [&](int64_t i) { return int64_t(bucket[i]); },
-                       [&](int64_t i) { return act + i * TILE_REC; });
+        // spill workgroups) and every token's output is the same bits on every run.  A pair takes
+        // it for both leaves (the counts, and so this choice, do not depend on that order).
+        emit_per_token(int64_t(cnt_all < cap ? cnt_all : cap), wave, WAVES,
+                       [&](int64_t i) { return int64_t(bucket[i]); }, [&](int64_t i) { return act + i * TILE_REC; });
+        if constexpr (PAIR)
+            emit_per_token(int64_t(cnt_r < cap ? cnt_r : cap), wave, WAVES,
+                           [&](int64_t i) { return int64_t(bucket[cap + i]); },
+                           [&](int64_t i) { return act + (cap + i) * TILE_REC; });
         return;
     }
-    const int cnt = cnt_all;
+    const int cnt = cnt_all + cnt_r;
     const uint32_t leaf1 = uint32_t(leaf + L);
     const int n = lane & 15, kq = lane >> 4;
     constexpr int SSZ = SRC == TSRC_BF16 ? 2 : 4;
@@ -763,22 +777,28 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             }
         }
     } else {
-        const int steps = (D + 4) / 4;
-        // level of step s for this lane, clamped to D
+        constexpr int VL = PAIR ? 1 : 0;  // virtual levels past D (the right leaf's row)
+        const int steps = (D + 4 + VL) / 4;
+        // (virtual) level of step s for this lane, clamped to D + VL
         int lvl_c[FSTEPS];
 #pragma unroll
-        for (int s = 0; s < FSTEPS; ++s) lvl_c[s] = 4 * s + kq <= D ? 4 * s + kq : D;
+        for (int s = 0; s < FSTEPS; ++s) lvl_c[s] = 4 * s + kq <= D + VL ? 4 * s + kq : D + VL;
         struct Raw {
             int32_t tok;
             float a[FSTEPS];
+            bool right;  // PAIR: the token is in the right leaf
         };
-        // token id of slot t0 + n and its activations at levels 4s + kq
+        // token id of list entry t0 + n (PAIR: the left leaf's slots, then the right leaf's) and
+        // its activations at levels 4s + kq (the leaf's at the virtual level)
         auto load_tile = [&](int t0, Raw& r) {
-            const int slot = t0 + n < cap ? t0 + n : cap - 1;
+            const int i = t0 + n;
+            r.right = PAIR && i >= cnt_all;
+            const int j = r.right ? i - cnt_all : i;
+            const int slot = (j < cap ? j : cap - 1) + (r.right ? cap : 0);
             r.tok = bucket[slot];
             const float* rec = act + int64_t(slot) * TILE_REC;
 #pragma unroll
-            for (int s = 0; s < FSTEPS; ++s) r.a[s] = rec[lvl_c[s]];
+            for (int s = 0; s < FSTEPS; ++s) r.a[s] = rec[lvl_c[s] <= D ? lvl_c[s] : D];
         };
         for (int g = wave; g < GROUPS; g += WAVES) {
             const int64_t col = int64_t(g) * 128 + (HALVES ? 4 : 8) * n;
@@ -787,7 +807,9 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             float4 w[FSTEPS][2];
 #pragma unroll
             for (int s = 0; s < FSTEPS; ++s) {
-                const int64_t at = (int64_t(leaf1 >> (D - lvl_c[s])) - 1) * H + col;
+                // node of the level: the ancestor of the leaf, or at the virtual level the right leaf
+                const int64_t node = lvl_c[s] <= D ? int64_t(leaf1 >> (D - lvl_c[s])) - 1 : int64_t(leaf1);
+                const int64_t at = node * H + col;
                 w[s][0] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at);
                 w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + (HALVES ? 64 : 4));
             }
@@ -803,7 +825,11 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 #pragma unroll
                     for (int s = 0; s < FSTEPS; ++s) {
                         if (s < steps) {
-                            const float a = in && 4 * s + kq <= D ? cur.a[s] : 0.0f;
+                            const int v = 4 * s + kq;
+                            // PAIR: the leaf activation at its own leaf's level, zero at the other's
+                            const bool use = PAIR ? (v < D || (v == D && !cur.right) || (v == D + 1 && cur.right))
+                                                  : v <= D;
+                            const float a = in && use ? cur.a[s] : 0.0f;
 #pragma unroll
                             for (int j = 0; j < NB; ++j)
                                 acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
@@ -1080,6 +1106,7 @@ struct Variant {
     const void* emit;
     const void* tile[3][3];  // [source TSRC_*][form: fp32 dst 3 parts, fp32 dst 2 parts, bf16 dst 2 parts]
     const void* tile_deep[3][3];  // the same for fp32 weights deeper than TILE_STEPS_SHALLOW steps
+    const void* tile_pair[3][3];  // fp32 weights: a workgroup per pair of sibling leaves
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -1093,6 +1120,11 @@ struct Variant {
     {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, FS>),                                   \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, FS>),                                    \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, FS>)}
+// leaf pairs with fp32 weights (bf16 weights repeat their single-leaf kernels, never chosen)
+#define FFF_TILES_PAIR(H, XB, WB, EL, ENV, SRC)                                                              \
+    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, TILE_MAX_STEPS, !(WB)>),                \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, TILE_MAX_STEPS, !(WB)>),                 \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, TILE_MAX_STEPS, !(WB)>)}
 // bf16 weights take one instantiation for both arrays
 #define FFF_TILE_STEPS(WB) ((WB) ? TILE_MAX_STEPS : TILE_STEPS_SHALLOW)
 #define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, WBLK, WNBLK, EL, ENV)                                         \
@@ -1105,6 +1137,8 @@ struct Variant {
             {FFF_TILES(H, XB, WB, EL, ENV, TSRC_NONE, TILE_MAX_STEPS),                                        \
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_F32, TILE_MAX_STEPS),                                         \
              FFF_TILES(H, XB, WB, EL, ENV, TSRC_BF16, TILE_MAX_STEPS)},                                       \
+            {FFF_TILES_PAIR(H, XB, WB, EL, ENV, TSRC_NONE), FFF_TILES_PAIR(H, XB, WB, EL, ENV, TSRC_F32),      \
+             FFF_TILES_PAIR(H, XB, WB, EL, ENV, TSRC_BF16)},                                                  \
             FFF_K(stack_kernel<L, NV, XB, WB, BLOCK, false>), FFF_K(descent_kernel<L, NV, false, WB, BLOCK, true>), \
             FFF_K(walk_kernel<WL, WNV, false, WB, WNBLK, true>), FFF_K(stack_kernel<L, NV, false, WB, BLOCK, true>), \
             "lanes=" #L ",nv=" #NV ",x_bf16=" #XB ",w_bf16=" #WB                                              \
@@ -1241,11 +1275,18 @@ static int out_src_kind(const Params& p) {
 // parts when the layer's output is bf16.
 static int tile_src_kind(const Params& p, int t) { return t > 0 ? int(TSRC_F32) : out_src_kind(p); }
 
-static const void* tile_kernel_for(const Variant& v, const Params& p, int t) {
+static const void* tile_kernel_for(const Variant& v, const Params& p, int t, bool pair) {
     const bool last = t == p.n_trees - 1;
     const int form = last && p.y_bf16 ? 2 : p.y_bf16 ? 1 : 0;
+    if (pair) return v.tile_pair[tile_src_kind(p, t)][form];
     return (p.depth + 4) / 4 <= TILE_STEPS_SHALLOW ? v.tile[tile_src_kind(p, t)][form]
                                                    : v.tile_deep[tile_src_kind(p, t)][form];
+}
+
+// Leaf pairs: with fp32 weights, when a leaf holds fewer tokens than one 16-row tile on average
+// (depth 11, 16384 tokens: 8), and the two virtual rows still fit the MFMA steps.
+static bool tile_pairs(const Params& p) {
+    return !p.w_bf16 && p.depth >= 5 && p.depth + 2 <= 4 * TILE_MAX_STEPS && p.n_tokens < (int64_t(16) << p.depth);
 }
 
 // The walk launch of the grouped and tiled plans: with 2, 4 or 8 trees one tree per workgroup
@@ -1386,10 +1427,12 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         Launch& W = plan->launch[plan->n_launch++];
         if (!plan_walk(p, *v, lds_levels_req, dev, plan, W)) return ST_UNSUPPORTED;
         Launch& E = plan->launch[plan->n_launch++];
-        E.kernel = tile_kernel_for(*v, p, 0);  // the first tree's; run_forward picks each tree's form
+        plan->tile_pair = tile_pairs(p) ? 1 : 0;
+        E.kernel = tile_kernel_for(*v, p, 0, plan->tile_pair);  // the first tree's; run_forward picks each tree's form
         E.block = 64 * tile_waves(p.hidden);
-        // per tree: one workgroup per leaf (a multiple of eight: leaves >= 32), then spill workgroups
-        E.grid = int(leaves) + dev.cu_count;
+        // per tree: one workgroup per leaf or pair of leaves (a multiple of eight: leaves >= 32), then
+        // spill workgroups
+        E.grid = int(leaves >> plan->tile_pair) + dev.cu_count;
         return ST_OK;
     }
 
@@ -1513,7 +1556,7 @@ static hipError_t run_tiled(const Params& p, const Plan& plan, void* workspace, 
     if (e != hipSuccess) return e;
     const Variant* v = find_variant(p);
     const Launch& E = plan.launch[2];
-    int leaf_blocks = int(leaves);
+    int leaf_blocks = int(leaves >> plan.tile_pair);
     const void* src0 = out_src_kind(p) == TSRC_NONE ? nullptr : p.out_mode == OUT_RESIDUAL ? p.x : p.y;
     // trees in order: tree t adds its contribution to the running sum of trees 0..t-1 (a fixed
     // order of the sum over trees, so the output bits do not depend on scheduling)
@@ -1523,7 +1566,7 @@ static hipError_t run_tiled(const Params& p, const Plan& plan, void* workspace, 
         qt.tile_src = t > 0 ? sum : src0;
         qt.tile_dst = t == int(T) - 1 ? p.y : sum;
         void* targs[] = {&qt, &leaf_blocks};
-        e = hipLaunchKernel(tile_kernel_for(*v, p, t), dim3(E.grid), dim3(E.block), targs, 0, stream);
+        e = hipLaunchKernel(tile_kernel_for(*v, p, t, plan.tile_pair), dim3(E.grid), dim3(E.block), targs, 0, stream);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

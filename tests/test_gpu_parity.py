@@ -551,6 +551,46 @@ def test_tiled_multi_tree_spills_deterministic(fff_lib):
     assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
 
 
+def test_tiled_leaf_pairs_plan(fff_lib):
+    """fp32 weights with fewer than 16 tokens per leaf on average take a tile workgroup per pair of
+    sibling leaves (depth <= 14); bf16 weights and fuller leaves one per leaf."""
+    def pairs(B, D, wd, T=1):
+        x = torch.zeros(B, 768, dtype=torch.float32, device=DEV)
+        w = torch.zeros(T, (2 << D) - 1, 768, dtype=TORCH_DT[wd], device=DEV)
+        s = fff_lib.describe(x, w, w, D, T, mode="tiled")
+        assert s.startswith("tiled<")
+        return int(s.split("leaf_pairs=")[1].split()[0])
+    assert pairs(16384, 11, "f32") == 1  # the paper's Table 2 shape: 8 tokens per leaf
+    assert pairs(32767, 11, "f32") == 1 and pairs(32768, 11, "f32") == 0
+    assert pairs(16384, 11, "bf16") == 0
+    assert pairs(3000, 14, "f32") == 1 and pairs(3000, 15, "f32") == 0  # two more rows fit 16 levels
+    assert pairs(4096, 9, "f32", T=4) == 1 and pairs(16384, 9, "f32", T=4) == 0
+
+
+@pytest.mark.parametrize("B,D,xd,yd", [(1, 11, "f32", "f32"), (7, 11, "f32", "bf16"), (100, 11, "bf16", "f32"),
+                                       (2049, 5, "f32", "f32"), (5000, 14, "f32", "f32"), (16384, 11, "f32", "f32")])
+def test_tiled_leaf_pairs(fff_lib, B, D, xd, yd):
+    """Leaf pairs against the oracle: empty and single siblings (1 to 100 tokens), depth 5 (the
+    fewest leaves), depth 14 (the two virtual rows fill the fourth step), the Table 2 shape."""
+    L = layer(280 + B + D, B, 768, D, 1, xd, "f32")
+    check_layer(fff_lib, f"tiled pairs B={B} D={D} {xd}/{yd}", L, D, 1, yd, mode="tiled")
+
+
+def test_tiled_leaf_pairs_spills_deterministic(fff_lib):
+    """Clustered tokens overflow some leaves: the pair of an overflowing leaf takes the per-token
+    emit for both siblings; two runs give the same bits."""
+    B, D = 20000, 11
+    x = synth.make_clustered_x(290, B, 768, "f32", n_centres=8)
+    wi, wo = synth.make_weights(290, 768, D, 1, "f32")
+    L = {"x": x, "w_in": wi, "w_out": wo}
+    assert "leaf_pairs=1" in fff_lib.describe(fff_lib.from_numpy(x, DEV), fff_lib.from_numpy(wi, DEV),
+                                              fff_lib.from_numpy(wo, DEV), D, 1, mode="tiled")
+    check_layer(fff_lib, "tiled pairs clustered", L, D, 1, "f32", mode="tiled")
+    a = run_fff(fff_lib, L, D, 1, "f32", mode="tiled")
+    b = run_fff(fff_lib, L, D, 1, "f32", mode="tiled")
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["nodes"], b["nodes"])
+
+
 def test_tiled_unsupported_shapes(fff_lib):
     L = layer(240, 64, 768, 4, 1, "f32", "f32")  # depth below 5
     with pytest.raises(fff_lib.FffError):
