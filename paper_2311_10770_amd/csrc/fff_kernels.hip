@@ -538,13 +538,13 @@ __device__ __forceinline__ void store_token_sd(const void* src, void* dst, float
 // form (p.tile_src, p.tile_dst); P2: two bf16 parts of each activation (the
 // layer's output is bf16) instead of three.  FSTEPS: MFMA steps of four levels
 // with fp32 weights (at least (D + 4) / 4; unused with bf16 weights).  PAIR (fp32
-// weights): a workgroup per pair of sibling leaves, whose tokens share one list of
-// tiles: the rows of levels 0 .. D-1 are common, and two virtual levels D and D+1
-// hold the left and the right leaf's row, each token's leaf activation going to its
-// own leaf's level and a zero to the other (at least (D + 5) / 4 steps).
+// a workgroup per pair of sibling leaves, whose tokens share one list of tiles: the
+// rows of levels 0 .. D-1 are common, and two virtual levels D and D+1 hold the left
+// and the right leaf's row, each token's leaf activation going to its own leaf's
+// level and a zero to the other (D + 2 <= 16 levels; with fp32 weights at least
+// (D + 5) / 4 steps).
 template <int CB, bool XBF, bool WBF, int ELANES, int ENV, int SRC, bool DBF, bool P2, int FSTEPS, bool PAIR = false>
 __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p, int leaf_blocks) {
-    static_assert(!PAIR || !WBF, "leaf pairs: fp32 weights");
     constexpr int H = 16 * CB;
     static_assert(H % 128 == 0, "128-column groups");
     constexpr int GROUPS = H / 128;
@@ -661,19 +661,35 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
         }
     };
 
+    constexpr int VL = PAIR ? 1 : 0;  // virtual levels past D (the right leaf's row)
+    // PAIR: the leaf activation at its own leaf's (virtual) level, zero at the other's
+    auto pick = [&](int v, float a, bool right, float aleaf) {
+        if constexpr (PAIR) return v < D ? a : v == D ? (right ? 0.0f : a) : v == D + 1 && right ? aleaf : 0.0f;
+        else return v <= D ? a : 0.0f;
+    };
+    // node of (virtual) level v <= D + VL: the ancestor of the leaf, or the right leaf
+    auto row_node = [&](int v) { return v <= D ? int64_t(leaf1 >> (D - v)) - 1 : int64_t(leaf1); };
     if constexpr (WBF) {
         constexpr int PARTS = P2 ? 2 : 3;
         const int h = kq & 1, part = kq >> 1;
         struct Raw {
             int32_t tok;
             float4 a0, a1;  // activations of levels 8h .. 8h+7
+            bool right;     // PAIR: the token is in the right leaf
+            float aleaf;    // PAIR: its leaf activation
         };
+        // token id of list entry t0 + n (PAIR: the left leaf's slots, then the right leaf's)
         auto load_tile = [&](int t0, Raw& r) {
-            const int slot = t0 + n < cap ? t0 + n : cap - 1;
+            const int i = t0 + n;
+            r.right = PAIR && i >= cnt_all;
+            const int j = r.right ? i - cnt_all : i;
+            const int slot = (j < cap ? j : cap - 1) + (r.right ? cap : 0);
             r.tok = bucket[slot];
-            const float4* rec = reinterpret_cast<const float4*>(act + int64_t(slot) * TILE_REC + 8 * h);
+            const float* recp = act + int64_t(slot) * TILE_REC;
+            const float4* rec = reinterpret_cast<const float4*>(recp + 8 * h);
             r.a0 = rec[0];
             r.a1 = rec[1];
+            r.aleaf = PAIR ? recp[D] : 0.0f;
         };
         for (int g = wave; g < GROUPS; g += WAVES) {
             const int64_t col = int64_t(g) * 128 + (HALVES ? 4 : 8) * n;
@@ -686,9 +702,9 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
                 for (int c = 0; c < 2; ++c)
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
-                        const int lvl = 8 * h + i <= D ? 8 * h + i : D;
+                        const int lvl = 8 * h + i <= D + VL ? 8 * h + i : D + VL;
                         row[c][i] = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(w_out) +
-                                                                    (int64_t(leaf1 >> (D - lvl)) - 1) * H + col + 64 * c);
+                                                                    row_node(lvl) * H + col + 64 * c);
                     }
 #pragma unroll
                 for (int c = 0; c < 2; ++c)
@@ -707,9 +723,8 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
                 uint4 row[8];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
-                    const int lvl = 8 * h + i <= D ? 8 * h + i : D;
-                    row[i] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(w_out) +
-                                                             (int64_t(leaf1 >> (D - lvl)) - 1) * H + col);
+                    const int lvl = 8 * h + i <= D + VL ? 8 * h + i : D + VL;
+                    row[i] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(w_out) + row_node(lvl) * H + col);
                 }
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
@@ -730,8 +745,8 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
                 uint32_t p0[4], p1[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const float x0 = in && 8 * h + 2 * q <= D ? av[2 * q] : 0.0f;
-                    const float x1 = in && 8 * h + 2 * q + 1 <= D ? av[2 * q + 1] : 0.0f;
+                    const float x0 = in ? pick(8 * h + 2 * q, av[2 * q], cur.right, cur.aleaf) : 0.0f;
+                    const float x1 = in ? pick(8 * h + 2 * q + 1, av[2 * q + 1], cur.right, cur.aleaf) : 0.0f;
                     const uint32_t hi = pack_bf16x2(x0, x1);
                     const float r0 = x0 - bf16_lo(hi), r1 = x1 - bf16_hi(hi);
                     const uint32_t mid = pack_bf16x2(r0, r1);
@@ -777,7 +792,6 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             }
         }
     } else {
-        constexpr int VL = PAIR ? 1 : 0;  // virtual levels past D (the right leaf's row)
         const int steps = (D + 4 + VL) / 4;
         // (virtual) level of step s for this lane, clamped to D + VL
         int lvl_c[FSTEPS];
@@ -807,9 +821,7 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
             float4 w[FSTEPS][2];
 #pragma unroll
             for (int s = 0; s < FSTEPS; ++s) {
-                // node of the level: the ancestor of the leaf, or at the virtual level the right leaf
-                const int64_t node = lvl_c[s] <= D ? int64_t(leaf1 >> (D - lvl_c[s])) - 1 : int64_t(leaf1);
-                const int64_t at = node * H + col;
+                const int64_t at = row_node(lvl_c[s]) * H + col;
                 w[s][0] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at);
                 w[s][1] = *reinterpret_cast<const float4*>(static_cast<const float*>(w_out) + at + (HALVES ? 64 : 4));
             }
@@ -825,11 +837,7 @@ __global__ __launch_bounds__(64 * tile_waves(16 * CB)) void tile_kernel(Params p
 #pragma unroll
                     for (int s = 0; s < FSTEPS; ++s) {
                         if (s < steps) {
-                            const int v = 4 * s + kq;
-                            // PAIR: the leaf activation at its own leaf's level, zero at the other's
-                            const bool use = PAIR ? (v < D || (v == D && !cur.right) || (v == D + 1 && cur.right))
-                                                  : v <= D;
-                            const float a = in && use ? cur.a[s] : 0.0f;
+                            const float a = in ? pick(4 * s + kq, cur.a[s], cur.right, cur.a[s]) : 0.0f;
 #pragma unroll
                             for (int j = 0; j < NB; ++j)
                                 acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
@@ -1106,7 +1114,7 @@ struct Variant {
     const void* emit;
     const void* tile[3][3];  // [source TSRC_*][form: fp32 dst 3 parts, fp32 dst 2 parts, bf16 dst 2 parts]
     const void* tile_deep[3][3];  // the same for fp32 weights deeper than TILE_STEPS_SHALLOW steps
-    const void* tile_pair[3][3];  // fp32 weights: a workgroup per pair of sibling leaves
+    const void* tile_pair[3][3];  // a workgroup per pair of sibling leaves
     const void* stack;
     // LayerNorm prologue: x widened to fp32 whatever its storage type
     const void* descent_norm;
@@ -1120,11 +1128,11 @@ struct Variant {
     {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, FS>),                                   \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, FS>),                                    \
      FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, FS>)}
-// leaf pairs with fp32 weights (bf16 weights repeat their single-leaf kernels, never chosen)
+// leaf pairs
 #define FFF_TILES_PAIR(H, XB, WB, EL, ENV, SRC)                                                              \
-    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, TILE_MAX_STEPS, !(WB)>),                \
-     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, TILE_MAX_STEPS, !(WB)>),                 \
-     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, TILE_MAX_STEPS, !(WB)>)}
+    {FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, false, TILE_MAX_STEPS, true>),                 \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, false, true, TILE_MAX_STEPS, true>),                  \
+     FFF_K(tile_kernel<H / 16, XB, WB, EL, ENV, SRC, true, true, TILE_MAX_STEPS, true>)}
 // bf16 weights take one instantiation for both arrays
 #define FFF_TILE_STEPS(WB) ((WB) ? TILE_MAX_STEPS : TILE_STEPS_SHALLOW)
 #define FFF_VARIANT(H, XB, WB, L, NV, WL, WNV, WBLK, WNBLK, EL, ENV)                                         \
@@ -1283,10 +1291,10 @@ static const void* tile_kernel_for(const Variant& v, const Params& p, int t, boo
                                                    : v.tile_deep[tile_src_kind(p, t)][form];
 }
 
-// Leaf pairs: with fp32 weights, when a leaf holds fewer tokens than one 16-row tile on average
-// (depth 11, 16384 tokens: 8), and the two virtual rows still fit the MFMA steps.
+// Leaf pairs: when a leaf holds fewer tokens than one 16-row tile on average (depth 11, 16384
+// tokens: 8), and the two virtual rows still fit the MFMA steps.
 static bool tile_pairs(const Params& p) {
-    return !p.w_bf16 && p.depth >= 5 && p.depth + 2 <= 4 * TILE_MAX_STEPS && p.n_tokens < (int64_t(16) << p.depth);
+    return p.depth >= 5 && p.depth + 2 <= 4 * TILE_MAX_STEPS && p.n_tokens < (int64_t(16) << p.depth);
 }
 
 // The walk launch of the grouped and tiled plans: with 2, 4 or 8 trees one tree per workgroup
@@ -1328,7 +1336,11 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         //   48M input elements, or 16 per leaf from 16M (depth 11 at 32768 tokens: 51 against
         //   60 us in bf16); at depth 9 in bf16 only from 96M (the fused kernel stays ahead below);
         //   with fp32 weights at depth >= 11 from 8 per leaf (16384 tokens: 64 against 67 us per
-        //   call, 61 against 67 back to back); in bf16 at depth >= 11 from 4 per leaf when the
+        //   call, 61 against 67 back to back), and from 2 per leaf where sibling leaves share a
+        //   workgroup (depth <= 14) and the input has 12M elements (depth 12, 16384 tokens: 65
+        //   against 75 us grouped; depth 14, 65536 tokens: 301 against 368; hidden 4096, depth 11,
+        //   4096 tokens: 111 against 124 fused; one per leaf loses: depth 14, 16384 tokens, 123
+        //   against 104 grouped); in bf16 at depth >= 11 from 4 per leaf when the
         //   rows are long (hidden 4096, 8192 tokens: 107 against 113 us; at hidden 768 the
         //   grouped emit is ahead at 4 per leaf, depth 13: 80 against 86 us);
         // * other single trees grouped by subtree at depth >= 11 from 48M elements, or from 16384
@@ -1336,9 +1348,10 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
         //   with fp32 weights at depth >= 5 from 65536 tokens (5-7 % ahead of the fused kernel);
         // * 2, 4 or 8 trees of depth >= 7 (the walk tree-affine: the workgroups of an XCD walk
         //   one tree, its top levels in LDS and its deep rows in that XCD's L2): with fp32 weights
-        //   leaf-tiled at depth >= 11 from 8 tokens per leaf and at depth >= 9 from 32 per leaf
-        //   (eight trees of depth 11, 65536 tokens: 1481 against 2556 us fused; four of depth 9:
-        //   554 against 665 at 65536 tokens, 149 against 160 at 16384), else grouped from
+        //   leaf-tiled at depth >= 11 from 8 tokens per leaf, at depth >= 10 from 16 and at
+        //   depth >= 9 from 32 per leaf (eight trees of depth 11, 65536 tokens: 1481 against
+        //   2556 us fused; four of depth 9: 554 against 665 at 65536 tokens, 149 against 160 at
+        //   16384; four of depth 10, 16384 tokens: 174 against 200), else grouped from
         //   65536 tokens (16384 with 8 trees); with bf16 weights grouped for 8 trees, for 4 from
         //   4096 tokens at depth >= 8 (65536 at depth 7), for 2 from 65536 tokens at depth >= 8
         //   (four trees of depth 9, 65536 tokens: 272 against 306 us);
@@ -1371,7 +1384,9 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
                  (!p.w_bf16 || p.depth >= 10 || elems >= (int64_t(96) << 20)) &&
                  ((big && p.n_tokens >= (int64_t(8) << p.depth)) ||
                   (one && elems >= (int64_t(16) << 20) && p.n_tokens >= (int64_t(16) << p.depth)) ||
-                  (one && !p.w_bf16 && p.depth >= 11 && p.n_tokens >= (int64_t(8) << p.depth)) ||
+                  (one && !p.w_bf16 && p.depth >= 11 &&
+                   (p.n_tokens >= (int64_t(8) << p.depth) ||
+                    (tile_pairs(p) && p.n_tokens >= (int64_t(2) << p.depth) && elems >= (int64_t(12) << 20)))) ||
                   (one && p.w_bf16 && p.depth >= 11 && p.hidden >= 2048 && p.n_tokens >= (int64_t(4) << p.depth))))
             mode = MODE_TILED;
         else if (one && int64_t(workspace_bytes) >= grouped_ws &&
@@ -1380,6 +1395,7 @@ int plan_forward(const Params& p, int mode, int lds_levels_req, int split_level_
             mode = MODE_GROUPED;
         else if (affine && !p.w_bf16 && tiled_ws > 0 && int64_t(workspace_bytes) >= tiled_ws &&
                  ((p.depth >= 11 && p.n_tokens >= (int64_t(8) << p.depth)) ||
+                  (p.depth >= 10 && p.n_tokens >= (int64_t(16) << p.depth)) ||
                   (p.depth >= 9 && p.n_tokens >= (int64_t(32) << p.depth))))
             mode = MODE_TILED;
         else if (affine && int64_t(workspace_bytes) >= grouped_ws && p.depth >= 7 &&

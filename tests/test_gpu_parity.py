@@ -358,7 +358,12 @@ def test_describe_names_the_kernel(fff_lib):
     xf = torch.zeros((16384, 768), dtype=torch.float32, device=DEV)
     wf = torch.zeros((1, (1 << 12) - 1, 768), dtype=torch.float32, device=DEV)
     assert fff_lib.describe(xf, wf, wf, 11, 1).startswith("tiled<")  # fp32, 16384 tokens: 8 per leaf
-    assert fff_lib.describe(xf[:8192], wf, wf, 11, 1).startswith("descent<")  # 4 per leaf
+    assert fff_lib.describe(xf[:8192], wf, wf, 11, 1).startswith("descent<")  # 4 per leaf, 6.3M elements
+    for d, B, want in ((12, 16384, "tiled<"), (13, 16384, "tiled<"), (14, 32768, "tiled<"), (14, 16384, "grouped<")):
+        xfd = torch.zeros((B, 768), dtype=torch.float32, device=DEV)  # fp32 leaf pairs from 2 per leaf, 12M
+        wfd = torch.zeros((1, (2 << d) - 1, 768), dtype=torch.float32, device=DEV)
+        assert fff_lib.describe(xfd, wfd, wfd, d, 1).startswith(want), (d, B)
+        del xfd, wfd
     xw = torch.zeros((8192, 4096), dtype=torch.bfloat16, device=DEV)
     ww = torch.zeros((1, (1 << 12) - 1, 4096), dtype=torch.bfloat16, device=DEV)
     assert fff_lib.describe(xw, ww, ww, 11, 1).startswith("tiled<")  # 4 per leaf, hidden 4096
@@ -552,8 +557,8 @@ def test_tiled_multi_tree_spills_deterministic(fff_lib):
 
 
 def test_tiled_leaf_pairs_plan(fff_lib):
-    """fp32 weights with fewer than 16 tokens per leaf on average take a tile workgroup per pair of
-    sibling leaves (depth <= 14); bf16 weights and fuller leaves one per leaf."""
+    """Fewer than 16 tokens per leaf on average take a tile workgroup per pair of sibling leaves
+    (depth <= 14); fuller leaves one per leaf."""
     def pairs(B, D, wd, T=1):
         x = torch.zeros(B, 768, dtype=torch.float32, device=DEV)
         w = torch.zeros(T, (2 << D) - 1, 768, dtype=TORCH_DT[wd], device=DEV)
@@ -562,7 +567,7 @@ def test_tiled_leaf_pairs_plan(fff_lib):
         return int(s.split("leaf_pairs=")[1].split()[0])
     assert pairs(16384, 11, "f32") == 1  # the paper's Table 2 shape: 8 tokens per leaf
     assert pairs(32767, 11, "f32") == 1 and pairs(32768, 11, "f32") == 0
-    assert pairs(16384, 11, "bf16") == 0
+    assert pairs(16384, 11, "bf16") == 1 and pairs(65536, 11, "bf16") == 0  # the headline: 32 per leaf
     assert pairs(3000, 14, "f32") == 1 and pairs(3000, 15, "f32") == 0  # two more rows fit 16 levels
     assert pairs(4096, 9, "f32", T=4) == 1 and pairs(16384, 9, "f32", T=4) == 0
 
@@ -800,6 +805,8 @@ def test_auto_multi_tree_deep_plans(fff_lib):
         return fff_lib.describe(x, w, w, d, T).split("<")[0]
     assert plan(4, 9, 16384, "f32") == "tiled"      # UltraFastBERT-4x9: 32 per leaf
     assert plan(4, 9, 8192, "f32") == "descent"     # 16 per leaf
+    assert plan(4, 10, 16384, "f32") == "tiled"     # 16 per leaf at depth 10
+    assert plan(4, 10, 8192, "f32") == "descent"
     assert plan(4, 8, 16384, "f32") == "descent"    # depth 8
     assert plan(8, 11, 65536, "f32") == "tiled"
     assert plan(2, 11, 16384, "f32") == "tiled"     # 8 per leaf at depth 11
