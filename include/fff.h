@@ -84,9 +84,14 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * workspace, rounded once by the last tree): fp32 MFMA for fp32 weights; for bf16 weights bf16 MFMA on the
  * activations split into bf16 parts (three parts: fp32 working accuracy; two,
  * relative error about 2^-17, when y is bf16 and either stored or the residual
- * of bf16 x).  When more tokens reach a leaf than its bucket holds, all of
- * that leaf's tokens take the per-token emit instead, so the output bits do
- * not depend on the order in which the walk filled the bucket's slots.  A call
+ * of bf16 x).  Below 16 tokens per leaf on average (depth <= 14) one
+ * workgroup takes a pair of sibling leaves: their tokens share the rows of
+ * levels 0..D-1 and fill one list of tiles, with the two leaves' rows as two
+ * extra rows of the product (each token's leaf activation on its own leaf's
+ * row, zero on the other).  When more tokens reach a leaf than its bucket
+ * holds, all of that leaf's tokens (with pairs, both leaves') take the
+ * per-token emit instead, so the output bits do not depend on the order in
+ * which the walk filled the bucket's slots.  A call
  * with more than (2^31 - 1) / (4 hidden) tokens (699050 at hidden 768) runs as
  * consecutive chunks of that many tokens, each a complete tiled forward (the
  * output stores use 32-bit offsets).  Needs the workspace of
@@ -122,13 +127,14 @@ typedef enum { FFF_ACT_GELU_ERF = 0, FFF_ACT_GELU_TANH = 1, FFF_ACT_IDENTITY = 2
  * workspace is large enough, TILED at depth 9..15 with at least 8 tokens per
  * leaf and 48M input elements (tokens x hidden), or 16 tokens per leaf and
  * 16M elements (bf16 W at depth 9: from 96M elements), and at depth 11 or
- * more with 8 tokens per leaf (fp32 W) or 4 per leaf at hidden 2048 or more
- * (bf16 W); else GROUPED at depth
+ * more with 8 tokens per leaf (fp32 W; from 2 per leaf at depth <= 14 with
+ * 12M elements) or 4 per leaf at hidden 2048 or more (bf16 W); else GROUPED
+ * at depth
  * 11 or more from 48M elements, or from 16384 tokens with fp32 W or 24M
  * elements, and with fp32 W at depth 5 or more from 65536 tokens; for 2, 4
  * or 8 trees of depth 7 or more (the walk tree-affine), with fp32 W TILED at
- * depth 11 or more from 8 tokens per leaf or at depth 9 or more from 32
- * tokens per leaf, else GROUPED from 65536 tokens (16384 with 8
+ * depth 11 or more from 8 tokens per leaf, at depth 10 from 16 or at depth 9
+ * or more from 32 tokens per leaf, else GROUPED from 65536 tokens (16384 with 8
  * trees), and with bf16 W GROUPED for 8 trees, for 4 from 4096 tokens at
  * depth 8 or more (65536 at depth 7) and for 2 from 65536 tokens at depth 8
  * or more; GROUPED for 8 trees up to 2048 tokens with bf16 W (4096 at depth
